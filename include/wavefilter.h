@@ -1,0 +1,230 @@
+/*
+ * wavefilter.h -- C ABI of the MI355X (gfx950) WaveFilter filter+attend path.
+ *
+ * WaveFilter (arXiv 2606.00724) replaces attention of a query block over a
+ * long cached prompt by attention over a small sparse cache that a
+ * coarse-to-fine wavelet search picks, per head:
+ *
+ *   1. wf_dwt_keys     J-level 1-D DWT of the cached prompt keys along the
+ *                      sequence (Section 2.2, eq. 5; Section 3.1, eq. 6).
+ *   2. wf_skim_score   perception weights softmax(Q A_J^T * scale) per query
+ *                      row (eq. 7), column sums W (eq. 8), top-S coarse
+ *                      regions (eq. 9 with the proportion given as a count).
+ *   3. wf_scan_select  the regions' tokens (eq. 10) scored the same way at
+ *                      token resolution (Section 3.2), top-k tokens -> mu^0.
+ *   4. wf_gather_kv    sparse cache [K[mu^0]; K_g], [V[mu^0]; V_g]
+ *                      (Section 3.2, last paragraph; Algorithm 1).
+ *   5. wf_sparse_attn  attention of the query block over the sparse cache,
+ *                      no mask (the cached-attention form of eq. 3).
+ *   6. wf_filter_attend  steps 1-5 fused; the sparse cache is never
+ *                      materialised.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - A "unit" is one (batch, head) pair; units are independent.  Tensors are
+ *    row-major and contiguous, unit-major, with the head dimension d fastest:
+ *        Q  [batch][heads][q_len][d]        K, V [batch][heads][ctx_len][d]
+ *        Kg, Vg [batch][heads][gen_len][d]  O    [batch][heads][q_len][d]
+ *  - Element type of Q, K, V, Kg, Vg, Ks, Vs and O is params->dtype
+ *    (WF_BF16 or WF_F32).  Coefficients, scores and all softmax arithmetic
+ *    are fp32; index outputs are int32.
+ *  - Every tensor pointer is device memory owned by the caller, 16-byte
+ *    aligned.  The library never allocates, frees or synchronises: kernels are
+ *    queued on `stream` (a hipStream_t; NULL = the default stream) and the
+ *    call returns before they finish.
+ *  - Calls that need scratch memory take a caller-owned device workspace of
+ *    at least wf_workspace_bytes(params, op) bytes (256-byte aligned).  Its
+ *    contents need no initialisation and are garbage afterwards; two calls
+ *    in flight at once must not share one workspace.
+ *  - Every argument is checked on the host before anything is queued.  A
+ *    rejected call returns a non-zero wf_status, queues nothing and records a
+ *    message that wf_last_error() returns (per thread).  The library never
+ *    aborts, throws or prints.  A failure reported by the HIP runtime while
+ *    queueing returns WF_ERR_HIP.
+ *  - Index sets are returned in ascending order.  Selection orders scores
+ *    descending and breaks exact ties by the lower index.
+ */
+#ifndef WAVEFILTER_H
+#define WAVEFILTER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum wf_status {
+    WF_OK = 0,
+    WF_ERR_INVALID_ARG = 1, /* null/misaligned pointer, size out of range   */
+    WF_ERR_UNSUPPORTED = 2, /* valid request this build does not implement  */
+    WF_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required   */
+    WF_ERR_HIP = 4          /* the HIP runtime reported an error            */
+} wf_status;
+
+/* Wavelet families (Section 2.2; the paper uses Haar throughout).
+ * Filters are orthonormal and applied in forward phase,
+ * A[n] = sum_m g_m y[2n+m], so Haar coefficient j of level J covers tokens
+ * 2^J j .. 2^J j + 2^J - 1, the region of eq. 10.
+ *   WF_HAAR: g = (1, 1)/sqrt2
+ *   WF_DB2:  Daubechies 4-tap, g = (1+r3, 3+r3, 3-r3, 1-r3)/(4 sqrt2)      */
+enum { WF_HAAR = 0, WF_DB2 = 1 };
+
+/* Right-end extension of each level's sequence for WF_DB2 (Haar never reads
+ * past the end): half-sample symmetric (y[N] = y[N-1], y[N+1] = y[N-2]) or
+ * periodic (y[N+i] = y[i]). */
+enum { WF_EXT_SYMMETRIC = 0, WF_EXT_PERIODIC = 1 };
+
+/* Element type of the tensors listed above. */
+enum { WF_BF16 = 0, WF_F32 = 1 };
+
+/* Operations whose workspace size wf_workspace_bytes reports. */
+enum { WF_OP_SKIM = 0, WF_OP_SCAN = 1, WF_OP_ATTN = 2, WF_OP_FUSED = 3 };
+
+/* Limits of this build. */
+enum {
+    WF_MAX_LEVELS = 10,  /* J                                   */
+    WF_MAX_Q_LEN = 256   /* B, rows of the query block          */
+};
+
+typedef struct wf_params {
+    int32_t batch;    /* >= 1                                                 */
+    int32_t heads;    /* >= 1; K/V heads equal query heads                    */
+    int32_t ctx_len;  /* L = |I_p|, prompt positions filtered; L % 2^J == 0  */
+    int32_t head_dim; /* d: 64 or 128                                         */
+    int32_t q_len;    /* B = |I~|, query rows: 1 .. WF_MAX_Q_LEN              */
+    int32_t gen_len;  /* G = |I_g| >= 0, tail rows always kept (never scored) */
+    int32_t levels;   /* J: 1 .. WF_MAX_LEVELS, 2^J <= L                      */
+    int32_t wavelet;  /* WF_HAAR or WF_DB2                                    */
+    int32_t boundary; /* WF_EXT_* (read for WF_DB2 only)                      */
+    int32_t dtype;    /* WF_BF16 or WF_F32                                    */
+    int32_t segments; /* S: coarse regions kept, 1 .. L >> J                  */
+    int32_t budget;   /* k >= 1: tokens kept; effective k_eff = min(k, S 2^J) */
+    float scale;      /* softmax scale for skim, scan and attention;
+                         0 selects 1/sqrt(d) (eqs. 1, 3 and 7)                */
+} wf_params;
+
+/* Bytes of workspace `op` needs for these parameters (0 if it needs none or
+ * the parameters are invalid). */
+size_t wf_workspace_bytes(const wf_params* p, int32_t op);
+
+/* k_eff = min(budget, segments * 2^levels), or -1 if p is invalid. */
+int32_t wf_effective_budget(const wf_params* p);
+
+/*
+ * Step 1 (eqs. 5-6): J-level DWT of the keys along the sequence.
+ *   K        [batch][heads][L][d]                 dtype
+ *   approx   [batch][heads][L >> J][d]            fp32 out: A_J
+ *   details  nullable; per unit the rows of D_1, then D_2, ... D_J,
+ *            [batch][heads][sum_{j=1..J} L >> j][d] fp32 out
+ */
+wf_status wf_dwt_keys(const wf_params* p, const void* K, float* approx,
+                      float* details, void* stream);
+
+/*
+ * Step 2 (eqs. 7-9): skim weights and the top-S coarse regions.
+ *   Q          [batch][heads][B][d]               dtype
+ *   approx     [batch][heads][L >> J][d]          fp32 (from wf_dwt_keys)
+ *   seg_score  [batch][heads][L >> J]             fp32 out: W
+ *   seg_idx    [batch][heads][S]                  int32 out, ascending
+ *   workspace  >= wf_workspace_bytes(p, WF_OP_SKIM)
+ */
+wf_status wf_skim_score(const wf_params* p, const void* Q, const float* approx,
+                        float* seg_score, int32_t* seg_idx, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
+ * Step 3 (eq. 10, then eqs. 7-9 at token resolution): the pool is the
+ * S 2^J tokens of the regions in seg_idx, in ascending order; each pool
+ * token gets W'_t = sum over query rows of its softmax weight (softmax over
+ * the pool only); the k_eff best tokens are returned.
+ *   Q          [batch][heads][B][d]               dtype
+ *   K          [batch][heads][L][d]               dtype
+ *   seg_idx    [batch][heads][S]                  int32, strictly ascending,
+ *                                                 each in [0, L >> J)
+ *   tok_score  nullable [batch][heads][S 2^J]     fp32 out: W' in pool order
+ *   tok_idx    [batch][heads][k_eff]              int32 out, ascending
+ *   workspace  >= wf_workspace_bytes(p, WF_OP_SCAN)
+ * Region ids are not range-checked on the device: out-of-range or unsorted
+ * ids are undefined behaviour (the host cannot read device memory).
+ */
+wf_status wf_scan_select(const wf_params* p, const void* Q, const void* K,
+                         const int32_t* seg_idx, float* tok_score,
+                         int32_t* tok_idx, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/*
+ * Step 4 (Section 3.2, last paragraph): the sparse cache.
+ *   K, V       [batch][heads][L][d]               dtype
+ *   tok_idx    [batch][heads][k_eff]              int32, each in [0, L)
+ *   Kg, Vg     [batch][heads][G][d]               dtype; NULL iff G == 0
+ *   Ks, Vs     [batch][heads][k_eff + G][d]       dtype out:
+ *              rows r < k_eff: K[tok_idx[r]]; then the G tail rows
+ */
+wf_status wf_gather_kv(const wf_params* p, const void* K, const void* V,
+                       const int32_t* tok_idx, const void* Kg, const void* Vg,
+                       void* Ks, void* Vs, void* stream);
+
+/*
+ * Step 5 (eq. 3 form): O = softmax(scale Q Ks^T) Vs over n_kv cache rows,
+ * every query row sees every row (bidirectional, no mask).
+ *   Q          [batch][heads][B][d]               dtype
+ *   Ks, Vs     [batch][heads][n_kv][d]            dtype, n_kv >= 1
+ *   O          [batch][heads][B][d]               dtype out (RNE for bf16)
+ *   workspace  >= wf_workspace_bytes(p, WF_OP_ATTN) (sized for n_kv up to
+ *              k_eff + G; a larger n_kv needs the workspace of a params copy
+ *              whose budget/segments/gen_len give that many rows)
+ */
+wf_status wf_sparse_attn(const wf_params* p, const void* Q, const void* Ks,
+                         const void* Vs, int32_t n_kv, void* O,
+                         void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/*
+ * Steps 1-5 fused for one layer of one denoising step.  The DWT never leaves
+ * the chip, and attention reads the selected K/V rows in place.
+ *   Q [batch][heads][B][d], K, V [batch][heads][L][d], Kg, Vg
+ *   [batch][heads][G][d] (NULL iff G == 0)      dtype
+ *   O          [batch][heads][B][d]               dtype out
+ *   tok_idx    nullable [batch][heads][k_eff]     int32 out: mu^0, ascending
+ *   seg_idx    nullable [batch][heads][S]         int32 out: the coarse
+ *              regions J_B of eq. 9, ascending
+ *   workspace  >= wf_workspace_bytes(p, WF_OP_FUSED)
+ */
+wf_status wf_filter_attend(const wf_params* p, const void* Q, const void* K,
+                           const void* V, const void* Kg, const void* Vg,
+                           void* O, int32_t* tok_idx, int32_t* seg_idx,
+                           void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * wf_filter_attend that also records HIP events around its kernels, for
+ * per-kernel timing.  events: array of n_events hipEvent_t handles created by
+ * the caller (timing enabled); events[0] is recorded before the first kernel
+ * and events[i] after the i-th kernel.  wf_filter_attend_kernels() gives the
+ * kernel count for these parameters; n_events must be at least that count
+ * plus one.  Same results as wf_filter_attend.
+ */
+wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
+                                 const void* K, const void* V, const void* Kg,
+                                 const void* Vg, void* O, int32_t* tok_idx,
+                                 int32_t* seg_idx, void* workspace,
+                                 size_t workspace_bytes, void* stream,
+                                 void** events, int32_t n_events);
+
+/* Kernels one wf_filter_attend call queues for these parameters, and the
+ * name of the i-th one (static strings), or -1 / NULL if p is invalid. */
+int32_t wf_filter_attend_kernels(const wf_params* p);
+const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i);
+
+/* Static description of a status code. */
+const char* wf_status_str(wf_status s);
+
+/* Detail of the last non-OK return on the calling thread ("" if none). */
+const char* wf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WAVEFILTER_H */

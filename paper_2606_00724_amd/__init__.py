@@ -1,0 +1,248 @@
+"""Python binding of libwavefilter.so, the gfx950 WaveFilter filter+attend path.
+
+Argument marshalling only: every ``wf_*`` function here forwards torch device
+tensors (pointers) and a HIP stream to the C entry point of the same name
+declared in include/wavefilter.h, and raises :class:`WfError` on a non-OK
+status.  Torch supplies device memory and streams; all arithmetic runs in the
+library's HIP kernels.  There is no fallback: importing this package fails if
+the library has not been built (``python -m paper_2606_00724_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwavefilter.so")
+
+HAAR, DB2 = 0, 1
+EXT_SYMMETRIC, EXT_PERIODIC = 0, 1
+BF16, F32 = 0, 1
+OP_SKIM, OP_SCAN, OP_ATTN, OP_FUSED = 0, 1, 2, 3
+MAX_LEVELS, MAX_Q_LEN = 10, 256
+
+_STATUS = {0: "WF_OK", 1: "WF_ERR_INVALID_ARG", 2: "WF_ERR_UNSUPPORTED",
+           3: "WF_ERR_WORKSPACE", 4: "WF_ERR_HIP"}
+
+EXPORTED = ("wf_workspace_bytes", "wf_effective_budget", "wf_dwt_keys",
+            "wf_skim_score", "wf_scan_select", "wf_gather_kv",
+            "wf_sparse_attn", "wf_filter_attend", "wf_filter_attend_timed",
+            "wf_filter_attend_kernels", "wf_filter_attend_kernel_name",
+            "wf_status_str", "wf_last_error")
+
+
+class WfParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "batch", "heads", "ctx_len", "head_dim", "q_len", "gen_len", "levels",
+        "wavelet", "boundary", "dtype", "segments", "budget")] + [
+        ("scale", ctypes.c_float)]
+
+    def as_dict(self) -> dict:
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class WfError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        self.status = status
+        self.status_name = _STATUS.get(status, str(status))
+        super().__init__(f"{self.status_name}: {message}")
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with "
+            "`python -m paper_2606_00724_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER(WfParams)
+    vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
+    sig = {
+        "wf_workspace_bytes": (sz, [P, i32]),
+        "wf_effective_budget": (i32, [P]),
+        "wf_dwt_keys": (ctypes.c_int, [P, vp, vp, vp, vp]),
+        "wf_skim_score": (ctypes.c_int, [P, vp, vp, vp, vp, vp, sz, vp]),
+        "wf_scan_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "wf_gather_kv": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "wf_sparse_attn": (ctypes.c_int, [P, vp, vp, vp, i32, vp, vp, sz, vp]),
+        "wf_filter_attend": (ctypes.c_int,
+                             [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "wf_filter_attend_timed": (ctypes.c_int,
+                                   [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                    vp, ctypes.POINTER(vp), i32]),
+        "wf_filter_attend_kernels": (i32, [P]),
+        "wf_filter_attend_kernel_name": (ctypes.c_char_p, [P, i32]),
+        "wf_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+        "wf_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def library() -> ctypes.CDLL:
+    return _lib
+
+
+# ------------------------------------------------------------ parameters
+
+def make_params(*, batch: int, heads: int, ctx_len: int, head_dim: int,
+                q_len: int, levels: int, segments: int, budget: int,
+                gen_len: int = 0, wavelet: str | int = "haar",
+                boundary: str | int = "symmetric", dtype: str | int = "bf16",
+                scale: float = 0.0) -> WfParams:
+    w = {"haar": HAAR, "db2": DB2}.get(wavelet, wavelet)
+    b = {"symmetric": EXT_SYMMETRIC, "periodic": EXT_PERIODIC}.get(boundary,
+                                                                   boundary)
+    dt = {"bf16": BF16, "f32": F32, torch.bfloat16: BF16,
+          torch.float32: F32}.get(dtype, dtype)
+    return WfParams(batch, heads, ctx_len, head_dim, q_len, gen_len, levels,
+                    w, b, dt, segments, budget, scale)
+
+
+def params_for(w, gen_len: int | None = None) -> WfParams:
+    """Parameters of a workload description (any object with the fields of
+    ``synth.Workload``)."""
+    return make_params(batch=w.batch, heads=w.heads, ctx_len=w.ctx_len,
+                       head_dim=w.head_dim, q_len=w.q_len, levels=w.levels,
+                       segments=w.segments, budget=w.budget,
+                       gen_len=w.gen_len if gen_len is None else gen_len,
+                       wavelet=w.wavelet, boundary=w.boundary, dtype=w.dtype)
+
+
+def torch_dtype(p: WfParams) -> torch.dtype:
+    return torch.bfloat16 if p.dtype == BF16 else torch.float32
+
+
+def workspace_bytes(p: WfParams, op: int) -> int:
+    return int(_lib.wf_workspace_bytes(ctypes.byref(p), op))
+
+
+def effective_budget(p: WfParams) -> int:
+    return int(_lib.wf_effective_budget(ctypes.byref(p)))
+
+
+def fused_kernel_names(p: WfParams) -> list[str]:
+    n = _lib.wf_filter_attend_kernels(ctypes.byref(p))
+    return [_lib.wf_filter_attend_kernel_name(ctypes.byref(p), i).decode()
+            for i in range(n)]
+
+
+# ------------------------------------------------------------ marshalling
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"expected a torch tensor, got {type(t).__name__}")
+    if t.device.type != "cuda":
+        raise ValueError("tensors passed to the WaveFilter library must be on "
+                         "a GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the WaveFilter library must be "
+                         "contiguous")
+    return t.data_ptr()
+
+
+def _ws(t) -> tuple[int | None, int]:
+    if t is None:
+        return None, 0
+    return _ptr(t), t.numel() * t.element_size()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise WfError(status, _lib.wf_last_error().decode())
+
+
+def wf_dwt_keys(p, K, approx, details=None, stream=None):
+    _check(_lib.wf_dwt_keys(ctypes.byref(p), _ptr(K), _ptr(approx),
+                            _ptr(details), _stream(stream)))
+
+
+def wf_skim_score(p, Q, approx, seg_score, seg_idx, workspace, stream=None):
+    ws, nb = _ws(workspace)
+    _check(_lib.wf_skim_score(ctypes.byref(p), _ptr(Q), _ptr(approx),
+                              _ptr(seg_score), _ptr(seg_idx), ws, nb,
+                              _stream(stream)))
+
+
+def wf_scan_select(p, Q, K, seg_idx, tok_score, tok_idx, workspace,
+                   stream=None):
+    ws, nb = _ws(workspace)
+    _check(_lib.wf_scan_select(ctypes.byref(p), _ptr(Q), _ptr(K),
+                               _ptr(seg_idx), _ptr(tok_score), _ptr(tok_idx),
+                               ws, nb, _stream(stream)))
+
+
+def wf_gather_kv(p, K, V, tok_idx, Kg, Vg, Ks, Vs, stream=None):
+    _check(_lib.wf_gather_kv(ctypes.byref(p), _ptr(K), _ptr(V), _ptr(tok_idx),
+                             _ptr(Kg), _ptr(Vg), _ptr(Ks), _ptr(Vs),
+                             _stream(stream)))
+
+
+def wf_sparse_attn(p, Q, Ks, Vs, n_kv, O, workspace, stream=None):
+    ws, nb = _ws(workspace)
+    _check(_lib.wf_sparse_attn(ctypes.byref(p), _ptr(Q), _ptr(Ks), _ptr(Vs),
+                               int(n_kv), _ptr(O), ws, nb, _stream(stream)))
+
+
+def wf_filter_attend(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
+                     stream=None):
+    ws, nb = _ws(workspace)
+    _check(_lib.wf_filter_attend(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V),
+                                 _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx),
+                                 _ptr(seg_idx), ws, nb, _stream(stream)))
+
+
+def wf_filter_attend_timed(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
+                           workspace, events, stream=None):
+    """``events``: sequence of raw hipEvent_t handles (ints)."""
+    ws, nb = _ws(workspace)
+    arr = (ctypes.c_void_p * len(events))(*events)
+    _check(_lib.wf_filter_attend_timed(ctypes.byref(p), _ptr(Q), _ptr(K),
+                                       _ptr(V), _ptr(Kg), _ptr(Vg), _ptr(O),
+                                       _ptr(tok_idx), _ptr(seg_idx), ws, nb,
+                                       _stream(stream), arr, len(events)))
+
+
+# ------------------------------------------------------------ allocation
+# Torch allocates the buffers; the library only reads and writes them.
+
+def alloc_workspace(p: WfParams, op: int, device) -> torch.Tensor | None:
+    nb = workspace_bytes(p, op)
+    if nb == 0:
+        return None
+    # torch's caching allocator returns 256-byte aligned blocks
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+def filter_attend(p: WfParams, Q, K, V, Kg=None, Vg=None, workspace=None,
+                  want_indices: bool = False, stream=None):
+    """Allocates O (and the index outputs) and runs wf_filter_attend.
+    Returns O, or (O, tok_idx, seg_idx) when want_indices."""
+    O = torch.empty_like(Q)
+    tok = seg = None
+    if want_indices:
+        tok = torch.empty((p.batch, p.heads, effective_budget(p)),
+                          dtype=torch.int32, device=Q.device)
+        seg = torch.empty((p.batch, p.heads, p.segments), dtype=torch.int32,
+                          device=Q.device)
+    if workspace is None:
+        workspace = alloc_workspace(p, OP_FUSED, Q.device)
+    wf_filter_attend(p, Q, K, V, Kg, Vg, O, tok, seg, workspace, stream)
+    return (O, tok, seg) if want_indices else O

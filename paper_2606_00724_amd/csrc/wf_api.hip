@@ -1,0 +1,419 @@
+// C ABI of the WaveFilter filter+attend path: argument checks, workspace
+// layout and the kernel sequence of every entry point (see wavefilter.h).
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "wf_kernels.hpp"
+#include "wf_launch.hpp"
+
+namespace wf {
+
+static thread_local char g_last_error[512] = "";
+
+static wf_status fail(wf_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+static wf_status ok() {
+  g_last_error[0] = '\0';
+  return WF_OK;
+}
+
+float effective_scale(const wf_params& p) {
+  return p.scale != 0.f ? p.scale : (float)(1.0 / std::sqrt((double)p.head_dim));
+}
+
+int device_cu_count() {
+  static thread_local int cached_dev = -1, cached_cus = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (dev != cached_dev) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+            hipSuccess ||
+        cus <= 0)
+      cus = 256;
+    cached_dev = dev;
+    cached_cus = cus;
+  }
+  return cached_cus;
+}
+
+// ------------------------------------------------------------ validation
+
+static wf_status check_params(const wf_params* p) {
+  if (!p) return fail(WF_ERR_INVALID_ARG, "params is NULL");
+  if (p->batch < 1 || p->heads < 1)
+    return fail(WF_ERR_INVALID_ARG, "batch (%d) and heads (%d) must be >= 1",
+                p->batch, p->heads);
+  if ((long)p->batch * p->heads > (1L << 24))
+    return fail(WF_ERR_UNSUPPORTED, "batch*heads = %ld exceeds 2^24",
+                (long)p->batch * p->heads);
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(WF_ERR_UNSUPPORTED, "head_dim %d: only 64 and 128 are built",
+                p->head_dim);
+  if (p->q_len < 1) return fail(WF_ERR_INVALID_ARG, "q_len %d < 1", p->q_len);
+  if (p->q_len > WF_MAX_Q_LEN)
+    return fail(WF_ERR_UNSUPPORTED, "q_len %d exceeds %d", p->q_len,
+                (int)WF_MAX_Q_LEN);
+  if (p->gen_len < 0) return fail(WF_ERR_INVALID_ARG, "gen_len %d < 0", p->gen_len);
+  if (p->levels < 1) return fail(WF_ERR_INVALID_ARG, "levels %d < 1", p->levels);
+  if (p->levels > WF_MAX_LEVELS)
+    return fail(WF_ERR_UNSUPPORTED, "levels %d exceeds %d", p->levels,
+                (int)WF_MAX_LEVELS);
+  if (p->ctx_len < (1 << p->levels))
+    return fail(WF_ERR_INVALID_ARG, "ctx_len %d is shorter than 2^levels = %d",
+                p->ctx_len, 1 << p->levels);
+  if (p->ctx_len > (1 << 30))
+    return fail(WF_ERR_UNSUPPORTED, "ctx_len %d exceeds 2^30", p->ctx_len);
+  if (p->ctx_len % (1 << p->levels) != 0)
+    return fail(WF_ERR_UNSUPPORTED,
+                "ctx_len %d is not a multiple of 2^levels = %d", p->ctx_len,
+                1 << p->levels);
+  if (p->wavelet != WF_HAAR && p->wavelet != WF_DB2)
+    return fail(WF_ERR_INVALID_ARG, "unknown wavelet %d", p->wavelet);
+  if (p->boundary != WF_EXT_SYMMETRIC && p->boundary != WF_EXT_PERIODIC)
+    return fail(WF_ERR_INVALID_ARG, "unknown boundary %d", p->boundary);
+  if (p->dtype != WF_BF16 && p->dtype != WF_F32)
+    return fail(WF_ERR_INVALID_ARG, "unknown dtype %d", p->dtype);
+  const int nJ = p->ctx_len >> p->levels;
+  if (p->segments < 1 || p->segments > nJ)
+    return fail(WF_ERR_INVALID_ARG, "segments %d outside [1, %d]", p->segments, nJ);
+  if (p->budget < 1) return fail(WF_ERR_INVALID_ARG, "budget %d < 1", p->budget);
+  if (!std::isfinite(p->scale))
+    return fail(WF_ERR_INVALID_ARG, "scale is not finite");
+  if ((long)p->batch * p->heads * ((long)p->budget < ((long)p->segments << p->levels)
+                                        ? (long)p->budget
+                                        : ((long)p->segments << p->levels)) +
+          (long)p->gen_len > (1L << 31))
+    return fail(WF_ERR_UNSUPPORTED, "sparse cache too large");
+  return WF_OK;
+}
+
+static wf_status check_ptr(const void* ptr, const char* name, bool nullable) {
+  if (!ptr) {
+    if (nullable) return WF_OK;
+    return fail(WF_ERR_INVALID_ARG, "%s is NULL", name);
+  }
+  if (((uintptr_t)ptr & 15u) != 0)
+    return fail(WF_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return WF_OK;
+}
+
+#define WF_TRY(expr)                 \
+  do {                               \
+    wf_status _s = (expr);           \
+    if (_s != WF_OK) return _s;      \
+  } while (0)
+
+#define WF_HIP(expr, what)                                                  \
+  do {                                                                      \
+    hipError_t _e = (expr);                                                 \
+    if (_e != hipSuccess)                                                   \
+      return fail(WF_ERR_HIP, "%s: %s", what, hipGetErrorString(_e));      \
+  } while (0)
+
+// ------------------------------------------------------------ workspace
+
+static size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t logits = 0, sstats = 0, W = 0, seg = 0, cstats = 0, wpool = 0,
+         tok = 0, part = 0, pstat = 0, total = 0;
+};
+
+static long keff_of(const wf_params& p) {
+  const long pool = (long)p.segments << p.levels;
+  return p.budget < pool ? p.budget : pool;
+}
+
+static Layout layout_for(const wf_params& p, int op, long attn_rows) {
+  Layout l;
+  const size_t U = (size_t)p.batch * p.heads, B = p.q_len;
+  const size_t nJ = (size_t)p.ctx_len >> p.levels;
+  const size_t P = (size_t)p.segments << p.levels;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += up256(bytes);
+    return at;
+  };
+  const bool skim = op == WF_OP_SKIM || op == WF_OP_FUSED;
+  const bool scan = op == WF_OP_SCAN || op == WF_OP_FUSED;
+  const bool attn = op == WF_OP_ATTN || op == WF_OP_FUSED;
+  if (skim) {
+    const SkimPlan sp = plan_skim(p, op == WF_OP_FUSED);
+    l.logits = take(U * B * nJ * sizeof(float));
+    l.sstats = take(U * sp.ntiles * 2 * B * sizeof(float));
+  }
+  if (op == WF_OP_FUSED) {
+    l.W = take(U * nJ * sizeof(float));
+    l.seg = take(U * p.segments * sizeof(int32_t));
+  }
+  if (scan) {
+    const ScanPlan cp = plan_scan(p);
+    l.cstats = take(U * cp.chunks * 2 * B * sizeof(float));
+    l.wpool = take(U * P * sizeof(float));
+  }
+  if (op == WF_OP_FUSED) l.tok = take(U * keff_of(p) * sizeof(int32_t));
+  if (attn) {
+    const AttnPlan ap = plan_attn(p, attn_rows);
+    l.part = take(U * ap.splits * B * p.head_dim * sizeof(float));
+    l.pstat = take(U * ap.splits * 2 * B * sizeof(float));
+  }
+  l.total = off;
+  return l;
+}
+
+static wf_status check_workspace(const void* ws, size_t have, size_t need) {
+  if (need == 0) return WF_OK;
+  if (!ws) return fail(WF_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (((uintptr_t)ws & 255u) != 0)
+    return fail(WF_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (have < need)
+    return fail(WF_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return WF_OK;
+}
+
+static inline char* at(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
+
+// ------------------------------------------------------------ fused sequence
+
+static const char* const kFusedNames[] = {
+    "skim_tile", "skim_select", "scan_stats", "scan_weights",
+    "scan_select", "sparse_attn", "attn_combine"};
+constexpr int kFusedKernels = 7;
+
+static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
+                            const void* V, const void* Kg, const void* Vg,
+                            void* O, int32_t* tok_idx, int32_t* seg_idx,
+                            void* ws, size_t ws_bytes, void* stream,
+                            void** events, int n_events) {
+  WF_TRY(check_params(p));
+  WF_TRY(check_ptr(Q, "Q", false));
+  WF_TRY(check_ptr(K, "K", false));
+  WF_TRY(check_ptr(V, "V", false));
+  WF_TRY(check_ptr(O, "O", false));
+  WF_TRY(check_ptr(tok_idx, "tok_idx", true));
+  WF_TRY(check_ptr(seg_idx, "seg_idx", true));
+  if (p->gen_len > 0) {
+    WF_TRY(check_ptr(Kg, "Kg", false));
+    WF_TRY(check_ptr(Vg, "Vg", false));
+  }
+  if (events && n_events < kFusedKernels + 1)
+    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, kFusedKernels + 1);
+  const long keff = keff_of(*p);
+  const long nrows = keff + p->gen_len;
+  const Layout l = layout_for(*p, WF_OP_FUSED, nrows);
+  WF_TRY(check_workspace(ws, ws_bytes, l.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const SkimPlan sp = plan_skim(*p, true);
+  float* logits = reinterpret_cast<float*>(at(ws, l.logits));
+  float* sstats = reinterpret_cast<float*>(at(ws, l.sstats));
+  float* W = reinterpret_cast<float*>(at(ws, l.W));
+  int32_t* seg = seg_idx ? seg_idx : reinterpret_cast<int32_t*>(at(ws, l.seg));
+  float* cstats = reinterpret_cast<float*>(at(ws, l.cstats));
+  float* wpool = reinterpret_cast<float*>(at(ws, l.wpool));
+  int32_t* tok = tok_idx ? tok_idx : reinterpret_cast<int32_t*>(at(ws, l.tok));
+  float* part = reinterpret_cast<float*>(at(ws, l.part));
+  float* pstat = reinterpret_cast<float*>(at(ws, l.pstat));
+  int k = 0;
+  auto mark = [&]() -> hipError_t {
+    if (!events) return hipSuccess;
+    return hipEventRecord(static_cast<hipEvent_t>(events[k]), s);
+  };
+  WF_HIP(mark(), "hipEventRecord");
+  WF_HIP(launch_skim_tiles(*p, true, Q, K, nullptr, logits, sstats, s), kFusedNames[k]);
+  ++k;
+  WF_HIP(mark(), "hipEventRecord");
+  WF_HIP(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s), kFusedNames[k]);
+  ++k;
+  WF_HIP(mark(), "hipEventRecord");
+  WF_HIP(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s), kFusedNames[k]);
+  ++k;
+  WF_HIP(mark(), "hipEventRecord");
+  WF_HIP(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s), kFusedNames[k]);
+  ++k;
+  WF_HIP(mark(), "hipEventRecord");
+  WF_HIP(launch_scan_select(*p, wpool, seg, tok, s), kFusedNames[k]);
+  ++k;
+  WF_HIP(mark(), "hipEventRecord");
+  WF_HIP(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
+                     part, pstat, s),
+         kFusedNames[k]);
+  ++k;
+  WF_HIP(mark(), "hipEventRecord");
+  WF_HIP(launch_attn_combine(*p, nrows, part, pstat, O, s), kFusedNames[k]);
+  ++k;
+  WF_HIP(mark(), "hipEventRecord");
+  return ok();
+}
+
+}  // namespace wf
+
+using namespace wf;
+
+extern "C" {
+
+size_t wf_workspace_bytes(const wf_params* p, int32_t op) {
+  if (check_params(p) != WF_OK) return 0;
+  if (op < WF_OP_SKIM || op > WF_OP_FUSED) return 0;
+  return layout_for(*p, op, keff_of(*p) + p->gen_len).total;
+}
+
+int32_t wf_effective_budget(const wf_params* p) {
+  if (check_params(p) != WF_OK) return -1;
+  return (int32_t)keff_of(*p);
+}
+
+wf_status wf_dwt_keys(const wf_params* p, const void* K, float* approx,
+                      float* details, void* stream) {
+  WF_TRY(check_params(p));
+  WF_TRY(check_ptr(K, "K", false));
+  WF_TRY(check_ptr(approx, "approx", false));
+  WF_TRY(check_ptr(details, "details", true));
+  (void)hipGetLastError();
+  WF_HIP(launch_dwt(*p, K, approx, details, static_cast<hipStream_t>(stream)),
+         "dwt");
+  return ok();
+}
+
+wf_status wf_skim_score(const wf_params* p, const void* Q, const float* approx,
+                        float* seg_score, int32_t* seg_idx, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  WF_TRY(check_params(p));
+  WF_TRY(check_ptr(Q, "Q", false));
+  WF_TRY(check_ptr(approx, "approx", false));
+  WF_TRY(check_ptr(seg_score, "seg_score", false));
+  WF_TRY(check_ptr(seg_idx, "seg_idx", false));
+  const Layout l = layout_for(*p, WF_OP_SKIM, 0);
+  WF_TRY(check_workspace(workspace, workspace_bytes, l.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const SkimPlan sp = plan_skim(*p, false);
+  float* logits = reinterpret_cast<float*>(at(workspace, l.logits));
+  float* sstats = reinterpret_cast<float*>(at(workspace, l.sstats));
+  (void)hipGetLastError();
+  WF_HIP(launch_skim_tiles(*p, false, Q, nullptr, approx, logits, sstats, s),
+         "skim_tile");
+  WF_HIP(launch_skim_select(*p, sp.ntiles, logits, sstats, seg_score, seg_idx, s),
+         "skim_select");
+  return ok();
+}
+
+wf_status wf_scan_select(const wf_params* p, const void* Q, const void* K,
+                         const int32_t* seg_idx, float* tok_score,
+                         int32_t* tok_idx, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  WF_TRY(check_params(p));
+  WF_TRY(check_ptr(Q, "Q", false));
+  WF_TRY(check_ptr(K, "K", false));
+  WF_TRY(check_ptr(seg_idx, "seg_idx", false));
+  WF_TRY(check_ptr(tok_score, "tok_score", true));
+  WF_TRY(check_ptr(tok_idx, "tok_idx", false));
+  const Layout l = layout_for(*p, WF_OP_SCAN, 0);
+  WF_TRY(check_workspace(workspace, workspace_bytes, l.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float* cstats = reinterpret_cast<float*>(at(workspace, l.cstats));
+  float* wpool = tok_score ? tok_score : reinterpret_cast<float*>(at(workspace, l.wpool));
+  (void)hipGetLastError();
+  WF_HIP(launch_scan_chunks(*p, 0, Q, K, seg_idx, cstats, wpool, s), "scan_stats");
+  WF_HIP(launch_scan_chunks(*p, 1, Q, K, seg_idx, cstats, wpool, s), "scan_weights");
+  WF_HIP(launch_scan_select(*p, wpool, seg_idx, tok_idx, s), "scan_select");
+  return ok();
+}
+
+wf_status wf_gather_kv(const wf_params* p, const void* K, const void* V,
+                       const int32_t* tok_idx, const void* Kg, const void* Vg,
+                       void* Ks, void* Vs, void* stream) {
+  WF_TRY(check_params(p));
+  WF_TRY(check_ptr(K, "K", false));
+  WF_TRY(check_ptr(V, "V", false));
+  WF_TRY(check_ptr(tok_idx, "tok_idx", false));
+  WF_TRY(check_ptr(Ks, "Ks", false));
+  WF_TRY(check_ptr(Vs, "Vs", false));
+  if (p->gen_len > 0) {
+    WF_TRY(check_ptr(Kg, "Kg", false));
+    WF_TRY(check_ptr(Vg, "Vg", false));
+  }
+  (void)hipGetLastError();
+  WF_HIP(launch_gather(*p, K, V, tok_idx, Kg, Vg, Ks, Vs,
+                       static_cast<hipStream_t>(stream)),
+         "gather");
+  return ok();
+}
+
+wf_status wf_sparse_attn(const wf_params* p, const void* Q, const void* Ks,
+                         const void* Vs, int32_t n_kv, void* O,
+                         void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  WF_TRY(check_params(p));
+  WF_TRY(check_ptr(Q, "Q", false));
+  WF_TRY(check_ptr(Ks, "Ks", false));
+  WF_TRY(check_ptr(Vs, "Vs", false));
+  WF_TRY(check_ptr(O, "O", false));
+  if (n_kv < 1) return fail(WF_ERR_INVALID_ARG, "n_kv %d < 1", n_kv);
+  const Layout l = layout_for(*p, WF_OP_ATTN, n_kv);
+  WF_TRY(check_workspace(workspace, workspace_bytes, l.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float* part = reinterpret_cast<float*>(at(workspace, l.part));
+  float* pstat = reinterpret_cast<float*>(at(workspace, l.pstat));
+  (void)hipGetLastError();
+  WF_HIP(launch_attn(*p, Q, Ks, Vs, nullptr, n_kv, nullptr, nullptr, 0, n_kv,
+                     part, pstat, s),
+         "sparse_attn");
+  WF_HIP(launch_attn_combine(*p, n_kv, part, pstat, O, s), "attn_combine");
+  return ok();
+}
+
+wf_status wf_filter_attend(const wf_params* p, const void* Q, const void* K,
+                           const void* V, const void* Kg, const void* Vg,
+                           void* O, int32_t* tok_idx, int32_t* seg_idx,
+                           void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  return fused_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
+                    workspace_bytes, stream, nullptr, 0);
+}
+
+wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
+                                 const void* K, const void* V, const void* Kg,
+                                 const void* Vg, void* O, int32_t* tok_idx,
+                                 int32_t* seg_idx, void* workspace,
+                                 size_t workspace_bytes, void* stream,
+                                 void** events, int32_t n_events) {
+  if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
+  for (int i = 0; i < n_events && i <= kFusedKernels; ++i)
+    if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
+  return fused_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
+                    workspace_bytes, stream, events, n_events);
+}
+
+int32_t wf_filter_attend_kernels(const wf_params* p) {
+  if (check_params(p) != WF_OK) return -1;
+  return kFusedKernels;
+}
+
+const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i) {
+  if (check_params(p) != WF_OK || i < 0 || i >= kFusedKernels) return nullptr;
+  return kFusedNames[i];
+}
+
+const char* wf_status_str(wf_status s) {
+  switch (s) {
+    case WF_OK: return "WF_OK";
+    case WF_ERR_INVALID_ARG: return "WF_ERR_INVALID_ARG";
+    case WF_ERR_UNSUPPORTED: return "WF_ERR_UNSUPPORTED";
+    case WF_ERR_WORKSPACE: return "WF_ERR_WORKSPACE";
+    case WF_ERR_HIP: return "WF_ERR_HIP";
+  }
+  return "WF_ERR_UNKNOWN";
+}
+
+const char* wf_last_error(void) { return g_last_error; }
+
+}  // extern "C"

@@ -1,0 +1,431 @@
+// Sparse cache and attention over it (Section 3.2, last paragraph; the
+// cached-attention form of eq. 3, bidirectional: no mask).
+//
+// The cache rows of a unit are split into chunks of kAttnChunk rows, one
+// workgroup each (split-KV); each workgroup writes its unnormalised partial
+// output with the per-row max and sum of exp, and a combine kernel merges the
+// splits.  In the fused path the rows are read in place: row r < k_eff is
+// K[tok[r]] / V[tok[r]], the rest are the tail rows K_g / V_g.
+//
+// bf16: S^T = K Q^T runs on v_mfma_f32_16x16x32_bf16 over 32-row sub-blocks.
+// The two 16-row MFMA tiles of a sub-block take rows 8(m/4) + m%4 and
+// 8(m/4) + 4 + m%4, so that lane group g ends up holding the scores of rows
+// 8g .. 8g+7 for query l%16 -- exactly the A operand of O = P V for the same
+// instruction.  V sits transposed in LDS so that its B operand is one 16-byte
+// read.  Online softmax (running max / sum per query row) spans the
+// sub-blocks.  fp32 uses v_mfma_f32_16x16x4_f32 on 16-row sub-blocks.
+#include "wf_device.hpp"
+#include "wf_kernels.hpp"
+#include "wf_launch.hpp"
+
+namespace wf {
+
+template <typename T>
+struct AttnPad {
+  static constexpr int value = 16 / sizeof(T);
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(kBlock) void attn_kernel(AttnArgs a) {
+  constexpr int NW = kBlock / kWave;
+  constexpr int KSTR = D + AttnPad<T>::value;
+  constexpr bool BF = sizeof(T) == 2;
+  // bf16: V transposed [D][chunk + 8]; fp32: V row-major [chunk][D + 4]
+  constexpr int VSTR = BF ? kAttnChunk + 8 : D + 4;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* Ks = reinterpret_cast<T*>(smem);
+  T* Vl = Ks + kAttnChunk * KSTR;
+
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / a.NS, sp = item % a.NS;
+  const long r0 = (long)sp * kAttnChunk;
+  const int nr = (int)min((long)kAttnChunk, (long)a.nrows - r0);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, col = lane & 15;
+
+  const T* Kb = reinterpret_cast<const T*>(a.K);
+  const T* Vb = reinterpret_cast<const T*>(a.V);
+  const T* Kt = reinterpret_cast<const T*>(a.Kg);
+  const T* Vt = reinterpret_cast<const T*>(a.Vg);
+  auto row_of = [&](const T* base, const T* tail, int r) -> const T* {
+    if (r >= nr) return nullptr;
+    const long rr = r0 + r;
+    if (a.tok) {
+      if (rr < a.nsel)
+        return base + ((long)u * a.L + a.tok[(long)u * a.nsel + rr]) * D;
+      return tail + ((long)u * a.G + (rr - a.nsel)) * D;
+    }
+    return base + ((long)u * a.nrows + rr) * D;
+  };
+
+  constexpr int EPV = 16 / sizeof(T);  // elements per 16-byte vector
+  constexpr int VPR = D / EPV;
+  for (int v = threadIdx.x; v < kAttnChunk * VPR; v += kBlock) {
+    const int r = v / VPR, k = v % VPR;
+    const T* ks = row_of(Kb, Kt, r);
+    const T* vs = row_of(Vb, Vt, r);
+    u32x4 kv = ks ? *reinterpret_cast<const u32x4*>(ks + k * EPV)
+                  : u32x4{0u, 0u, 0u, 0u};
+    u32x4 vv = vs ? *reinterpret_cast<const u32x4*>(vs + k * EPV)
+                  : u32x4{0u, 0u, 0u, 0u};
+    *reinterpret_cast<u32x4*>(Ks + r * KSTR + k * EPV) = kv;
+    if constexpr (BF) {
+      uint16_t* vt = reinterpret_cast<uint16_t*>(Vl);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt[(k * EPV + 2 * e) * VSTR + r] = (uint16_t)(vv[e] & 0xffffu);
+        vt[(k * EPV + 2 * e + 1) * VSTR + r] = (uint16_t)(vv[e] >> 16);
+      }
+    } else {
+      *reinterpret_cast<u32x4*>(Vl + r * VSTR + k * EPV) = vv;
+    }
+  }
+  __syncthreads();
+
+  const int nqb = (a.B + 15) / 16;
+  const int tsplit = nqb == 1 ? 4 : (nqb == 2 ? 2 : 1);
+  const int part = wave % tsplit;
+  const int qstep = NW / tsplit;
+  const int R = kAttnChunk / tsplit;
+  const int rb = part * R;
+  const int re = min(rb + R, nr);
+  const T* Qunit = reinterpret_cast<const T*>(a.Q) + (long)u * a.B * D;
+
+  f32x4 O[D / 16];
+  float m_run = -INFINITY, l_run = 0.f;
+  int qb = wave / tsplit;
+  for (; qb < nqb; qb += qstep) {
+#pragma unroll
+    for (int cb = 0; cb < D / 16; ++cb) O[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run = -INFINITY;
+    l_run = 0.f;
+    const T* qrow = Qunit + (long)min(qb * 16 + col, a.B - 1) * D;
+    if constexpr (BF) {
+      u32x4 qreg[D / 32];
+#pragma unroll
+      for (int s = 0; s < D / 32; ++s)
+        qreg[s] = *reinterpret_cast<const u32x4*>(qrow + 32 * s + 8 * g);
+      for (int sb = rb; sb < re; sb += 32) {
+        const int rx = sb + 8 * (col >> 2) + (col & 3);
+        f32x4 ax = {0.f, 0.f, 0.f, 0.f}, ay = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s) {
+          u32x4 kx = *reinterpret_cast<const u32x4*>(Ks + rx * KSTR + 32 * s + 8 * g);
+          u32x4 ky = *reinterpret_cast<const u32x4*>(Ks + (rx + 4) * KSTR + 32 * s + 8 * g);
+          ax = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, kx), __builtin_bit_cast(bf16x8, qreg[s]),
+              ax, 0, 0, 0);
+          ay = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, ky), __builtin_bit_cast(bf16x8, qreg[s]),
+              ay, 0, 0, 0);
+        }
+        // lane holds scores of rows sb + 8g + e (e < 8) for query col
+        float sv[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          sv[i] = (sb + 8 * g + i < re) ? ax[i] * a.scale : -INFINITY;
+          sv[4 + i] = (sb + 8 * g + 4 + i < re) ? ay[i] * a.scale : -INFINITY;
+        }
+        float mb = sv[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
+        mb = fmaxf(mb, __shfl_xor(mb, 16));
+        mb = fmaxf(mb, __shfl_xor(mb, 32));
+        const float m_new = fmaxf(m_run, mb);
+        const float alpha = __expf(m_run - m_new);
+        float pv[8], ps = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pv[e] = sv[e] > -INFINITY ? __expf(sv[e] - m_new) : 0.f;
+          ps += pv[e];
+        }
+        ps += __shfl_xor(ps, 16);
+        ps += __shfl_xor(ps, 32);
+        l_run = l_run * alpha + ps;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float ai = __shfl(alpha, 4 * g + i);
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
+        }
+        u32x4 pp = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                    pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
+        const uint16_t* vt = reinterpret_cast<const uint16_t*>(Vl);
+#pragma unroll
+        for (int cb = 0; cb < D / 16; ++cb) {
+          u32x4 vb = *reinterpret_cast<const u32x4*>(vt + (cb * 16 + col) * VSTR + sb + 8 * g);
+          O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, pp), __builtin_bit_cast(bf16x8, vb),
+              O[cb], 0, 0, 0);
+        }
+        m_run = m_new;
+      }
+    } else {
+      for (int sb = rb; sb < re; sb += 16) {
+        f32x4 acc = tile_dot_f32<D>(reinterpret_cast<const float*>(Ks) + (sb + col) * KSTR,
+                                    reinterpret_cast<const float*>(qrow),
+                                    f32x4{0.f, 0.f, 0.f, 0.f});
+        // lane holds scores of rows sb + 4g + i for query col
+        float sv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          sv[i] = (sb + 4 * g + i < re) ? acc[i] * a.scale : -INFINITY;
+        float mb = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+        mb = fmaxf(mb, __shfl_xor(mb, 16));
+        mb = fmaxf(mb, __shfl_xor(mb, 32));
+        const float m_new = fmaxf(m_run, mb);
+        const float alpha = __expf(m_run - m_new);
+        float pv[4], ps = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pv[i] = sv[i] > -INFINITY ? __expf(sv[i] - m_new) : 0.f;
+          ps += pv[i];
+        }
+        ps += __shfl_xor(ps, 16);
+        ps += __shfl_xor(ps, 32);
+        l_run = l_run * alpha + ps;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float ai = __shfl(alpha, 4 * g + i);
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
+        }
+        const float* vl = reinterpret_cast<const float*>(Vl);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) {
+            const float vb = vl[(sb + 4 * g + i) * VSTR + cb * 16 + col];
+            O[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i], vb, O[cb], 0, 0, 0);
+          }
+        }
+        m_run = m_new;
+      }
+    }
+    if (tsplit == 1) {
+      float* po = a.part + ((long)u * a.NS + sp) * a.B * D;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = qb * 16 + 4 * g + i;
+        if (q < a.B) {
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) po[(long)q * D + cb * 16 + col] = O[cb][i];
+        }
+      }
+      const int q = qb * 16 + col;
+      if (g == 0 && q < a.B) {
+        float* ps = a.pstat + ((long)u * a.NS + sp) * 2 * a.B;
+        ps[q] = m_run;
+        ps[a.B + q] = l_run;
+      }
+    }
+  }
+
+  if (tsplit > 1) {
+    // each wave ran exactly one query block; merge the row parts in LDS
+    qb = wave / tsplit;
+    __syncthreads();
+    float* cO = reinterpret_cast<float*>(smem);  // [NW][16][D]
+    float* cm = cO + NW * 16 * D;                 // [NW][16]
+    float* cl = cm + NW * 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int cb = 0; cb < D / 16; ++cb)
+        cO[(wave * 16 + 4 * g + i) * D + cb * 16 + col] = O[cb][i];
+    }
+    if (g == 0) {
+      cm[wave * 16 + col] = m_run;
+      cl[wave * 16 + col] = l_run;
+    }
+    __syncthreads();
+    if (part == 0) {
+      float* po = a.part + ((long)u * a.NS + sp) * a.B * D;
+      float* ps = a.pstat + ((long)u * a.NS + sp) * 2 * a.B;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rr = 4 * g + i;
+        const int q = qb * 16 + rr;
+        float M = -INFINITY;
+        for (int pp = 0; pp < tsplit; ++pp) M = fmaxf(M, cm[(wave + pp) * 16 + rr]);
+        float lsum = 0.f;
+        float wgt[4];
+        for (int pp = 0; pp < 4; ++pp) {
+          const float mp = pp < tsplit ? cm[(wave + pp) * 16 + rr] : -INFINITY;
+          wgt[pp] = mp > -INFINITY ? __expf(mp - M) : 0.f;
+          if (pp < tsplit) lsum += wgt[pp] * cl[(wave + pp) * 16 + rr];
+        }
+        if (q < a.B) {
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) {
+            float o = 0.f;
+            for (int pp = 0; pp < tsplit; ++pp)
+              o += wgt[pp] * cO[((wave + pp) * 16 + rr) * D + cb * 16 + col];
+            po[(long)q * D + cb * 16 + col] = o;
+          }
+          if (col == 0) {
+            ps[q] = M;
+            ps[a.B + q] = lsum;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, int D) {
+  const int u = blockIdx.x / a.B, q = blockIdx.x % a.B;
+  const float* ps = a.pstat + (long)u * a.NS * 2 * a.B;
+  float M = -INFINITY;
+  for (int s = 0; s < a.NS; ++s) M = fmaxf(M, ps[(long)s * 2 * a.B + q]);
+  float lsum = 0.f;
+  for (int s = 0; s < a.NS; ++s)
+    lsum += ps[(long)s * 2 * a.B + a.B + q] * __expf(ps[(long)s * 2 * a.B + q] - M);
+  const float inv = 1.f / lsum;
+  T* O = reinterpret_cast<T*>(a.O) + ((long)u * a.B + q) * D;
+  for (int ch = threadIdx.x; ch < D; ch += blockDim.x) {
+    float o = 0.f;
+    for (int s = 0; s < a.NS; ++s)
+      o += a.part[(((long)u * a.NS + s) * a.B + q) * D + ch] *
+           __expf(ps[(long)s * 2 * a.B + q] - M);
+    store_elem<T>(O, ch, o * inv);
+  }
+}
+
+// Sparse cache rows: [K[tok]; Kg] and [V[tok]; Vg], 16 bytes per thread.
+__global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a) {
+  const int vpr = a.D * a.elem / 16;
+  const long rows = (long)a.keff + a.G;
+  const long total = (long)a.U * rows * vpr;
+  for (long v = (long)blockIdx.x * kBlock + threadIdx.x; v < total;
+       v += (long)gridDim.x * kBlock) {
+    const long ur = v / vpr;
+    const int k = (int)(v % vpr);
+    const int u = (int)(ur / rows);
+    const long r = ur % rows;
+    const unsigned char* ks;
+    const unsigned char* vs;
+    const long row_bytes = (long)a.D * a.elem;
+    if (r < a.keff) {
+      const long t = a.tok[(long)u * a.keff + r];
+      ks = (const unsigned char*)a.K + ((long)u * a.L + t) * row_bytes;
+      vs = (const unsigned char*)a.V + ((long)u * a.L + t) * row_bytes;
+    } else {
+      ks = (const unsigned char*)a.Kg + ((long)u * a.G + (r - a.keff)) * row_bytes;
+      vs = (const unsigned char*)a.Vg + ((long)u * a.G + (r - a.keff)) * row_bytes;
+    }
+    const long dst = ur * row_bytes + (long)k * 16;
+    *reinterpret_cast<u32x4*>((unsigned char*)a.Ks + dst) =
+        *reinterpret_cast<const u32x4*>(ks + k * 16);
+    *reinterpret_cast<u32x4*>((unsigned char*)a.Vs + dst) =
+        *reinterpret_cast<const u32x4*>(vs + k * 16);
+  }
+}
+
+// ------------------------------------------------------------ host side
+
+AttnPlan plan_attn(const wf_params& p, long nrows) {
+  AttnPlan a;
+  a.splits = (int)((nrows + kAttnChunk - 1) / kAttnChunk);
+  const int D = p.head_dim;
+  size_t stage;
+  if (p.dtype == WF_BF16)
+    stage = (size_t)kAttnChunk * (D + 8) * 2 + (size_t)D * (kAttnChunk + 8) * 2;
+  else
+    stage = (size_t)kAttnChunk * (D + 4) * 4 * 2;
+  const size_t comb = (size_t)4 * 16 * D * 4 + (size_t)2 * 4 * 16 * 4;
+  a.lds_bytes = std::max(stage, comb);
+  return a;
+}
+
+template <typename T, int D>
+static hipError_t attn_launch(const AttnArgs& a, size_t lds, hipStream_t s) {
+  auto kern = attn_kernel<T, D>;
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)(a.U * a.NS)), dim3(kBlock), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
+                       const void* V, const int32_t* tok, int nsel,
+                       const void* Kg, const void* Vg, int G, long nrows,
+                       float* part, float* pstat, hipStream_t s) {
+  const AttnPlan pl = plan_attn(p, nrows);
+  AttnArgs a;
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.tok = tok;
+  a.Kg = Kg;
+  a.Vg = Vg;
+  a.part = part;
+  a.pstat = pstat;
+  a.O = nullptr;
+  a.U = p.batch * p.heads;
+  a.L = p.ctx_len;
+  a.B = p.q_len;
+  a.nsel = nsel;
+  a.G = G;
+  a.nrows = (int)nrows;
+  a.NS = pl.splits;
+  a.scale = effective_scale(p);
+  const bool d128 = p.head_dim == 128;
+  if (p.dtype == WF_BF16)
+    return d128 ? attn_launch<bf16_t, 128>(a, pl.lds_bytes, s)
+                : attn_launch<bf16_t, 64>(a, pl.lds_bytes, s);
+  return d128 ? attn_launch<float, 128>(a, pl.lds_bytes, s)
+              : attn_launch<float, 64>(a, pl.lds_bytes, s);
+}
+
+hipError_t launch_attn_combine(const wf_params& p, long nrows,
+                               const float* part, const float* pstat, void* O,
+                               hipStream_t s) {
+  AttnArgs a{};
+  a.part = const_cast<float*>(part);
+  a.pstat = const_cast<float*>(pstat);
+  a.O = O;
+  a.U = p.batch * p.heads;
+  a.B = p.q_len;
+  a.NS = plan_attn(p, nrows).splits;
+  const dim3 grid((unsigned)(a.U * a.B));
+  if (p.dtype == WF_BF16)
+    hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, grid, dim3(128), 0, s, a,
+                       p.head_dim);
+  else
+    hipLaunchKernelGGL(attn_combine_kernel<float>, grid, dim3(128), 0, s, a,
+                       p.head_dim);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const wf_params& p, const void* K, const void* V,
+                         const int32_t* tok, const void* Kg, const void* Vg,
+                         void* Ks, void* Vs, hipStream_t s) {
+  GatherArgs a;
+  a.K = K;
+  a.V = V;
+  a.tok = tok;
+  a.Kg = Kg;
+  a.Vg = Vg;
+  a.Ks = Ks;
+  a.Vs = Vs;
+  a.U = p.batch * p.heads;
+  a.L = p.ctx_len;
+  a.D = p.head_dim;
+  a.keff = wf_effective_budget(&p);
+  a.G = p.gen_len;
+  a.elem = p.dtype == WF_BF16 ? 2 : 4;
+  const long total = (long)a.U * (a.keff + a.G) * (a.D * a.elem / 16);
+  const long blocks = std::min((total + kBlock - 1) / kBlock,
+                               (long)device_cu_count() * 16);
+  hipLaunchKernelGGL(gather_kernel, dim3((unsigned)std::max(1L, blocks)),
+                     dim3(kBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace wf

@@ -1,0 +1,272 @@
+// Device building blocks shared by the WaveFilter gfx950 kernels: element
+// conversions, 16x16 MFMA tile products, a block-wide scan and a
+// deterministic top-k selection.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wf {
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+struct bf16_t {
+  uint16_t bits;
+};
+
+// ------------------------------------------------------------ conversions
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) {
+  return __uint_as_float(w << 16);
+}
+__device__ __forceinline__ float bf16_hi(uint32_t w) {
+  return __uint_as_float(w & 0xffff0000u);
+}
+
+// Round-to-nearest-even float -> bf16 bits (NaN stays NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* p, long i);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, long i) {
+  return p[i];
+}
+template <>
+__device__ __forceinline__ float load_elem<bf16_t>(const bf16_t* p, long i) {
+  return __uint_as_float((uint32_t)p[i].bits << 16);
+}
+
+template <typename T>
+__device__ __forceinline__ void store_elem(T* p, long i, float v);
+template <>
+__device__ __forceinline__ void store_elem<float>(float* p, long i, float v) {
+  p[i] = v;
+}
+template <>
+__device__ __forceinline__ void store_elem<bf16_t>(bf16_t* p, long i, float v) {
+  p[i].bits = (uint16_t)f32_to_bf16_bits(v);
+}
+
+// ------------------------------------------------------------ MFMA tiles
+//
+// A 16x16 output tile C[m][n] = sum_c Arow_m[c] * Brow_n[c], where lane l
+// supplies row m = l % 16 of A and row n = l % 16 of B (both stored with
+// channels contiguous).  On return lane l holds C[4 (l / 16) + i][l % 16] in
+// element i.
+//
+// bf16 rows use v_mfma_f32_16x16x32_bf16: lane group g = l / 16 feeds
+// channels 8g .. 8g+7 of every 32-channel step.  fp32 rows use
+// v_mfma_f32_16x16x4_f32 with the channel order permuted so that lane group g
+// walks the contiguous channel range [g D/4, (g+1) D/4): the reduction runs
+// over every channel exactly once either way.
+
+template <int D>
+__device__ __forceinline__ f32x4 tile_dot_bf16(const bf16_t* a_row,
+                                               const bf16_t* b_row,
+                                               f32x4 acc) {
+  const int g = (threadIdx.x & 63) >> 4;
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) {
+    u32x4 a = *reinterpret_cast<const u32x4*>(a_row + 32 * s + 8 * g);
+    u32x4 b = *reinterpret_cast<const u32x4*>(b_row + 32 * s + 8 * g);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+        __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0,
+        0, 0);
+  }
+  return acc;
+}
+
+template <int D>
+__device__ __forceinline__ f32x4 tile_dot_f32(const float* a_row,
+                                              const float* b_row, f32x4 acc) {
+  const int g = (threadIdx.x & 63) >> 4;
+  const float* a = a_row + g * (D / 4);
+  const float* b = b_row + g * (D / 4);
+#pragma unroll
+  for (int s4 = 0; s4 < D / 16; ++s4) {
+    f32x4 av = *reinterpret_cast<const f32x4*>(a + 4 * s4);
+    f32x4 bv = *reinterpret_cast<const f32x4*>(b + 4 * s4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], bv[e], acc, 0, 0, 0);
+  }
+  return acc;
+}
+
+template <typename T, int D>
+__device__ __forceinline__ f32x4 tile_dot(const T* a_row, const T* b_row,
+                                          f32x4 acc);
+template <>
+__device__ __forceinline__ f32x4 tile_dot<bf16_t, 64>(const bf16_t* a,
+                                                      const bf16_t* b,
+                                                      f32x4 c) {
+  return tile_dot_bf16<64>(a, b, c);
+}
+template <>
+__device__ __forceinline__ f32x4 tile_dot<bf16_t, 128>(const bf16_t* a,
+                                                       const bf16_t* b,
+                                                       f32x4 c) {
+  return tile_dot_bf16<128>(a, b, c);
+}
+template <>
+__device__ __forceinline__ f32x4 tile_dot<float, 64>(const float* a,
+                                                     const float* b, f32x4 c) {
+  return tile_dot_f32<64>(a, b, c);
+}
+template <>
+__device__ __forceinline__ f32x4 tile_dot<float, 128>(const float* a,
+                                                      const float* b,
+                                                      f32x4 c) {
+  return tile_dot_f32<128>(a, b, c);
+}
+
+// ------------------------------------------------------------ reductions
+
+__device__ __forceinline__ float wave_max16(float v) {
+  // max over the 16 lanes that share l / 16
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Block-wide exclusive prefix sum of one value per thread; `total` receives
+// the block sum.  `wsum` is LDS scratch of NT / 64 words.  Every thread of the
+// block must call it.
+template <int NT>
+__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum,
+                                         uint32_t& total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[wid] = x;
+  __syncthreads();
+  uint32_t base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    uint32_t s = wsum[w];
+    base += (w < wid) ? s : 0u;
+    tot += s;
+  }
+  __syncthreads();
+  total = tot;
+  return base + x - v;
+}
+
+// Order-preserving map of a float to uint32 (larger float -> larger key).
+__device__ __forceinline__ uint32_t order_key(float x) {
+  uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+template <int NT>
+struct SelectShared {
+  uint32_t hist[256];
+  uint32_t wsum[NT / 64];
+  uint32_t digit;
+  uint32_t above;
+};
+
+// Picks the k largest of score[0..n) (ties: lower index first) and writes
+// map(i) for the picked positions i in ascending order of i to out[0..k).
+// Requires 1 <= k <= n and NT >= 256.  score may live in LDS or global
+// memory; it must be visible to the whole block.  Radix select on the
+// order-preserving keys (four 8-bit digits) finds the k-th key; a block scan
+// over the positions in index order then emits every larger key and the
+// lowest-indexed copies of the k-th key.
+template <int NT, typename Map>
+__device__ void block_select_topk(const float* score, int n, int k,
+                                  int32_t* out, Map map,
+                                  SelectShared<NT>& sh) {
+  static_assert(NT >= 256 && NT % 64 == 0, "block too small for the select");
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0, mask = 0;
+  uint32_t need = (uint32_t)k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 256; i += NT) sh.hist[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += NT) {
+      uint32_t key = order_key(score[i]);
+      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    // thread t < 256 looks at digit 255 - t: descending digit order
+    uint32_t c = (tid < 256) ? sh.hist[255 - tid] : 0u;
+    uint32_t total;
+    uint32_t before = block_exclusive_scan<NT>(c, sh.wsum, total);
+    if (tid < 256 && before < need && before + c >= need) {
+      sh.digit = 255u - (uint32_t)tid;
+      sh.above = before;
+    }
+    __syncthreads();
+    prefix |= sh.digit << shift;
+    mask |= 255u << shift;
+    need -= sh.above;
+    __syncthreads();
+  }
+  // prefix is now the k-th largest key; `need` copies of it are taken.
+  constexpr int ITEMS = 16;
+  uint32_t taken_base = 0, eq_base = 0;
+  for (int base = 0; base < n; base += NT * ITEMS) {
+    const int start = base + tid * ITEMS;
+    uint32_t gt_bits = 0, eq_bits = 0;
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j) {
+      int i = start + j;
+      if (i < n) {
+        uint32_t key = order_key(score[i]);
+        gt_bits |= (key > prefix ? 1u : 0u) << j;
+        eq_bits |= (key == prefix ? 1u : 0u) << j;
+      }
+    }
+    uint32_t eq_cnt = __popc(eq_bits), eq_tot;
+    uint32_t eq_before = eq_base + block_exclusive_scan<NT>(eq_cnt, sh.wsum, eq_tot);
+    uint32_t take_eq = 0;
+    if (need > eq_before) take_eq = min(need - eq_before, eq_cnt);
+    uint32_t take_cnt = __popc(gt_bits) + take_eq, take_tot;
+    uint32_t pos = taken_base + block_exclusive_scan<NT>(take_cnt, sh.wsum, take_tot);
+    uint32_t eq_seen = 0;
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j) {
+      int i = start + j;
+      bool gt = (gt_bits >> j) & 1u;
+      bool eq = (eq_bits >> j) & 1u;
+      if (gt || (eq && eq_seen < take_eq)) {
+        if (pos < (uint32_t)k) out[pos] = map(i);
+        ++pos;
+      }
+      eq_seen += eq ? 1u : 0u;
+    }
+    taken_base += take_tot;
+    eq_base += eq_tot;
+  }
+}
+
+// ------------------------------------------------------------ launch shape
+
+// Maps the hardware workgroup id to a logical id so that consecutive logical
+// ids run on the same XCD (workgroups are dealt round-robin over the 8 XCDs).
+__device__ __forceinline__ int xcd_swizzle(int bid, int nblocks) {
+  if ((nblocks & 7) != 0) return bid;
+  return (bid & 7) * (nblocks >> 3) + (bid >> 3);
+}
+
+}  // namespace wf

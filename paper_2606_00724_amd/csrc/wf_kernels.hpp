@@ -1,0 +1,92 @@
+// Kernel argument blocks and launch helpers shared by the WaveFilter
+// kernels (device side) and the C-ABI (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wf {
+
+constexpr int kBlock = 256;        // threads per workgroup, all kernels
+constexpr int kMaxCoefTile = 64;   // coarse coefficients per skim tile
+constexpr int kScanChunk = 128;    // pool tokens per scan workgroup
+constexpr int kAttnChunk = 128;    // cache rows per attention workgroup
+constexpr int kCoefPad = 4;        // fp32 pad per LDS coefficient row
+
+enum CoefSource { kHaarSum = 0, kCascade = 1, kFromApprox = 2 };
+
+struct DwtArgs {
+  const void* K;       // [U][L][D]
+  float* approx;       // [U][nJ][D]
+  float* details;      // nullable, [U][L - nJ][D]
+  int U, L, D, J, nJ;
+  int cps;             // coefficients per stream
+  int streams;         // streams per workgroup tile
+  int ntiles;          // tiles per unit
+  int boundary;        // 0 symmetric, 1 periodic
+};
+
+struct SkimTileArgs {
+  const void* K;        // [U][L][D]      (Haar sum / cascade)
+  const float* approx;  // [U][nJ][D]     (from approx)
+  const void* Q;        // [U][B][D]
+  float* logits;        // [U][B][nJ]
+  float* stats;         // [U][ntiles][2][B]: row max, then row sum of exp
+  int U, L, B, J, nJ;
+  int cpt;              // coefficients per tile
+  int ntiles;           // tiles per unit
+  int boundary;
+  float scale;
+};
+
+struct SkimSelectArgs {
+  const float* logits;  // [U][B][nJ]
+  const float* stats;   // [U][ntiles][2][B]
+  float* W;             // [U][nJ] out
+  int32_t* seg;         // [U][S] out
+  int U, B, nJ, ntiles, S;
+};
+
+struct ScanArgs {
+  const void* Q;        // [U][B][D]
+  const void* K;        // [U][L][D]
+  const int32_t* seg;   // [U][S]
+  float* stats;         // [U][C][2][B]
+  float* wpool;         // [U][P]  (weights mode)
+  int U, L, B, J, S, P, C;
+  float scale;
+};
+
+struct ScanSelectArgs {
+  const float* wpool;   // [U][P]
+  const int32_t* seg;   // [U][S]
+  int32_t* tok;         // [U][keff]
+  int U, J, S, P, keff;
+};
+
+struct GatherArgs {
+  const void* K;        // [U][L][D]
+  const void* V;
+  const int32_t* tok;   // [U][keff]
+  const void* Kg;       // [U][G][D]
+  const void* Vg;
+  void* Ks;             // [U][keff + G][D]
+  void* Vs;
+  int U, L, D, keff, G, elem;
+};
+
+struct AttnArgs {
+  const void* Q;        // [U][B][D]
+  const void* K;        // rows: [U][L][D] indexed by tok, or [U][nrows][D]
+  const void* V;
+  const int32_t* tok;   // nullable: rows are contiguous when null
+  const void* Kg;       // [U][G][D] tail (indexed mode only)
+  const void* Vg;
+  float* part;          // [U][NS][B][D] unnormalised partial outputs
+  float* pstat;         // [U][NS][2][B] partial row max, row sum
+  void* O;              // [U][B][D]
+  int U, L, B, nsel, G, nrows, NS;
+  float scale;
+};
+
+}  // namespace wf

@@ -1,0 +1,74 @@
+// Host-side plans and launchers of the WaveFilter kernels (used by the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "wavefilter.h"
+
+namespace wf {
+
+// Scores up to this many floats are staged in LDS by the select kernels.
+constexpr int kSelectLdsFloats = 16384;
+
+struct DwtPlan {
+  int streams;  // streams per workgroup
+  int cps;      // coefficients per stream
+  int ntiles;   // workgroups per unit
+};
+
+struct SkimPlan {
+  int source;        // CoefSource
+  int cpt;           // coefficients per tile
+  int ntiles;        // tiles per unit
+  size_t lds_bytes;  // dynamic LDS of the tile kernel
+};
+
+struct ScanPlan {
+  int chunks;        // pool chunks per unit
+  size_t lds_bytes;  // dynamic LDS of the chunk kernels
+};
+
+struct AttnPlan {
+  int splits;        // cache-row chunks per unit
+  size_t lds_bytes;
+};
+
+float effective_scale(const wf_params& p);
+int device_cu_count();
+
+DwtPlan plan_dwt(const wf_params& p);
+SkimPlan plan_skim(const wf_params& p, bool fused);
+ScanPlan plan_scan(const wf_params& p);
+AttnPlan plan_attn(const wf_params& p, long nrows);
+
+hipError_t launch_dwt(const wf_params& p, const void* K, float* approx,
+                      float* details, hipStream_t s);
+hipError_t launch_skim_tiles(const wf_params& p, bool fused, const void* Q,
+                             const void* K, const float* approx, float* logits,
+                             float* stats, hipStream_t s);
+hipError_t launch_skim_select(const wf_params& p, int ntiles,
+                              const float* logits, const float* stats,
+                              float* W, int32_t* seg, hipStream_t s);
+hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
+                              const void* K, const int32_t* seg, float* stats,
+                              float* wpool, hipStream_t s);
+hipError_t launch_scan_select(const wf_params& p, const float* wpool,
+                              const int32_t* seg, int32_t* tok,
+                              hipStream_t s);
+hipError_t launch_gather(const wf_params& p, const void* K, const void* V,
+                         const int32_t* tok, const void* Kg, const void* Vg,
+                         void* Ks, void* Vs, hipStream_t s);
+hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
+                       const void* V, const int32_t* tok, int nsel,
+                       const void* Kg, const void* Vg, int G, long nrows,
+                       float* part, float* pstat, hipStream_t s);
+hipError_t launch_attn_combine(const wf_params& p, long nrows,
+                               const float* part, const float* pstat, void* O,
+                               hipStream_t s);
+
+}  // namespace wf

@@ -1,0 +1,671 @@
+// DWT of the cached prompt keys (eqs. 5-6) and the skim: perception weights
+// of the query block over the level-J approximation (eq. 7), their column
+// sums W (eq. 8) and the top-S coarse regions (eq. 9).
+//
+// Layout: one unit = one (batch, head) pair; K is [U][L][D] with channels
+// contiguous.  The DWT runs along the sequence independently per channel.
+//
+//  * Haar in the fused path: the level-J approximation of block j is
+//    2^{-J/2} times the sum of its 2^J rows (the orthonormal pyramid
+//    collapses to a block sum), so a wave streams rows with 16-byte loads,
+//    accumulates in fp32 registers and finishes the block with cross-lane
+//    butterflies.
+//  * Daubechies-2 (and the staged transform that also returns details):
+//    every lane owns two channels and runs the filter-bank cascade along the
+//    sequence, level by level, with three samples of state per level; the
+//    half-sample symmetric extension is applied per level at the true end.
+//  * The skim epilogue multiplies the fp32 coefficient tile (in LDS) with
+//    the query block on fp32 MFMA (v_mfma_f32_16x16x4_f32), then writes the
+//    logits and per-tile row max / row sum of exponentials.  A per-unit
+//    kernel merges the tiles' row statistics, forms W and selects.
+#include "wf_device.hpp"
+#include "wf_kernels.hpp"
+#include "wf_launch.hpp"
+
+namespace wf {
+
+struct Taps {
+  float g[4];
+  float h[4];
+  float inv_norm;  // 2^{-J/2}, for the Haar block sum
+};
+
+struct F2 {
+  float x, y;
+};
+
+__device__ __forceinline__ F2 load_pair(const bf16_t* p) {
+  uint32_t w = *reinterpret_cast<const uint32_t*>(p);
+  return F2{bf16_lo(w), bf16_hi(w)};
+}
+__device__ __forceinline__ F2 load_pair(const float* p) {
+  u32x2 w = *reinterpret_cast<const u32x2*>(p);
+  return F2{__uint_as_float(w[0]), __uint_as_float(w[1])};
+}
+
+// ------------------------------------------------------------ cascade
+
+// Filter-bank cascade over one stream of rows for one channel pair.  Level j
+// (1..J) consumes samples y^{j-1}[i] in increasing i and, after every odd i,
+// emits y^j[n] = sum_m g_m y^{j-1}[2n+m] (and the detail with h), with
+// n = (i - (M-1)) / 2.  Samples pushed before the stream's first aligned
+// coefficient produce emissions with smaller indices, which sinks ignore.
+template <int M, int J, bool DET>
+struct Cascade {
+  F2 s1[J + 1], s2[J + 1], s3[J + 1];  // y[i-1], y[i-2], y[i-3] per level
+  float g0, g1, g2, g3, h0, h1, h2, h3;
+  long L;
+  bool symmetric;
+
+  __device__ void init(const Taps& t, long L_, bool sym) {
+    g0 = t.g[0]; g1 = t.g[1]; g2 = t.g[2]; g3 = t.g[3];
+    h0 = t.h[0]; h1 = t.h[1]; h2 = t.h[2]; h3 = t.h[3];
+    L = L_;
+    symmetric = sym;
+#pragma unroll
+    for (int j = 0; j <= J; ++j) {
+      s1[j] = F2{0.f, 0.f};
+      s2[j] = F2{0.f, 0.f};
+      s3[j] = F2{0.f, 0.f};
+    }
+  }
+
+  template <int j, class Sink>
+  __device__ __forceinline__ void feed(long i, F2 v, Sink& sink) {
+    if (i & 1) {
+      long n;
+      F2 a, d;
+      if constexpr (M == 2) {
+        n = (i - 1) >> 1;
+        a.x = g0 * s1[j].x + g1 * v.x;
+        a.y = g0 * s1[j].y + g1 * v.y;
+        if constexpr (DET) {
+          d.x = h0 * s1[j].x + h1 * v.x;
+          d.y = h0 * s1[j].y + h1 * v.y;
+        }
+      } else {
+        n = (i - 3) >> 1;
+        a.x = g0 * s3[j].x + g1 * s2[j].x + g2 * s1[j].x + g3 * v.x;
+        a.y = g0 * s3[j].y + g1 * s2[j].y + g2 * s1[j].y + g3 * v.y;
+        if constexpr (DET) {
+          d.x = h0 * s3[j].x + h1 * s2[j].x + h2 * s1[j].x + h3 * v.x;
+          d.y = h0 * s3[j].y + h1 * s2[j].y + h2 * s1[j].y + h3 * v.y;
+        }
+      }
+      if constexpr (DET) sink.detail(j, n, d);
+      if constexpr (j < J) {
+        push<j + 1>(n, a, sink);
+      } else {
+        sink.approx(n, a);
+      }
+    }
+    s3[j] = s2[j];
+    s2[j] = s1[j];
+    s1[j] = v;
+  }
+
+  // Pushes y^{j-1}[i].  After the last sample of a level (i = N - 1) the
+  // symmetric mode continues with y[N] = y[N-1] and y[N+1] = y[N-2]
+  // (half-sample symmetric extension); a loop keeps one copy of the deeper
+  // levels' code.
+  template <int j, class Sink>
+  __device__ __forceinline__ void push(long i, F2 v, Sink& sink) {
+    int reps = 1;
+    const F2 prev = s1[j];
+    if constexpr (M == 4) {
+      if (symmetric && i == (L >> (j - 1)) - 1) reps = 3;
+    }
+#pragma unroll 1
+    for (int r = 0; r < reps; ++r) {
+      const F2 x = (r == 2) ? prev : v;
+      feed<j>(i + r, x, sink);
+    }
+  }
+};
+
+// Rows a stream reads past its own 2^J-aligned range: level-J coefficient n
+// of a 4-tap bank depends on rows 2^J n .. 2^J n + 3 (2^J - 1), so the last
+// owned coefficient needs 2^{J+1} - 2 extra rows; a 2-tap bank needs none.
+__host__ __device__ constexpr long cascade_halo(int M, int J) {
+  return M == 4 ? (2L << J) - 2 : 0;
+}
+
+// Streams rows [t0, t_stop) of one unit into the cascade (periodic extension
+// reads row t mod L), 16 loads in flight per lane.
+template <int M, int J, bool DET, typename T, class Sink>
+__device__ void run_stream(Cascade<M, J, DET>& cas, const T* Kunit, int D,
+                           int cp, long t0, long t_stop, long L, Sink& sink) {
+  constexpr int U = 16;
+  for (long t = t0; t < t_stop; t += U) {
+    F2 v[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      long tt = t + k;
+      if (tt < t_stop) {
+        long row = tt < L ? tt : tt % L;
+        v[k] = load_pair(Kunit + row * D + 2 * cp);
+      } else {
+        v[k] = F2{0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      if (t + k < t_stop) cas.template push<1>(t + k, v[k], sink);
+    }
+  }
+}
+
+struct GlobalSink {
+  float* aout;     // approximation, unit base + 2 cp
+  float* dout;     // details, unit base + 2 cp, nullable
+  long n0, n1;     // level-J rows owned by the stream
+  long L;
+  int J, D;
+  __device__ __forceinline__ void store2(float* p, F2 a) {
+    *reinterpret_cast<float2*>(p) = make_float2(a.x, a.y);
+  }
+  __device__ __forceinline__ void approx(long n, F2 a) {
+    if (n >= n0 && n < n1) store2(aout + n * D, a);
+  }
+  __device__ __forceinline__ void detail(int j, long n, F2 d) {
+    const long lo = n0 << (J - j), hi = n1 << (J - j);
+    if (dout && n >= lo && n < hi) {
+      const long row = (L - (L >> (j - 1))) + n;  // D_1 rows come first
+      store2(dout + row * D, d);
+    }
+  }
+};
+
+struct LdsSink {
+  float* coef;  // tile base + 2 cp
+  long nbase;   // coefficient index of tile row 0
+  long n0, n1;  // rows owned by the stream
+  int stride;
+  __device__ __forceinline__ void approx(long n, F2 a) {
+    if (n >= n0 && n < n1) {
+      float* p = coef + (n - nbase) * stride;
+      p[0] = a.x;
+      p[1] = a.y;
+    }
+  }
+  __device__ __forceinline__ void detail(int, long, F2) {}
+};
+
+// ------------------------------------------------------------ staged DWT
+
+template <int M, int J, typename T>
+__global__ __launch_bounds__(kBlock) void dwt_kernel(DwtArgs a, Taps taps) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lps = a.D / 2;             // lanes per stream
+  const int spw = kWave / lps;         // streams per wave
+  const int cp = lane % lps;
+  const int sid = wave * spw + lane / lps;
+  const int u = blockIdx.x / a.ntiles;
+  const int tile = blockIdx.x % a.ntiles;
+  const long n0 = ((long)tile * a.streams + sid) * a.cps;
+  if (u >= a.U || n0 >= a.nJ) return;  // no barrier in this kernel
+  const long n1 = min(n0 + (long)a.cps, (long)a.nJ);
+  const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * a.D;
+  GlobalSink sink;
+  sink.aout = a.approx + (long)u * a.nJ * a.D + 2 * cp;
+  sink.dout = a.details ? a.details + (long)u * (a.L - a.nJ) * a.D + 2 * cp
+                        : nullptr;
+  sink.n0 = n0;
+  sink.n1 = n1;
+  sink.L = a.L;
+  sink.J = J;
+  sink.D = a.D;
+  Cascade<M, J, true> cas;
+  const bool sym = (M == 4) && a.boundary == 0;
+  cas.init(taps, a.L, sym);
+  const long t0 = n0 << J;
+  long t_stop = (n1 << J) + cascade_halo(M, J);
+  if (sym || M == 2) t_stop = min(t_stop, (long)a.L);
+  run_stream<M, J, true, T>(cas, Kunit, a.D, cp, t0, t_stop, a.L, sink);
+}
+
+// ------------------------------------------------------------ skim tiles
+
+// Haar level-J approximation of tile rows [n0, n0 + ncoef) into LDS.
+template <typename T, int D>
+__device__ void haar_sum_tile(const T* Kunit, long n0, int ncoef, int J,
+                              float inv_norm, float* coef) {
+  constexpr int CPL = 16 / sizeof(T);  // channels per lane (16-byte load)
+  constexpr int LPR = D / CPL;         // lanes per row
+  constexpr int RPL = kWave / LPR;     // rows per wave load
+  constexpr int STRIDE = D + kCoefPad;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rsub = lane / LPR, csub = lane % LPR;
+  const int blk = 1 << J;
+  const int G = blk > RPL ? blk : RPL;  // rows per group
+  const int loads = G / RPL;
+  const int cpg = G / blk;               // coefficients per group
+  const int red = blk < RPL ? blk : RPL; // rows reduced across lanes
+  const long tok0 = n0 << J;
+  const long tok_end = (n0 + ncoef) << J;
+  const int ngroups = (int)(((long)ncoef * blk + G - 1) / G);
+  for (int grp = wave; grp < ngroups; grp += kBlock / kWave) {
+    float acc[CPL];
+#pragma unroll
+    for (int e = 0; e < CPL; ++e) acc[e] = 0.f;
+    const long r0 = tok0 + (long)grp * G + rsub;
+    for (int i0 = 0; i0 < loads; i0 += 8) {
+      u32x4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const long t = r0 + (long)(i0 + k) * RPL;
+        if (i0 + k < loads && t < tok_end)
+          v[k] = *reinterpret_cast<const u32x4*>(Kunit + t * D + csub * CPL);
+        else
+          v[k] = u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[2 * e] += bf16_lo(v[k][e]);
+            acc[2 * e + 1] += bf16_hi(v[k][e]);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] += __uint_as_float(v[k][e]);
+        }
+      }
+    }
+    for (int s = 1; s < red; s <<= 1) {
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) acc[e] += __shfl_xor(acc[e], LPR * s);
+    }
+    if (rsub % red == 0) {
+      const int c = grp * cpg + rsub / blk;
+      if (c < ncoef) {
+        float* dst = coef + c * STRIDE + csub * CPL;
+#pragma unroll
+        for (int e = 0; e < CPL; ++e) dst[e] = acc[e] * inv_norm;
+      }
+    }
+  }
+}
+
+// Cascade level-J approximation of tile rows [n0, n0 + ncoef) into LDS.
+// The tile is split into one stream per half/whole wave.
+template <int M, int J, typename T, int D>
+__device__ void cascade_tile(const T* Kunit, long L, long n0, int ncoef,
+                             int cpt, bool sym, const Taps& taps,
+                             float* coef) {
+  constexpr int LPS = D / 2;
+  constexpr int SPW = kWave / LPS;
+  constexpr int NSTREAM = (kBlock / kWave) * SPW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int cp = lane % LPS;
+  const int sid = wave * SPW + lane / LPS;
+  const int cps = cpt / NSTREAM;
+  const long s0 = n0 + (long)sid * cps;
+  const long s1 = min(s0 + (long)cps, n0 + (long)ncoef);
+  if (s0 >= s1) return;
+  LdsSink sink;
+  sink.coef = coef + 2 * cp;
+  sink.nbase = n0;
+  sink.n0 = s0;
+  sink.n1 = s1;
+  sink.stride = D + kCoefPad;
+  Cascade<M, J, false> cas;
+  cas.init(taps, L, sym);
+  const long t0 = s0 << J;
+  long t_stop = (s1 << J) + cascade_halo(M, J);
+  if (sym || M == 2) t_stop = min(t_stop, L);
+  run_stream<M, J, false, T>(cas, Kunit, D, cp, t0, t_stop, L, sink);
+}
+
+// logits[q][n0 + c] = scale * <Q_q, coef_c> for the tile, plus per-row max
+// and sum of exp over the tile's columns.
+template <typename T, int D>
+__device__ void skim_epilogue(const SkimTileArgs& a, int u, int tile, long n0,
+                              int ncoef, const float* coef) {
+  constexpr int STRIDE = D + kCoefPad;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, col = lane & 15;
+  const int nqb = (a.B + 15) / 16;
+  const int ncb = (ncoef + 15) / 16;
+  const T* Qunit = reinterpret_cast<const T*>(a.Q) + (long)u * a.B * D;
+  for (int qb = wave; qb < nqb; qb += kBlock / kWave) {
+    // A operand: query row (clamped), channels [g D/4, (g+1) D/4)
+    const int qrow = min(qb * 16 + col, a.B - 1);
+    float qv[D / 4];
+    const T* qsrc = Qunit + (long)qrow * D + g * (D / 4);
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int v = 0; v < D / 32; ++v) {
+        u32x4 w = *reinterpret_cast<const u32x4*>(qsrc + 8 * v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          qv[8 * v + 2 * e] = bf16_lo(w[e]);
+          qv[8 * v + 2 * e + 1] = bf16_hi(w[e]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < D / 16; ++v) {
+        f32x4 w = *reinterpret_cast<const f32x4*>(qsrc + 4 * v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qv[4 * v + e] = w[e];
+      }
+    }
+    f32x4 acc[kMaxCoefTile / 16];
+#pragma unroll
+    for (int cb = 0; cb < kMaxCoefTile / 16; ++cb) {
+      acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (cb < ncb) {
+        const float* crow = coef + (cb * 16 + col) * STRIDE + g * (D / 4);
+#pragma unroll
+        for (int s4 = 0; s4 < D / 16; ++s4) {
+          f32x4 cv = *reinterpret_cast<const f32x4*>(crow + 4 * s4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[4 * s4 + e],
+                                                           cv[e], acc[cb], 0,
+                                                           0, 0);
+        }
+      }
+    }
+    // lane holds logit[q = 16 qb + 4 g + i][c = 16 cb + col]
+    float m[4], z[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int cb = 0; cb < kMaxCoefTile / 16; ++cb) {
+        const int c = cb * 16 + col;
+        const bool ok = cb < ncb && c < ncoef;
+        const float v = ok ? acc[cb][i] * a.scale : -INFINITY;
+        acc[cb][i] = v;
+        mx = fmaxf(mx, v);
+      }
+      m[i] = wave_max16(mx);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float s = 0.f;
+#pragma unroll
+      for (int cb = 0; cb < kMaxCoefTile / 16; ++cb) {
+        const int c = cb * 16 + col;
+        if (cb < ncb && c < ncoef) s += __expf(acc[cb][i] - m[i]);
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o);
+      z[i] = s;
+    }
+    float* lg = a.logits + (long)u * a.B * a.nJ + n0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int q = qb * 16 + 4 * g + i;
+      if (q < a.B) {
+#pragma unroll
+        for (int cb = 0; cb < kMaxCoefTile / 16; ++cb) {
+          const int c = cb * 16 + col;
+          if (cb < ncb && c < ncoef) lg[(long)q * a.nJ + c] = acc[cb][i];
+        }
+      }
+    }
+    if (col == 0) {
+      float* st = a.stats + ((long)u * a.ntiles + tile) * 2 * a.B;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = qb * 16 + 4 * g + i;
+        if (q < a.B) {
+          st[q] = m[i];
+          st[a.B + q] = z[i];
+        }
+      }
+    }
+  }
+}
+
+template <int SRC, int M, int J, typename T, int D>
+__global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
+                                                           Taps taps) {
+  extern __shared__ float coef[];  // [cpt][D + kCoefPad]
+  const int total = a.U * a.ntiles;
+  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    const int u = item / a.ntiles;
+    const int tile = item % a.ntiles;
+    const long n0 = (long)tile * a.cpt;
+    const int ncoef = (int)min((long)a.cpt, (long)a.nJ - n0);
+    if constexpr (SRC == kHaarSum) {
+      const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
+      haar_sum_tile<T, D>(Kunit, n0, ncoef, a.J, taps.inv_norm, coef);
+    } else if constexpr (SRC == kCascade) {
+      const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
+      cascade_tile<M, J, T, D>(Kunit, a.L, n0, ncoef, a.cpt,
+                               M == 4 && a.boundary == 0, taps, coef);
+    } else {
+      const float* src = a.approx + ((long)u * a.nJ + n0) * D;
+      for (int v = threadIdx.x; v < ncoef * (D / 4); v += kBlock) {
+        const int c = v / (D / 4), k = v % (D / 4);
+        *reinterpret_cast<f32x4*>(coef + c * (D + kCoefPad) + 4 * k) =
+            *reinterpret_cast<const f32x4*>(src + (long)c * D + 4 * k);
+      }
+    }
+    __syncthreads();
+    skim_epilogue<T, D>(a, u, tile, n0, ncoef, coef);
+    __syncthreads();
+  }
+}
+
+// One workgroup per unit: merge the tiles' row statistics, form W (eq. 8) and
+// select the top-S regions (eq. 9).
+__global__ __launch_bounds__(kBlock) void skim_select_kernel(SkimSelectArgs a,
+                                                             int w_in_lds) {
+  __shared__ float row_max[WF_MAX_Q_LEN];
+  __shared__ float row_inv[WF_MAX_Q_LEN];
+  __shared__ SelectShared<kBlock> sh;
+  extern __shared__ float wsh[];
+  const int u = blockIdx.x;
+  const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
+  for (int q = threadIdx.x; q < a.B; q += kBlock) {
+    float mx = -INFINITY;
+    for (int t = 0; t < a.ntiles; ++t) mx = fmaxf(mx, st[(long)t * 2 * a.B + q]);
+    float z = 0.f;
+    for (int t = 0; t < a.ntiles; ++t)
+      z += st[(long)t * 2 * a.B + a.B + q] *
+           __expf(st[(long)t * 2 * a.B + q] - mx);
+    row_max[q] = mx;
+    row_inv[q] = 1.f / z;
+  }
+  __syncthreads();
+  const float* lg = a.logits + (long)u * a.B * a.nJ;
+  float* W = a.W + (long)u * a.nJ;
+  for (int j = threadIdx.x; j < a.nJ; j += kBlock) {
+    float w = 0.f;
+    for (int q = 0; q < a.B; ++q)
+      w += __expf(lg[(long)q * a.nJ + j] - row_max[q]) * row_inv[q];
+    W[j] = w;
+    if (w_in_lds) wsh[j] = w;
+  }
+  __syncthreads();
+  const float* src = w_in_lds ? wsh : W;
+  block_select_topk<kBlock>(src, a.nJ, a.S, a.seg + (long)u * a.S,
+                            [](int i) { return (int32_t)i; }, sh);
+}
+
+// ------------------------------------------------------------ host side
+
+static Taps make_taps(int wavelet, int J) {
+  Taps t{};
+  const double r2 = std::sqrt(2.0);
+  if (wavelet == WF_HAAR) {
+    t.g[0] = t.g[1] = (float)(1.0 / r2);
+    t.h[0] = (float)(1.0 / r2);
+    t.h[1] = (float)(-1.0 / r2);
+  } else {
+    const double r3 = std::sqrt(3.0), den = 4.0 * r2;
+    const double g[4] = {(1 + r3) / den, (3 + r3) / den, (3 - r3) / den,
+                         (1 - r3) / den};
+    for (int m = 0; m < 4; ++m) {
+      t.g[m] = (float)g[m];
+      t.h[m] = (float)((m % 2 == 0 ? 1.0 : -1.0) * g[3 - m]);
+    }
+  }
+  t.inv_norm = (float)std::pow(2.0, -0.5 * J);
+  return t;
+}
+
+template <int M, typename T>
+static hipError_t dwt_dispatch(const DwtArgs& a, const Taps& taps, dim3 grid,
+                               hipStream_t s) {
+  switch (a.J) {
+#define WF_DWT_CASE(JJ)                                                  \
+  case JJ:                                                               \
+    hipLaunchKernelGGL((dwt_kernel<M, JJ, T>), grid, dim3(kBlock), 0, s, \
+                       a, taps);                                         \
+    break;
+    WF_DWT_CASE(1) WF_DWT_CASE(2) WF_DWT_CASE(3) WF_DWT_CASE(4)
+    WF_DWT_CASE(5) WF_DWT_CASE(6) WF_DWT_CASE(7) WF_DWT_CASE(8)
+    WF_DWT_CASE(9) WF_DWT_CASE(10)
+#undef WF_DWT_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+DwtPlan plan_dwt(const wf_params& p) {
+  DwtPlan d;
+  const int spw = kWave / (p.head_dim / 2);
+  d.streams = (kBlock / kWave) * spw;
+  d.cps = std::max(1, 2048 >> p.levels);
+  const long nJ = (long)p.ctx_len >> p.levels;
+  const long per_tile = (long)d.streams * d.cps;
+  d.ntiles = (int)((nJ + per_tile - 1) / per_tile);
+  return d;
+}
+
+hipError_t launch_dwt(const wf_params& p, const void* K, float* approx,
+                      float* details, hipStream_t s) {
+  DwtPlan pl = plan_dwt(p);
+  DwtArgs a;
+  a.K = K;
+  a.approx = approx;
+  a.details = details;
+  a.U = p.batch * p.heads;
+  a.L = p.ctx_len;
+  a.D = p.head_dim;
+  a.J = p.levels;
+  a.nJ = p.ctx_len >> p.levels;
+  a.cps = pl.cps;
+  a.streams = pl.streams;
+  a.ntiles = pl.ntiles;
+  a.boundary = p.boundary;
+  const Taps taps = make_taps(p.wavelet, p.levels);
+  dim3 grid((unsigned)(a.U * a.ntiles));
+  const bool haar = p.wavelet == WF_HAAR;
+  if (p.dtype == WF_BF16)
+    return haar ? dwt_dispatch<2, bf16_t>(a, taps, grid, s)
+                : dwt_dispatch<4, bf16_t>(a, taps, grid, s);
+  return haar ? dwt_dispatch<2, float>(a, taps, grid, s)
+              : dwt_dispatch<4, float>(a, taps, grid, s);
+}
+
+SkimPlan plan_skim(const wf_params& p, bool fused) {
+  SkimPlan k;
+  const int J = p.levels;
+  if (!fused) {
+    k.source = kFromApprox;
+    k.cpt = kMaxCoefTile;
+  } else if (p.wavelet == WF_HAAR) {
+    k.source = kHaarSum;
+    k.cpt = std::min(kMaxCoefTile, std::max(16, 2048 >> J));
+  } else {
+    k.source = kCascade;
+    k.cpt = kMaxCoefTile;  // 4 (d=128) or 8 (d=64) streams of 16 or 8
+  }
+  const long nJ = (long)p.ctx_len >> J;
+  k.ntiles = (int)((nJ + k.cpt - 1) / k.cpt);
+  k.lds_bytes = (size_t)k.cpt * (p.head_dim + kCoefPad) * sizeof(float);
+  return k;
+}
+
+template <int SRC, int M, int J, typename T, int D>
+static hipError_t skim_launch_one(const SkimTileArgs& a, const Taps& taps,
+                                  size_t lds, hipStream_t s) {
+  auto kern = skim_tile_kernel<SRC, M, J, T, D>;
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+      &per_cu, reinterpret_cast<const void*>(kern), kBlock, lds);
+  if (e != hipSuccess) return e;
+  const long total = (long)a.U * a.ntiles;
+  const long cap = (long)std::max(1, per_cu) * device_cu_count();
+  dim3 grid((unsigned)std::min(total, cap));
+  hipLaunchKernelGGL(kern, grid, dim3(kBlock), lds, s, a, taps);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t skim_dispatch(int source, const SkimTileArgs& a,
+                                const Taps& taps, size_t lds, hipStream_t s) {
+  if (source == kHaarSum) return skim_launch_one<kHaarSum, 2, 1, T, D>(a, taps, lds, s);
+  if (source == kFromApprox) return skim_launch_one<kFromApprox, 2, 1, T, D>(a, taps, lds, s);
+  switch (a.J) {
+#define WF_SKIM_CASE(JJ) \
+  case JJ:               \
+    return skim_launch_one<kCascade, 4, JJ, T, D>(a, taps, lds, s);
+    WF_SKIM_CASE(1) WF_SKIM_CASE(2) WF_SKIM_CASE(3) WF_SKIM_CASE(4)
+    WF_SKIM_CASE(5) WF_SKIM_CASE(6) WF_SKIM_CASE(7) WF_SKIM_CASE(8)
+    WF_SKIM_CASE(9) WF_SKIM_CASE(10)
+#undef WF_SKIM_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_skim_tiles(const wf_params& p, bool fused, const void* Q,
+                             const void* K, const float* approx, float* logits,
+                             float* stats, hipStream_t s) {
+  const SkimPlan pl = plan_skim(p, fused);
+  SkimTileArgs a;
+  a.K = K;
+  a.approx = approx;
+  a.Q = Q;
+  a.logits = logits;
+  a.stats = stats;
+  a.U = p.batch * p.heads;
+  a.L = p.ctx_len;
+  a.B = p.q_len;
+  a.J = p.levels;
+  a.nJ = p.ctx_len >> p.levels;
+  a.cpt = pl.cpt;
+  a.ntiles = pl.ntiles;
+  a.boundary = p.boundary;
+  a.scale = effective_scale(p);
+  const Taps taps = make_taps(p.wavelet, p.levels);
+  if (p.dtype == WF_BF16)
+    return p.head_dim == 128
+               ? skim_dispatch<bf16_t, 128>(pl.source, a, taps, pl.lds_bytes, s)
+               : skim_dispatch<bf16_t, 64>(pl.source, a, taps, pl.lds_bytes, s);
+  return p.head_dim == 128
+             ? skim_dispatch<float, 128>(pl.source, a, taps, pl.lds_bytes, s)
+             : skim_dispatch<float, 64>(pl.source, a, taps, pl.lds_bytes, s);
+}
+
+hipError_t launch_skim_select(const wf_params& p, int ntiles,
+                              const float* logits, const float* stats,
+                              float* W, int32_t* seg, hipStream_t s) {
+  SkimSelectArgs a;
+  a.logits = logits;
+  a.stats = stats;
+  a.W = W;
+  a.seg = seg;
+  a.U = p.batch * p.heads;
+  a.B = p.q_len;
+  a.nJ = p.ctx_len >> p.levels;
+  a.ntiles = ntiles;
+  a.S = p.segments;
+  const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
+  const size_t lds = in_lds ? (size_t)a.nJ * sizeof(float) : 0;
+  hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kBlock),
+                     lds, s, a, in_lds);
+  return hipGetLastError();
+}
+
+}  // namespace wf

@@ -28,13 +28,14 @@ Recipe for one (layer, batch, head) unit, all in float64:
   * queries: Q = z / sqrt(d) + 2 u
   * values:  V = v
   * rounding: once, on the host: float64 -> float32 (round to nearest even),
-    then for bf16 workloads float32 -> bfloat16 (torch, round to nearest even).
+    then for bf16 workloads float32 -> bfloat16 (round to nearest even on
+    the dropped 16 bits, the same rule as torch's conversion).
 """
 from __future__ import annotations
 
 import math
 import os
-from concurrent.futures import ProcessPoolExecutor
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field, replace
 
 import numpy as np
@@ -157,28 +158,41 @@ def unit_f64(w: Workload, layer: int, batch: int, head: int):
     return Q, K, v
 
 
-def round_host(x: np.ndarray, dtype: str):
-    """Round a float64 array once to the workload dtype; returns a torch
-    tensor (float32 or bfloat16) on the CPU."""
-    import torch
-    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+def _bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float64 -> float32 (round to nearest even) -> bfloat16 bits (round to
+    nearest even on the 16 dropped bits); inputs are finite."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    u = u.astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def _rounded(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
-        return t.to(torch.bfloat16)
+        return _bf16_bits(x)
     if dtype == "f32":
-        return t
+        return np.ascontiguousarray(x, dtype=np.float32)
     raise ValueError(f"unknown dtype {dtype!r}")
 
 
+def _to_torch(a: np.ndarray, dtype: str):
+    import torch
+    if dtype == "bf16":
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)
+    return torch.from_numpy(a)
+
+
+def round_host(x: np.ndarray, dtype: str):
+    """Round a float64 array once to the workload dtype; returns a torch
+    tensor (float32 or bfloat16) on the CPU."""
+    return _to_torch(_rounded(x, dtype), dtype)
+
+
 def _unit_rounded(args):
+    # numpy only: runs in worker threads
     w, layer, b, h = args
     Q, K, V = unit_f64(w, layer, b, h)
-    # float32 bytes of the rounded values travel back to the parent; bf16 is
-    # recovered exactly from them.
-    out = []
-    for x in (Q, K, V):
-        t = round_host(x, w.dtype)
-        out.append(t.float().numpy())
-    return b, h, out
+    return b, h, [_rounded(x, w.dtype) for x in (Q, K, V)]
 
 
 def make_inputs(w: Workload, layer: int = 0, workers: int | None = None):
@@ -186,6 +200,9 @@ def make_inputs(w: Workload, layer: int = 0, workers: int | None = None):
 
     Returns torch CPU tensors Q [batch, heads, B, d], K and V
     [batch, heads, L, d] in the workload dtype (bfloat16 or float32).
+    Units are drawn in worker threads (numpy's generators and scipy's filter
+    release the GIL); no process is forked, since a fork would inherit the
+    parent's OpenMP state and can deadlock.
     """
     import torch
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -195,18 +212,20 @@ def make_inputs(w: Workload, layer: int = 0, workers: int | None = None):
     jobs = [(w, layer, b, h) for b in range(w.batch) for h in range(w.heads)]
     if workers is None:
         workers = min(16, os.cpu_count() or 1, len(jobs))
+
+    def put(b, h, arrs):
+        q, k, v = (_to_torch(a, w.dtype) for a in arrs)
+        Q[b, h] = q
+        K[b, h] = k
+        V[b, h] = v
+
     if workers <= 1 or len(jobs) == 1:
-        results = map(_unit_rounded, jobs)
-        for b, h, (q, k, v) in results:
-            Q[b, h] = torch.from_numpy(q).to(tdt)
-            K[b, h] = torch.from_numpy(k).to(tdt)
-            V[b, h] = torch.from_numpy(v).to(tdt)
+        for job in jobs:
+            put(*_unit_rounded(job))
     else:
-        with ProcessPoolExecutor(max_workers=workers) as ex:
-            for b, h, (q, k, v) in ex.map(_unit_rounded, jobs, chunksize=1):
-                Q[b, h] = torch.from_numpy(q).to(tdt)
-                K[b, h] = torch.from_numpy(k).to(tdt)
-                V[b, h] = torch.from_numpy(v).to(tdt)
+        with ThreadPoolExecutor(max_workers=workers) as ex:
+            for b, h, arrs in ex.map(_unit_rounded, jobs):
+                put(b, h, arrs)
     return Q, K, V
 
 
