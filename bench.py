@@ -1,0 +1,252 @@
+"""Benchmark of the fused WaveFilter filter+attend step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one wf_filter_attend call: DWT + skim, coarse top-S, token scan,
+top-k and sparse attention for every (batch, head) unit of one layer of one
+denoising step.  Inputs are seeded synthetic tensors (synth.WORKLOADS),
+resident in HBM before timing starts.  Prints one JSON line:
+
+  value       context tokens filtered+attended per second per layer
+              (batch * ctx_len / step time)
+  roofline    the dominant kernel (skim_tile: streams every key once)
+              against MI355X's 8 TB/s HBM peak; durations come from HIP
+              events recorded between the kernels of each timed step
+  cpu_baseline  the fp64 CPU oracle on the same workload, on this host
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = ("context tokens filtered+attended/sec per layer @32K ctx; "
+          "% of HBM peak")
+
+
+def algorithmic_bytes(w, keff: int) -> dict:
+    """Bytes the method must move per unit (each counted once): every key
+    (DWT + skim), the pool keys re-read by the scan, the selected values,
+    the query block in and the output out."""
+    e = 2 if w.dtype == "bf16" else 4
+    d = w.head_dim
+    pool = w.segments << w.levels
+    per_unit = {
+        "keys": w.ctx_len * d * e,
+        "pool": pool * d * e,
+        "values": keff * d * e,
+        "q_and_o": 2 * w.q_len * d * e,
+    }
+    per_unit["total"] = sum(per_unit.values())
+    # skim_tile reads every key and the query block once
+    per_unit["skim_tile"] = per_unit["keys"] + w.q_len * d * e
+    return per_unit
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime torch already loaded."""
+
+    def __init__(self, n: int):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [
+            ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            h = ctypes.c_void_p()
+            if self.lib.hipEventCreate(ctypes.byref(h)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev.append(h.value)
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        out = ctypes.c_float()
+        self.lib.hipEventSynchronize(ctypes.c_void_p(self.ev[b]))
+        if self.lib.hipEventElapsedTime(ctypes.byref(out),
+                                        ctypes.c_void_p(self.ev[a]),
+                                        ctypes.c_void_p(self.ev[b])) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(out.value)
+
+    def close(self):
+        for e in self.ev:
+            self.lib.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def cpu_baseline(w, Q, K, V) -> dict:
+    """The oracle as it stands, on every unit of the layer, in chunks of 16
+    units (only the oracle calls are timed)."""
+    import oracle
+    oracle.build(force=False)
+    U = w.units
+    q = Q.reshape(U, w.q_len, w.head_dim)
+    k = K.reshape(U, w.ctx_len, w.head_dim)
+    v = V.reshape(U, w.ctx_len, w.head_dim)
+    chunk = 16
+    elapsed = 0.0
+    for u0 in range(0, U, chunk):
+        qa, ka, va = (oracle._f64(x[u0:u0 + chunk]) for x in (q, k, v))
+        t0 = time.perf_counter()
+        oracle.filter_attend(qa, ka, va, w.levels, w.segments, w.budget,
+                             wavelet=w.wavelet, boundary=w.boundary)
+        elapsed += time.perf_counter() - t0
+        del qa, ka, va
+    tokens = w.batch * w.ctx_len
+    return {"value": tokens / elapsed, "unit": "tokens/s",
+            "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"all {U} (batch, head) units of one {w.name} layer, "
+                      f"fp64, OpenMP over units, {chunk} units per call; "
+                      f"{elapsed:.2f} s",
+            "seconds": elapsed}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="headline32k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file with measured HBM bytes per skim_tile "
+                         "launch (from rocprofv3 counters)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; the per-(batch, "
+              "head) units would shard across GPUs with no exchange, but no "
+              "multi-GPU path is built", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+    import paper_2606_00724_amd as wf
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    w = synth.WORKLOADS[args.workload]
+    print(f"[bench] generating {w.name} inputs", file=sys.stderr, flush=True)
+    Q, K, V = synth.make_inputs(w)
+    dev = torch.device("cuda:0")
+    p = wf.params_for(w, gen_len=0)
+    keff = wf.effective_budget(p)
+    Qd, Kd, Vd = Q.to(dev), K.to(dev), V.to(dev)
+    O = torch.empty_like(Qd)
+    tok = torch.empty((w.batch, w.heads, keff), dtype=torch.int32, device=dev)
+    ws = wf.alloc_workspace(p, wf.OP_FUSED, dev)
+    names = wf.fused_kernel_names(p)
+    ev = HipEvents((len(names) + 1) * args.steps)
+    stream = torch.cuda.current_stream()
+
+    def step_plain():
+        wf.wf_filter_attend(p, Qd, Kd, Vd, None, None, O, tok, None, ws,
+                            stream)
+
+    def step_timed(i):
+        base = i * (len(names) + 1)
+        wf.wf_filter_attend_timed(p, Qd, Kd, Vd, None, None, O, tok, None,
+                                  ws, ev.ev[base:base + len(names) + 1],
+                                  stream)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step_plain()
+    torch.cuda.synchronize()
+
+    # timed region: K steps, HIP events between the kernels of every step
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step_timed(i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    per_kernel = {n: 0.0 for n in names}
+    for i in range(args.steps):
+        base = i * (len(names) + 1)
+        for j, n in enumerate(names):
+            per_kernel[n] += ev.elapsed_ms(base + j, base + j + 1)
+    per_kernel = {n: t / args.steps for n, t in per_kernel.items()}
+    ev.close()
+
+    # the same K steps without events, for comparison
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        step_plain()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step_plain = t_start.elapsed_time(t_end) / args.steps
+
+    alg = algorithmic_bytes(w, keff)
+    U = w.units
+    tokens = w.batch * w.ctx_len
+    value = tokens / (ms_step * 1e-3)
+    dom = "skim_tile"
+    dom_ms = per_kernel[dom]
+    achieved = alg["skim_tile"] * U / (dom_ms * 1e-3) / 1e9
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": w.description,
+            "batch": w.batch, "heads": w.heads, "ctx_len": w.ctx_len,
+            "head_dim": w.head_dim, "q_len": w.q_len, "levels": w.levels,
+            "wavelet": w.wavelet, "segments": w.segments,
+            "budget": w.budget, "k_eff": keff, "gen_len": 0,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dom,
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg["skim_tile"] * U,
+            "avg_launch_ms": dom_ms,
+        },
+        "path_hbm_frac": alg["total"] * U / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "path_algorithmic_bytes": alg["total"] * U,
+        "kernel_ms": per_kernel,
+        "ms_per_step_without_events": ms_step_plain,
+        "host_wall_s": wall,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, Q, K, V)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
