@@ -14,258 +14,326 @@
 // instruction.  V sits transposed in LDS so that its B operand is one 16-byte
 // read.  Online softmax (running max / sum per query row) spans the
 // sub-blocks.  fp32 uses v_mfma_f32_16x16x4_f32 on 16-row sub-blocks.
+#include <type_traits>
+
 #include "wf_device.hpp"
 #include "wf_kernels.hpp"
 #include "wf_launch.hpp"
 
 namespace wf {
 
-template <typename T>
-struct AttnPad {
-  static constexpr int value = 16 / sizeof(T);
+// Absolute cache row rr of unit u: K[tok[rr]] for rr < nsel, then the tail
+// rows; contiguous rows when tok is null.  Rows outside [r_lo, r_hi) of the
+// current chunk are zero.
+template <typename T, int D>
+struct CacheRows {
+  const T* base;
+  const T* tail;
+  const int32_t* tok;   // unit's token list or null
+  long unit_rows;       // rows per unit in `base` (L, or nrows when contiguous)
+  int u, nsel, G;
+  long r0;
+  int nr;
+  __device__ __forceinline__ const T* operator()(int r) const {
+    if (r >= nr) return nullptr;
+    const long rr = r0 + r;
+    if (tok) {
+      if (rr < nsel) return base + ((long)u * unit_rows + tok[rr]) * D;
+      return tail + ((long)u * G + (rr - nsel)) * D;
+    }
+    return base + ((long)u * unit_rows + rr) * D;
+  }
+};
+
+// bf16 V chunk in token-pair layout: dword [m][c] holds channel c of rows
+// 2m (low half) and 2m+1 (high half), so the PV operand of rows 8g .. 8g+7
+// is four dword reads.  Thread t stages pairs of 8-channel vectors.
+template <int D, int NT>
+struct VPairStager {
+  static constexpr int VPR = D / 8;                       // vectors per row
+  static constexpr int ITEMS = (kAttnChunk / 2) * VPR;    // (pair, vector)
+  static constexpr int PER_THREAD = (ITEMS + NT - 1) / NT;
+  static constexpr int VPS = D + 4;                       // dwords per pair row
+  u32x4 lo[PER_THREAD], hi[PER_THREAD];
+
+  template <class Src>
+  __device__ __forceinline__ void load(const Src& src) {
+    const bf16_t* pa[PER_THREAD];
+    const bf16_t* pb[PER_THREAD];
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int v = i * NT + threadIdx.x;
+      const int m = v / VPR;
+      pa[i] = v < ITEMS ? src(2 * m) : nullptr;
+      pb[i] = v < ITEMS ? src(2 * m + 1) : nullptr;
+    }
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int k = (i * NT + threadIdx.x) % VPR;
+      lo[i] = pa[i] ? *reinterpret_cast<const u32x4*>(pa[i] + 8 * k) : u32x4{0u, 0u, 0u, 0u};
+      hi[i] = pb[i] ? *reinterpret_cast<const u32x4*>(pb[i] + 8 * k) : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+
+  __device__ __forceinline__ void store(uint32_t* dst) const {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int v = i * NT + threadIdx.x;
+      if (v < ITEMS) {
+        const int m = v / VPR, k = v % VPR;
+        u32x4 w0, w1;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          w0[2 * e] = (lo[i][e] & 0xffffu) | (hi[i][e] << 16);
+          w0[2 * e + 1] = (lo[i][e] >> 16) | (hi[i][e] & 0xffff0000u);
+          w1[2 * e] = (lo[i][e + 2] & 0xffffu) | (hi[i][e + 2] << 16);
+          w1[2 * e + 1] = (lo[i][e + 2] >> 16) | (hi[i][e + 2] & 0xffff0000u);
+        }
+        uint32_t* row = dst + m * VPS + 8 * k;
+        *reinterpret_cast<u32x4*>(row) = w0;
+        *reinterpret_cast<u32x4*>(row + 4) = w1;
+      }
+    }
+  }
 };
 
 template <typename T, int D>
 __global__ __launch_bounds__(kBlock) void attn_kernel(AttnArgs a) {
   constexpr int NW = kBlock / kWave;
-  constexpr int KSTR = D + AttnPad<T>::value;
   constexpr bool BF = sizeof(T) == 2;
-  // bf16: V transposed [D][chunk + 8]; fp32: V row-major [chunk][D + 4]
-  constexpr int VSTR = BF ? kAttnChunk + 8 : D + 4;
+  using KStager = RowStager<T, D, kAttnChunk, kBlock>;
+  constexpr int KSTR = KStager::STRIDE;
+  using VStage = typename std::conditional<BF, VPairStager<D, kBlock>,
+                                           RowStager<T, D, kAttnChunk, kBlock>>::type;
+  // fp32 V is row-major with stride D + 4 floats; bf16 V is the pair layout
+  constexpr int VPS = D + 4;
   extern __shared__ __align__(16) unsigned char smem[];
   T* Ks = reinterpret_cast<T*>(smem);
-  T* Vl = Ks + kAttnChunk * KSTR;
+  uint32_t* Vl = reinterpret_cast<uint32_t*>(Ks + kAttnChunk * KSTR);
 
   const int item = xcd_swizzle(blockIdx.x, gridDim.x);
   const int u = item / a.NS, sp = item % a.NS;
-  const long r0 = (long)sp * kAttnChunk;
-  const int nr = (int)min((long)kAttnChunk, (long)a.nrows - r0);
+  const long rb0 = (long)sp * a.rps;
+  const long re0 = min(rb0 + (long)a.rps, (long)a.nrows);
+  const int nchunks = (int)((re0 - rb0 + kAttnChunk - 1) / kAttnChunk);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, col = lane & 15;
 
-  const T* Kb = reinterpret_cast<const T*>(a.K);
-  const T* Vb = reinterpret_cast<const T*>(a.V);
-  const T* Kt = reinterpret_cast<const T*>(a.Kg);
-  const T* Vt = reinterpret_cast<const T*>(a.Vg);
-  auto row_of = [&](const T* base, const T* tail, int r) -> const T* {
-    if (r >= nr) return nullptr;
-    const long rr = r0 + r;
-    if (a.tok) {
-      if (rr < a.nsel)
-        return base + ((long)u * a.L + a.tok[(long)u * a.nsel + rr]) * D;
-      return tail + ((long)u * a.G + (rr - a.nsel)) * D;
-    }
-    return base + ((long)u * a.nrows + rr) * D;
-  };
-
-  constexpr int EPV = 16 / sizeof(T);  // elements per 16-byte vector
-  constexpr int VPR = D / EPV;
-  for (int v = threadIdx.x; v < kAttnChunk * VPR; v += kBlock) {
-    const int r = v / VPR, k = v % VPR;
-    const T* ks = row_of(Kb, Kt, r);
-    const T* vs = row_of(Vb, Vt, r);
-    u32x4 kv = ks ? *reinterpret_cast<const u32x4*>(ks + k * EPV)
-                  : u32x4{0u, 0u, 0u, 0u};
-    u32x4 vv = vs ? *reinterpret_cast<const u32x4*>(vs + k * EPV)
-                  : u32x4{0u, 0u, 0u, 0u};
-    *reinterpret_cast<u32x4*>(Ks + r * KSTR + k * EPV) = kv;
-    if constexpr (BF) {
-      uint16_t* vt = reinterpret_cast<uint16_t*>(Vl);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt[(k * EPV + 2 * e) * VSTR + r] = (uint16_t)(vv[e] & 0xffffu);
-        vt[(k * EPV + 2 * e + 1) * VSTR + r] = (uint16_t)(vv[e] >> 16);
-      }
-    } else {
-      *reinterpret_cast<u32x4*>(Vl + r * VSTR + k * EPV) = vv;
-    }
-  }
-  __syncthreads();
+  CacheRows<T, D> ksrc, vsrc;
+  ksrc.base = reinterpret_cast<const T*>(a.K);
+  vsrc.base = reinterpret_cast<const T*>(a.V);
+  ksrc.tail = reinterpret_cast<const T*>(a.Kg);
+  vsrc.tail = reinterpret_cast<const T*>(a.Vg);
+  ksrc.tok = vsrc.tok = a.tok ? a.tok + (long)u * a.nsel : nullptr;
+  ksrc.unit_rows = vsrc.unit_rows = a.tok ? (long)a.L : (long)a.nrows;
+  ksrc.u = vsrc.u = u;
+  ksrc.nsel = vsrc.nsel = a.nsel;
+  ksrc.G = vsrc.G = a.G;
 
   const int nqb = (a.B + 15) / 16;
   const int tsplit = nqb == 1 ? 4 : (nqb == 2 ? 2 : 1);
+  const int qpg = NW / tsplit;                 // query blocks per group
+  const int ngroups = (nqb + qpg - 1) / qpg;
   const int part = wave % tsplit;
-  const int qstep = NW / tsplit;
-  const int R = kAttnChunk / tsplit;
-  const int rb = part * R;
-  const int re = min(rb + R, nr);
+  const int R = kAttnChunk / tsplit;           // chunk rows per wave
   const T* Qunit = reinterpret_cast<const T*>(a.Q) + (long)u * a.B * D;
+  float* po_base = a.part + ((long)u * a.NS + sp) * a.B * D;
+  float* ps_base = a.pstat + ((long)u * a.NS + sp) * 2 * a.B;
 
-  f32x4 O[D / 16];
-  float m_run = -INFINITY, l_run = 0.f;
-  int qb = wave / tsplit;
-  for (; qb < nqb; qb += qstep) {
+  KStager kst;
+  VStage vst;
+  for (int grp = 0; grp < ngroups; ++grp) {
+    const int qb = grp * qpg + wave / tsplit;
+    const bool active = qb < nqb;
+    const T* qrow = Qunit + (long)min(qb * 16 + col, a.B - 1) * D;
+    f32x4 O[D / 16];
 #pragma unroll
     for (int cb = 0; cb < D / 16; ++cb) O[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m_run = -INFINITY;
-    l_run = 0.f;
-    const T* qrow = Qunit + (long)min(qb * 16 + col, a.B - 1) * D;
+    float m_run = -INFINITY, l_run = 0.f;
+    u32x4 qreg[BF ? D / 32 : 1];
     if constexpr (BF) {
-      u32x4 qreg[D / 32];
 #pragma unroll
       for (int s = 0; s < D / 32; ++s)
         qreg[s] = *reinterpret_cast<const u32x4*>(qrow + 32 * s + 8 * g);
-      for (int sb = rb; sb < re; sb += 32) {
-        const int rx = sb + 8 * (col >> 2) + (col & 3);
-        f32x4 ax = {0.f, 0.f, 0.f, 0.f}, ay = {0.f, 0.f, 0.f, 0.f};
+    }
+    ksrc.r0 = vsrc.r0 = rb0;
+    ksrc.nr = vsrc.nr = (int)min((long)kAttnChunk, re0 - rb0);
+    kst.load(ksrc);
+    vst.load(vsrc);
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int nr = (int)min((long)kAttnChunk, re0 - (rb0 + (long)ch * kAttnChunk));
+      __syncthreads();  // previous chunk (or group) done with the LDS
+      kst.store(Ks);
+      if constexpr (BF) vst.store(Vl);
+      else vst.store(reinterpret_cast<T*>(Vl));
+      __syncthreads();
+      if (ch + 1 < nchunks) {
+        ksrc.r0 = vsrc.r0 = rb0 + (long)(ch + 1) * kAttnChunk;
+        ksrc.nr = vsrc.nr = (int)min((long)kAttnChunk, re0 - ksrc.r0);
+        kst.load(ksrc);
+        vst.load(vsrc);
+      }
+      if (!active) continue;
+      const int rb = part * R;
+      const int re = min(rb + R, nr);
+      if constexpr (BF) {
+        for (int sb = rb; sb < re; sb += 32) {
+          const int rx = sb + 8 * (col >> 2) + (col & 3);
+          f32x4 ax = {0.f, 0.f, 0.f, 0.f}, ay = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s) {
-          u32x4 kx = *reinterpret_cast<const u32x4*>(Ks + rx * KSTR + 32 * s + 8 * g);
-          u32x4 ky = *reinterpret_cast<const u32x4*>(Ks + (rx + 4) * KSTR + 32 * s + 8 * g);
-          ax = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, kx), __builtin_bit_cast(bf16x8, qreg[s]),
-              ax, 0, 0, 0);
-          ay = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, ky), __builtin_bit_cast(bf16x8, qreg[s]),
-              ay, 0, 0, 0);
+          for (int s = 0; s < D / 32; ++s) {
+            u32x4 kx = *reinterpret_cast<const u32x4*>(Ks + rx * KSTR + 32 * s + 8 * g);
+            u32x4 ky = *reinterpret_cast<const u32x4*>(Ks + (rx + 4) * KSTR + 32 * s + 8 * g);
+            ax = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, kx), __builtin_bit_cast(bf16x8, qreg[s]), ax, 0, 0, 0);
+            ay = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, ky), __builtin_bit_cast(bf16x8, qreg[s]), ay, 0, 0, 0);
+          }
+          // lane holds scores of rows sb + 8g + e (e < 8) for query col
+          float sv[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            sv[i] = (sb + 8 * g + i < re) ? ax[i] * a.scale : -INFINITY;
+            sv[4 + i] = (sb + 8 * g + 4 + i < re) ? ay[i] * a.scale : -INFINITY;
+          }
+          float mb = sv[0];
+#pragma unroll
+          for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
+          mb = fmaxf(mb, __shfl_xor(mb, 16));
+          mb = fmaxf(mb, __shfl_xor(mb, 32));
+          const float m_new = fmaxf(m_run, mb);
+          const float alpha = __expf(m_run - m_new);
+          float pv[8], ps = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            pv[e] = sv[e] > -INFINITY ? __expf(sv[e] - m_new) : 0.f;
+            ps += pv[e];
+          }
+          ps += __shfl_xor(ps, 16);
+          ps += __shfl_xor(ps, 32);
+          l_run = l_run * alpha + ps;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float ai = __shfl(alpha, 4 * g + i);
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
+          }
+          u32x4 pp = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                      pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
+          const uint32_t* vrow = Vl + ((sb >> 1) + 4 * g) * VPS + col;
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) {
+            u32x4 vb = {vrow[cb * 16], vrow[VPS + cb * 16], vrow[2 * VPS + cb * 16],
+                        vrow[3 * VPS + cb * 16]};
+            O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, pp), __builtin_bit_cast(bf16x8, vb), O[cb], 0, 0, 0);
+          }
+          m_run = m_new;
         }
-        // lane holds scores of rows sb + 8g + e (e < 8) for query col
-        float sv[8];
+      } else {
+        const float* Kf = reinterpret_cast<const float*>(Ks);
+        const float* Vf = reinterpret_cast<const float*>(Vl);
+        for (int sb = rb; sb < re; sb += 16) {
+          f32x4 acc = tile_dot_f32<D>(Kf + (sb + col) * KSTR,
+                                      reinterpret_cast<const float*>(qrow),
+                                      f32x4{0.f, 0.f, 0.f, 0.f});
+          // lane holds scores of rows sb + 4g + i for query col
+          float sv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) sv[i] = (sb + 4 * g + i < re) ? acc[i] * a.scale : -INFINITY;
+          float mb = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+          mb = fmaxf(mb, __shfl_xor(mb, 16));
+          mb = fmaxf(mb, __shfl_xor(mb, 32));
+          const float m_new = fmaxf(m_run, mb);
+          const float alpha = __expf(m_run - m_new);
+          float pv[4], ps = 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pv[i] = sv[i] > -INFINITY ? __expf(sv[i] - m_new) : 0.f;
+            ps += pv[i];
+          }
+          ps += __shfl_xor(ps, 16);
+          ps += __shfl_xor(ps, 32);
+          l_run = l_run * alpha + ps;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float ai = __shfl(alpha, 4 * g + i);
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb) {
+              const float vb = Vf[(sb + 4 * g + i) * VPS + cb * 16 + col];
+              O[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i], vb, O[cb], 0, 0, 0);
+            }
+          }
+          m_run = m_new;
+        }
+      }
+    }
+
+    if (tsplit == 1) {
+      if (active) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          sv[i] = (sb + 8 * g + i < re) ? ax[i] * a.scale : -INFINITY;
-          sv[4 + i] = (sb + 8 * g + 4 + i < re) ? ay[i] * a.scale : -INFINITY;
+          const int q = qb * 16 + 4 * g + i;
+          if (q < a.B) {
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb) po_base[(long)q * D + cb * 16 + col] = O[cb][i];
+          }
         }
-        float mb = sv[0];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
-        mb = fmaxf(mb, __shfl_xor(mb, 16));
-        mb = fmaxf(mb, __shfl_xor(mb, 32));
-        const float m_new = fmaxf(m_run, mb);
-        const float alpha = __expf(m_run - m_new);
-        float pv[8], ps = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          pv[e] = sv[e] > -INFINITY ? __expf(sv[e] - m_new) : 0.f;
-          ps += pv[e];
+        const int q = qb * 16 + col;
+        if (g == 0 && q < a.B) {
+          ps_base[q] = m_run;
+          ps_base[a.B + q] = l_run;
         }
-        ps += __shfl_xor(ps, 16);
-        ps += __shfl_xor(ps, 32);
-        l_run = l_run * alpha + ps;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float ai = __shfl(alpha, 4 * g + i);
-#pragma unroll
-          for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
-        }
-        u32x4 pp = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
-                    pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
-        const uint16_t* vt = reinterpret_cast<const uint16_t*>(Vl);
-#pragma unroll
-        for (int cb = 0; cb < D / 16; ++cb) {
-          u32x4 vb = *reinterpret_cast<const u32x4*>(vt + (cb * 16 + col) * VSTR + sb + 8 * g);
-          O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, pp), __builtin_bit_cast(bf16x8, vb),
-              O[cb], 0, 0, 0);
-        }
-        m_run = m_new;
       }
     } else {
-      for (int sb = rb; sb < re; sb += 16) {
-        f32x4 acc = tile_dot_f32<D>(reinterpret_cast<const float*>(Ks) + (sb + col) * KSTR,
-                                    reinterpret_cast<const float*>(qrow),
-                                    f32x4{0.f, 0.f, 0.f, 0.f});
-        // lane holds scores of rows sb + 4g + i for query col
-        float sv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          sv[i] = (sb + 4 * g + i < re) ? acc[i] * a.scale : -INFINITY;
-        float mb = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-        mb = fmaxf(mb, __shfl_xor(mb, 16));
-        mb = fmaxf(mb, __shfl_xor(mb, 32));
-        const float m_new = fmaxf(m_run, mb);
-        const float alpha = __expf(m_run - m_new);
-        float pv[4], ps = 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          pv[i] = sv[i] > -INFINITY ? __expf(sv[i] - m_new) : 0.f;
-          ps += pv[i];
-        }
-        ps += __shfl_xor(ps, 16);
-        ps += __shfl_xor(ps, 32);
-        l_run = l_run * alpha + ps;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float ai = __shfl(alpha, 4 * g + i);
-#pragma unroll
-          for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
-        }
-        const float* vl = reinterpret_cast<const float*>(Vl);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-#pragma unroll
-          for (int cb = 0; cb < D / 16; ++cb) {
-            const float vb = vl[(sb + 4 * g + i) * VSTR + cb * 16 + col];
-            O[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[i], vb, O[cb], 0, 0, 0);
-          }
-        }
-        m_run = m_new;
-      }
-    }
-    if (tsplit == 1) {
-      float* po = a.part + ((long)u * a.NS + sp) * a.B * D;
+      // one group; the tsplit waves of a query block merge their row parts
+      __syncthreads();
+      float* cO = reinterpret_cast<float*>(smem);  // [NW][16][D]
+      float* cm = cO + NW * 16 * D;                 // [NW][16]
+      float* cl = cm + NW * 16;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int q = qb * 16 + 4 * g + i;
-        if (q < a.B) {
 #pragma unroll
-          for (int cb = 0; cb < D / 16; ++cb) po[(long)q * D + cb * 16 + col] = O[cb][i];
-        }
+        for (int cb = 0; cb < D / 16; ++cb)
+          cO[(wave * 16 + 4 * g + i) * D + cb * 16 + col] = O[cb][i];
       }
-      const int q = qb * 16 + col;
-      if (g == 0 && q < a.B) {
-        float* ps = a.pstat + ((long)u * a.NS + sp) * 2 * a.B;
-        ps[q] = m_run;
-        ps[a.B + q] = l_run;
+      if (g == 0) {
+        cm[wave * 16 + col] = m_run;
+        cl[wave * 16 + col] = l_run;
       }
-    }
-  }
-
-  if (tsplit > 1) {
-    // each wave ran exactly one query block; merge the row parts in LDS
-    qb = wave / tsplit;
-    __syncthreads();
-    float* cO = reinterpret_cast<float*>(smem);  // [NW][16][D]
-    float* cm = cO + NW * 16 * D;                 // [NW][16]
-    float* cl = cm + NW * 16;
+      __syncthreads();
+      if (part == 0 && active) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 4; ++i) {
+          const int rr = 4 * g + i;
+          const int q = qb * 16 + rr;
+          float M = -INFINITY;
+          for (int pp = 0; pp < tsplit; ++pp) M = fmaxf(M, cm[(wave + pp) * 16 + rr]);
+          float lsum = 0.f;
+          float wgt[4];
 #pragma unroll
-      for (int cb = 0; cb < D / 16; ++cb)
-        cO[(wave * 16 + 4 * g + i) * D + cb * 16 + col] = O[cb][i];
-    }
-    if (g == 0) {
-      cm[wave * 16 + col] = m_run;
-      cl[wave * 16 + col] = l_run;
-    }
-    __syncthreads();
-    if (part == 0) {
-      float* po = a.part + ((long)u * a.NS + sp) * a.B * D;
-      float* ps = a.pstat + ((long)u * a.NS + sp) * 2 * a.B;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int rr = 4 * g + i;
-        const int q = qb * 16 + rr;
-        float M = -INFINITY;
-        for (int pp = 0; pp < tsplit; ++pp) M = fmaxf(M, cm[(wave + pp) * 16 + rr]);
-        float lsum = 0.f;
-        float wgt[4];
-        for (int pp = 0; pp < 4; ++pp) {
-          const float mp = pp < tsplit ? cm[(wave + pp) * 16 + rr] : -INFINITY;
-          wgt[pp] = mp > -INFINITY ? __expf(mp - M) : 0.f;
-          if (pp < tsplit) lsum += wgt[pp] * cl[(wave + pp) * 16 + rr];
-        }
-        if (q < a.B) {
-#pragma unroll
-          for (int cb = 0; cb < D / 16; ++cb) {
-            float o = 0.f;
-            for (int pp = 0; pp < tsplit; ++pp)
-              o += wgt[pp] * cO[((wave + pp) * 16 + rr) * D + cb * 16 + col];
-            po[(long)q * D + cb * 16 + col] = o;
+          for (int pp = 0; pp < 4; ++pp) {
+            const float mp = pp < tsplit ? cm[(wave + pp) * 16 + rr] : -INFINITY;
+            wgt[pp] = mp > -INFINITY ? __expf(mp - M) : 0.f;
+            if (pp < tsplit) lsum += wgt[pp] * cl[(wave + pp) * 16 + rr];
           }
-          if (col == 0) {
-            ps[q] = M;
-            ps[a.B + q] = lsum;
+          if (q < a.B) {
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb) {
+              float o = 0.f;
+              for (int pp = 0; pp < tsplit; ++pp)
+                o += wgt[pp] * cO[((wave + pp) * 16 + rr) * D + cb * 16 + col];
+              po_base[(long)q * D + cb * 16 + col] = o;
+            }
+            if (col == 0) {
+              ps_base[q] = M;
+              ps_base[a.B + q] = lsum;
+            }
           }
         }
       }
@@ -327,11 +395,18 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a) {
 
 AttnPlan plan_attn(const wf_params& p, long nrows) {
   AttnPlan a;
-  a.splits = (int)((nrows + kAttnChunk - 1) / kAttnChunk);
+  const long U = (long)p.batch * p.heads;
+  const long chunks = std::max(1L, (nrows + kAttnChunk - 1) / kAttnChunk);
+  // about 512 workgroups: splits of whole chunks; every split is non-empty
+  const long want = std::max(1L, (512 + U - 1) / U);
+  const long splits = std::min(chunks, want);
+  const long cps = (chunks + splits - 1) / splits;
+  a.rps = (int)(cps * kAttnChunk);
+  a.splits = (int)((nrows + a.rps - 1) / a.rps);
   const int D = p.head_dim;
   size_t stage;
   if (p.dtype == WF_BF16)
-    stage = (size_t)kAttnChunk * (D + 8) * 2 + (size_t)D * (kAttnChunk + 8) * 2;
+    stage = (size_t)kAttnChunk * (D + 8) * 2 + (size_t)(kAttnChunk / 2) * (D + 4) * 4;
   else
     stage = (size_t)kAttnChunk * (D + 4) * 4 * 2;
   const size_t comb = (size_t)4 * 16 * D * 4 + (size_t)2 * 4 * 16 * 4;
@@ -374,6 +449,7 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
   a.G = G;
   a.nrows = (int)nrows;
   a.NS = pl.splits;
+  a.rps = pl.rps;
   a.scale = effective_scale(p);
   const bool d128 = p.head_dim == 128;
   if (p.dtype == WF_BF16)

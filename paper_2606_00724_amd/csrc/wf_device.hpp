@@ -260,6 +260,91 @@ __device__ void block_select_topk(const float* score, int n, int k,
   }
 }
 
+// ------------------------------------------------------------ LDS staging
+
+// Rows of D elements moved to LDS in 16-byte vectors, row stride D plus one
+// vector of padding.  Vector v of a chunk is (row v / VPR, column v % VPR);
+// thread t owns vectors t, t + NT, ...  Loads go to registers first (all of a
+// thread's loads in flight together), then to LDS, so a chunk can be
+// prefetched while the previous one is consumed.
+template <typename T, int D, int ROWS, int NT>
+struct RowStager {
+  static constexpr int EPV = 16 / sizeof(T);
+  static constexpr int VPR = D / EPV;
+  static constexpr int STRIDE = D + EPV;
+  static constexpr int PER_THREAD = (ROWS * VPR + NT - 1) / NT;
+  u32x4 buf[PER_THREAD];
+
+  // src(r) -> row pointer, or nullptr for a zero row; r < ROWS
+  template <class Src>
+  __device__ __forceinline__ void load(Src src) {
+    const T* rowp[PER_THREAD];
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int v = i * NT + threadIdx.x;
+      rowp[i] = v < ROWS * VPR ? src(v / VPR) : nullptr;
+    }
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int v = i * NT + threadIdx.x;
+      buf[i] = rowp[i] ? *reinterpret_cast<const u32x4*>(rowp[i] + (v % VPR) * EPV)
+                       : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+
+  __device__ __forceinline__ void store(T* dst) const {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int v = i * NT + threadIdx.x;
+      if (v < ROWS * VPR)
+        *reinterpret_cast<u32x4*>(dst + (v / VPR) * STRIDE + (v % VPR) * EPV) = buf[i];
+    }
+  }
+
+  // bf16 only: store transposed, dst[c * TSTRIDE + r] = row r, channel c
+  template <int TSTRIDE>
+  __device__ __forceinline__ void store_transposed(uint16_t* dst) const {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int v = i * NT + threadIdx.x;
+      if (v < ROWS * VPR) {
+        const int r = v / VPR, c0 = (v % VPR) * 8;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          dst[(c0 + 2 * e) * TSTRIDE + r] = (uint16_t)(buf[i][e] & 0xffffu);
+          dst[(c0 + 2 * e + 1) * TSTRIDE + r] = (uint16_t)(buf[i][e] >> 16);
+        }
+      }
+    }
+  }
+};
+
+// Copies `rows` (runtime, any count) rows to LDS, 8 loads in flight per
+// thread; src(r) -> row pointer.
+template <typename T, int D, int NT, class Src>
+__device__ __forceinline__ void stage_rows_any(T* dst, int rows, Src src) {
+  constexpr int EPV = 16 / sizeof(T);
+  constexpr int VPR = D / EPV;
+  constexpr int STRIDE = D + EPV;
+  constexpr int BATCH = 8;
+  const int total = rows * VPR;
+  for (int base = 0; base < total; base += BATCH * NT) {
+    u32x4 buf[BATCH];
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      const int v = base + i * NT + threadIdx.x;
+      buf[i] = v < total ? *reinterpret_cast<const u32x4*>(src(v / VPR) + (v % VPR) * EPV)
+                         : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      const int v = base + i * NT + threadIdx.x;
+      if (v < total)
+        *reinterpret_cast<u32x4*>(dst + (v / VPR) * STRIDE + (v % VPR) * EPV) = buf[i];
+    }
+  }
+}
+
 // ------------------------------------------------------------ launch shape
 
 // Maps the hardware workgroup id to a logical id so that consecutive logical

@@ -54,6 +54,7 @@ struct ScanArgs {
   float* stats;         // [U][C][2][B]
   float* wpool;         // [U][P]  (weights mode)
   int U, L, B, J, S, P, C;
+  int span;             // pool positions per workgroup (multiple of the chunk)
   float scale;
 };
 
@@ -86,6 +87,7 @@ struct AttnArgs {
   float* pstat;         // [U][NS][2][B] partial row max, row sum
   void* O;              // [U][B][D]
   int U, L, B, nsel, G, nrows, NS;
+  int rps;              // cache rows per split (multiple of the chunk)
   float scale;
 };
 

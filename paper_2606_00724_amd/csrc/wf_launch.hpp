@@ -29,12 +29,14 @@ struct SkimPlan {
 };
 
 struct ScanPlan {
-  int chunks;        // pool chunks per unit
+  int chunks;        // workgroups per unit
+  int span;          // pool positions per workgroup
   size_t lds_bytes;  // dynamic LDS of the chunk kernels
 };
 
 struct AttnPlan {
-  int splits;        // cache-row chunks per unit
+  int splits;        // workgroups (row splits) per unit
+  int rps;           // cache rows per split
   size_t lds_bytes;
 };
 

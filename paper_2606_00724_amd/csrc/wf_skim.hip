@@ -455,38 +455,47 @@ __global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
 
 // One workgroup per unit: merge the tiles' row statistics, form W (eq. 8) and
 // select the top-S regions (eq. 9).
-__global__ __launch_bounds__(kBlock) void skim_select_kernel(SkimSelectArgs a,
-                                                             int w_in_lds) {
+constexpr int kSelectBlock = 1024;
+
+__global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArgs a,
+                                                                   int w_in_lds) {
   __shared__ float row_max[WF_MAX_Q_LEN];
   __shared__ float row_inv[WF_MAX_Q_LEN];
-  __shared__ SelectShared<kBlock> sh;
+  __shared__ SelectShared<kSelectBlock> sh;
   extern __shared__ float wsh[];
   const int u = blockIdx.x;
   const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
-  for (int q = threadIdx.x; q < a.B; q += kBlock) {
+  for (int q = threadIdx.x; q < a.B; q += kSelectBlock) {
     float mx = -INFINITY;
     for (int t = 0; t < a.ntiles; ++t) mx = fmaxf(mx, st[(long)t * 2 * a.B + q]);
     float z = 0.f;
     for (int t = 0; t < a.ntiles; ++t)
-      z += st[(long)t * 2 * a.B + a.B + q] *
-           __expf(st[(long)t * 2 * a.B + q] - mx);
+      z += st[(long)t * 2 * a.B + a.B + q] * __expf(st[(long)t * 2 * a.B + q] - mx);
     row_max[q] = mx;
     row_inv[q] = 1.f / z;
   }
   __syncthreads();
   const float* lg = a.logits + (long)u * a.B * a.nJ;
   float* W = a.W + (long)u * a.nJ;
-  for (int j = threadIdx.x; j < a.nJ; j += kBlock) {
+  constexpr int RB = 8;  // rows in flight per thread
+  for (int j = threadIdx.x; j < a.nJ; j += kSelectBlock) {
     float w = 0.f;
-    for (int q = 0; q < a.B; ++q)
-      w += __expf(lg[(long)q * a.nJ + j] - row_max[q]) * row_inv[q];
+    for (int q0 = 0; q0 < a.B; q0 += RB) {
+      float v[RB];
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+        v[i] = q0 + i < a.B ? lg[(long)(q0 + i) * a.nJ + j] : 0.f;
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+        if (q0 + i < a.B) w += __expf(v[i] - row_max[q0 + i]) * row_inv[q0 + i];
+    }
     W[j] = w;
     if (w_in_lds) wsh[j] = w;
   }
   __syncthreads();
   const float* src = w_in_lds ? wsh : W;
-  block_select_topk<kBlock>(src, a.nJ, a.S, a.seg + (long)u * a.S,
-                            [](int i) { return (int32_t)i; }, sh);
+  block_select_topk<kSelectBlock>(src, a.nJ, a.S, a.seg + (long)u * a.S,
+                                  [](int i) { return (int32_t)i; }, sh);
 }
 
 // ------------------------------------------------------------ host side
@@ -663,7 +672,7 @@ hipError_t launch_skim_select(const wf_params& p, int ntiles,
   a.S = p.segments;
   const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
   const size_t lds = in_lds ? (size_t)a.nJ * sizeof(float) : 0;
-  hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kBlock),
+  hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kSelectBlock),
                      lds, s, a, in_lds);
   return hipGetLastError();
 }
