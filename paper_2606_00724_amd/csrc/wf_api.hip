@@ -87,6 +87,8 @@ static wf_status check_params(const wf_params* p) {
   if (p->budget < 1) return fail(WF_ERR_INVALID_ARG, "budget %d < 1", p->budget);
   if (!std::isfinite(p->scale))
     return fail(WF_ERR_INVALID_ARG, "scale is not finite");
+  if (p->dtype == WF_BF16 && plan_scan(*p).nbuf < 2)
+    return fail(WF_ERR_UNSUPPORTED, "query block and pool range do not fit the LDS ring");
   if ((long)p->batch * p->heads * ((long)p->budget < ((long)p->segments << p->levels)
                                         ? (long)p->budget
                                         : ((long)p->segments << p->levels)) +

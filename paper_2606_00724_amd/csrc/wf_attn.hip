@@ -341,6 +341,249 @@ __global__ __launch_bounds__(kBlock) void attn_kernel(AttnArgs a) {
   }
 }
 
+// ------------------------------------------------------------ bf16 ring path
+//
+// Chunks of kRingRows cache rows (K and V) stream into an LDS ring through
+// direct global->LDS loads; rows stay in their natural row-major form with
+// swizzled 16-byte granules.  The PV B operand (8 consecutive rows of one
+// channel per lane) comes from two ds_read_b64_tr_b16: in each 16-lane group,
+// lane i points at row t0 + i/4, channels c0 + 4(i%4) .. +3, and receives
+// rows t0 .. t0+3 of channel c0 + i.
+constexpr int kRingRows = 64;
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+template <int D>
+struct RingRowPtr {
+  const bf16_t* base;
+  const bf16_t* tail;
+  const int32_t* toks;  // LDS: token ids of the split's selected rows, or null
+  long unit_rows;       // rows per unit in `base`
+  long r0, rlast;       // absolute first row of the chunk, last valid row
+  long split_r0;        // first row of the split (toks[0])
+  int u, nsel, G;
+  __device__ __forceinline__ const bf16_t* operator()(int r) const {
+    const long rr = min(r0 + r, rlast);
+    if (toks) {
+      if (rr < nsel) return base + ((long)u * unit_rows + toks[rr - split_r0]) * D;
+      return tail + ((long)u * G + (rr - nsel)) * D;
+    }
+    return base + ((long)u * unit_rows + rr) * D;
+  }
+};
+
+template <int D>
+__global__ __launch_bounds__(kBlock) void attn_ring_kernel(AttnArgs a) {
+  constexpr int NW = kBlock / kWave;
+  constexpr int CR = kRingRows;
+  constexpr int G = D / 8;
+  constexpr int CHB = CR * 2 * D;            // bytes of one K (or V) chunk
+  constexpr int IPW = CR * G / (64 * NW);    // loads per wave per matrix
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ring = smem;                                       // [nbuf][K, V]
+  int32_t* toks = reinterpret_cast<int32_t*>(smem + (size_t)a.nbuf * 2 * CHB);
+
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / a.NS, sp = item % a.NS;
+  const long rb0 = (long)sp * a.rps;
+  const long re0 = min(rb0 + (long)a.rps, (long)a.nrows);
+  const int nch = (int)((re0 - rb0 + CR - 1) / CR);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, col = lane & 15;
+
+  if (a.tok) {
+    const long hi = min(re0, (long)a.nsel);
+    for (long i = rb0 + threadIdx.x; i < hi; i += kBlock)
+      toks[i - rb0] = a.tok[(long)u * a.nsel + i];
+  }
+  __syncthreads();
+
+  RingRowPtr<D> kp, vp;
+  kp.base = reinterpret_cast<const bf16_t*>(a.K);
+  vp.base = reinterpret_cast<const bf16_t*>(a.V);
+  kp.tail = reinterpret_cast<const bf16_t*>(a.Kg);
+  vp.tail = reinterpret_cast<const bf16_t*>(a.Vg);
+  kp.toks = vp.toks = a.tok ? toks : nullptr;
+  kp.unit_rows = vp.unit_rows = a.tok ? (long)a.L : (long)a.nrows;
+  kp.rlast = vp.rlast = re0 - 1;
+  kp.split_r0 = vp.split_r0 = rb0;
+  kp.u = vp.u = u;
+  kp.nsel = vp.nsel = a.nsel;
+  kp.G = vp.G = a.G;
+
+  const int nqb = (a.B + 15) / 16;
+  const int tsplit = nqb <= 2 ? 2 : 1;       // row halves per query block
+  const int qpg = NW / tsplit;
+  const int ngroups = (nqb + qpg - 1) / qpg;
+  const int part = wave % tsplit;
+  const int R = CR / tsplit;
+  const bf16_t* Qunit = reinterpret_cast<const bf16_t*>(a.Q) + (long)u * a.B * D;
+  float* po_base = a.part + ((long)u * a.NS + sp) * a.B * D;
+  float* ps_base = a.pstat + ((long)u * a.NS + sp) * 2 * a.B;
+  const uint32_t ring_lds = lds_offset(ring);
+  const int nbuf = a.nbuf;
+
+  for (int grp = 0; grp < ngroups; ++grp) {
+    const int qb = grp * qpg + wave / tsplit;
+    const bool active = qb < nqb;
+    const bf16_t* qrow = Qunit + (long)min(qb * 16 + col, a.B - 1) * D;
+    u32x4 qreg[D / 32];
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s)
+      qreg[s] = *reinterpret_cast<const u32x4*>(qrow + 32 * s + 8 * g);
+    f32x4 O[D / 16];
+#pragma unroll
+    for (int cb = 0; cb < D / 16; ++cb) O[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+    // consume the q operand before async loads are queued, so that the
+    // compiler's own wait for it sits here and not inside the loop below
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s) asm volatile("" ::"v"(qreg[s]));
+    // ring of nbuf slots, nbuf - 1 chunks in flight ahead of the one consumed
+    for (int k = 0; k < nch && k < nbuf - 1; ++k) {
+      kp.r0 = vp.r0 = rb0 + (long)k * CR;
+      issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(k * 2 * CHB), kp);
+      issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(k * 2 * CHB + CHB), vp);
+    }
+    for (int ch = 0; ch < nch; ++ch) {
+      const int nr = (int)min((long)CR, re0 - (rb0 + (long)ch * CR));
+      wait_vmcnt_chunks<2 * IPW>(min(nch - 1 - ch, nbuf - 2));
+      lds_barrier();  // chunk ch visible; everyone is past chunk ch - 1
+      if (ch + nbuf - 1 < nch) {
+        kp.r0 = vp.r0 = rb0 + (long)(ch + nbuf - 1) * CR;
+        const uint32_t slot = ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * 2 * CHB);
+        issue_chunk<CR, G, NW>(slot, kp);
+        issue_chunk<CR, G, NW>(slot + CHB, vp);
+      }
+      const unsigned char* Kb = ring + (ch % nbuf) * 2 * CHB;
+      const unsigned char* Vb = Kb + CHB;
+      if (active) {
+        const int rb = part * R;
+        const int re = min(rb + R, nr);
+        for (int sb = rb; sb < re; sb += 32) {
+          const int rx = sb + 8 * (col >> 2) + (col & 3);
+          f32x4 ax = {0.f, 0.f, 0.f, 0.f}, ay = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < D / 32; ++s) {
+            const u32x4 kx = *reinterpret_cast<const u32x4*>(Kb + granule_offset<G>(rx, 4 * s + g));
+            const u32x4 ky = *reinterpret_cast<const u32x4*>(Kb + granule_offset<G>(rx + 4, 4 * s + g));
+            ax = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, kx), __builtin_bit_cast(bf16x8, qreg[s]), ax, 0, 0, 0);
+            ay = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, ky), __builtin_bit_cast(bf16x8, qreg[s]), ay, 0, 0, 0);
+          }
+          // lane holds scores of rows sb + 8g + e (e < 8) for query col
+          float sv[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            sv[i] = (sb + 8 * g + i < re) ? ax[i] * a.scale : -INFINITY;
+            sv[4 + i] = (sb + 8 * g + 4 + i < re) ? ay[i] * a.scale : -INFINITY;
+          }
+          float mb = sv[0];
+#pragma unroll
+          for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
+          mb = fmaxf(mb, __shfl_xor(mb, 16));
+          mb = fmaxf(mb, __shfl_xor(mb, 32));
+          const float m_new = fmaxf(m_run, mb);
+          const float alpha = __expf(m_run - m_new);
+          float pv[8], ps = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            pv[e] = sv[e] > -INFINITY ? __expf(sv[e] - m_new) : 0.f;
+            ps += pv[e];
+          }
+          ps += __shfl_xor(ps, 16);
+          ps += __shfl_xor(ps, 32);
+          l_run = l_run * alpha + ps;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float ai = __shfl(alpha, 4 * g + i);
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
+          }
+          const u32x4 pp = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                            pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
+          const int t0 = sb + 8 * g + (col >> 2);
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) {
+            const int gran = 2 * cb + ((col & 3) >> 1);
+            const int byte = 8 * (col & 1);
+            const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4i16*)(size_t)(lds_offset(Vb + granule_offset<G>(t0, gran) + byte)));
+            const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4i16*)(size_t)(lds_offset(Vb + granule_offset<G>(t0 + 4, gran) + byte)));
+            const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
+            const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
+            const u32x4 vb = {l2[0], l2[1], h2[0], h2[1]};
+            O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, pp), __builtin_bit_cast(bf16x8, vb), O[cb], 0, 0, 0);
+          }
+          m_run = m_new;
+        }
+      }
+    }
+    lds_barrier();  // the ring is idle before it is refilled or reused
+
+    if (tsplit == 1) {
+      if (active) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int q = qb * 16 + 4 * g + i;
+          if (q < a.B) {
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb) po_base[(long)q * D + cb * 16 + col] = O[cb][i];
+          }
+        }
+        const int q = qb * 16 + col;
+        if (g == 0 && q < a.B) {
+          ps_base[q] = m_run;
+          ps_base[a.B + q] = l_run;
+        }
+      }
+    } else {
+      // one group; the two waves of a query block merge their row halves
+      // (the ring is idle: every wave passed the barrier after the loop)
+      float* cO = reinterpret_cast<float*>(smem);  // [NW][16][D]
+      float* cm = cO + NW * 16 * D;                 // [NW][16]
+      float* cl = cm + NW * 16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int cb = 0; cb < D / 16; ++cb)
+          cO[(wave * 16 + 4 * g + i) * D + cb * 16 + col] = O[cb][i];
+      }
+      if (g == 0) {
+        cm[wave * 16 + col] = m_run;
+        cl[wave * 16 + col] = l_run;
+      }
+      lds_barrier();
+      if (part == 0 && active) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int rr = 4 * g + i;
+          const int q = qb * 16 + rr;
+          const float m0 = cm[wave * 16 + rr], m1 = cm[(wave + 1) * 16 + rr];
+          const float M = fmaxf(m0, m1);
+          const float w0 = m0 > -INFINITY ? __expf(m0 - M) : 0.f;
+          const float w1 = m1 > -INFINITY ? __expf(m1 - M) : 0.f;
+          const float lsum = w0 * cl[wave * 16 + rr] + w1 * cl[(wave + 1) * 16 + rr];
+          if (q < a.B) {
+#pragma unroll
+            for (int cb = 0; cb < D / 16; ++cb)
+              po_base[(long)q * D + cb * 16 + col] =
+                  w0 * cO[(wave * 16 + rr) * D + cb * 16 + col] +
+                  w1 * cO[((wave + 1) * 16 + rr) * D + cb * 16 + col];
+            if (col == 0) {
+              ps_base[q] = M;
+              ps_base[a.B + q] = lsum;
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, int D) {
   const int u = blockIdx.x / a.B, q = blockIdx.x % a.B;
@@ -394,8 +637,27 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a) {
 // ------------------------------------------------------------ host side
 
 AttnPlan plan_attn(const wf_params& p, long nrows) {
-  AttnPlan a;
+  AttnPlan a{};
   const long U = (long)p.batch * p.heads;
+  const int D = p.head_dim;
+  if (p.dtype == WF_BF16) {
+    // one workgroup per CU streaming its rows through the LDS ring
+    const long chunks = std::max(1L, (nrows + kRingRows - 1) / kRingRows);
+    const long want = std::max(1L, (long)(device_cu_count() + U - 1) / U);
+    long splits = std::min(chunks, want);
+    splits = std::max(splits, (nrows + 4095) / 4096);  // at most 4096 rows each
+    const long cps = (chunks + splits - 1) / splits;
+    a.rps = (int)(cps * kRingRows);
+    a.splits = (int)((nrows + a.rps - 1) / a.rps);
+    const size_t stage = (size_t)2 * kRingRows * 2 * D;      // K + V chunk
+    const size_t toks = (size_t)a.rps * sizeof(int32_t);
+    const size_t budget = 160 * 1024 - 1024;
+    a.nbuf = (int)std::min<size_t>(4, (budget - toks) / stage);
+    if (a.nbuf < 2) a.nbuf = 0;  // rejected by the caller
+    const size_t comb = (size_t)4 * 16 * D * 4 + (size_t)2 * 4 * 16 * 4;
+    a.lds_bytes = std::max((size_t)a.nbuf * stage, comb) + toks;
+    return a;
+  }
   const long chunks = std::max(1L, (nrows + kAttnChunk - 1) / kAttnChunk);
   // about 512 workgroups: splits of whole chunks; every split is non-empty
   const long want = std::max(1L, (512 + U - 1) / U);
@@ -403,12 +665,7 @@ AttnPlan plan_attn(const wf_params& p, long nrows) {
   const long cps = (chunks + splits - 1) / splits;
   a.rps = (int)(cps * kAttnChunk);
   a.splits = (int)((nrows + a.rps - 1) / a.rps);
-  const int D = p.head_dim;
-  size_t stage;
-  if (p.dtype == WF_BF16)
-    stage = (size_t)kAttnChunk * (D + 8) * 2 + (size_t)(kAttnChunk / 2) * (D + 4) * 4;
-  else
-    stage = (size_t)kAttnChunk * (D + 4) * 4 * 2;
+  const size_t stage = (size_t)kAttnChunk * (D + 4) * 4 * 2;
   const size_t comb = (size_t)4 * 16 * D * 4 + (size_t)2 * 4 * 16 * 4;
   a.lds_bytes = std::max(stage, comb);
   return a;
@@ -416,7 +673,10 @@ AttnPlan plan_attn(const wf_params& p, long nrows) {
 
 template <typename T, int D>
 static hipError_t attn_launch(const AttnArgs& a, size_t lds, hipStream_t s) {
-  auto kern = attn_kernel<T, D>;
+  auto kern = [] {
+    if constexpr (sizeof(T) == 2) return attn_ring_kernel<D>;
+    else return attn_kernel<T, D>;
+  }();
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -450,6 +710,7 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
   a.nrows = (int)nrows;
   a.NS = pl.splits;
   a.rps = pl.rps;
+  a.nbuf = pl.nbuf;
   a.scale = effective_scale(p);
   const bool d128 = p.head_dim == 128;
   if (p.dtype == WF_BF16)

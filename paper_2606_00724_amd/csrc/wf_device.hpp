@@ -345,6 +345,89 @@ __device__ __forceinline__ void stage_rows_any(T* dst, int rows, Src src) {
   }
 }
 
+// ------------------------------------------------------------ async LDS fill
+//
+// gfx950 loads 16 bytes per lane straight from global memory into LDS
+// (global_load_lds_dwordx4): lane l's bytes land at M0 + 16 l.  The load is
+// issued through inline asm so that the compiler does not drain every
+// outstanding load before each LDS read; the code waits explicitly with
+// wait_vmcnt_chunks(), which is exact because vector-memory operations
+// complete in issue order.  Between issue and wait a wave issues no other
+// vector-memory operation.
+
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// M0 is saved and restored inside the statement: the compiler may keep a
+// value of its own there.
+__device__ __forceinline__ void async_load16(const void* g, uint32_t lds_byte) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(lds_byte)
+      : "memory");
+}
+
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS
+// operations, not for outstanding global loads.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Wait until at most k * IPW vector-memory operations of this wave are
+// outstanding (k = chunks allowed to remain in flight, 0..3).
+template <int IPW>
+__device__ __forceinline__ void wait_vmcnt_chunks(int k) {
+  static_assert(3 * IPW <= 63, "vmcnt field is 6 bits");
+  switch (k) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(IPW) : "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * IPW) : "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * IPW) : "memory"); break;
+  }
+}
+
+// Rows of G 16-byte granules stored unpadded in LDS; granule k of row r
+// lives in slot k ^ swz(r).  For the access patterns below (16 rows at one
+// granule; rows 8(m/4)+m%4 of a 32-row block) the slots, hence the banks,
+// differ across the 16 lanes that share a lane group.
+template <int G>
+__device__ __forceinline__ int granule_swz(int r) {
+  if constexpr (G >= 16) return (r & 15) ^ (((r >> 4) & 1) << 2);
+  return ((r >> 1) & 7) ^ (((r >> 4) & 1) << 1);
+}
+
+template <int G>
+__device__ __forceinline__ int granule_offset(int r, int k) {
+  return r * (16 * G) + 16 * (k ^ granule_swz<G>(r));
+}
+
+// Queues one chunk of CR rows (G granules each) into LDS at lds_base:
+// instruction i of wave w fills bytes [1024 (w IPW + i), +1024), i.e. rows
+// (w IPW + i) 64/G .. +64/G.  rowptr(r) returns a valid global row address
+// for every r < CR (callers clamp rows past their range).
+template <int CR, int G, int NW, class RowPtr>
+__device__ __forceinline__ void issue_chunk(uint32_t lds_base, const RowPtr& rowptr) {
+  constexpr int RPI = 64 / G;
+  constexpr int IPW = CR * G / (64 * NW);
+  static_assert(IPW * 64 * NW == CR * G, "chunk must fill whole instructions");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int inst = wave * IPW + i;
+    const int r = inst * RPI + lane / G;
+    const int k = (lane % G) ^ granule_swz<G>(r);
+    const unsigned char* g = reinterpret_cast<const unsigned char*>(rowptr(r)) + 16 * k;
+    async_load16(g, __builtin_amdgcn_readfirstlane(lds_base + 1024u * inst));
+  }
+}
+
 // ------------------------------------------------------------ launch shape
 
 // Maps the hardware workgroup id to a logical id so that consecutive logical

@@ -55,6 +55,8 @@ struct ScanArgs {
   float* wpool;         // [U][P]  (weights mode)
   int U, L, B, J, S, P, C;
   int span;             // pool positions per workgroup (multiple of the chunk)
+  int nbuf;             // LDS ring depth (bf16 path)
+  int seg_cap;          // region ids staged per workgroup (bf16 path)
   float scale;
 };
 
@@ -88,6 +90,7 @@ struct AttnArgs {
   void* O;              // [U][B][D]
   int U, L, B, nsel, G, nrows, NS;
   int rps;              // cache rows per split (multiple of the chunk)
+  int nbuf;             // LDS ring depth (bf16 path)
   float scale;
 };
 

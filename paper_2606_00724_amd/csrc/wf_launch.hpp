@@ -31,12 +31,15 @@ struct SkimPlan {
 struct ScanPlan {
   int chunks;        // workgroups per unit
   int span;          // pool positions per workgroup
+  int nbuf;          // LDS ring depth (bf16)
+  int seg_cap;       // region ids staged per workgroup (bf16)
   size_t lds_bytes;  // dynamic LDS of the chunk kernels
 };
 
 struct AttnPlan {
   int splits;        // workgroups (row splits) per unit
   int rps;           // cache rows per split
+  int nbuf;          // LDS ring depth (bf16)
   size_t lds_bytes;
 };
 

@@ -200,6 +200,203 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
   }
 }
 
+// bf16 pool rows through an LDS ring filled by direct global->LDS loads.
+// Row r of the chunk at p0 is pool position min(p0 + r, plast) (rows past
+// the range repeat the last valid row and are masked).
+template <int D>
+struct PoolRowPtr {
+  const bf16_t* Kunit;
+  const int32_t* segs;  // LDS: region ids from s_lo on
+  long p0, plast;
+  int J, mask, s_lo;
+  __device__ __forceinline__ const bf16_t* operator()(int r) const {
+    const long p = min(p0 + r, plast);
+    const long sg = segs[(int)(p >> J) - s_lo];
+    return Kunit + ((sg << J) | (p & mask)) * D;
+  }
+};
+
+// Online (max, sum of exp) update of a running pair with one new value set.
+__device__ __forceinline__ void stat_merge(float& m, float& z, float m2, float z2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;
+  z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
+  m = mn;
+}
+
+template <int WEIGHTS, int D>
+__global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
+  constexpr int NW = kBlock / kWave;
+  constexpr int CR = kScanChunk;
+  constexpr int G = D / 8;             // 16-byte granules per row
+  constexpr int CHB = CR * 2 * D;      // bytes per chunk buffer
+  constexpr int IPW = CR * G / (64 * NW);
+  constexpr int QSTR = D + 8;
+  constexpr int TBW = CR / 16 / NW;    // token blocks per wave
+  constexpr int QPG = 4;               // query blocks held in registers
+  constexpr int S32 = D / 32;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ring = smem;                                            // [nbuf][CHB]
+  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem + (size_t)a.nbuf * CHB);  // [B][QSTR]
+  int32_t* segs = reinterpret_cast<int32_t*>(Qs + (size_t)a.B * QSTR);  // [seg_cap]
+  float* red = reinterpret_cast<float*>(segs + a.seg_cap);
+  const int nqb = (a.B + 15) / 16;
+  float* part = red;                   // [nqb][NW][16][2]
+  float* rowa = red + nqb * NW * 32;   // weights: M_q
+  float* rowb = rowa + a.B;            // weights: 1/Z_q
+  float* wsum = rowb + a.B;            // weights: W' of the range
+
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / a.C, c = item % a.C;
+  const long pb = (long)c * a.span;
+  const long pe = min(pb + (long)a.span, (long)a.P);
+  const int nch = (int)((pe - pb + CR - 1) / CR);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, col = lane & 15;
+
+  const int s_lo = (int)(pb >> a.J);
+  const int ns = (int)((pe - 1) >> a.J) - s_lo + 1;
+  for (int i = threadIdx.x; i < ns; i += kBlock) segs[i] = a.seg[(long)u * a.S + s_lo + i];
+  const bf16_t* Qunit = reinterpret_cast<const bf16_t*>(a.Q) + (long)u * a.B * D;
+  stage_rows_any<bf16_t, D, kBlock>(Qs, a.B, [&](int r) { return Qunit + (long)r * D; });
+  if constexpr (WEIGHTS) {
+    const float* stt = a.stats + (long)u * a.C * 2 * a.B;
+    for (int q = threadIdx.x; q < a.B; q += kBlock) {
+      float mx = -INFINITY, z = 0.f;
+      for (int k = 0; k < a.C; ++k)
+        stat_merge(mx, z, stt[(long)k * 2 * a.B + q], stt[(long)k * 2 * a.B + a.B + q]);
+      rowa[q] = mx;
+      rowb[q] = 1.f / z;
+    }
+  }
+  __syncthreads();  // every regular load above has been consumed
+
+  PoolRowPtr<D> rp;
+  rp.Kunit = reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.L * D;
+  rp.segs = segs;
+  rp.plast = pe - 1;
+  rp.J = a.J;
+  rp.mask = (1 << a.J) - 1;
+  rp.s_lo = s_lo;
+  const uint32_t ring_lds = lds_offset(ring);
+  const int nbuf = a.nbuf;
+
+  for (int qg = 0; qg < nqb; qg += QPG) {
+    // query operands of this group, in registers for the whole range
+    u32x4 qreg[QPG][S32];
+#pragma unroll
+    for (int j = 0; j < QPG; ++j) {
+      const bf16_t* arow = Qs + min((qg + j) * 16 + col, a.B - 1) * QSTR;
+#pragma unroll
+      for (int s = 0; s < S32; ++s)
+        qreg[j][s] = *reinterpret_cast<const u32x4*>(arow + 32 * s + 8 * g);
+    }
+    float sm[QPG][4], sz[QPG][4];  // per-lane running row max / sum of exp
+#pragma unroll
+    for (int j = 0; j < QPG; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sm[j][i] = -INFINITY;
+        sz[j][i] = 0.f;
+      }
+    // ring of nbuf slots, nbuf - 1 chunks in flight ahead of the one consumed
+    for (int k = 0; k < nch && k < nbuf - 1; ++k) {
+      rp.p0 = pb + (long)k * CR;
+      issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(k * CHB), rp);
+    }
+    for (int ch = 0; ch < nch; ++ch) {
+      const long p0 = pb + (long)ch * CR;
+      const int np = (int)min((long)CR, pe - p0);
+      wait_vmcnt_chunks<IPW>(min(nch - 1 - ch, nbuf - 2));
+      lds_barrier();  // chunk ch visible; everyone is past chunk ch - 1
+      if (ch + nbuf - 1 < nch) {
+        rp.p0 = pb + (long)(ch + nbuf - 1) * CR;
+        issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rp);
+      }
+      const unsigned char* buf = ring + (ch % nbuf) * CHB;
+#pragma unroll
+      for (int k = 0; k < TBW; ++k) {
+        const int row = (wave * TBW + k) * 16 + col;
+        const bool ok = row < np;
+        u32x4 bv[S32];
+#pragma unroll
+        for (int s = 0; s < S32; ++s)
+          bv[s] = *reinterpret_cast<const u32x4*>(buf + granule_offset<G>(row, 4 * s + g));
+        float wk = 0.f;
+#pragma unroll
+        for (int j = 0; j < QPG; ++j) {
+          if (qg + j >= nqb) break;
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < S32; ++s)
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, qreg[j][s]), __builtin_bit_cast(bf16x8, bv[s]),
+                acc, 0, 0, 0);
+          // lane holds logit[q = 16 (qg + j) + 4 g + i][p = p0 + row]
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float v = acc[i] * a.scale;
+            if constexpr (!WEIGHTS) {
+              if (ok) {
+                if (v > sm[j][i]) {
+                  sz[j][i] = sz[j][i] * __expf(sm[j][i] - v) + 1.f;
+                  sm[j][i] = v;
+                } else {
+                  sz[j][i] += __expf(v - sm[j][i]);
+                }
+              }
+            } else {
+              const int q = (qg + j) * 16 + 4 * g + i;
+              if (q < a.B) wk += __expf(v - rowa[q]) * rowb[q];
+            }
+          }
+        }
+        if constexpr (WEIGHTS) {
+          wk += __shfl_xor(wk, 16);
+          wk += __shfl_xor(wk, 32);
+          // query groups add up in place: the same lane owns this position
+          // in every group
+          if (g == 0 && ok) wsum[p0 - pb + row] = (qg == 0 ? 0.f : wsum[p0 - pb + row]) + wk;
+        }
+      }
+    }
+    if constexpr (!WEIGHTS) {
+      // merge the 16 lanes of each row, then the waves, through LDS
+#pragma unroll
+      for (int j = 0; j < QPG; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) {
+            const float m2 = __shfl_xor(sm[j][i], o), z2 = __shfl_xor(sz[j][i], o);
+            stat_merge(sm[j][i], sz[j][i], m2, z2);
+          }
+          if (col == 0 && qg + j < nqb) {
+            part[(((qg + j) * NW + wave) * 16 + 4 * g + i) * 2] = sm[j][i];
+            part[(((qg + j) * NW + wave) * 16 + 4 * g + i) * 2 + 1] = sz[j][i];
+          }
+        }
+      }
+    }
+    lds_barrier();  // the ring is idle; `part` / `wsum` complete
+  }
+  if constexpr (!WEIGHTS) {
+    float* stt = a.stats + ((long)u * a.C + c) * 2 * a.B;
+    for (int q = threadIdx.x; q < a.B; q += kBlock) {
+      const int qb = q >> 4, r = q & 15;
+      float mx = -INFINITY, z = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+        stat_merge(mx, z, part[((qb * NW + w) * 16 + r) * 2], part[((qb * NW + w) * 16 + r) * 2 + 1]);
+      stt[q] = mx;
+      stt[a.B + q] = z;
+    }
+  } else {
+    float* dst = a.wpool + (long)u * a.P + pb;
+    for (int i = threadIdx.x; i < (int)(pe - pb); i += kBlock) dst[i] = wsum[i];
+  }
+}
+
 constexpr int kScanSelectBlock = 1024;
 
 __global__ __launch_bounds__(kScanSelectBlock) void scan_select_kernel(
@@ -222,34 +419,63 @@ __global__ __launch_bounds__(kScanSelectBlock) void scan_select_kernel(
 
 // ------------------------------------------------------------ host side
 
+// LDS a workgroup may use (gfx950: 160 KiB per CU), with a little margin.
+constexpr size_t kLdsBudget = 160 * 1024 - 1024;
+
 ScanPlan plan_scan(const wf_params& p) {
-  ScanPlan s;
+  ScanPlan s{};
   const long P = (long)p.segments << p.levels;
   const long U = (long)p.batch * p.heads;
   const long chunks = (P + kScanChunk - 1) / kScanChunk;
-  // about 1024 workgroups; each covers 1..8 chunks of the pool
+  const int nqb = (p.q_len + 15) / 16;
+  const size_t red_base = ((size_t)nqb * 4 * 16 * 2 + (size_t)2 * p.q_len) * sizeof(float);
+  if (p.dtype == WF_BF16) {
+    // one workgroup per CU, each streaming a long range through the ring
+    const long want = std::max(1L, (long)(device_cu_count() + U - 1) / U);
+    long C = std::min(chunks, want);
+    long cpw = (chunks + C - 1) / C;
+    cpw = std::min(cpw, 32L);  // at most 4096 positions per workgroup
+    s.span = (int)(cpw * kScanChunk);
+    s.chunks = (int)((P + s.span - 1) / s.span);
+    s.seg_cap = (s.span >> p.levels) + 2;
+    const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
+    const size_t other = (size_t)p.q_len * (p.head_dim + 8) * 2 +
+                         (size_t)s.seg_cap * 4 + red_base +
+                         (size_t)s.span * sizeof(float);
+    s.nbuf = (int)std::min<size_t>(4, (kLdsBudget - std::min(other, kLdsBudget)) / chb);
+    s.lds_bytes = s.nbuf * chb + other;
+    if (s.nbuf < 2) s.nbuf = 0;  // rejected by the caller
+    return s;
+  }
+  // fp32: register-staged chunks, about 1024 workgroups of 1..8 chunks
   const long cpw = std::max(1L, std::min(8L, U * chunks / 1024));
   s.span = (int)(cpw * kScanChunk);
   s.chunks = (int)((P + s.span - 1) / s.span);
-  const size_t elem = p.dtype == WF_BF16 ? 2 : 4;
-  const size_t stride = (size_t)p.head_dim * elem + 16;
-  const int nqb = (p.q_len + 15) / 16;
-  const size_t red = ((size_t)nqb * 4 * 16 * 2 + (size_t)2 * p.q_len) * sizeof(float);
-  s.lds_bytes = (size_t)(p.q_len + kScanChunk) * stride + red;
+  const size_t stride = (size_t)p.head_dim * 4 + 16;
+  s.lds_bytes = (size_t)(p.q_len + kScanChunk) * stride + red_base;
   return s;
+}
+
+template <class Kernel>
+static hipError_t launch_with_lds(Kernel kern, dim3 grid, size_t lds, hipStream_t s,
+                                  const ScanArgs& a) {
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, grid, dim3(kBlock), lds, s, a);
+  return hipGetLastError();
 }
 
 template <int WEIGHTS, typename T, int D>
 static hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t s) {
-  if (lds > 65536) {
-    hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(scan_chunk_kernel<WEIGHTS, T, D>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL((scan_chunk_kernel<WEIGHTS, T, D>),
-                     dim3((unsigned)(a.U * a.C)), dim3(kBlock), lds, s, a);
-  return hipGetLastError();
+  const dim3 grid((unsigned)(a.U * a.C));
+  if constexpr (sizeof(T) == 2)
+    return launch_with_lds(scan_ring_kernel<WEIGHTS, D>, grid, lds, s, a);
+  else
+    return launch_with_lds(scan_chunk_kernel<WEIGHTS, T, D>, grid, lds, s, a);
 }
 
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
@@ -270,6 +496,8 @@ hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
   a.P = p.segments << p.levels;
   a.C = pl.chunks;
   a.span = pl.span;
+  a.nbuf = pl.nbuf;
+  a.seg_cap = pl.seg_cap;
   a.scale = effective_scale(p);
   const bool bf = p.dtype == WF_BF16, d128 = p.head_dim == 128;
   if (weights) {
