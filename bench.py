@@ -9,9 +9,10 @@ resident in HBM before timing starts.  Prints one JSON line:
 
   value       context tokens filtered+attended per second per layer
               (batch * ctx_len / step time)
-  roofline    the dominant kernel (skim_tile: streams every key once)
-              against MI355X's 8 TB/s HBM peak; durations come from HIP
-              events recorded between the kernels of each timed step
+  roofline    the dominant kernel (the first of the sequence, token_skim
+              or skim_tile: it streams every key once) against MI355X's
+              8 TB/s HBM peak; durations come from HIP events recorded
+              between the kernels of each timed step
   cpu_baseline  the fp64 CPU oracle on the same workload, on this host
 """
 from __future__ import annotations
@@ -46,8 +47,8 @@ def algorithmic_bytes(w, keff: int) -> dict:
         "q_and_o": 2 * w.q_len * d * e,
     }
     per_unit["total"] = sum(per_unit.values())
-    # skim_tile reads every key and the query block once
-    per_unit["skim_tile"] = per_unit["keys"] + w.q_len * d * e
+    # the skim kernel reads every key and the query block once
+    per_unit["skim"] = per_unit["keys"] + w.q_len * d * e
     return per_unit
 
 
@@ -116,9 +117,12 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="headline32k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="before timing, run one plain 1 GiB device-to-device "
+                         "copy (a known-size kernel for scaling HBM counters)")
     ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per skim_tile "
-                         "launch (from rocprofv3 counters)")
+                    help="JSON file with measured HBM bytes per launch of "
+                         "the skim kernel (from rocprofv3 counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; the per-(batch, "
@@ -158,6 +162,12 @@ def main() -> int:
                                   ws, ev.ev[base:base + len(names) + 1],
                                   stream)
 
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
         step_plain()
@@ -200,9 +210,9 @@ def main() -> int:
     U = w.units
     tokens = w.batch * w.ctx_len
     value = tokens / (ms_step * 1e-3)
-    dom = "skim_tile"
+    dom = names[0]
     dom_ms = per_kernel[dom]
-    achieved = alg["skim_tile"] * U / (dom_ms * 1e-3) / 1e9
+    achieved = alg["skim"] * U / (dom_ms * 1e-3) / 1e9
     traffic = None
     if args.traffic and os.path.exists(args.traffic):
         traffic = json.load(open(args.traffic)).get("bytes_per_launch")
@@ -234,7 +244,7 @@ def main() -> int:
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
-            "algorithmic_bytes_per_launch": alg["skim_tile"] * U,
+            "algorithmic_bytes_per_launch": alg["skim"] * U,
             "avg_launch_ms": dom_ms,
         },
         "path_hbm_frac": alg["total"] * U / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,

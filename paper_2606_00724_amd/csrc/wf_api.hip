@@ -125,8 +125,8 @@ static wf_status check_ptr(const void* ptr, const char* name, bool nullable) {
 static size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t logits = 0, sstats = 0, W = 0, seg = 0, cstats = 0, wpool = 0,
-         tok = 0, part = 0, pstat = 0, total = 0;
+  size_t logits = 0, sstats = 0, W = 0, seg = 0, cstats = 0,
+         wpool = 0, tok = 0, part = 0, pstat = 0, total = 0;
 };
 
 static long keff_of(const wf_params& p) {
@@ -134,6 +134,10 @@ static long keff_of(const wf_params& p) {
   return p.budget < pool ? p.budget : pool;
 }
 
+// Regions of the workspace, each 256-byte aligned.  The fused entry point on
+// the token-level path keeps a log-sum-exp per (block, query) beside each
+// coarse logit instead of the scan's per-workgroup statistics, and its
+// cstats region holds the pool's final (max, sum) pair per query.
 static Layout layout_for(const wf_params& p, int op, long attn_rows) {
   Layout l;
   const size_t U = (size_t)p.batch * p.heads, B = p.q_len;
@@ -145,10 +149,15 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     off += up256(bytes);
     return at;
   };
+  const bool fast = op == WF_OP_FUSED && fast_path(p);
   const bool skim = op == WF_OP_SKIM || op == WF_OP_FUSED;
   const bool scan = op == WF_OP_SCAN || op == WF_OP_FUSED;
   const bool attn = op == WF_OP_ATTN || op == WF_OP_FUSED;
-  if (skim) {
+  if (fast) {
+    const FastPlan fp = plan_fast(p);
+    l.logits = take(U * nJ * 2 * B * sizeof(float));  // block rows: logits, log-sum-exps
+    l.sstats = take(U * fp.R * 2 * B * sizeof(float));
+  } else if (skim) {
     const SkimPlan sp = plan_skim(p, op == WF_OP_FUSED);
     l.logits = take(U * B * nJ * sizeof(float));
     l.sstats = take(U * sp.ntiles * 2 * B * sizeof(float));
@@ -159,7 +168,7 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
   }
   if (scan) {
     const ScanPlan cp = plan_scan(p);
-    l.cstats = take(U * cp.chunks * 2 * B * sizeof(float));
+    l.cstats = take(U * (fast ? 1 : cp.chunks) * 2 * B * sizeof(float));
     l.wpool = take(U * P * sizeof(float));
   }
   if (op == WF_OP_FUSED) l.tok = take(U * keff_of(p) * sizeof(int32_t));
@@ -186,10 +195,22 @@ static inline char* at(void* ws, size_t off) { return static_cast<char*>(ws) + o
 
 // ------------------------------------------------------------ fused sequence
 
-static const char* const kFusedNames[] = {
+// Kernel sequences of the fused entry point.  The general path scores the
+// coarse coefficients and runs both passes of the token scan; the token-level
+// path (bf16, Haar, 3..5 levels, <= 64 query rows) derives the scan's
+// normalisers from the skim's block statistics.
+static const char* const kGeneralNames[] = {
     "skim_tile", "skim_select", "scan_stats", "scan_weights",
     "scan_select", "sparse_attn", "attn_combine"};
-constexpr int kFusedKernels = 7;
+static const char* const kFastNames[] = {
+    "token_skim", "skim_select", "scan_weights", "scan_select",
+    "sparse_attn", "attn_combine"};
+constexpr int kMaxFusedKernels = 7;
+
+static int fused_kernels(const wf_params& p) { return fast_path(p) ? 6 : 7; }
+static const char* const* fused_names(const wf_params& p) {
+  return fast_path(p) ? kFastNames : kGeneralNames;
+}
 
 static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
                             const void* V, const void* Kg, const void* Vg,
@@ -207,15 +228,16 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
     WF_TRY(check_ptr(Kg, "Kg", false));
     WF_TRY(check_ptr(Vg, "Vg", false));
   }
-  if (events && n_events < kFusedKernels + 1)
-    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, kFusedKernels + 1);
+  const int nk = fused_kernels(*p);
+  const char* const* names = fused_names(*p);
+  if (events && n_events < nk + 1)
+    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, nk + 1);
   const long keff = keff_of(*p);
   const long nrows = keff + p->gen_len;
   const Layout l = layout_for(*p, WF_OP_FUSED, nrows);
   WF_TRY(check_workspace(ws, ws_bytes, l.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  const SkimPlan sp = plan_skim(*p, true);
   float* logits = reinterpret_cast<float*>(at(ws, l.logits));
   float* sstats = reinterpret_cast<float*>(at(ws, l.sstats));
   float* W = reinterpret_cast<float*>(at(ws, l.W));
@@ -230,30 +252,31 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
     if (!events) return hipSuccess;
     return hipEventRecord(static_cast<hipEvent_t>(events[k]), s);
   };
+  // launch one kernel of the sequence, bracketed by events when timed
+  auto step = [&](hipError_t launched) -> wf_status {
+    if (launched != hipSuccess)
+      return fail(WF_ERR_HIP, "%s: %s", names[k], hipGetErrorString(launched));
+    ++k;
+    hipError_t e = mark();
+    if (e != hipSuccess) return fail(WF_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    return WF_OK;
+  };
   WF_HIP(mark(), "hipEventRecord");
-  WF_HIP(launch_skim_tiles(*p, true, Q, K, nullptr, logits, sstats, s), kFusedNames[k]);
-  ++k;
-  WF_HIP(mark(), "hipEventRecord");
-  WF_HIP(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s), kFusedNames[k]);
-  ++k;
-  WF_HIP(mark(), "hipEventRecord");
-  WF_HIP(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s), kFusedNames[k]);
-  ++k;
-  WF_HIP(mark(), "hipEventRecord");
-  WF_HIP(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s), kFusedNames[k]);
-  ++k;
-  WF_HIP(mark(), "hipEventRecord");
-  WF_HIP(launch_scan_select(*p, wpool, seg, tok, s), kFusedNames[k]);
-  ++k;
-  WF_HIP(mark(), "hipEventRecord");
-  WF_HIP(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
-                     part, pstat, s),
-         kFusedNames[k]);
-  ++k;
-  WF_HIP(mark(), "hipEventRecord");
-  WF_HIP(launch_attn_combine(*p, nrows, part, pstat, O, s), kFusedNames[k]);
-  ++k;
-  WF_HIP(mark(), "hipEventRecord");
+  if (fast_path(*p)) {
+    WF_TRY(step(launch_token_skim(*p, Q, K, logits, sstats, s)));
+    WF_TRY(step(launch_fast_select(*p, logits, sstats, W, seg, cstats, s)));
+    WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s, 1)));
+  } else {
+    const SkimPlan sp = plan_skim(*p, true);
+    WF_TRY(step(launch_skim_tiles(*p, true, Q, K, nullptr, logits, sstats, s)));
+    WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
+    WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
+    WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s)));
+  }
+  WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
+  WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
+                          part, pstat, s)));
+  WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
   return ok();
 }
 
@@ -389,7 +412,7 @@ wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
                                  size_t workspace_bytes, void* stream,
                                  void** events, int32_t n_events) {
   if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
-  for (int i = 0; i < n_events && i <= kFusedKernels; ++i)
+  for (int i = 0; i < n_events && i <= kMaxFusedKernels; ++i)
     if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
   return fused_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
                     workspace_bytes, stream, events, n_events);
@@ -397,12 +420,12 @@ wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
 
 int32_t wf_filter_attend_kernels(const wf_params* p) {
   if (check_params(p) != WF_OK) return -1;
-  return kFusedKernels;
+  return fused_kernels(*p);
 }
 
 const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i) {
-  if (check_params(p) != WF_OK || i < 0 || i >= kFusedKernels) return nullptr;
-  return kFusedNames[i];
+  if (check_params(p) != WF_OK || i < 0 || i >= fused_kernels(*p)) return nullptr;
+  return fused_names(*p)[i];
 }
 
 const char* wf_status_str(wf_status s) {

@@ -1,0 +1,438 @@
+// Token-level skim for bf16 keys with the Haar wavelet at 3..5 levels and a
+// query block of at most 64 rows.
+//
+// The Haar approximation of block j at level J is 2^{-J/2} times the sum of
+// its 2^J keys (eq. 5 with the Haar filter, applied J times), and the skim
+// logit is linear in the key, so the coarse logit of eq. 7 is the scaled sum
+// of the block's token logits:  l_qj = 2^{-J/2} sum_{t in block j} s_qt,
+// s_qt = scale <Q_q, K_t>.  One pass over the keys therefore computes every
+// token logit on bf16 MFMA and reduces it per block to
+//   * the coarse logit l_qj                        (input of eqs. 7-8)
+//   * the block log-sum-exp  e_qj = log sum_{t in block j} exp(s_qt)
+// stored per block as a row of B coarse logits followed by a row of B
+// log-sum-exps ([U][nJ][2][B]).
+// The second gives the softmax normalisers of the token scan over the
+// selected pool (Section 3.2) without a separate pass over the pool:
+//   M_q = max_{j in seg} e_qj,   Z_q = sum_{j in seg} exp(e_qj - M_q),
+// with M_q at or above every pool logit of query q.
+//
+// The keys stream through an LDS ring filled by direct global->LDS loads;
+// see token_skim_kernel for the roles of its waves.
+#include "wf_device.hpp"
+#include "wf_kernels.hpp"
+#include "wf_launch.hpp"
+
+namespace wf {
+
+// one running (max, sum of exp) pair absorbs another
+__device__ __forceinline__ void stat_absorb(float& m, float& z, float m2, float z2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;
+  z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
+  m = mn;
+}
+
+// one value joins a running (max, sum of exp) pair
+__device__ __forceinline__ void stat_add(float& m, float& z, float x) {
+  if (x > m) {
+    z = z * __expf(m - x) + 1.f;
+    m = x;
+  } else {
+    z += __expf(x - m);
+  }
+}
+
+// Workgroup of the token-level skim: 8 waves, wave w scores the 32-token
+// slice w % 4 of every 128-token chunk against query rows 32 (w / 4) + 0..31.
+// Every wave puts its block results into an LDS batch laid out as the
+// global array; waves 0..3 issue every ring load and store nothing to global
+// memory, waves 4..7 issue no loads and copy each finished batch out as one
+// contiguous run.  (Stores count in the same per-wave counter as the ring
+// loads, so a loading wave that also stored would wait for its stores at
+// every ring wait; and few long write runs interleave with the key stream
+// more cheaply than many short ones.)
+constexpr int kTokBlock = 512;
+
+// Lane l of a wave holds, after the 32x32x16 products of its slice, the
+// logits of query 32 (w / 4) + l % 32 with the slice's tokens
+//   8 (v / 4) + 4 (l / 32) + v % 4,   v < 16,
+// so block b (of 2^J tokens, J = 3, 4, 5) of the slice is the lane's values
+// v in [b 2^J / 2, (b + 1) 2^J / 2) together with the same values of lane
+// l ^ 32.  Each lane keeps NST of the slice's 32 / 2^J blocks: block 0 in the
+// lanes l < 32 (J = 5), block l / 32 (J = 4), blocks 2 (l / 32) + n, n < 2
+// (J = 3).
+template <int J>
+struct SliceBlocks {
+  static constexpr int NBLK = 32 >> J;         // blocks per slice
+  static constexpr int VPB = 16 / NBLK;        // lane values per block
+  static constexpr int NST = J == 3 ? 2 : 1;   // blocks kept per lane
+  static constexpr int BPC = 128 >> J;         // blocks per 128-token chunk
+  static constexpr int BATCH = 1 << (J - 2);   // chunks per LDS batch (16 KiB at 64 queries)
+  __device__ static int block(int n, int hi) { return J == 5 ? 0 : J == 4 ? hi : 2 * hi + n; }
+  __device__ static bool keeps(int hi) { return J != 5 || hi == 0; }
+};
+
+// LDS bytes of one token-skim batch slot (block rows of 2 * B floats)
+template <int J>
+constexpr size_t token_batch_bytes(int B) {
+  return (size_t)SliceBlocks<J>::BATCH * SliceBlocks<J>::BPC * 2 * B * sizeof(float);
+}
+
+template <int D, int J>
+__global__ __launch_bounds__(kTokBlock) void token_skim_kernel(TokenSkimArgs a) {
+  constexpr int NW = kTokBlock / kWave;  // 8
+  constexpr int NIW = NW / 2;            // loading waves
+  constexpr int CR = kScanChunk;         // tokens per chunk
+  constexpr int G = D / 8;               // 16-byte granules per key row
+  constexpr int CHB = CR * 2 * D;
+  constexpr int IPW = CR * G / (64 * NIW);
+  constexpr int KS = D / 16;             // k-steps of the 32x32x16 product
+  using SB = SliceBlocks<J>;
+  constexpr int NBLK = SB::NBLK, VPB = SB::VPB, NST = SB::NST, BPC = SB::BPC, BATCH = SB::BATCH;
+  static_assert(J >= 3 && J <= 5, "blocks of 8, 16 or 32 tokens");
+  static_assert(CR == 32 * NIW, "four 32-token slices per chunk");
+  const int B = a.B;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ring = smem;                                            // [nbuf][CHB]
+  float* red = reinterpret_cast<float*>(smem + (size_t)a.nbuf * CHB);  // [NW][32][2]
+  float* batch = red + NW * 64;  // [2][BATCH * BPC][2][B]: coarse logits, then log-sum-exps
+  const int slot_floats = BATCH * BPC * 2 * B;
+
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / a.R, r = item % a.R;
+  const long tb = (long)r * a.span;
+  const long te = min(tb + (long)a.span, (long)a.L);
+  const int nch = (int)((te - tb + CR - 1) / CR);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ts = wave & 3, qt = wave >> 2;
+  const bool loader = qt == 0;
+  const int hi = lane >> 5, col = lane & 31;
+  const int q = 32 * qt + col;
+  const bool live = 32 * qt < B;  // wave-uniform: this query tile has rows
+
+  const bf16_t* qrow = reinterpret_cast<const bf16_t*>(a.Q) + ((long)u * B + min(q, B - 1)) * D;
+  u32x4 qreg[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) qreg[s] = *reinterpret_cast<const u32x4*>(qrow + 16 * s + 8 * hi);
+  // the query operand is consumed here, before any ring load is queued, so
+  // that no wait for it lands inside the ring loop
+#pragma unroll
+  for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qreg[s]));
+
+  struct Rows {
+    const bf16_t* Kunit;
+    long c0, tlast;
+    __device__ __forceinline__ const bf16_t* operator()(int r) const {
+      return Kunit + min(c0 + r, tlast) * D;
+    }
+  } rows{reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.L * D, tb, te - 1};
+  const uint32_t ring_lds = lds_offset(ring);
+  const int nbuf = a.nbuf;
+  if (loader) {
+    for (int k = 0; k < nch && k < nbuf - 1; ++k) {
+      rows.c0 = tb + (long)k * CR;
+      issue_chunk<CR, G, NIW>(ring_lds + (uint32_t)(k * CHB), rows);
+    }
+  }
+
+  float* out = a.blocks + (long)u * a.nJ * 2 * B;  // [nJ][2][B]
+  const long jend = te >> J;                        // blocks of this range end here
+  const float c2 = a.scale * 1.44269504088896341f;  // scale * log2(e)
+  const float cl = a.scale * a.norm;
+  const bool keeps = SB::keeps(hi);
+  const bool vec = (B & 1) == 0;  // block rows are 16-byte multiples
+
+  // waves 4..7: copy batch k (its blocks inside the range) to global memory
+  auto copy_batch = [&](int k) {
+    const long jb0 = (tb >> J) + (long)k * BATCH * BPC;
+    const int nb = (int)min((long)(BATCH * BPC), jend - jb0);
+    const int nf = nb * 2 * B;
+    const float* src = batch + (k & 1) * slot_floats;
+    float* dst = out + jb0 * 2 * B;
+    const int t = (wave - NIW) * 64 + lane;
+    if (vec) {
+      for (int i = t; i < nf / 4; i += NIW * 64)
+        reinterpret_cast<float4*>(dst)[i] = reinterpret_cast<const float4*>(src)[i];
+    } else {
+      for (int i = t; i < nf; i += NIW * 64) dst[i] = src[i];
+    }
+  };
+
+  float cm = -INFINITY, cz = 0.f;  // running max / sum of exp of the kept coarse logits
+  for (int ch = 0; ch < nch; ++ch) {
+    const long c0 = tb + (long)ch * CR;
+    if (loader) wait_vmcnt_chunks<IPW>(min(nch - 1 - ch, nbuf - 2));
+    lds_barrier();
+    if (loader) {
+      if (ch + nbuf - 1 < nch) {
+        rows.c0 = tb + (long)(ch + nbuf - 1) * CR;
+        issue_chunk<CR, G, NIW>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rows);
+      }
+    } else if (ch > 0 && ch % BATCH == 0) {
+      copy_batch(ch / BATCH - 1);
+    }
+    const long slice0 = c0 + 32 * ts;
+    if (!live || slice0 >= te) continue;  // uniform per wave; no barrier follows
+    const unsigned char* buf = ring + (ch % nbuf) * CHB;
+    const int row = 32 * ts + col;
+    f32x16 acc = {};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const u32x4 ka = *reinterpret_cast<const u32x4*>(buf + granule_offset<G>(row, 2 * s + hi));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
+                                                    __builtin_bit_cast(bf16x8, qreg[s]), acc, 0, 0, 0);
+    }
+    // raw block sums and maxima, completed with the partner lane l ^ 32
+    float bs[NBLK], bm[NBLK], be[NBLK];
+#pragma unroll
+    for (int b = 0; b < NBLK; ++b) {
+      bs[b] = 0.f;
+      bm[b] = -INFINITY;
+#pragma unroll
+      for (int v = b * VPB; v < (b + 1) * VPB; ++v) {
+        bs[b] += acc[v];
+        bm[b] = fmaxf(bm[b], acc[v]);
+      }
+      bs[b] += __shfl_xor(bs[b], 32);
+      bm[b] = fmaxf(bm[b], __shfl_xor(bm[b], 32));
+      const float off = -bm[b] * c2;
+      be[b] = 0.f;
+#pragma unroll
+      for (int v = b * VPB; v < (b + 1) * VPB; ++v) be[b] += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, off));
+      be[b] += __shfl_xor(be[b], 32);
+    }
+    float* slot = batch + ((ch / BATCH) & 1) * slot_floats;
+    const int bl0 = (ch % BATCH) * BPC + ((32 * ts) >> J);  // slice's first block in the batch
+#pragma unroll
+    for (int n = 0; n < NST; ++n) {
+      const int b = SB::block(n, hi);
+      // b takes at most two values across the wave: select, do not index
+      float s_ = bs[0], m_ = bm[0], e_ = be[0];
+#pragma unroll
+      for (int k = 1; k < NBLK; ++k)
+        if (b == k) {
+          s_ = bs[k];
+          m_ = bm[k];
+          e_ = be[k];
+        }
+      const float l = s_ * cl;
+      if (keeps && q < B && (slice0 >> J) + b < jend) {
+        stat_add(cm, cz, l);
+        slot[(bl0 + b) * 2 * B + q] = l;
+        slot[((bl0 + b) * 2 + 1) * B + q] = fmaf(m_, a.scale, __logf(e_));
+      }
+    }
+  }
+  __syncthreads();  // the last batch is complete in LDS
+  if (!loader) copy_batch((nch - 1) / BATCH);
+
+  // merge the running coarse statistics: partner lanes, then the four
+  // slices of the query tile
+  {
+    const float m2 = __shfl_xor(cm, 32), z2 = __shfl_xor(cz, 32);
+    stat_absorb(cm, cz, m2, z2);
+  }
+  if (hi == 0) {
+    red[(wave * 32 + col) * 2] = cm;
+    red[(wave * 32 + col) * 2 + 1] = cz;
+  }
+  __syncthreads();
+  float* ws = a.wstats + ((long)u * a.R + r) * 2 * B;
+  for (int qq = threadIdx.x; qq < B; qq += kTokBlock) {
+    const int t = qq >> 5, c = qq & 31;
+    float mx = -INFINITY, z = 0.f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int w = 4 * t + k;
+      stat_absorb(mx, z, red[(w * 32 + c) * 2], red[(w * 32 + c) * 2 + 1]);
+    }
+    ws[qq] = mx;
+    ws[B + qq] = z;
+  }
+}
+
+// One workgroup per unit: the coarse softmax normalisers (merged over the
+// ranges), W (eq. 8), the top-S regions (eq. 9), then the scan's pool
+// normalisers from the selected blocks' token statistics.
+constexpr int kFastSelectBlock = 1024;
+
+__global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelectArgs a,
+                                                                       int w_in_lds) {
+  constexpr int NT = kFastSelectBlock;
+  __shared__ float row_max[16 * kFastMaxQBlocks];
+  __shared__ float row_inv[16 * kFastMaxQBlocks];
+  __shared__ float part_m[NT], part_z[NT];
+  __shared__ SelectShared<NT> sh;
+  extern __shared__ float wsh[];
+  const int u = blockIdx.x;
+  const int B = a.B, nJ = a.nJ;
+  const float* ws = a.wstats + (long)u * a.R * 2 * B;
+  for (int q = threadIdx.x; q < B; q += NT) {
+    float mx = -INFINITY, z = 0.f;
+    for (int r = 0; r < a.R; ++r)
+      stat_absorb(mx, z, ws[(long)r * 2 * B + q], ws[(long)r * 2 * B + B + q]);
+    row_max[q] = mx;
+    row_inv[q] = 1.f / z;
+  }
+  __syncthreads();
+  // W_j = sum_q softmax_j(l_q.): four threads per block j, 16 queries each
+  const float* lg = a.blocks + (long)u * nJ * 2 * B;  // row j: logits at 2 j B
+  float* W = a.W + (long)u * nJ;
+  const bool vec = (B & 3) == 0;
+  for (int base = 0; base < 4 * nJ; base += NT) {
+    const int t = base + threadIdx.x;
+    const int j = t >> 2, q0 = 16 * (t & 3);
+    float w = 0.f;
+    if (t < 4 * nJ && q0 < B) {
+      const float* row = lg + (long)j * 2 * B + q0;
+      const int nq = min(16, B - q0);
+      if (vec) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (4 * k < nq) {
+            const float4 v = *reinterpret_cast<const float4*>(row + 4 * k);
+            const int q = q0 + 4 * k;
+            w += __expf(v.x - row_max[q]) * row_inv[q] +
+                 __expf(v.y - row_max[q + 1]) * row_inv[q + 1] +
+                 __expf(v.z - row_max[q + 2]) * row_inv[q + 2] +
+                 __expf(v.w - row_max[q + 3]) * row_inv[q + 3];
+          }
+        }
+      } else {
+        for (int k = 0; k < nq; ++k) w += __expf(row[k] - row_max[q0 + k]) * row_inv[q0 + k];
+      }
+    }
+    w += __shfl_xor(w, 1);
+    w += __shfl_xor(w, 2);
+    if (t < 4 * nJ && (t & 3) == 0) {
+      W[j] = w;
+      if (w_in_lds) wsh[j] = w;
+    }
+  }
+  __syncthreads();
+  int32_t* seg = a.seg + (long)u * a.S;
+  block_select_topk<NT>(w_in_lds ? wsh : W, nJ, a.S, seg, [](int i) { return (int32_t)i; }, sh);
+  __syncthreads();
+  // pool normalisers: thread (q, part) folds selected blocks part, part + parts, ...
+  const int parts = NT / B;
+  const int q = threadIdx.x % B, part = threadIdx.x / B;
+  float mx = -INFINITY, z = 0.f;
+  if (part < parts) {
+    const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
+    for (int s = part; s < a.S; s += parts) stat_absorb(mx, z, lse[(long)seg[s] * 2 * B + q], 1.f);
+  }
+  part_m[threadIdx.x] = mx;
+  part_z[threadIdx.x] = z;
+  __syncthreads();
+  if (threadIdx.x < B) {
+    float m2 = -INFINITY, z2 = 0.f;
+    for (int k = 0; k < parts; ++k)
+      stat_absorb(m2, z2, part_m[k * B + threadIdx.x], part_z[k * B + threadIdx.x]);
+    float* ps = a.pstats + (long)u * 2 * B;
+    ps[threadIdx.x] = m2;
+    ps[B + threadIdx.x] = z2;
+  }
+}
+
+// ------------------------------------------------------------ host side
+
+bool fast_path(const wf_params& p) {
+  // a positive scale keeps the block maximum of the raw products the maximum
+  // of the scaled logits
+  return p.dtype == WF_BF16 && p.wavelet == WF_HAAR && p.levels >= 3 && p.levels <= 5 &&
+         p.q_len <= 16 * kFastMaxQBlocks && effective_scale(p) > 0.f;
+}
+
+FastPlan plan_fast(const wf_params& p) {
+  FastPlan f{};
+  const long U = (long)p.batch * p.heads;
+  const long chunks = ((long)p.ctx_len + kScanChunk - 1) / kScanChunk;
+  const long want = std::max(1L, (long)(device_cu_count() + U - 1) / U);
+  const long R = std::min(chunks, want);
+  const long cpr = (chunks + R - 1) / R;
+  f.span = (int)(cpr * kScanChunk);
+  f.R = (int)(((long)p.ctx_len + f.span - 1) / f.span);
+  const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
+  // wave reduction pairs, then two batch slots of block results
+  const size_t bb = p.levels == 3 ? token_batch_bytes<3>(p.q_len)
+                    : p.levels == 4 ? token_batch_bytes<4>(p.q_len)
+                                    : token_batch_bytes<5>(p.q_len);
+  const size_t red = (size_t)(kTokBlock / kWave) * 32 * 2 * sizeof(float) + 2 * bb;
+  // three chunks in flight measured best with the per-chunk compute
+  f.nbuf = (int)std::min<size_t>(3, (160 * 1024 - 1024 - red) / chb);
+  f.lds_bytes = f.nbuf * chb + red;
+  return f;
+}
+
+template <int D, int J>
+static hipError_t token_skim_launch(const TokenSkimArgs& a, size_t lds, hipStream_t s) {
+  auto kern = token_skim_kernel<D, J>;
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)(a.U * a.R)), dim3(kTokBlock), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t token_skim_dispatch(int J, const TokenSkimArgs& a, size_t lds, hipStream_t s) {
+  switch (J) {
+    case 3: return token_skim_launch<D, 3>(a, lds, s);
+    case 4: return token_skim_launch<D, 4>(a, lds, s);
+    case 5: return token_skim_launch<D, 5>(a, lds, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, float* blocks,
+                             float* wstats, hipStream_t s) {
+  if (!fast_path(p)) return hipErrorInvalidValue;
+  const FastPlan f = plan_fast(p);
+  TokenSkimArgs a;
+  a.K = K;
+  a.Q = Q;
+  a.blocks = blocks;
+  a.wstats = wstats;
+  a.U = p.batch * p.heads;
+  a.L = p.ctx_len;
+  a.B = p.q_len;
+  a.nJ = p.ctx_len >> p.levels;
+  a.R = f.R;
+  a.span = f.span;
+  a.nbuf = f.nbuf;
+  a.scale = effective_scale(p);
+  a.norm = (float)std::pow(2.0, -0.5 * p.levels);
+  return p.head_dim == 128 ? token_skim_dispatch<128>(p.levels, a, f.lds_bytes, s)
+                           : token_skim_dispatch<64>(p.levels, a, f.lds_bytes, s);
+}
+
+hipError_t launch_fast_select(const wf_params& p, const float* blocks, const float* wstats,
+                              float* W, int32_t* seg, float* pstats, hipStream_t s) {
+  if (!fast_path(p)) return hipErrorInvalidValue;
+  const FastPlan f = plan_fast(p);
+  FastSelectArgs a;
+  a.blocks = blocks;
+  a.wstats = wstats;
+  a.W = W;
+  a.seg = seg;
+  a.pstats = pstats;
+  a.U = p.batch * p.heads;
+  a.B = p.q_len;
+  a.nJ = p.ctx_len >> p.levels;
+  a.R = f.R;
+  a.S = p.segments;
+  const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
+  const size_t lds = in_lds ? (size_t)a.nJ * sizeof(float) : 0;
+  if (lds > 32768) {  // with the static arrays, past the default 64 KiB
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fast_select_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(fast_select_kernel, dim3((unsigned)a.U), dim3(kFastSelectBlock), lds, s, a,
+                     in_lds);
+  return hipGetLastError();
+}
+
+}  // namespace wf

@@ -54,6 +54,7 @@ struct ScanArgs {
   float* stats;         // [U][C][2][B]
   float* wpool;         // [U][P]  (weights mode)
   int U, L, B, J, S, P, C;
+  int Cs;               // (max, sum) slices in `stats`: C, or 1 when precomputed
   int span;             // pool positions per workgroup (multiple of the chunk)
   int nbuf;             // LDS ring depth (bf16 path)
   int seg_cap;          // region ids staged per workgroup (bf16 path)
@@ -92,6 +93,30 @@ struct AttnArgs {
   int rps;              // cache rows per split (multiple of the chunk)
   int nbuf;             // LDS ring depth (bf16 path)
   float scale;
+};
+
+constexpr int kFastMaxQBlocks = 4;  // query rows <= 64 on the token-level skim
+
+struct TokenSkimArgs {
+  const void* K;        // [U][L][D] bf16
+  const void* Q;        // [U][B][D] bf16
+  float* blocks;        // [U][nJ][2][B]: coarse logits, then log-sum-exps of
+                        // the block's token logits
+  float* wstats;        // [U][R][2][B] coarse-logit max and sum of exp per range
+  int U, L, B, nJ, R;
+  int span;             // tokens per range (multiple of the chunk)
+  int nbuf;             // LDS ring depth
+  float scale;          // logit scale
+  float norm;           // 2^{-J/2}
+};
+
+struct FastSelectArgs {
+  const float* blocks;  // [U][nJ][2][B]
+  const float* wstats;  // [U][R][2][B]
+  float* W;             // [U][nJ] out
+  int32_t* seg;         // [U][S] out
+  float* pstats;        // [U][2][B] out: pool max, pool sum of exp
+  int U, B, nJ, R, S;
 };
 
 }  // namespace wf

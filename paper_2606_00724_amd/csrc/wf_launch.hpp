@@ -43,6 +43,13 @@ struct AttnPlan {
   size_t lds_bytes;
 };
 
+struct FastPlan {
+  int R;             // ranges (workgroups) per unit
+  int span;          // tokens per range
+  int nbuf;          // LDS ring depth
+  size_t lds_bytes;
+};
+
 float effective_scale(const wf_params& p);
 int device_cu_count();
 
@@ -50,6 +57,17 @@ DwtPlan plan_dwt(const wf_params& p);
 SkimPlan plan_skim(const wf_params& p, bool fused);
 ScanPlan plan_scan(const wf_params& p);
 AttnPlan plan_attn(const wf_params& p, long nrows);
+
+// The fused path streams the keys once with token-level scores when the keys
+// are bf16, the wavelet is Haar with 3..5 levels and the query block has at
+// most 64 rows; the scan then needs only its weights pass.
+bool fast_path(const wf_params& p);
+FastPlan plan_fast(const wf_params& p);
+hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K,
+                             float* blocks, float* wstats, hipStream_t s);
+hipError_t launch_fast_select(const wf_params& p, const float* blocks,
+                              const float* wstats, float* W, int32_t* seg,
+                              float* pstats, hipStream_t s);
 
 hipError_t launch_dwt(const wf_params& p, const void* K, float* approx,
                       float* details, hipStream_t s);
@@ -59,9 +77,11 @@ hipError_t launch_skim_tiles(const wf_params& p, bool fused, const void* Q,
 hipError_t launch_skim_select(const wf_params& p, int ntiles,
                               const float* logits, const float* stats,
                               float* W, int32_t* seg, hipStream_t s);
+// stat_slices: 0 when `stats` holds one (max, sum) slice per scan workgroup
+// (written by the stats pass), 1 when it holds the pool's final pair.
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
                               const void* K, const int32_t* seg, float* stats,
-                              float* wpool, hipStream_t s);
+                              float* wpool, hipStream_t s, int stat_slices = 0);
 hipError_t launch_scan_select(const wf_params& p, const float* wpool,
                               const int32_t* seg, int32_t* tok,
                               hipStream_t s);

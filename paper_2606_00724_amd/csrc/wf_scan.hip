@@ -78,12 +78,12 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
   if constexpr (WEIGHTS) {
     float* row_max = red;
     float* row_inv = red + a.B;
-    const float* stt = a.stats + (long)u * a.C * 2 * a.B;
+    const float* stt = a.stats + (long)u * a.Cs * 2 * a.B;
     for (int q = threadIdx.x; q < a.B; q += kBlock) {
       float mx = -INFINITY;
-      for (int k = 0; k < a.C; ++k) mx = fmaxf(mx, stt[(long)k * 2 * a.B + q]);
+      for (int k = 0; k < a.Cs; ++k) mx = fmaxf(mx, stt[(long)k * 2 * a.B + q]);
       float z = 0.f;
-      for (int k = 0; k < a.C; ++k) {
+      for (int k = 0; k < a.Cs; ++k) {
         const float mk = stt[(long)k * 2 * a.B + q];
         if (mk > -INFINITY) z += stt[(long)k * 2 * a.B + a.B + q] * __expf(mk - mx);
       }
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
   }
   if constexpr (!WEIGHTS) {
     __syncthreads();
-    float* stt = a.stats + ((long)u * a.C + c) * 2 * a.B;
+    float* stt = a.stats + ((long)u * a.Cs + c) * 2 * a.B;
     for (int q = threadIdx.x; q < a.B; q += kBlock) {
       stt[q] = run_m[q];
       stt[a.B + q] = run_z[q];
@@ -260,10 +260,10 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
   const bf16_t* Qunit = reinterpret_cast<const bf16_t*>(a.Q) + (long)u * a.B * D;
   stage_rows_any<bf16_t, D, kBlock>(Qs, a.B, [&](int r) { return Qunit + (long)r * D; });
   if constexpr (WEIGHTS) {
-    const float* stt = a.stats + (long)u * a.C * 2 * a.B;
+    const float* stt = a.stats + (long)u * a.Cs * 2 * a.B;
     for (int q = threadIdx.x; q < a.B; q += kBlock) {
       float mx = -INFINITY, z = 0.f;
-      for (int k = 0; k < a.C; ++k)
+      for (int k = 0; k < a.Cs; ++k)
         stat_merge(mx, z, stt[(long)k * 2 * a.B + q], stt[(long)k * 2 * a.B + a.B + q]);
       rowa[q] = mx;
       rowb[q] = 1.f / z;
@@ -381,7 +381,7 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
     lds_barrier();  // the ring is idle; `part` / `wsum` complete
   }
   if constexpr (!WEIGHTS) {
-    float* stt = a.stats + ((long)u * a.C + c) * 2 * a.B;
+    float* stt = a.stats + ((long)u * a.Cs + c) * 2 * a.B;
     for (int q = threadIdx.x; q < a.B; q += kBlock) {
       const int qb = q >> 4, r = q & 15;
       float mx = -INFINITY, z = 0.f;
@@ -480,7 +480,7 @@ static hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t s) {
 
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
                               const void* K, const int32_t* seg, float* stats,
-                              float* wpool, hipStream_t s) {
+                              float* wpool, hipStream_t s, int stat_slices) {
   const ScanPlan pl = plan_scan(p);
   ScanArgs a;
   a.Q = Q;
@@ -495,6 +495,7 @@ hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
   a.S = p.segments;
   a.P = p.segments << p.levels;
   a.C = pl.chunks;
+  a.Cs = stat_slices > 0 ? stat_slices : pl.chunks;
   a.span = pl.span;
   a.nbuf = pl.nbuf;
   a.seg_cap = pl.seg_cap;

@@ -125,6 +125,29 @@ def test_budget_and_workspace_arithmetic(wfpkg):
     assert wfpkg.fused_kernel_names(p)[0] == "skim_tile"
 
 
+@pytest.mark.parametrize("change,path", [
+    (dict(), "general"),                                   # fp32 keys
+    (dict(dtype="bf16"), "token"),
+    (dict(dtype="bf16", levels=5), "token"),
+    (dict(dtype="bf16", levels=2), "general"),             # blocks < 8 tokens
+    (dict(dtype="bf16", levels=6), "general"),             # blocks > 32 tokens
+    (dict(dtype="bf16", q_len=65), "general"),             # > 64 query rows
+    (dict(dtype="bf16", wavelet="db2"), "general"),
+])
+def test_fused_kernel_sequence_follows_the_path(wfpkg, change, path):
+    p = _params(wfpkg, **change)
+    names = wfpkg.fused_kernel_names(p)
+    if path == "token":
+        assert names == ["token_skim", "skim_select", "scan_weights",
+                         "scan_select", "sparse_attn", "attn_combine"]
+    else:
+        assert names == ["skim_tile", "skim_select", "scan_stats",
+                         "scan_weights", "scan_select", "sparse_attn",
+                         "attn_combine"]
+    # the token path's workspace holds block statistics, not scan slices
+    assert wfpkg.workspace_bytes(p, wfpkg.OP_FUSED) > 0
+
+
 def test_binding_rejects_host_tensors(wfpkg):
     import torch
     p = _params(wfpkg)

@@ -62,6 +62,18 @@ EDGE = {
                        segments=24, budget=77),
     "ragged_tiles": V_("rag", ctx_len=8 * (64 * 3 + 5), levels=3, segments=50,
                        budget=333, q_len=64, **_BF),
+    # token-level skim (bf16, Haar, 3..5 levels, <= 64 query rows): lengths
+    # that end inside a 32-token slice and inside a 128-token chunk, query
+    # blocks that end inside a 16-row tile, one range per chunk and several
+    "tok_j3_b17_d64": V_("tj3", ctx_len=8 * (16 * 24 + 5), levels=3,
+                         segments=40, budget=150, q_len=17, **_BF),
+    "tok_j4_b48_d128": V_("tj4", ctx_len=16 * (8 * 24 + 3), head_dim=128,
+                          levels=4, segments=30, budget=200, q_len=48, **_BF),
+    "tok_j5_b1_d64": V_("tj5", ctx_len=32 * 70, levels=5, segments=12,
+                        budget=100, q_len=1, **_BF),
+    "tok_j5_b64_long": V_("tj5l", batch=2, heads=8, ctx_len=32 * 1001,
+                          head_dim=128, levels=5, segments=64, budget=700,
+                          q_len=64, **_BF),
 }
 
 FULL = ["tiny", "layer8b", "long16k", "headline32k", "stress128k"]
