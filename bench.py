@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import hashlib
 import json
 import math
 import os
@@ -29,6 +30,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+COUNTERS = os.path.join(ROOT, "profiles", "token_skim_headline32k_counters.md")
+# sources of the token-level skim kernel, fingerprinted with its counters
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_00724_amd", "csrc", f)
+                  for f in ("wf_fast.hip", "wf_device.hpp", "wf_kernels.hpp")]
 METRIC = ("context tokens filtered+attended/sec per layer @32K ctx; "
           "% of HBM peak")
 
@@ -83,9 +88,33 @@ class HipEvents:
             self.lib.hipEventDestroy(ctypes.c_void_p(e))
 
 
-def cpu_baseline(w, Q, K, V) -> dict:
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, or None when
+    it covers another kernel or workload or the kernel sources changed
+    since the counters were taken."""
+    if not os.path.exists(COUNTERS):
+        return None
+    fields = {}
+    for line in open(COUNTERS):
+        key, sep, val = line.partition(":")
+        if sep and key.strip() in ("kernel", "workload",
+                                   "traffic_bytes_per_launch",
+                                   "source_sha256"):
+            fields[key.strip()] = val.strip()
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    if (fields.get("kernel") != kernel or fields.get("workload") != workload
+            or fields.get("source_sha256") != h.hexdigest()):
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
+def cpu_baseline(w, Q, K, V, min_seconds: float = 10.0) -> dict:
     """The oracle as it stands, on every unit of the layer, in chunks of 16
-    units (only the oracle calls are timed)."""
+    units, repeated until about min_seconds of oracle time have passed (at
+    most 50 passes; only the oracle calls are timed)."""
     import oracle
     oracle.build(force=False)
     U = w.units
@@ -94,19 +123,22 @@ def cpu_baseline(w, Q, K, V) -> dict:
     v = V.reshape(U, w.ctx_len, w.head_dim)
     chunk = 16
     elapsed = 0.0
-    for u0 in range(0, U, chunk):
-        qa, ka, va = (oracle._f64(x[u0:u0 + chunk]) for x in (q, k, v))
-        t0 = time.perf_counter()
-        oracle.filter_attend(qa, ka, va, w.levels, w.segments, w.budget,
-                             wavelet=w.wavelet, boundary=w.boundary)
-        elapsed += time.perf_counter() - t0
-        del qa, ka, va
-    tokens = w.batch * w.ctx_len
+    passes = 0
+    while passes < 50 and (passes == 0 or elapsed < min_seconds):
+        for u0 in range(0, U, chunk):
+            qa, ka, va = (oracle._f64(x[u0:u0 + chunk]) for x in (q, k, v))
+            t0 = time.perf_counter()
+            oracle.filter_attend(qa, ka, va, w.levels, w.segments, w.budget,
+                                 wavelet=w.wavelet, boundary=w.boundary)
+            elapsed += time.perf_counter() - t0
+            del qa, ka, va
+        passes += 1
+    tokens = w.batch * w.ctx_len * passes
     return {"value": tokens / elapsed, "unit": "tokens/s",
             "cores": oracle.max_threads(), "kind": "oracle",
             "sample": f"all {U} (batch, head) units of one {w.name} layer, "
-                      f"fp64, OpenMP over units, {chunk} units per call; "
-                      f"{elapsed:.2f} s",
+                      f"{passes} passes, fp64, OpenMP over units, {chunk} "
+                      f"units per call; {elapsed:.2f} s",
             "seconds": elapsed}
 
 
@@ -120,9 +152,7 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before timing, run one plain 1 GiB device-to-device "
                          "copy (a known-size kernel for scaling HBM counters)")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per launch of "
-                         "the skim kernel (from rocprofv3 counters)")
+
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; the per-(batch, "
@@ -213,9 +243,7 @@ def main() -> int:
     dom = names[0]
     dom_ms = per_kernel[dom]
     achieved = alg["skim"] * U / (dom_ms * 1e-3) / 1e9
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+    traffic = measured_traffic(dom, w.name)
     result = {
         "metric": METRIC,
         "value": value,

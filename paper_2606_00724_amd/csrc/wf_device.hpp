@@ -145,33 +145,6 @@ __device__ __forceinline__ float wave_max16(float v) {
   return v;
 }
 
-// Block-wide exclusive prefix sum of one value per thread; `total` receives
-// the block sum.  `wsum` is LDS scratch of NT / 64 words.  Every thread of the
-// block must call it.
-template <int NT>
-__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum,
-                                         uint32_t& total) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    uint32_t y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wsum[wid] = x;
-  __syncthreads();
-  uint32_t base = 0, tot = 0;
-#pragma unroll
-  for (int w = 0; w < NT / 64; ++w) {
-    uint32_t s = wsum[w];
-    base += (w < wid) ? s : 0u;
-    tot += s;
-  }
-  __syncthreads();
-  total = tot;
-  return base + x - v;
-}
-
 // Order-preserving map of a float to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t order_key(float x) {
   uint32_t u = __float_as_uint(x);
@@ -180,84 +153,126 @@ __device__ __forceinline__ uint32_t order_key(float x) {
 
 template <int NT>
 struct SelectShared {
-  uint32_t hist[256];
-  uint32_t wsum[NT / 64];
-  uint32_t digit;
-  uint32_t above;
+  uint32_t hist[3][256];       // digit histograms, used in turn by the passes
+  uint32_t wsum[2][NT / 64];   // per-wave packed counts, used in turn by tiles
 };
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
 
 // Picks the k largest of score[0..n) (ties: lower index first) and writes
 // map(i) for the picked positions i in ascending order of i to out[0..k).
-// Requires 1 <= k <= n and NT >= 256.  score may live in LDS or global
-// memory; it must be visible to the whole block.  Radix select on the
-// order-preserving keys (four 8-bit digits) finds the k-th key; a block scan
-// over the positions in index order then emits every larger key and the
-// lowest-indexed copies of the k-th key.
+// Requires 1 <= k <= n and 64 <= NT <= 1024.  score may live in LDS or
+// global memory; it must be visible to the whole block, and every thread of
+// the block must call this.
+//
+// Radix select on order-preserving keys, one 8-bit digit per pass from the
+// top: the candidates' digit histogram is built with LDS atomics, then every
+// wave scans the 256 bins itself to find the digit holding the need-th
+// largest candidate, so a pass costs one barrier (three histograms rotate so
+// that the next one is cleared while the current one fills).  The last pass
+// leaves the k-th largest key and the number of its copies to take.  The
+// output positions then follow from one block scan of packed (greater,
+// equal) counts over the positions in index order:
+//   pos = #greater before + min(#equal before, copies to take).
 template <int NT, typename Map>
-__device__ void block_select_topk(const float* score, int n, int k,
-                                  int32_t* out, Map map,
+__device__ void block_select_topk(const float* score, int n, int k, int32_t* out, Map map,
                                   SelectShared<NT>& sh) {
-  static_assert(NT >= 256 && NT % 64 == 0, "block too small for the select");
-  const int tid = threadIdx.x;
-  uint32_t prefix = 0, mask = 0;
-  uint32_t need = (uint32_t)k;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = tid; i < 256; i += NT) sh.hist[i] = 0;
-    __syncthreads();
+  static_assert(NT >= 64 && NT <= 1024 && NT % 64 == 0, "block of whole waves");
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  for (int i = tid; i < 256; i += NT) sh.hist[0][i] = 0;
+  __syncthreads();
+  uint32_t prefix = 0, mask = 0, need = (uint32_t)k;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    uint32_t* h = sh.hist[pass % 3];
+    // the histogram of the next pass was last read two passes ago
+    if (pass < 3)
+      for (int i = tid; i < 256; i += NT) sh.hist[(pass + 1) % 3][i] = 0;
     for (int i = tid; i < n; i += NT) {
-      uint32_t key = order_key(score[i]);
-      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+      const uint32_t key = order_key(score[i]);
+      if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
     }
     __syncthreads();
-    // thread t < 256 looks at digit 255 - t: descending digit order
-    uint32_t c = (tid < 256) ? sh.hist[255 - tid] : 0u;
-    uint32_t total;
-    uint32_t before = block_exclusive_scan<NT>(c, sh.wsum, total);
-    if (tid < 256 && before < need && before + c >= need) {
-      sh.digit = 255u - (uint32_t)tid;
-      sh.above = before;
+    // lane l looks at digits 255 - 4l - j, j < 4 (descending)
+    uint32_t c[4], sum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      c[j] = h[255 - 4 * lane - j];
+      sum += c[j];
     }
-    __syncthreads();
-    prefix |= sh.digit << shift;
+    uint32_t before = wave_inclusive_scan(sum) - sum;
+    int hit = 0;
+    uint32_t hit_above = 0;
+    bool found = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (!found && before < need && before + c[j] >= need) {
+        found = true;
+        hit = j;
+        hit_above = before;
+      }
+      before += c[j];
+    }
+    const int src = __ffsll((unsigned long long)__ballot(found)) - 1;
+    const uint32_t digit = (uint32_t)__shfl(255 - 4 * lane - hit, src);
+    const uint32_t above = (uint32_t)__shfl((int)hit_above, src);
+    prefix |= digit << shift;
     mask |= 255u << shift;
-    need -= sh.above;
-    __syncthreads();
+    need -= above;
   }
   // prefix is now the k-th largest key; `need` copies of it are taken.
-  constexpr int ITEMS = 16;
-  uint32_t taken_base = 0, eq_base = 0;
-  for (int base = 0; base < n; base += NT * ITEMS) {
+  constexpr int ITEMS = 16;  // per-tile counts stay below 2^16
+  uint32_t gt_base = 0, eq_base = 0;
+  int tile = 0;
+  for (int base = 0; base < n; base += NT * ITEMS, ++tile) {
     const int start = base + tid * ITEMS;
     uint32_t gt_bits = 0, eq_bits = 0;
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j) {
-      int i = start + j;
+      const int i = start + j;
       if (i < n) {
-        uint32_t key = order_key(score[i]);
+        const uint32_t key = order_key(score[i]);
         gt_bits |= (key > prefix ? 1u : 0u) << j;
         eq_bits |= (key == prefix ? 1u : 0u) << j;
       }
     }
-    uint32_t eq_cnt = __popc(eq_bits), eq_tot;
-    uint32_t eq_before = eq_base + block_exclusive_scan<NT>(eq_cnt, sh.wsum, eq_tot);
-    uint32_t take_eq = 0;
-    if (need > eq_before) take_eq = min(need - eq_before, eq_cnt);
-    uint32_t take_cnt = __popc(gt_bits) + take_eq, take_tot;
-    uint32_t pos = taken_base + block_exclusive_scan<NT>(take_cnt, sh.wsum, take_tot);
-    uint32_t eq_seen = 0;
+    const uint32_t packed = ((uint32_t)__popc(gt_bits) << 16) | (uint32_t)__popc(eq_bits);
+    const uint32_t incl = wave_inclusive_scan(packed);
+    uint32_t* ws = sh.wsum[tile & 1];
+    if (lane == 63) ws[wid] = incl;
+    __syncthreads();
+    uint32_t wbefore = 0, wtot = 0;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) {
+      const uint32_t v = ws[w];
+      wbefore += (w < wid) ? v : 0u;
+      wtot += v;
+    }
+    const uint32_t ex = wbefore + incl - packed;
+    const uint32_t eq_before = eq_base + (ex & 0xffffu);
+    uint32_t pos = gt_base + (ex >> 16) + min(eq_before, need);
+    uint32_t eq_seen = eq_before;
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j) {
-      int i = start + j;
-      bool gt = (gt_bits >> j) & 1u;
-      bool eq = (eq_bits >> j) & 1u;
-      if (gt || (eq && eq_seen < take_eq)) {
-        if (pos < (uint32_t)k) out[pos] = map(i);
+      const bool gt = (gt_bits >> j) & 1u;
+      const bool eq = (eq_bits >> j) & 1u;
+      if (gt || (eq && eq_seen < need)) {
+        if (pos < (uint32_t)k) out[pos] = map(start + j);
         ++pos;
       }
       eq_seen += eq ? 1u : 0u;
     }
-    taken_base += take_tot;
-    eq_base += eq_tot;
+    gt_base += wtot >> 16;
+    eq_base += wtot & 0xffffu;
   }
 }
 
