@@ -376,18 +376,31 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
 }
 
 // M0 is saved and restored inside the statement: the compiler may keep a
-// value of its own there.
+// value of its own there.  STREAM marks data read exactly once (the `nt`
+// cache policy): it then does not displace data that later kernels re-read.
+template <bool STREAM = false>
 __device__ __forceinline__ void async_load16(const void* g, uint32_t lds_byte) {
   uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(g), "s"(lds_byte)
-      : "memory");
+  if constexpr (STREAM)
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off nt\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(g), "s"(lds_byte)
+        : "memory");
+  else
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(g), "s"(lds_byte)
+        : "memory");
 }
 
 // Workgroup barrier for LDS traffic only: waits for this wave's LDS
@@ -428,7 +441,7 @@ __device__ __forceinline__ int granule_offset(int r, int k) {
 // instruction i of wave w fills bytes [1024 (w IPW + i), +1024), i.e. rows
 // (w IPW + i) 64/G .. +64/G.  rowptr(r) returns a valid global row address
 // for every r < CR (callers clamp rows past their range).
-template <int CR, int G, int NW, class RowPtr>
+template <int CR, int G, int NW, bool STREAM = false, class RowPtr>
 __device__ __forceinline__ void issue_chunk(uint32_t lds_base, const RowPtr& rowptr) {
   constexpr int RPI = 64 / G;
   constexpr int IPW = CR * G / (64 * NW);
@@ -440,7 +453,7 @@ __device__ __forceinline__ void issue_chunk(uint32_t lds_base, const RowPtr& row
     const int r = inst * RPI + lane / G;
     const int k = (lane % G) ^ granule_swz<G>(r);
     const unsigned char* g = reinterpret_cast<const unsigned char*>(rowptr(r)) + 16 * k;
-    async_load16(g, __builtin_amdgcn_readfirstlane(lds_base + 1024u * inst));
+    async_load16<STREAM>(g, __builtin_amdgcn_readfirstlane(lds_base + 1024u * inst));
   }
 }
 

@@ -44,6 +44,8 @@ __device__ __forceinline__ void stat_add(float& m, float& z, float x) {
 
 // Workgroup of the token-level skim: 8 waves, wave w scores the 32-token
 // slice w % 4 of every 128-token chunk against query rows 32 (w / 4) + 0..31.
+// The keys are read exactly once and are loaded with the streaming (nt)
+// policy, which keeps them from evicting the block rows before those leave.
 // Every wave puts its block results into an LDS batch laid out as the
 // global array; waves 0..3 issue every ring load and store nothing to global
 // memory, waves 4..7 issue no loads and copy each finished batch out as one
@@ -131,7 +133,7 @@ __global__ __launch_bounds__(kTokBlock) void token_skim_kernel(TokenSkimArgs a) 
   if (loader) {
     for (int k = 0; k < nch && k < nbuf - 1; ++k) {
       rows.c0 = tb + (long)k * CR;
-      issue_chunk<CR, G, NIW>(ring_lds + (uint32_t)(k * CHB), rows);
+      issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(k * CHB), rows);
     }
   }
 
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(kTokBlock) void token_skim_kernel(TokenSkimArgs a) 
     if (loader) {
       if (ch + nbuf - 1 < nch) {
         rows.c0 = tb + (long)(ch + nbuf - 1) * CR;
-        issue_chunk<CR, G, NIW>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rows);
+        issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rows);
       }
     } else if (ch > 0 && ch % BATCH == 0) {
       copy_batch(ch / BATCH - 1);
