@@ -54,9 +54,16 @@ def _load():
     lib.wf_ref_filter_attend.argtypes = [
         dp, dp, dp, dp, dp, i, i, i, i, i, i, i, i, i, l, d, dp, lp]
     lib.wf_ref_max_threads.argtypes = []
+    lib.wf_ref_recursion_count.argtypes = [d, l]
+    lib.wf_ref_recursion_count.restype = ctypes.c_long
+    lib.wf_ref_recursive_select.argtypes = [dp, dp, i, i, i, i, i, i, dp, d,
+                                            lp, lp, lp]
+    lib.wf_ref_filter_attend_recursive.argtypes = [
+        dp, dp, dp, dp, dp, i, i, i, i, i, i, i, i, dp, d, dp, lp, lp]
     for name in ("wf_ref_dwt", "wf_ref_skim", "wf_ref_topk", "wf_ref_scan",
                  "wf_ref_attn", "wf_ref_filter_attend_unit",
-                 "wf_ref_filter_attend", "wf_ref_max_threads"):
+                 "wf_ref_filter_attend", "wf_ref_max_threads",
+                 "wf_ref_recursive_select", "wf_ref_filter_attend_recursive"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -228,6 +235,60 @@ def filter_attend(Q, K, V, levels: int, segments: int, budget: int,
         wavelet_code(wavelet), boundary_code(boundary), segments, budget,
         scale, _dp(O), _lp(tok)), "filter_attend")
     return O, tok
+
+
+def recursion_count(m: float, n: int) -> int:
+    """c = max(1, ceil(m n)) capped at n, m taken as given (double)."""
+    return int(_load().wf_ref_recursion_count(float(m), int(n)))
+
+
+def recursive_select(Q, K, levels: int, proportions, wavelet: str = "haar",
+                     boundary: str = "symmetric",
+                     scale: float | None = None):
+    """R1 for one unit.  proportions[b - 1] = m_b, b = 1..levels.
+    Returns (tok = mu^0 ascending, counts [levels] with c_b at b - 1)."""
+    Q, K = _f64(Q), _f64(K)
+    B, d = Q.shape
+    L = K.shape[0]
+    prop = _f64(np.asarray(proportions, dtype=np.float64))
+    if prop.size != levels:
+        raise ValueError("one proportion per scale")
+    scale = default_scale(d) if scale is None else scale
+    counts = np.empty(levels, dtype=np.int64)
+    tok = np.empty(L, dtype=np.int64)
+    n_tok = np.zeros(1, dtype=np.int64)
+    _check(_load().wf_ref_recursive_select(
+        _dp(Q), _dp(K), B, L, d, levels, wavelet_code(wavelet),
+        boundary_code(boundary), _dp(prop), scale, _lp(counts), _lp(tok),
+        _lp(n_tok)), "recursive_select")
+    return tok[:int(n_tok[0])].copy(), counts
+
+
+def filter_attend_recursive(Q, K, V, levels: int, proportions,
+                            wavelet: str = "haar",
+                            boundary: str = "symmetric", Kg=None, Vg=None,
+                            scale: float | None = None):
+    """R1 + O7-O8 over many units (OpenMP).  Q [U, B, d], K/V [U, L, d].
+    Returns (O [U, B, d], tok list of per-unit mu^0 arrays)."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    U, B, d = Q.shape
+    L = K.shape[1]
+    G = 0 if Kg is None else int(Kg.shape[1])
+    kg = _f64(Kg) if G else None
+    vg = _f64(Vg) if G else None
+    prop = _f64(np.asarray(proportions, dtype=np.float64))
+    if prop.size != levels:
+        raise ValueError("one proportion per scale")
+    scale = default_scale(d) if scale is None else scale
+    O = np.empty((U, B, d))
+    tok = np.empty((U, L), dtype=np.int64)
+    n_tok = np.empty(U, dtype=np.int64)
+    _check(_load().wf_ref_filter_attend_recursive(
+        _dp(Q), _dp(K), _dp(V), _dp(kg) if G else _null_d(),
+        _dp(vg) if G else _null_d(), U, L, d, B, G, levels,
+        wavelet_code(wavelet), boundary_code(boundary), _dp(prop), scale,
+        _dp(O), _lp(tok), _lp(n_tok)), "filter_attend_recursive")
+    return O, [tok[u, :n_tok[u]].copy() for u in range(U)]
 
 
 def max_threads() -> int:

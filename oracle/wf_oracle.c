@@ -26,6 +26,9 @@
  *       paragraph; Algorithm 1, sparse-cache step).
  *   O8  attention of the query block over the sparse cache, no mask
  *       (the cached-attention form of eq. 3).
+ *   R1  the paper's full multi-scale recursion (eqs. 9-11, Algorithm 1):
+ *       scales B..1 with selection proportions m_b, each scale a DWT of the
+ *       gathered candidate keys, then O7-O8 over the final positions.
  *
  * Readings where the paper is silent (each is also listed in the design
  * notes of the repository):
@@ -354,6 +357,116 @@ int wf_ref_filter_attend(const double* Q, const double* K, const double* V,
             kg, vg, L, d, B, G, levels, wavelet, boundary, S, budget, scale,
             O + (size_t)u * B * d, NULL, NULL, NULL, NULL,
             tok ? tok + (size_t)u * keff : NULL);
+        failures += (rc != 0);
+    }
+    return failures == 0 ? 0 : -1;
+}
+
+/*
+ * Multi-scale recursive filtering of one unit (Section 3.2, eqs. 9-11;
+ * Algorithm 1, the loop over scales) with scale B = `levels` and selection
+ * proportions m_b = prop[b - 1], b = 1..B:
+ *
+ *   mu^B = all L prompt positions (ascending)
+ *   for b = B, B-1, .., 1:
+ *     C_b  = b-level DWT of the gathered keys K[mu^b], taken as one sequence
+ *            (eq. 11; at b = B this is eq. 6 on the whole prompt)
+ *     W    = column sums of softmax(scale Q C_b^T), softmax over C_b's rows
+ *            only (eqs. 7-8 on the current candidates)
+ *     J_b  = the c_b best rows of W (eq. 9), ties to the lower index,
+ *            c_b = max(1, ceil(m_b n_b)) with n_b = |mu^b| / 2^b, at most n_b
+ *     mu^{b-1} = { mu^b[2^b j + r] : j in J_b ascending, r < 2^b }
+ *            (eq. 10, composed with mu^b so that indices stay prompt
+ *            positions)
+ *   tok = mu^0, ascending, 2 c_1 positions.
+ *
+ * counts [levels] (nullable) receives c_b at index b - 1; tok must hold
+ * L entries (the largest possible mu^0); *n_tok receives |mu^0|.
+ */
+long wf_ref_recursion_count(double m, long n) {
+    long c = (long)ceil(m * (double)n);
+    if (c < 1) c = 1;
+    if (c > n) c = n;
+    return c;
+}
+
+int wf_ref_recursive_select(const double* Q, const double* K, int B, int L,
+                            int d, int levels, int wavelet, int boundary,
+                            const double* prop, double scale, long* counts,
+                            long* tok, long* n_tok) {
+    if (levels < 1 || L < 2 || (L % (1 << levels)) != 0) return -1;
+    for (int b = 1; b <= levels; ++b)
+        if (!(prop[b - 1] > 0.0 && prop[b - 1] <= 1.0)) return -1;
+    long* mu = (long*)malloc(sizeof(long) * (size_t)L);
+    long* next = (long*)malloc(sizeof(long) * (size_t)L);
+    double* X = (double*)malloc(sizeof(double) * (size_t)L * d);
+    double* C = (double*)malloc(sizeof(double) * (size_t)L * d);
+    double* W = (double*)malloc(sizeof(double) * (size_t)L);
+    double* logit = (double*)malloc(sizeof(double) * (size_t)B * L);
+    long* pick = (long*)malloc(sizeof(long) * (size_t)L);
+    int rc = -1;
+    if (!mu || !next || !X || !C || !W || !logit || !pick) goto done;
+    long m = L; /* |mu^b| */
+    for (long t = 0; t < L; ++t) mu[t] = t;
+    for (int b = levels; b >= 1; --b) {
+        long run = 1L << b;
+        long n = m / run;
+        /* eq. 11: gather, then a b-level transform of the gathered sequence */
+        for (long t = 0; t < m; ++t)
+            memcpy(X + (size_t)t * d, K + (size_t)mu[t] * d, sizeof(double) * d);
+        if (wf_ref_dwt(X, (int)m, d, b, wavelet, boundary, C, NULL) != 0) goto done;
+        /* eqs. 7-8 over the n coefficients of this scale */
+        ref_column_softmax_sum(Q, C, B, n, d, scale, W, logit);
+        /* eq. 9 with a proportion */
+        long c = wf_ref_recursion_count(prop[b - 1], n);
+        if (counts) counts[b - 1] = c;
+        if (wf_ref_topk(W, n, c, pick) != 0) goto done;
+        /* eq. 10 through mu^b */
+        for (long i = 0; i < c; ++i)
+            for (long r = 0; r < run; ++r) next[i * run + r] = mu[pick[i] * run + r];
+        m = c * run;
+        memcpy(mu, next, sizeof(long) * (size_t)m);
+    }
+    memcpy(tok, mu, sizeof(long) * (size_t)m);
+    *n_tok = m;
+    rc = 0;
+done:
+    free(mu); free(next); free(X); free(C); free(W); free(logit); free(pick);
+    return rc;
+}
+
+/*
+ * The recursive path for `units` units: R1 above, then O7-O8 over
+ * [K[mu^0]; K_g].  Arrays as in wf_ref_filter_attend; tok [units][L]
+ * (nullable) receives mu^0 in its first n_tok entries, n_tok [units]
+ * (nullable) its size.
+ */
+int wf_ref_filter_attend_recursive(const double* Q, const double* K,
+                                   const double* V, const double* Kg,
+                                   const double* Vg, int units, int L, int d,
+                                   int B, int G, int levels, int wavelet,
+                                   int boundary, const double* prop,
+                                   double scale, double* O, long* tok,
+                                   long* n_tok) {
+    int failures = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(+ : failures)
+    for (int u = 0; u < units; ++u) {
+        long* t = (long*)malloc(sizeof(long) * (size_t)L);
+        long nt = 0;
+        int rc = t ? wf_ref_recursive_select(Q + (size_t)u * B * d,
+                                             K + (size_t)u * L * d, B, L, d,
+                                             levels, wavelet, boundary, prop,
+                                             scale, NULL, t, &nt)
+                   : -1;
+        if (rc == 0)
+            rc = wf_ref_attn(Q + (size_t)u * B * d, K + (size_t)u * L * d,
+                             V + (size_t)u * L * d, t, nt,
+                             G ? Kg + (size_t)u * G * d : NULL,
+                             G ? Vg + (size_t)u * G * d : NULL, G, B, d, scale,
+                             O + (size_t)u * B * d);
+        if (rc == 0 && tok) memcpy(tok + (size_t)u * L, t, sizeof(long) * (size_t)nt);
+        if (rc == 0 && n_tok) n_tok[u] = nt;
+        free(t);
         failures += (rc != 0);
     }
     return failures == 0 ? 0 : -1;

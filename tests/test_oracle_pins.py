@@ -432,3 +432,167 @@ def test_generator_is_deterministic():
     # keys have (roughly) the stated marginal variance 1 + 0.3^2 off-needle
     Q, K, V = synth.unit_f64(synth.WORKLOADS["layer8b"], 0, 0, 0)
     assert 0.8 < K[:1000].var() < 1.4
+
+
+# ------------------------------------------------- recursion (R1, eqs. 9-11)
+
+def _haar_recursion_numpy(Q, K, levels, props, scale):
+    """The recursion with the Haar transform of each gathered sequence taken
+    from its closed form (2^{-b/2} times sums of aligned 2^b runs of the
+    gathered rows), eqs. 7-9 written out with numpy, and the count rule
+    c = max(1, ceil(m n)).  Shares nothing with the oracle but the inputs."""
+    L, d = K.shape
+    mu = np.arange(L)
+    for b in range(levels, 0, -1):
+        run = 1 << b
+        n = mu.size // run
+        C = K[mu].reshape(n, run, d).sum(axis=1) * 2.0 ** (-b / 2)
+        s = scale * (Q @ C.T)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        W = (p / p.sum(axis=1, keepdims=True)).sum(axis=0)
+        c = min(n, max(1, math.ceil(props[b - 1] * n)))
+        order = np.lexsort((np.arange(n), -W))
+        J = np.sort(order[:c])
+        mu = mu.reshape(n, run)[J].reshape(-1)
+    return mu
+
+
+@pytest.mark.parametrize("levels,props", [
+    (1, [0.3]), (2, [0.5, 0.4]), (3, [0.6, 0.5, 0.25]), (5, [0.9, 0.7, 0.5, 0.5, 0.2])])
+def test_recursion_haar_matches_closed_form_route(ref, levels, props):
+    """Haar: the transform of a gathered sequence is 2^{-b/2} times sums of
+    its aligned runs, so a numpy recursion built on that closed form must pick
+    the same positions at every scale."""
+    rng = _rng(100 + levels)
+    L, d, B = 256, 8, 5
+    K = rng.standard_normal((L, d))
+    Q = rng.standard_normal((B, d)) * 0.7
+    tok, counts = ref.recursive_select(Q, K, levels, props, "haar")
+    want = _haar_recursion_numpy(Q, K, levels, props, 1 / math.sqrt(d))
+    np.testing.assert_array_equal(tok, want)
+    assert tok.size == 2 * counts[0]
+    assert np.all(np.diff(tok) > 0)
+
+
+def test_recursion_counts_follow_the_proportions(ref):
+    """c_b = max(1, ceil(m_b n_b)) with n_B = L / 2^B and n_b = 2 c_{b+1}."""
+    rng = _rng(7)
+    L, levels = 512, 4
+    props = [0.3, 0.55, 0.01, 0.75]
+    tok, counts = ref.recursive_select(rng.standard_normal((3, 4)),
+                                       rng.standard_normal((L, 4)), levels,
+                                       props)
+    n = L >> levels
+    want = {}
+    for b in range(levels, 0, -1):
+        c = min(n, max(1, math.ceil(props[b - 1] * n)))
+        want[b] = c
+        n = 2 * c
+    assert [int(counts[b - 1]) for b in range(1, levels + 1)] == \
+        [want[b] for b in range(1, levels + 1)]
+    assert tok.size == 2 * want[1]
+    assert ref.recursion_count(0.01, 64) == 1          # at least one
+    assert ref.recursion_count(1.0, 64) == 64
+    assert ref.recursion_count(0.5, 63) == 32          # rounds up
+
+
+@pytest.mark.parametrize("wavelet,boundary", [("haar", "symmetric"),
+                                              ("db2", "symmetric"),
+                                              ("db2", "periodic")])
+def test_recursion_keep_all_is_every_position(ref, wavelet, boundary):
+    """All m_b = 1: every scale keeps every coefficient, so mu^0 is the whole
+    prompt and the attention is dense attention."""
+    rng = _rng(11)
+    L, d, B = 128, 6, 4
+    Q, K, V = (rng.standard_normal(s) for s in ((B, d), (L, d), (L, d)))
+    tok, _ = ref.recursive_select(Q, K, 3, [1.0, 1.0, 1.0], wavelet, boundary)
+    np.testing.assert_array_equal(tok, np.arange(L))
+    O, toks = ref.filter_attend_recursive(Q[None], K[None], V[None], 3,
+                                          [1.0] * 3, wavelet, boundary)
+    s = Q @ K.T / math.sqrt(d)
+    p = np.exp(s - s.max(axis=1, keepdims=True))
+    dense = (p / p.sum(axis=1, keepdims=True)) @ V
+    np.testing.assert_allclose(O[0], dense, rtol=0, atol=1e-12)
+
+
+def test_recursion_constant_keys_keep_the_first_positions(ref):
+    """Equal keys tie every weight at every scale; ties go to the lower
+    index, so mu^0 is the first 2 c_1 positions."""
+    L, levels = 256, 3
+    K = np.full((L, 5), 0.25)
+    Q = _rng(3).standard_normal((4, 5))
+    props = [0.5, 0.25, 0.5]
+    tok, counts = ref.recursive_select(Q, K, levels, props, "db2")
+    np.testing.assert_array_equal(tok, np.arange(2 * counts[0]))
+
+
+def test_recursion_single_query_ranks_by_block_logit(ref):
+    """One query row: the softmax is monotone, so each scale keeps the c_b
+    candidates of largest coarse logit <Q, C_b[j]>."""
+    rng = _rng(21)
+    L, d = 128, 7
+    K = rng.standard_normal((L, d))
+    q = rng.standard_normal((1, d))
+    tok, counts = ref.recursive_select(q, K, 2, [0.5, 0.25], "haar")
+    mu = np.arange(L)
+    for b in (2, 1):
+        n = mu.size >> b
+        C = K[mu].reshape(n, 1 << b, d).sum(axis=1)  # positive rescaling
+        s = (q @ C.T)[0]
+        c = int(counts[b - 1])
+        J = np.sort(np.argsort(-s, kind="stable")[:c])
+        mu = mu.reshape(n, 1 << b)[J].reshape(-1)
+    np.testing.assert_array_equal(tok, mu)
+
+
+def test_recursion_query_permutation_invariance(ref):
+    rng = _rng(5)
+    Q = rng.standard_normal((6, 8))
+    K = rng.standard_normal((256, 8))
+    a, _ = ref.recursive_select(Q, K, 3, [0.5, 0.5, 0.25], "db2")
+    b, _ = ref.recursive_select(Q[::-1].copy(), K, 3, [0.5, 0.5, 0.25], "db2")
+    np.testing.assert_array_equal(a, b)
+
+
+def test_recursion_db2_periodic_keep_all_matches_the_pyramid(ref):
+    """With every scale keeping everything the gathered sequence at scale b is
+    the whole prompt, so eq. 11's transform must equal the b-level transform
+    of the prompt (a periodic db2 pyramid of the oracle's own O1, pinned
+    above); checked through the first scale's ranking: a single query ranks
+    the whole prompt by <q, A_B[j]>."""
+    rng = _rng(9)
+    L, d = 128, 5
+    K = rng.standard_normal((L, d))
+    q = rng.standard_normal((1, d))
+    A = ref.dwt(K, 2, "db2", "periodic")
+    c = ref.recursion_count(0.25, L >> 2)
+    tok, _ = ref.recursive_select(q, K, 2, [1.0, 0.25], "db2", "periodic")
+    J = np.sort(np.argsort(-(q @ A.T)[0], kind="stable")[:c])
+    want = (J[:, None] * 4 + np.arange(4)).reshape(-1)
+    np.testing.assert_array_equal(tok, want)
+
+
+def test_recursion_db2_gathers_before_transforming(ref):
+    """eq. 11 transforms the gathered keys as one sequence: for db2 the
+    filter reads across the joins between kept regions, so the second scale
+    is not the prompt's pyramid restricted to the kept regions.  With one
+    query, the second scale's ranking follows <q, DWT(K[mu^1])>."""
+    rng = _rng(13)
+    L, d = 256, 4
+    K = rng.standard_normal((L, d))
+    q = rng.standard_normal((1, d))
+    tok, counts = ref.recursive_select(q, K, 2, [0.25, 0.25], "db2")
+    A2 = ref.dwt(K, 2, "db2")
+    c2 = int(counts[1])
+    J2 = np.sort(np.argsort(-(q @ A2.T)[0], kind="stable")[:c2])
+    mu1 = (J2[:, None] * 4 + np.arange(4)).reshape(-1)
+    C1 = ref.dwt(K[mu1], 1, "db2")                  # gathered, then transformed
+    c1 = int(counts[0])
+    J1 = np.sort(np.argsort(-(q @ C1.T)[0], kind="stable")[:c1])
+    want = mu1.reshape(-1, 2)[J1].reshape(-1)
+    np.testing.assert_array_equal(tok, want)
+    # the pyramid restricted to the kept regions would rank differently here
+    A1 = ref.dwt(K, 1, "db2")
+    kept = mu1.reshape(-1, 2)[:, 0] // 2
+    J1_pyr = np.sort(np.argsort(-(q @ A1[kept].T)[0], kind="stable")[:c1])
+    assert not np.array_equal(J1_pyr, J1)
