@@ -217,6 +217,68 @@ wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
 int32_t wf_filter_attend_kernels(const wf_params* p);
 const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i);
 
+/* ---------------------------------------------------------------------
+ * Multi-scale recursive filtering (Section 3.2, eqs. 9-11; Algorithm 1,
+ * the loop over scales).  Scale B = p->levels; selection proportions
+ * m_b = proportions[b - 1] for b = 1..B (host array of p->levels floats,
+ * each in (0, 1]).  Per unit:
+ *
+ *   mu^B = all ctx_len positions
+ *   for b = B .. 1:
+ *     candidates: the b-level Haar coefficients of the gathered keys
+ *       K[mu^b] -- n_B = ctx_len / 2^B at b = B, n_b = 2 c_{b+1} below
+ *       (the two halves of every kept block; for Haar, eq. 11's transform
+ *       of the gathered sequence is exactly these block coefficients)
+ *     weights: eqs. 7-8 over the n_b candidates only
+ *     keep: the c_b best (eq. 9; ties to the lower index), where
+ *       c_b = max(1, ceil(m_b * n_b)) evaluated in double from the float
+ *       m_b, at most n_b
+ *     mu^{b-1}: the positions of the kept blocks (eq. 10 through mu^b)
+ *   then attention over [K[mu^0]; Kg], [V[mu^0]; Vg] as in wf_filter_attend.
+ *
+ * mu^0 has 2 c_1 positions, ascending.  p->segments and p->budget are not
+ * used.  This build runs the recursion for the Haar wavelet (the paper's
+ * setting); db2 returns WF_ERR_UNSUPPORTED.
+ * --------------------------------------------------------------------- */
+
+/* c_b for every scale into counts[b - 1] (host array of p->levels).
+ * INVALID_ARG for a NULL array or a proportion outside (0, 1]. */
+wf_status wf_recursion_counts(const wf_params* p, const float* proportions,
+                              int32_t* counts);
+
+/* Workspace bytes wf_filter_attend_recursive needs, or 0 for invalid
+ * parameters. */
+size_t wf_recursive_workspace_bytes(const wf_params* p,
+                                    const float* proportions);
+
+/* The recursion and the attention, asynchronous on `stream`.  Q, K, V, Kg,
+ * Vg and O as in wf_filter_attend; tok_idx (nullable, device,
+ * [batch][heads][2 c_1]) receives mu^0.  The workspace is caller-owned
+ * device memory, 256-byte aligned, of at least
+ * wf_recursive_workspace_bytes(p, proportions) bytes.  Errors as in
+ * wf_filter_attend; UNSUPPORTED for a wavelet other than Haar. */
+wf_status wf_filter_attend_recursive(const wf_params* p,
+                                     const float* proportions, const void* Q,
+                                     const void* K, const void* V,
+                                     const void* Kg, const void* Vg, void* O,
+                                     int32_t* tok_idx, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
+/* Same, recording events[i] before kernel i and events[n] after the last
+ * (n = wf_filter_attend_recursive_kernels(p); n_events >= n + 1). */
+wf_status wf_filter_attend_recursive_timed(
+    const wf_params* p, const float* proportions, const void* Q, const void* K,
+    const void* V, const void* Kg, const void* Vg, void* O, int32_t* tok_idx,
+    void* workspace, size_t workspace_bytes, void* stream, void** events,
+    int32_t n_events);
+
+/* Kernels one recursive call queues (2 per scale, then the attention and
+ * its combine) and the name of the i-th one, or -1 / NULL if p is
+ * invalid. */
+int32_t wf_filter_attend_recursive_kernels(const wf_params* p);
+const char* wf_filter_attend_recursive_kernel_name(const wf_params* p,
+                                                   int32_t i);
+
 /* Static description of a status code. */
 const char* wf_status_str(wf_status s);
 

@@ -30,6 +30,10 @@ EXPORTED = ("wf_workspace_bytes", "wf_effective_budget", "wf_dwt_keys",
             "wf_skim_score", "wf_scan_select", "wf_gather_kv",
             "wf_sparse_attn", "wf_filter_attend", "wf_filter_attend_timed",
             "wf_filter_attend_kernels", "wf_filter_attend_kernel_name",
+            "wf_recursion_counts", "wf_recursive_workspace_bytes",
+            "wf_filter_attend_recursive", "wf_filter_attend_recursive_timed",
+            "wf_filter_attend_recursive_kernels",
+            "wf_filter_attend_recursive_kernel_name",
             "wf_status_str", "wf_last_error")
 
 
@@ -58,6 +62,7 @@ def _load() -> ctypes.CDLL:
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.POINTER(WfParams)
     vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
+    fp, ip = ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)
     sig = {
         "wf_workspace_bytes": (sz, [P, i32]),
         "wf_effective_budget": (i32, [P]),
@@ -73,6 +78,17 @@ def _load() -> ctypes.CDLL:
                                     vp, ctypes.POINTER(vp), i32]),
         "wf_filter_attend_kernels": (i32, [P]),
         "wf_filter_attend_kernel_name": (ctypes.c_char_p, [P, i32]),
+        "wf_recursion_counts": (ctypes.c_int, [P, fp, ip]),
+        "wf_recursive_workspace_bytes": (sz, [P, fp]),
+        "wf_filter_attend_recursive": (ctypes.c_int,
+                                       [P, fp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                        sz, vp]),
+        "wf_filter_attend_recursive_timed": (ctypes.c_int,
+                                             [P, fp, vp, vp, vp, vp, vp, vp,
+                                              vp, vp, sz, vp,
+                                              ctypes.POINTER(vp), i32]),
+        "wf_filter_attend_recursive_kernels": (i32, [P]),
+        "wf_filter_attend_recursive_kernel_name": (ctypes.c_char_p, [P, i32]),
         "wf_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "wf_last_error": (ctypes.c_char_p, []),
     }
@@ -218,6 +234,69 @@ def wf_filter_attend_timed(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
                                        _ptr(V), _ptr(Kg), _ptr(Vg), _ptr(O),
                                        _ptr(tok_idx), _ptr(seg_idx), ws, nb,
                                        _stream(stream), arr, len(events)))
+
+
+# ------------------------------------------------------------ recursion
+# proportions: one float per scale, m_b at index b - 1 (host values).
+
+def _props(p: WfParams, proportions):
+    vals = [float(m) for m in proportions]
+    if len(vals) != p.levels:
+        raise ValueError(f"{p.levels} proportions needed, got {len(vals)}")
+    return (ctypes.c_float * len(vals))(*vals)
+
+
+def recursion_counts(p: WfParams, proportions) -> list[int]:
+    """c_b per scale (index b - 1); mu^0 has 2 c_1 positions."""
+    out = (ctypes.c_int32 * p.levels)()
+    _check(_lib.wf_recursion_counts(ctypes.byref(p), _props(p, proportions),
+                                    out))
+    return list(out)
+
+
+def recursive_workspace_bytes(p: WfParams, proportions) -> int:
+    return int(_lib.wf_recursive_workspace_bytes(ctypes.byref(p),
+                                                 _props(p, proportions)))
+
+
+def recursive_kernel_names(p: WfParams) -> list[str]:
+    n = _lib.wf_filter_attend_recursive_kernels(ctypes.byref(p))
+    return [_lib.wf_filter_attend_recursive_kernel_name(ctypes.byref(p),
+                                                        i).decode()
+            for i in range(n)]
+
+
+def wf_filter_attend_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok_idx,
+                               workspace, stream=None):
+    ws, nb = _ws(workspace)
+    _check(_lib.wf_filter_attend_recursive(
+        ctypes.byref(p), _props(p, proportions), _ptr(Q), _ptr(K), _ptr(V),
+        _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx), ws, nb, _stream(stream)))
+
+
+def wf_filter_attend_recursive_timed(p, proportions, Q, K, V, Kg, Vg, O,
+                                     tok_idx, workspace, events, stream=None):
+    ws, nb = _ws(workspace)
+    arr = (ctypes.c_void_p * len(events))(*events)
+    _check(_lib.wf_filter_attend_recursive_timed(
+        ctypes.byref(p), _props(p, proportions), _ptr(Q), _ptr(K), _ptr(V),
+        _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx), ws, nb, _stream(stream),
+        arr, len(events)))
+
+
+def filter_attend_recursive(p: WfParams, proportions, Q, K, V, Kg=None,
+                            Vg=None, workspace=None, stream=None):
+    """Allocates O, mu^0 and the workspace; returns (O, tok_idx)."""
+    counts = recursion_counts(p, proportions)
+    O = torch.empty_like(Q)
+    tok = torch.empty((p.batch, p.heads, 2 * counts[0]), dtype=torch.int32,
+                      device=Q.device)
+    if workspace is None:
+        nb = recursive_workspace_bytes(p, proportions)
+        workspace = torch.empty(nb, dtype=torch.uint8, device=Q.device)
+    wf_filter_attend_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok,
+                               workspace, stream)
+    return O, tok
 
 
 # ------------------------------------------------------------ allocation

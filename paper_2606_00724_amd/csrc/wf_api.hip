@@ -46,7 +46,14 @@ int device_cu_count() {
 
 // ------------------------------------------------------------ validation
 
-static wf_status check_params(const wf_params* p) {
+#define WF_TRY_SHAPE(expr)           \
+  do {                               \
+    wf_status _s = (expr);           \
+    if (_s != WF_OK) return _s;      \
+  } while (0)
+
+// Fields every entry point uses (not segments, budget).
+static wf_status check_shape(const wf_params* p) {
   if (!p) return fail(WF_ERR_INVALID_ARG, "params is NULL");
   if (p->batch < 1 || p->heads < 1)
     return fail(WF_ERR_INVALID_ARG, "batch (%d) and heads (%d) must be >= 1",
@@ -81,18 +88,24 @@ static wf_status check_params(const wf_params* p) {
     return fail(WF_ERR_INVALID_ARG, "unknown boundary %d", p->boundary);
   if (p->dtype != WF_BF16 && p->dtype != WF_F32)
     return fail(WF_ERR_INVALID_ARG, "unknown dtype %d", p->dtype);
+  if (!std::isfinite(p->scale))
+    return fail(WF_ERR_INVALID_ARG, "scale is not finite");
+  return WF_OK;
+}
+
+static wf_status check_params(const wf_params* p) {
+  WF_TRY_SHAPE(check_shape(p));
   const int nJ = p->ctx_len >> p->levels;
   if (p->segments < 1 || p->segments > nJ)
     return fail(WF_ERR_INVALID_ARG, "segments %d outside [1, %d]", p->segments, nJ);
   if (p->budget < 1) return fail(WF_ERR_INVALID_ARG, "budget %d < 1", p->budget);
-  if (!std::isfinite(p->scale))
-    return fail(WF_ERR_INVALID_ARG, "scale is not finite");
   if (p->dtype == WF_BF16 && plan_scan(*p).nbuf < 2)
     return fail(WF_ERR_UNSUPPORTED, "query block and pool range do not fit the LDS ring");
-  if ((long)p->batch * p->heads * ((long)p->budget < ((long)p->segments << p->levels)
-                                        ? (long)p->budget
-                                        : ((long)p->segments << p->levels)) +
-          (long)p->gen_len > (1L << 31))
+  if ((long)p->batch * p->heads *
+          (((long)p->budget < ((long)p->segments << p->levels)
+                ? (long)p->budget
+                : ((long)p->segments << p->levels)) +
+           (long)p->gen_len) > (1L << 31))
     return fail(WF_ERR_UNSUPPORTED, "sparse cache too large");
   return WF_OK;
 }
@@ -280,6 +293,140 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
   return ok();
 }
 
+// ------------------------------------------------------------ recursion
+
+// Validates the recursion's parameters and fills counts[b - 1] = c_b.
+static wf_status check_recursion(const wf_params* p, const float* prop, int32_t* counts) {
+  WF_TRY(check_shape(p));
+  if (!prop) return fail(WF_ERR_INVALID_ARG, "proportions is NULL");
+  long n = (long)p->ctx_len >> p->levels;
+  for (int b = p->levels; b >= 1; --b) {
+    const float m = prop[b - 1];
+    if (!(m > 0.f && m <= 1.f))
+      return fail(WF_ERR_INVALID_ARG, "proportion m_%d = %g outside (0, 1]", b, (double)m);
+    long c = (long)std::ceil((double)m * (double)n);
+    c = std::max(1L, std::min(c, n));
+    counts[b - 1] = (int32_t)c;
+    n = 2 * c;
+  }
+  if ((long)p->batch * p->heads * (2L * counts[0] + p->gen_len) > (1L << 31))
+    return fail(WF_ERR_UNSUPPORTED, "sparse cache too large");
+  return WF_OK;
+}
+
+struct RecLayout {
+  size_t logits = 0, stats = 0, W = 0, sel[2] = {0, 0}, tok = 0, part = 0, pstat = 0,
+         total = 0;
+};
+
+static RecLayout rec_layout(const wf_params& p, const int32_t* counts) {
+  RecLayout l;
+  const RecPlan rp = plan_recursion(p, counts);
+  const size_t U = (size_t)p.batch * p.heads, B = p.q_len;
+  const long nrows = 2L * counts[0] + p.gen_len;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += up256(bytes);
+    return at;
+  };
+  l.logits = take(U * B * rp.max_n * sizeof(float));
+  l.stats = take(U * rp.max_tiles * 2 * B * sizeof(float));
+  l.W = take(U * rp.max_n * sizeof(float));
+  l.sel[0] = take(U * rp.max_keep * sizeof(int32_t));
+  l.sel[1] = take(U * rp.max_keep * sizeof(int32_t));
+  l.tok = take(U * 2 * counts[0] * sizeof(int32_t));
+  const AttnPlan ap = plan_attn(p, nrows);
+  l.part = take(U * ap.splits * B * p.head_dim * sizeof(float));
+  l.pstat = take(U * ap.splits * 2 * B * sizeof(float));
+  l.total = off;
+  return l;
+}
+
+static const char* const kRecTileNames[WF_MAX_LEVELS] = {
+    "rec_tiles_b1", "rec_tiles_b2", "rec_tiles_b3", "rec_tiles_b4", "rec_tiles_b5",
+    "rec_tiles_b6", "rec_tiles_b7", "rec_tiles_b8", "rec_tiles_b9", "rec_tiles_b10"};
+static const char* const kRecSelectNames[WF_MAX_LEVELS] = {
+    "rec_select_b1", "rec_select_b2", "rec_select_b3", "rec_select_b4", "rec_select_b5",
+    "rec_select_b6", "rec_select_b7", "rec_select_b8", "rec_select_b9", "rec_select_b10"};
+
+static int rec_kernels(const wf_params& p) { return 2 * p.levels + 2; }
+
+static const char* rec_kernel_name(const wf_params& p, int i) {
+  if (i < 2 * p.levels) {
+    const int b = p.levels - i / 2;
+    return (i % 2 == 0 ? kRecTileNames : kRecSelectNames)[b - 1];
+  }
+  return i == 2 * p.levels ? "sparse_attn" : "attn_combine";
+}
+
+static wf_status recursive_impl(const wf_params* p, const float* prop, const void* Q,
+                                const void* K, const void* V, const void* Kg,
+                                const void* Vg, void* O, int32_t* tok_idx, void* ws,
+                                size_t ws_bytes, void* stream, void** events,
+                                int n_events) {
+  int32_t counts[WF_MAX_LEVELS];
+  WF_TRY(check_recursion(p, prop, counts));
+  if (p->wavelet != WF_HAAR)
+    return fail(WF_ERR_UNSUPPORTED, "the recursion is built for the Haar wavelet only");
+  WF_TRY(check_ptr(Q, "Q", false));
+  WF_TRY(check_ptr(K, "K", false));
+  WF_TRY(check_ptr(V, "V", false));
+  WF_TRY(check_ptr(O, "O", false));
+  WF_TRY(check_ptr(tok_idx, "tok_idx", true));
+  if (p->gen_len > 0) {
+    WF_TRY(check_ptr(Kg, "Kg", false));
+    WF_TRY(check_ptr(Vg, "Vg", false));
+  }
+  const int nk = rec_kernels(*p);
+  if (events && n_events < nk + 1)
+    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, nk + 1);
+  const RecLayout l = rec_layout(*p, counts);
+  WF_TRY(check_workspace(ws, ws_bytes, l.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  float* logits = reinterpret_cast<float*>(at(ws, l.logits));
+  float* stats = reinterpret_cast<float*>(at(ws, l.stats));
+  float* W = reinterpret_cast<float*>(at(ws, l.W));
+  int32_t* sel[2] = {reinterpret_cast<int32_t*>(at(ws, l.sel[0])),
+                     reinterpret_cast<int32_t*>(at(ws, l.sel[1]))};
+  int32_t* tok = tok_idx ? tok_idx : reinterpret_cast<int32_t*>(at(ws, l.tok));
+  float* part = reinterpret_cast<float*>(at(ws, l.part));
+  float* pstat = reinterpret_cast<float*>(at(ws, l.pstat));
+  int k = 0;
+  auto mark = [&]() -> hipError_t {
+    if (!events) return hipSuccess;
+    return hipEventRecord(static_cast<hipEvent_t>(events[k]), s);
+  };
+  auto step = [&](hipError_t launched) -> wf_status {
+    if (launched != hipSuccess)
+      return fail(WF_ERR_HIP, "%s: %s", rec_kernel_name(*p, k), hipGetErrorString(launched));
+    ++k;
+    hipError_t e = mark();
+    if (e != hipSuccess) return fail(WF_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    return WF_OK;
+  };
+  WF_HIP(mark(), "hipEventRecord");
+  long n = (long)p->ctx_len >> p->levels;
+  const int32_t* parent = nullptr;
+  int npar = 0;
+  for (int b = p->levels; b >= 1; --b) {
+    int32_t* out = b == 1 ? tok : sel[b & 1];
+    WF_TRY(step(launch_rec_tiles(*p, b, n, parent, npar, Q, K, logits, stats, s)));
+    WF_TRY(step(launch_rec_select(*p, b, n, counts[b - 1], parent, npar, logits, stats, W,
+                                  out, s)));
+    parent = out;
+    npar = counts[b - 1];
+    n = 2L * counts[b - 1];
+  }
+  const int nsel = 2 * counts[0];
+  const long nrows = (long)nsel + p->gen_len;
+  WF_TRY(step(launch_attn(*p, Q, K, V, tok, nsel, Kg, Vg, p->gen_len, nrows, part, pstat,
+                          s)));
+  WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
+  return ok();
+}
+
 }  // namespace wf
 
 using namespace wf;
@@ -426,6 +573,54 @@ int32_t wf_filter_attend_kernels(const wf_params* p) {
 const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i) {
   if (check_params(p) != WF_OK || i < 0 || i >= fused_kernels(*p)) return nullptr;
   return fused_names(*p)[i];
+}
+
+wf_status wf_recursion_counts(const wf_params* p, const float* proportions,
+                              int32_t* counts) {
+  int32_t c[WF_MAX_LEVELS];
+  if (!counts) return fail(WF_ERR_INVALID_ARG, "counts is NULL");
+  WF_TRY(check_recursion(p, proportions, c));
+  for (int b = 0; b < p->levels; ++b) counts[b] = c[b];
+  return ok();
+}
+
+size_t wf_recursive_workspace_bytes(const wf_params* p, const float* proportions) {
+  int32_t c[WF_MAX_LEVELS];
+  if (check_recursion(p, proportions, c) != WF_OK) return 0;
+  return rec_layout(*p, c).total;
+}
+
+wf_status wf_filter_attend_recursive(const wf_params* p, const float* proportions,
+                                     const void* Q, const void* K, const void* V,
+                                     const void* Kg, const void* Vg, void* O,
+                                     int32_t* tok_idx, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  return recursive_impl(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, workspace,
+                        workspace_bytes, stream, nullptr, 0);
+}
+
+wf_status wf_filter_attend_recursive_timed(const wf_params* p, const float* proportions,
+                                           const void* Q, const void* K, const void* V,
+                                           const void* Kg, const void* Vg, void* O,
+                                           int32_t* tok_idx, void* workspace,
+                                           size_t workspace_bytes, void* stream,
+                                           void** events, int32_t n_events) {
+  if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
+  WF_TRY(check_shape(p));
+  for (int i = 0; i < n_events && i <= rec_kernels(*p); ++i)
+    if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
+  return recursive_impl(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, workspace,
+                        workspace_bytes, stream, events, n_events);
+}
+
+int32_t wf_filter_attend_recursive_kernels(const wf_params* p) {
+  if (check_shape(p) != WF_OK) return -1;
+  return rec_kernels(*p);
+}
+
+const char* wf_filter_attend_recursive_kernel_name(const wf_params* p, int32_t i) {
+  if (check_shape(p) != WF_OK || i < 0 || i >= rec_kernels(*p)) return nullptr;
+  return rec_kernel_name(*p, i);
 }
 
 const char* wf_status_str(wf_status s) {

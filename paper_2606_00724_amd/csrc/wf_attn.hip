@@ -38,7 +38,8 @@ struct CacheRows {
     if (r >= nr) return nullptr;
     const long rr = r0 + r;
     if (tok) {
-      if (rr < nsel) return base + ((long)u * unit_rows + tok[rr]) * D;
+      if (rr < nsel)
+        return base + ((long)u * unit_rows + min(max((long)tok[rr], 0L), unit_rows - 1)) * D;
       return tail + ((long)u * G + (rr - nsel)) * D;
     }
     return base + ((long)u * unit_rows + rr) * D;
@@ -365,7 +366,10 @@ struct RingRowPtr {
   __device__ __forceinline__ const bf16_t* operator()(int r) const {
     const long rr = min(r0 + r, rlast);
     if (toks) {
-      if (rr < nsel) return base + ((long)u * unit_rows + toks[rr - split_r0]) * D;
+      // token ids are clamped into the unit: a bad id cannot leave K / V
+      if (rr < nsel)
+        return base + ((long)u * unit_rows +
+                       min(max((long)toks[rr - split_r0], 0L), unit_rows - 1)) * D;
       return tail + ((long)u * G + (rr - nsel)) * D;
     }
     return base + ((long)u * unit_rows + rr) * D;
@@ -619,7 +623,7 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a) {
     const unsigned char* vs;
     const long row_bytes = (long)a.D * a.elem;
     if (r < a.keff) {
-      const long t = a.tok[(long)u * a.keff + r];
+      const long t = min(max((long)a.tok[(long)u * a.keff + r], 0L), (long)a.L - 1);
       ks = (const unsigned char*)a.K + ((long)u * a.L + t) * row_bytes;
       vs = (const unsigned char*)a.V + ((long)u * a.L + t) * row_bytes;
     } else {

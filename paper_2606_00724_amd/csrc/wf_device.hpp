@@ -168,9 +168,9 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   return x;
 }
 
-// Picks the k largest of score[0..n) (ties: lower index first) and writes
-// map(i) for the picked positions i in ascending order of i to out[0..k).
-// Requires 1 <= k <= n and 64 <= NT <= 1024.  score may live in LDS or
+// Picks the k largest of score[0..n) (ties: lower index first) and calls
+// emit(pos, i) for each picked position i, pos = its rank in ascending order
+// of i (0..k-1).  Requires 1 <= k <= n and 64 <= NT <= 1024.  score may live in LDS or
 // global memory; it must be visible to the whole block, and every thread of
 // the block must call this.
 //
@@ -183,8 +183,8 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
 // output positions then follow from one block scan of packed (greater,
 // equal) counts over the positions in index order:
 //   pos = #greater before + min(#equal before, copies to take).
-template <int NT, typename Map>
-__device__ void block_select_topk(const float* score, int n, int k, int32_t* out, Map map,
+template <int NT, typename Emit>
+__device__ void block_select_topk(const float* score, int n, int k, Emit emit,
                                   SelectShared<NT>& sh) {
   static_assert(NT >= 64 && NT <= 1024 && NT % 64 == 0, "block of whole waves");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -266,7 +266,7 @@ __device__ void block_select_topk(const float* score, int n, int k, int32_t* out
       const bool gt = (gt_bits >> j) & 1u;
       const bool eq = (eq_bits >> j) & 1u;
       if (gt || (eq && eq_seen < need)) {
-        if (pos < (uint32_t)k) out[pos] = map(start + j);
+        if (pos < (uint32_t)k) emit(pos, start + j);
         ++pos;
       }
       eq_seen += eq ? 1u : 0u;

@@ -313,7 +313,8 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
   }
   __syncthreads();
   int32_t* seg = a.seg + (long)u * a.S;
-  block_select_topk<NT>(w_in_lds ? wsh : W, nJ, a.S, seg, [](int i) { return (int32_t)i; }, sh);
+  block_select_topk<NT>(w_in_lds ? wsh : W, nJ, a.S,
+                        [&](uint32_t pos, int i) { seg[pos] = i; }, sh);
   __syncthreads();
   // pool normalisers: thread (q, part) folds selected blocks part, part + parts, ...
   const int parts = NT / B;

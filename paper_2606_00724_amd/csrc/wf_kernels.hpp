@@ -32,6 +32,9 @@ struct SkimTileArgs {
   const void* Q;        // [U][B][D]
   float* logits;        // [U][B][nJ]
   float* stats;         // [U][ntiles][2][B]: row max, then row sum of exp
+  const int32_t* parent;  // nullable: coefficient n is block 2 parent[n/2] + n%2
+                          // of level J ([U][npar], ascending block ids at J + 1)
+  int npar;
   int U, L, B, J, nJ;
   int cpt;              // coefficients per tile
   int ntiles;           // tiles per unit
@@ -43,7 +46,10 @@ struct SkimSelectArgs {
   const float* logits;  // [U][B][nJ]
   const float* stats;   // [U][ntiles][2][B]
   float* W;             // [U][nJ] out
-  int32_t* seg;         // [U][S] out
+  int32_t* seg;         // [U][S] out (block ids), or [U][2S] tokens when pairs
+  const int32_t* parent;  // nullable: candidate n is block 2 parent[n/2] + n%2
+  int npar;
+  int pairs;            // emit the two tokens of each kept 2-token block
   int U, B, nJ, ntiles, S;
 };
 

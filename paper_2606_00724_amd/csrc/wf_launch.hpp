@@ -50,6 +50,13 @@ struct FastPlan {
   size_t lds_bytes;
 };
 
+// Workspace extents of the multi-scale recursion (maxima over its scales).
+struct RecPlan {
+  long max_n = 0;      // candidates of the widest scale
+  int max_tiles = 0;   // coefficient tiles of the widest scale
+  long max_keep = 0;   // kept blocks of the widest selection
+};
+
 float effective_scale(const wf_params& p);
 int device_cu_count();
 
@@ -74,6 +81,18 @@ hipError_t launch_dwt(const wf_params& p, const void* K, float* approx,
 hipError_t launch_skim_tiles(const wf_params& p, bool fused, const void* Q,
                              const void* K, const float* approx, float* logits,
                              float* stats, hipStream_t s);
+// One scale b of the multi-scale recursion (Haar).  Tiles: the coarse
+// logits of its n candidates (all 2^b-blocks when parent is null, else the
+// two halves of each block in parent [U][npar]).  Select: the eq. 8 weights
+// and the top `keep`, written to out as block ids (b > 1) or as the two
+// tokens of each kept block (b = 1).
+RecPlan plan_recursion(const wf_params& p, const int32_t* counts);
+hipError_t launch_rec_tiles(const wf_params& p, int b, long n, const int32_t* parent,
+                            int npar, const void* Q, const void* K, float* logits,
+                            float* stats, hipStream_t s);
+hipError_t launch_rec_select(const wf_params& p, int b, long n, int keep,
+                             const int32_t* parent, int npar, const float* logits,
+                             const float* stats, float* W, int32_t* out, hipStream_t s);
 hipError_t launch_skim_select(const wf_params& p, int ntiles,
                               const float* logits, const float* stats,
                               float* W, int32_t* seg, hipStream_t s);

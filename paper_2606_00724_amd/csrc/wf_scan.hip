@@ -27,13 +27,13 @@ template <typename T, int D>
 struct PoolRows {
   const T* Kunit;
   const int32_t* seg;
-  long p0;
+  long p0, last;  // last: the unit's last row (region ids are clamped to it)
   int np, J, mask;
   __device__ __forceinline__ const T* operator()(int r) const {
     if (r >= np) return nullptr;
     const long p = p0 + r;
     const long tok = ((long)seg[p >> J] << J) | (p & mask);
-    return Kunit + tok * D;
+    return Kunit + min(max(tok, 0L), last) * D;
   }
 };
 
@@ -69,6 +69,7 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
   src.seg = a.seg + (long)u * a.S;
   src.J = a.J;
   src.mask = (1 << a.J) - 1;
+  src.last = (long)a.L - 1;
   src.p0 = pb;
   src.np = (int)min((long)kScanChunk, pe - pb);
   Stager st;
@@ -208,11 +209,12 @@ struct PoolRowPtr {
   const bf16_t* Kunit;
   const int32_t* segs;  // LDS: region ids from s_lo on
   long p0, plast;
+  long last;            // the unit's last row (region ids are clamped to it)
   int J, mask, s_lo;
   __device__ __forceinline__ const bf16_t* operator()(int r) const {
     const long p = min(p0 + r, plast);
     const long sg = segs[(int)(p >> J) - s_lo];
-    return Kunit + ((sg << J) | (p & mask)) * D;
+    return Kunit + min(max((sg << J) | (p & mask), 0L), last) * D;
   }
 };
 
@@ -275,6 +277,7 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
   rp.Kunit = reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.L * D;
   rp.segs = segs;
   rp.plast = pe - 1;
+  rp.last = (long)a.L - 1;
   rp.J = a.J;
   rp.mask = (1 << a.J) - 1;
   rp.s_lo = s_lo;
@@ -412,9 +415,10 @@ __global__ __launch_bounds__(kScanSelectBlock) void scan_select_kernel(
   const int32_t* seg = a.seg + (long)u * a.S;
   const int J = a.J;
   const int mask = (1 << J) - 1;
+  int32_t* tok = a.tok + (long)u * a.keff;
   block_select_topk<kScanSelectBlock>(
-      w_in_lds ? wsh : W, a.P, a.keff, a.tok + (long)u * a.keff,
-      [=](int p) { return (int32_t)((seg[p >> J] << J) | (p & mask)); }, sh);
+      w_in_lds ? wsh : W, a.P, a.keff,
+      [&](uint32_t pos, int p) { tok[pos] = (seg[p >> J] << J) | (p & mask); }, sh);
 }
 
 // ------------------------------------------------------------ host side

@@ -227,9 +227,10 @@ __global__ __launch_bounds__(kBlock) void dwt_kernel(DwtArgs a, Taps taps) {
 // ------------------------------------------------------------ skim tiles
 
 // Haar level-J approximation of tile rows [n0, n0 + ncoef) into LDS.
-template <typename T, int D>
+// Coefficient n covers tokens bid(n) 2^J .. bid(n) 2^J + 2^J - 1.
+template <typename T, int D, class BlockId>
 __device__ void haar_sum_tile(const T* Kunit, long n0, int ncoef, int J,
-                              float inv_norm, float* coef) {
+                              float inv_norm, float* coef, const BlockId& bid) {
   constexpr int CPL = 16 / sizeof(T);  // channels per lane (16-byte load)
   constexpr int LPR = D / CPL;         // lanes per row
   constexpr int RPL = kWave / LPR;     // rows per wave load
@@ -241,23 +242,24 @@ __device__ void haar_sum_tile(const T* Kunit, long n0, int ncoef, int J,
   const int loads = G / RPL;
   const int cpg = G / blk;               // coefficients per group
   const int red = blk < RPL ? blk : RPL; // rows reduced across lanes
-  const long tok0 = n0 << J;
-  const long tok_end = (n0 + ncoef) << J;
-  const int ngroups = (int)(((long)ncoef * blk + G - 1) / G);
+  const long rows = (long)ncoef << J;  // tile rows, in coefficient order
+  const int ngroups = (int)((rows + G - 1) / G);
   for (int grp = wave; grp < ngroups; grp += kBlock / kWave) {
     float acc[CPL];
 #pragma unroll
     for (int e = 0; e < CPL; ++e) acc[e] = 0.f;
-    const long r0 = tok0 + (long)grp * G + rsub;
+    const long r0 = (long)grp * G + rsub;
     for (int i0 = 0; i0 < loads; i0 += 8) {
       u32x4 v[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const long t = r0 + (long)(i0 + k) * RPL;
-        if (i0 + k < loads && t < tok_end)
+        const long r = r0 + (long)(i0 + k) * RPL;
+        if (i0 + k < loads && r < rows) {
+          const long t = ((long)bid(n0 + (r >> J)) << J) + (r & (blk - 1));
           v[k] = *reinterpret_cast<const u32x4*>(Kunit + t * D + csub * CPL);
-        else
+        } else {
           v[k] = u32x4{0u, 0u, 0u, 0u};
+        }
       }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -434,7 +436,17 @@ __global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
     const int ncoef = (int)min((long)a.cpt, (long)a.nJ - n0);
     if constexpr (SRC == kHaarSum) {
       const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
-      haar_sum_tile<T, D>(Kunit, n0, ncoef, a.J, taps.inv_norm, coef);
+      if (a.parent) {
+        // block ids are clamped into the unit: a bad id cannot leave K
+        const int32_t* par = a.parent + (long)u * a.npar;
+        const long last = ((long)a.L >> a.J) - 1;
+        haar_sum_tile<T, D>(Kunit, n0, ncoef, a.J, taps.inv_norm, coef, [=](long n) {
+          return min(max(2L * par[n >> 1] + (n & 1), 0L), last);
+        });
+      } else {
+        haar_sum_tile<T, D>(Kunit, n0, ncoef, a.J, taps.inv_norm, coef,
+                            [](long n) { return n; });
+      }
     } else if constexpr (SRC == kCascade) {
       const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
       cascade_tile<M, J, T, D>(Kunit, a.L, n0, ncoef, a.cpt,
@@ -494,8 +506,22 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
   }
   __syncthreads();
   const float* src = w_in_lds ? wsh : W;
-  block_select_topk<kSelectBlock>(src, a.nJ, a.S, a.seg + (long)u * a.S,
-                                  [](int i) { return (int32_t)i; }, sh);
+  // candidate n is block n, or on a refinement scale child n % 2 of kept
+  // block parent[n / 2]; the last scale emits the two tokens of each block
+  const int32_t* par = a.parent ? a.parent + (long)u * a.npar : nullptr;
+  auto block_of = [&](int n) -> int32_t { return par ? 2 * par[n >> 1] + (n & 1) : n; };
+  if (a.pairs) {
+    int32_t* tok = a.seg + (long)u * 2 * a.S;
+    block_select_topk<kSelectBlock>(src, a.nJ, a.S, [&](uint32_t pos, int n) {
+      const int32_t id = block_of(n);
+      tok[2 * pos] = 2 * id;
+      tok[2 * pos + 1] = 2 * id + 1;
+    }, sh);
+  } else {
+    int32_t* seg = a.seg + (long)u * a.S;
+    block_select_topk<kSelectBlock>(src, a.nJ, a.S,
+                                    [&](uint32_t pos, int n) { seg[pos] = block_of(n); }, sh);
+  }
 }
 
 // ------------------------------------------------------------ host side
@@ -628,53 +654,111 @@ static hipError_t skim_dispatch(int source, const SkimTileArgs& a,
   }
 }
 
-hipError_t launch_skim_tiles(const wf_params& p, bool fused, const void* Q,
-                             const void* K, const float* approx, float* logits,
-                             float* stats, hipStream_t s) {
-  const SkimPlan pl = plan_skim(p, fused);
+// Haar coefficient tile size at level J.
+static int haar_cpt(int J) { return std::min(kMaxCoefTile, std::max(16, 2048 >> J)); }
+
+static hipError_t skim_tiles_common(const wf_params& p, int source, int cpt, int J,
+                                    long nJ, const int32_t* parent, int npar,
+                                    const void* Q, const void* K, const float* approx,
+                                    float* logits, float* stats, hipStream_t s) {
   SkimTileArgs a;
   a.K = K;
   a.approx = approx;
   a.Q = Q;
   a.logits = logits;
   a.stats = stats;
+  a.parent = parent;
+  a.npar = npar;
   a.U = p.batch * p.heads;
   a.L = p.ctx_len;
   a.B = p.q_len;
-  a.J = p.levels;
-  a.nJ = p.ctx_len >> p.levels;
-  a.cpt = pl.cpt;
-  a.ntiles = pl.ntiles;
+  a.J = J;
+  a.nJ = (int)nJ;
+  a.cpt = cpt;
+  a.ntiles = (int)((nJ + cpt - 1) / cpt);
   a.boundary = p.boundary;
   a.scale = effective_scale(p);
-  const Taps taps = make_taps(p.wavelet, p.levels);
+  const size_t lds = (size_t)cpt * (p.head_dim + kCoefPad) * sizeof(float);
+  const Taps taps = make_taps(p.wavelet, J);
   if (p.dtype == WF_BF16)
-    return p.head_dim == 128
-               ? skim_dispatch<bf16_t, 128>(pl.source, a, taps, pl.lds_bytes, s)
-               : skim_dispatch<bf16_t, 64>(pl.source, a, taps, pl.lds_bytes, s);
-  return p.head_dim == 128
-             ? skim_dispatch<float, 128>(pl.source, a, taps, pl.lds_bytes, s)
-             : skim_dispatch<float, 64>(pl.source, a, taps, pl.lds_bytes, s);
+    return p.head_dim == 128 ? skim_dispatch<bf16_t, 128>(source, a, taps, lds, s)
+                             : skim_dispatch<bf16_t, 64>(source, a, taps, lds, s);
+  return p.head_dim == 128 ? skim_dispatch<float, 128>(source, a, taps, lds, s)
+                           : skim_dispatch<float, 64>(source, a, taps, lds, s);
+}
+
+hipError_t launch_skim_tiles(const wf_params& p, bool fused, const void* Q,
+                             const void* K, const float* approx, float* logits,
+                             float* stats, hipStream_t s) {
+  const SkimPlan pl = plan_skim(p, fused);
+  return skim_tiles_common(p, pl.source, pl.cpt, p.levels, (long)p.ctx_len >> p.levels,
+                           nullptr, 0, Q, K, approx, logits, stats, s);
+}
+
+static hipError_t skim_select_common(const wf_params& p, long nJ, int ntiles, int S,
+                                     const int32_t* parent, int npar, int pairs,
+                                     const float* logits, const float* stats, float* W,
+                                     int32_t* out, hipStream_t s) {
+  SkimSelectArgs a;
+  a.logits = logits;
+  a.stats = stats;
+  a.W = W;
+  a.seg = out;
+  a.parent = parent;
+  a.npar = npar;
+  a.pairs = pairs;
+  a.U = p.batch * p.heads;
+  a.B = p.q_len;
+  a.nJ = (int)nJ;
+  a.ntiles = ntiles;
+  a.S = S;
+  const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
+  const size_t lds = in_lds ? (size_t)a.nJ * sizeof(float) : 0;
+  if (lds > 32768) {  // with the static arrays, past the default 64 KiB
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(skim_select_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kSelectBlock),
+                     lds, s, a, in_lds);
+  return hipGetLastError();
 }
 
 hipError_t launch_skim_select(const wf_params& p, int ntiles,
                               const float* logits, const float* stats,
                               float* W, int32_t* seg, hipStream_t s) {
-  SkimSelectArgs a;
-  a.logits = logits;
-  a.stats = stats;
-  a.W = W;
-  a.seg = seg;
-  a.U = p.batch * p.heads;
-  a.B = p.q_len;
-  a.nJ = p.ctx_len >> p.levels;
-  a.ntiles = ntiles;
-  a.S = p.segments;
-  const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
-  const size_t lds = in_lds ? (size_t)a.nJ * sizeof(float) : 0;
-  hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kSelectBlock),
-                     lds, s, a, in_lds);
-  return hipGetLastError();
+  return skim_select_common(p, (long)p.ctx_len >> p.levels, ntiles, p.segments, nullptr, 0,
+                            0, logits, stats, W, seg, s);
+}
+
+RecPlan plan_recursion(const wf_params& p, const int32_t* counts) {
+  RecPlan r{};
+  long n = (long)p.ctx_len >> p.levels;
+  for (int b = p.levels; b >= 1; --b) {
+    const int cpt = haar_cpt(b);
+    const int ntiles = (int)((n + cpt - 1) / cpt);
+    r.max_n = std::max(r.max_n, n);
+    r.max_tiles = std::max(r.max_tiles, ntiles);
+    r.max_keep = std::max(r.max_keep, (long)counts[b - 1]);
+    n = 2L * counts[b - 1];
+  }
+  return r;
+}
+
+hipError_t launch_rec_tiles(const wf_params& p, int b, long n, const int32_t* parent,
+                            int npar, const void* Q, const void* K, float* logits,
+                            float* stats, hipStream_t s) {
+  return skim_tiles_common(p, kHaarSum, haar_cpt(b), b, n, parent, npar, Q, K, nullptr,
+                           logits, stats, s);
+}
+
+hipError_t launch_rec_select(const wf_params& p, int b, long n, int keep,
+                             const int32_t* parent, int npar, const float* logits,
+                             const float* stats, float* W, int32_t* out, hipStream_t s) {
+  const int cpt = haar_cpt(b);
+  const int ntiles = (int)((n + cpt - 1) / cpt);
+  return skim_select_common(p, n, ntiles, keep, parent, npar, b == 1 ? 1 : 0, logits,
+                            stats, W, out, s);
 }
 
 }  // namespace wf

@@ -66,6 +66,8 @@ class Workload:
     seed: int
     layers: int = 1
     gen_len: int = 0      # G, always-kept generation tail (K_g, V_g)
+    # multi-scale recursion: m_b at index b - 1 (empty: the two-stage path)
+    proportions: tuple = ()
     description: str = field(default="", compare=False)
 
     @property
@@ -122,6 +124,27 @@ _add(Workload("stress128k", batch=1, heads=32, ctx_len=131072, head_dim=128,
               segments=_pool_segments(131072, 6, 4096), budget=4096, seed=4,
               description="128K stress: 32 heads, d=128, L=131072, B=32, "
                           "bf16, Daubechies-2 J=6 symmetric, budget 4096"))
+
+
+# The paper's own schedule (scales B..1, proportions m_b) on the inputs of
+# two of the workloads above (same seeds, hence the same tensors).
+_add(Workload("recursion8b", batch=1, heads=32, ctx_len=4096, head_dim=128,
+              q_len=32, dtype="bf16", rho=0.95, needles=4, wavelet="haar",
+              boundary="symmetric", levels=3,
+              segments=_pool_segments(4096, 3, 512), budget=512, seed=1,
+              proportions=(0.5, 0.5, 0.25),
+              description="8B-DLM layer with the multi-scale recursion: 32 "
+                          "heads, d=128, L=4096, B=32, bf16, Haar, scales "
+                          "3..1, m = (0.25, 0.5, 0.5) from the top"))
+_add(Workload("recursion32k", batch=4, heads=32, ctx_len=32768, head_dim=128,
+              q_len=64, dtype="bf16", rho=0.98, needles=8, wavelet="haar",
+              boundary="symmetric", levels=2,
+              segments=_pool_segments(32768, 2, 2048), budget=2048, seed=3,
+              proportions=(0.5, 0.25),
+              description="32K context with the multi-scale recursion at the "
+                          "paper's scale B=2: batch 4, 32 heads, d=128, "
+                          "L=32768, B=64, bf16, Haar, m_2=0.25, m_1=0.5 "
+                          "(4096 positions kept)"))
 
 
 def needle_starts(w: Workload, layer: int, batch: int) -> np.ndarray:

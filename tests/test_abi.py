@@ -165,3 +165,54 @@ def test_product_path_does_not_use_the_oracle():
                 text = open(os.path.join(dirpath, f)).read().lower()
                 assert "oracle" not in text, f
     assert "oracle" not in open(HEADER).read().lower()
+
+
+# ------------------------------------------------------------ recursion
+
+@pytest.mark.parametrize("levels,props", [
+    (1, [0.25]), (2, [0.5, 0.25]), (3, [0.3, 0.55, 0.01]),
+    (5, [0.9, 0.7, 0.5, 0.5, 0.125])])
+def test_recursion_counts_match_the_oracle(wfpkg, ref, levels, props):
+    """The library's count arithmetic equals the oracle's on the same
+    (float32) proportions: c_b = max(1, ceil(m_b n_b)), n_b = 2 c_{b+1}."""
+    import numpy as np
+    p = _params(wfpkg, ctx_len=2048, levels=levels, dtype="bf16")
+    got = wfpkg.recursion_counts(p, props)
+    n = 2048 >> levels
+    want = [0] * levels
+    for b in range(levels, 0, -1):
+        want[b - 1] = ref.recursion_count(float(np.float32(props[b - 1])), n)
+        n = 2 * want[b - 1]
+    assert got == want
+    assert wfpkg.recursive_workspace_bytes(p, props) > 0
+
+
+@pytest.mark.parametrize("props", [[0.0, 0.5], [1.5, 0.5], [float("nan"), 1.0],
+                                   [0.5, -0.1]])
+def test_recursion_rejects_bad_proportions(wfpkg, props):
+    lib = wfpkg.library()
+    p = _params(wfpkg, levels=2, dtype="bf16")
+    arr = (ctypes.c_float * 2)(*props)
+    out = (ctypes.c_int32 * 2)()
+    assert lib.wf_recursion_counts(ctypes.byref(p), arr, out) == 1
+    assert lib.wf_recursive_workspace_bytes(ctypes.byref(p), arr) == 0
+    assert lib.wf_recursion_counts(ctypes.byref(p), None, out) == 1
+
+
+def test_recursion_db2_is_unsupported(wfpkg):
+    """The GPU recursion is built for Haar; db2 is refused before any
+    pointer is used."""
+    lib = wfpkg.library()
+    p = _params(wfpkg, levels=2, dtype="bf16", wavelet="db2")
+    arr = (ctypes.c_float * 2)(0.5, 0.5)
+    good = ctypes.c_void_p(256)
+    assert lib.wf_filter_attend_recursive(ctypes.byref(p), arr, good, good,
+                                          good, None, None, good, None, good,
+                                          1 << 30, None) == 2
+
+
+def test_recursion_kernel_sequence(wfpkg):
+    p = _params(wfpkg, levels=3, dtype="bf16")
+    assert wfpkg.recursive_kernel_names(p) == [
+        "rec_tiles_b3", "rec_select_b3", "rec_tiles_b2", "rec_select_b2",
+        "rec_tiles_b1", "rec_select_b1", "sparse_attn", "attn_combine"]
