@@ -38,13 +38,18 @@ METRIC = ("context tokens filtered+attended/sec per layer @32K ctx; "
           "% of HBM peak")
 
 
-def algorithmic_bytes(w, keff: int) -> dict:
+def algorithmic_bytes(w, keff: int, counts=None) -> dict:
     """Bytes the method must move per unit (each counted once): every key
-    (DWT + skim), the pool keys re-read by the scan, the selected values,
-    the query block in and the output out."""
+    (DWT + skim), the candidate keys re-read by the finer scales (the pool
+    of the scan; for the multi-scale recursion the kept blocks of every
+    scale above the last), the selected values, the query block in and the
+    output out."""
     e = 2 if w.dtype == "bf16" else 4
     d = w.head_dim
-    pool = w.segments << w.levels
+    if counts:  # recursion: |mu^b| = 2^{b+1} c_{b+1} positions at scale b < B
+        pool = sum(counts[b] << (b + 1) for b in range(len(counts) - 1))
+    else:
+        pool = w.segments << w.levels
     per_unit = {
         "keys": w.ctx_len * d * e,
         "pool": pool * d * e,
@@ -115,6 +120,8 @@ def cpu_baseline(w, Q, K, V, min_seconds: float = 10.0) -> dict:
     """The oracle as it stands, on every unit of the layer, in chunks of 16
     units, repeated until about min_seconds of oracle time have passed (at
     most 50 passes; only the oracle calls are timed)."""
+    import numpy as np
+
     import oracle
     oracle.build(force=False)
     U = w.units
@@ -128,8 +135,15 @@ def cpu_baseline(w, Q, K, V, min_seconds: float = 10.0) -> dict:
         for u0 in range(0, U, chunk):
             qa, ka, va = (oracle._f64(x[u0:u0 + chunk]) for x in (q, k, v))
             t0 = time.perf_counter()
-            oracle.filter_attend(qa, ka, va, w.levels, w.segments, w.budget,
-                                 wavelet=w.wavelet, boundary=w.boundary)
+            if w.proportions:
+                oracle.filter_attend_recursive(
+                    qa, ka, va, w.levels,
+                    [float(np.float32(m)) for m in w.proportions],
+                    wavelet=w.wavelet, boundary=w.boundary)
+            else:
+                oracle.filter_attend(qa, ka, va, w.levels, w.segments,
+                                     w.budget, wavelet=w.wavelet,
+                                     boundary=w.boundary)
             elapsed += time.perf_counter() - t0
             del qa, ka, va
         passes += 1
@@ -173,24 +187,40 @@ def main() -> int:
     Q, K, V = synth.make_inputs(w)
     dev = torch.device("cuda:0")
     p = wf.params_for(w, gen_len=0)
-    keff = wf.effective_budget(p)
+    recursive = bool(w.proportions)
+    counts = wf.recursion_counts(p, w.proportions) if recursive else None
+    keff = 2 * counts[0] if recursive else wf.effective_budget(p)
     Qd, Kd, Vd = Q.to(dev), K.to(dev), V.to(dev)
     O = torch.empty_like(Qd)
     tok = torch.empty((w.batch, w.heads, keff), dtype=torch.int32, device=dev)
-    ws = wf.alloc_workspace(p, wf.OP_FUSED, dev)
-    names = wf.fused_kernel_names(p)
+    if recursive:
+        ws = torch.empty(wf.recursive_workspace_bytes(p, w.proportions),
+                         dtype=torch.uint8, device=dev)
+        names = wf.recursive_kernel_names(p)
+    else:
+        ws = wf.alloc_workspace(p, wf.OP_FUSED, dev)
+        names = wf.fused_kernel_names(p)
     ev = HipEvents((len(names) + 1) * args.steps)
     stream = torch.cuda.current_stream()
 
     def step_plain():
-        wf.wf_filter_attend(p, Qd, Kd, Vd, None, None, O, tok, None, ws,
-                            stream)
+        if recursive:
+            wf.wf_filter_attend_recursive(p, w.proportions, Qd, Kd, Vd, None,
+                                          None, O, tok, ws, stream)
+        else:
+            wf.wf_filter_attend(p, Qd, Kd, Vd, None, None, O, tok, None, ws,
+                                stream)
 
     def step_timed(i):
         base = i * (len(names) + 1)
-        wf.wf_filter_attend_timed(p, Qd, Kd, Vd, None, None, O, tok, None,
-                                  ws, ev.ev[base:base + len(names) + 1],
-                                  stream)
+        evs = ev.ev[base:base + len(names) + 1]
+        if recursive:
+            wf.wf_filter_attend_recursive_timed(p, w.proportions, Qd, Kd, Vd,
+                                                None, None, O, tok, ws, evs,
+                                                stream)
+        else:
+            wf.wf_filter_attend_timed(p, Qd, Kd, Vd, None, None, O, tok,
+                                      None, ws, evs, stream)
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -236,7 +266,7 @@ def main() -> int:
     per_kernel = {n: t / args.steps for n, t in per_kernel.items()}
     ev.close()
 
-    alg = algorithmic_bytes(w, keff)
+    alg = algorithmic_bytes(w, keff, counts)
     U = w.units
     tokens = w.batch * w.ctx_len
     value = tokens / (ms_step * 1e-3)
@@ -261,8 +291,10 @@ def main() -> int:
             "workload": w.description,
             "batch": w.batch, "heads": w.heads, "ctx_len": w.ctx_len,
             "head_dim": w.head_dim, "q_len": w.q_len, "levels": w.levels,
-            "wavelet": w.wavelet, "segments": w.segments,
-            "budget": w.budget, "k_eff": keff, "gen_len": 0,
+            "wavelet": w.wavelet, "gen_len": 0,
+            **({"proportions": list(w.proportions), "counts": counts,
+                "kept_positions": keff} if recursive else
+               {"segments": w.segments, "budget": w.budget, "k_eff": keff}),
         },
         "roofline": {
             "bound": "hbm",

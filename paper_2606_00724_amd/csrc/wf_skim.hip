@@ -227,66 +227,97 @@ __global__ __launch_bounds__(kBlock) void dwt_kernel(DwtArgs a, Taps taps) {
 // ------------------------------------------------------------ skim tiles
 
 // Haar level-J approximation of tile rows [n0, n0 + ncoef) into LDS.
-// Coefficient n covers tokens bid(n) 2^J .. bid(n) 2^J + 2^J - 1.
-template <typename T, int D, class BlockId>
-__device__ void haar_sum_tile(const T* Kunit, long n0, int ncoef, int J,
-                              float inv_norm, float* coef, const BlockId& bid) {
+// Coefficient n covers tokens bid(n) 2^J .. bid(n) 2^J + 2^J - 1.  A wave
+// sums groups of G = max(2^J, RPL) rows (RPL rows per 16-byte wave load):
+// one coefficient per group, or RPL / 2^J of them reduced across lanes.
+// LOADS = G / RPL loads per group (8 stands for 8 or more); small groups
+// are taken 8 / LOADS at a time so that a lane always has 8 loads in flight.
+template <typename T, int D, int LOADS, class BlockId>
+__device__ void haar_sum_tile_groups(const T* Kunit, long n0, int ncoef, int J,
+                                     float inv_norm, float* coef, const BlockId& bid) {
   constexpr int CPL = 16 / sizeof(T);  // channels per lane (16-byte load)
   constexpr int LPR = D / CPL;         // lanes per row
   constexpr int RPL = kWave / LPR;     // rows per wave load
   constexpr int STRIDE = D + kCoefPad;
+  constexpr int NW = kBlock / kWave;
+  constexpr int GPI = LOADS >= 8 ? 1 : 8 / LOADS;  // groups per iteration
+  constexpr int LPI = LOADS >= 8 ? 8 : LOADS;      // loads per group and batch
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rsub = lane / LPR, csub = lane % LPR;
   const int blk = 1 << J;
-  const int G = blk > RPL ? blk : RPL;  // rows per group
-  const int loads = G / RPL;
-  const int cpg = G / blk;               // coefficients per group
-  const int red = blk < RPL ? blk : RPL; // rows reduced across lanes
-  const long rows = (long)ncoef << J;  // tile rows, in coefficient order
+  const int G = blk > RPL ? blk : RPL;
+  const int cpg = G / blk;                // coefficients per group
+  const int red = blk < RPL ? blk : RPL;  // rows reduced across lanes
+  const long rows = (long)ncoef << J;     // tile rows, in coefficient order
   const int ngroups = (int)((rows + G - 1) / G);
-  for (int grp = wave; grp < ngroups; grp += kBlock / kWave) {
-    float acc[CPL];
+  const int nloads = LOADS >= 8 ? G / RPL : 1;  // batches of LPI loads per group
+  for (int gb = wave; gb < ngroups; gb += NW * GPI) {
+    float acc[GPI][CPL];
 #pragma unroll
-    for (int e = 0; e < CPL; ++e) acc[e] = 0.f;
-    const long r0 = (long)grp * G + rsub;
-    for (int i0 = 0; i0 < loads; i0 += 8) {
-      u32x4 v[8];
+    for (int gi = 0; gi < GPI; ++gi)
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const long r = r0 + (long)(i0 + k) * RPL;
-        if (i0 + k < loads && r < rows) {
-          const long t = ((long)bid(n0 + (r >> J)) << J) + (r & (blk - 1));
-          v[k] = *reinterpret_cast<const u32x4*>(Kunit + t * D + csub * CPL);
-        } else {
-          v[k] = u32x4{0u, 0u, 0u, 0u};
-        }
-      }
+      for (int e = 0; e < CPL; ++e) acc[gi][e] = 0.f;
+    for (int i0 = 0; i0 < nloads; i0 += LPI) {
+      u32x4 v[GPI][LPI];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        if constexpr (sizeof(T) == 2) {
+      for (int gi = 0; gi < GPI; ++gi)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            acc[2 * e] += bf16_lo(v[k][e]);
-            acc[2 * e + 1] += bf16_hi(v[k][e]);
+        for (int li = 0; li < LPI; ++li) {
+          const int grp = gb + gi * NW;
+          const long r = (long)grp * G + rsub + (long)(i0 + li) * RPL;
+          if (grp < ngroups && r < rows) {
+            const long t = ((long)bid(n0 + (r >> J)) << J) + (r & (blk - 1));
+            v[gi][li] = *reinterpret_cast<const u32x4*>(Kunit + t * D + csub * CPL);
+          } else {
+            v[gi][li] = u32x4{0u, 0u, 0u, 0u};
           }
-        } else {
+        }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc[e] += __uint_as_float(v[k][e]);
+      for (int gi = 0; gi < GPI; ++gi)
+#pragma unroll
+        for (int li = 0; li < LPI; ++li) {
+          if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              acc[gi][2 * e] += bf16_lo(v[gi][li][e]);
+              acc[gi][2 * e + 1] += bf16_hi(v[gi][li][e]);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[gi][e] += __uint_as_float(v[gi][li][e]);
+          }
+        }
+    }
+#pragma unroll
+    for (int gi = 0; gi < GPI; ++gi) {
+      for (int sh = 1; sh < red; sh <<= 1) {
+#pragma unroll
+        for (int e = 0; e < CPL; ++e) acc[gi][e] += __shfl_xor(acc[gi][e], LPR * sh);
+      }
+      const int grp = gb + gi * NW;
+      if (grp < ngroups && rsub % red == 0) {
+        const int c = grp * cpg + rsub / blk;
+        if (c < ncoef) {
+          float* dst = coef + c * STRIDE + csub * CPL;
+#pragma unroll
+          for (int e = 0; e < CPL; ++e) dst[e] = acc[gi][e] * inv_norm;
         }
       }
     }
-    for (int s = 1; s < red; s <<= 1) {
-#pragma unroll
-      for (int e = 0; e < CPL; ++e) acc[e] += __shfl_xor(acc[e], LPR * s);
-    }
-    if (rsub % red == 0) {
-      const int c = grp * cpg + rsub / blk;
-      if (c < ncoef) {
-        float* dst = coef + c * STRIDE + csub * CPL;
-#pragma unroll
-        for (int e = 0; e < CPL; ++e) dst[e] = acc[e] * inv_norm;
-      }
-    }
+  }
+}
+
+template <typename T, int D, class BlockId>
+__device__ void haar_sum_tile(const T* Kunit, long n0, int ncoef, int J, float inv_norm,
+                              float* coef, const BlockId& bid) {
+  constexpr int RPL = kWave / (D / (16 / (int)sizeof(T)));
+  const int blk = 1 << J;
+  const int loads = (blk > RPL ? blk : RPL) / RPL;
+  switch (loads) {
+    case 1: haar_sum_tile_groups<T, D, 1>(Kunit, n0, ncoef, J, inv_norm, coef, bid); break;
+    case 2: haar_sum_tile_groups<T, D, 2>(Kunit, n0, ncoef, J, inv_norm, coef, bid); break;
+    case 4: haar_sum_tile_groups<T, D, 4>(Kunit, n0, ncoef, J, inv_norm, coef, bid); break;
+    default: haar_sum_tile_groups<T, D, 8>(Kunit, n0, ncoef, J, inv_norm, coef, bid); break;
   }
 }
 
@@ -489,6 +520,36 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
   __syncthreads();
   const float* lg = a.logits + (long)u * a.B * a.nJ;
   float* W = a.W + (long)u * a.nJ;
+  if ((a.nJ & 3) == 0) {
+    // four adjacent columns per thread, 8 query rows of loads in flight
+    constexpr int QB = 8;
+    for (int j4 = threadIdx.x; j4 < a.nJ / 4; j4 += kSelectBlock) {
+      float w[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int q0 = 0; q0 < a.B; q0 += QB) {
+        float4 v[QB];
+#pragma unroll
+        for (int i = 0; i < QB; ++i)
+          v[i] = q0 + i < a.B ? *reinterpret_cast<const float4*>(lg + (long)(q0 + i) * a.nJ + 4 * j4)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int i = 0; i < QB; ++i) {
+          if (q0 + i < a.B) {
+            const float m = row_max[q0 + i], r = row_inv[q0 + i];
+            w[0] += __expf(v[i].x - m) * r;
+            w[1] += __expf(v[i].y - m) * r;
+            w[2] += __expf(v[i].z - m) * r;
+            w[3] += __expf(v[i].w - m) * r;
+          }
+        }
+      }
+      *reinterpret_cast<float4*>(W + 4 * j4) = make_float4(w[0], w[1], w[2], w[3]);
+      if (w_in_lds) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) wsh[4 * j4 + e] = w[e];
+      }
+    }
+    __syncthreads();
+  } else {
   constexpr int RB = 8;  // rows in flight per thread
   for (int j = threadIdx.x; j < a.nJ; j += kSelectBlock) {
     float w = 0.f;
@@ -505,6 +566,7 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
     if (w_in_lds) wsh[j] = w;
   }
   __syncthreads();
+  }
   const float* src = w_in_lds ? wsh : W;
   // candidate n is block n, or on a refinement scale child n % 2 of kept
   // block parent[n / 2]; the last scale emits the two tokens of each block
