@@ -79,7 +79,8 @@ enum { WF_EXT_SYMMETRIC = 0, WF_EXT_PERIODIC = 1 };
 enum { WF_BF16 = 0, WF_F32 = 1 };
 
 /* Operations whose workspace size wf_workspace_bytes reports. */
-enum { WF_OP_SKIM = 0, WF_OP_SCAN = 1, WF_OP_ATTN = 2, WF_OP_FUSED = 3 };
+enum { WF_OP_SKIM = 0, WF_OP_SCAN = 1, WF_OP_ATTN = 2, WF_OP_FUSED = 3,
+       WF_OP_CACHED = 4 };
 
 /* Limits of this build. */
 enum {
@@ -216,6 +217,41 @@ wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
  * name of the i-th one (static strings), or -1 / NULL if p is invalid. */
 int32_t wf_filter_attend_kernels(const wf_params* p);
 const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i);
+
+/* ---------------------------------------------------------------------
+ * One step with the coarse prompt keys cached across denoising steps.  The
+ * cache update of eq. 4 rewrites only the generation rows, so the prompt's
+ * level-J approximation A_J (eq. 6) stays valid from step to step: compute
+ * it once with wf_dwt_keys and pass it to every later step.  The step then
+ * reads A_J ([batch][heads][ctx_len >> levels][d] fp32, as wf_dwt_keys
+ * writes it) instead of all of K; K is still read for the pool and the
+ * selected rows.  Results are those of wf_filter_attend with that A_J.
+ *   approx     device, from wf_dwt_keys with the same params
+ *   workspace  >= wf_workspace_bytes(p, WF_OP_CACHED)
+ * Other arguments and errors as in wf_filter_attend.
+ * --------------------------------------------------------------------- */
+wf_status wf_filter_attend_cached(const wf_params* p, const void* Q,
+                                  const float* approx, const void* K,
+                                  const void* V, const void* Kg,
+                                  const void* Vg, void* O, int32_t* tok_idx,
+                                  int32_t* seg_idx, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* Same, recording events[i] before kernel i and events[n] after the last
+ * (n = wf_filter_attend_cached_kernels(p); n_events >= n + 1). */
+wf_status wf_filter_attend_cached_timed(const wf_params* p, const void* Q,
+                                        const float* approx, const void* K,
+                                        const void* V, const void* Kg,
+                                        const void* Vg, void* O,
+                                        int32_t* tok_idx, int32_t* seg_idx,
+                                        void* workspace,
+                                        size_t workspace_bytes, void* stream,
+                                        void** events, int32_t n_events);
+
+/* Kernels one cached call queues and the name of the i-th one, or -1 /
+ * NULL if p is invalid. */
+int32_t wf_filter_attend_cached_kernels(const wf_params* p);
+const char* wf_filter_attend_cached_kernel_name(const wf_params* p, int32_t i);
 
 /* ---------------------------------------------------------------------
  * Multi-scale recursive filtering (Section 3.2, eqs. 9-11; Algorithm 1,

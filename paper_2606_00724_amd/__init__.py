@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libwavefilter.so")
 HAAR, DB2 = 0, 1
 EXT_SYMMETRIC, EXT_PERIODIC = 0, 1
 BF16, F32 = 0, 1
-OP_SKIM, OP_SCAN, OP_ATTN, OP_FUSED = 0, 1, 2, 3
+OP_SKIM, OP_SCAN, OP_ATTN, OP_FUSED, OP_CACHED = 0, 1, 2, 3, 4
 MAX_LEVELS, MAX_Q_LEN = 10, 256
 
 _STATUS = {0: "WF_OK", 1: "WF_ERR_INVALID_ARG", 2: "WF_ERR_UNSUPPORTED",
@@ -30,6 +30,9 @@ EXPORTED = ("wf_workspace_bytes", "wf_effective_budget", "wf_dwt_keys",
             "wf_skim_score", "wf_scan_select", "wf_gather_kv",
             "wf_sparse_attn", "wf_filter_attend", "wf_filter_attend_timed",
             "wf_filter_attend_kernels", "wf_filter_attend_kernel_name",
+            "wf_filter_attend_cached", "wf_filter_attend_cached_timed",
+            "wf_filter_attend_cached_kernels",
+            "wf_filter_attend_cached_kernel_name",
             "wf_recursion_counts", "wf_recursive_workspace_bytes",
             "wf_filter_attend_recursive", "wf_filter_attend_recursive_timed",
             "wf_filter_attend_recursive_kernels",
@@ -78,6 +81,15 @@ def _load() -> ctypes.CDLL:
                                     vp, ctypes.POINTER(vp), i32]),
         "wf_filter_attend_kernels": (i32, [P]),
         "wf_filter_attend_kernel_name": (ctypes.c_char_p, [P, i32]),
+        "wf_filter_attend_cached": (ctypes.c_int,
+                                    [P, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                     vp, sz, vp]),
+        "wf_filter_attend_cached_timed": (ctypes.c_int,
+                                          [P, vp, vp, vp, vp, vp, vp, vp, vp,
+                                           vp, vp, sz, vp, ctypes.POINTER(vp),
+                                           i32]),
+        "wf_filter_attend_cached_kernels": (i32, [P]),
+        "wf_filter_attend_cached_kernel_name": (ctypes.c_char_p, [P, i32]),
         "wf_recursion_counts": (ctypes.c_int, [P, fp, ip]),
         "wf_recursive_workspace_bytes": (sz, [P, fp]),
         "wf_filter_attend_recursive": (ctypes.c_int,
@@ -234,6 +246,62 @@ def wf_filter_attend_timed(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
                                        _ptr(V), _ptr(Kg), _ptr(Vg), _ptr(O),
                                        _ptr(tok_idx), _ptr(seg_idx), ws, nb,
                                        _stream(stream), arr, len(events)))
+
+
+# ------------------------------------------------------------ cached A_J
+# A_J of the prompt keys (wf_dwt_keys) reused by every later step.
+
+def cached_kernel_names(p: WfParams) -> list[str]:
+    n = _lib.wf_filter_attend_cached_kernels(ctypes.byref(p))
+    return [_lib.wf_filter_attend_cached_kernel_name(ctypes.byref(p),
+                                                     i).decode()
+            for i in range(n)]
+
+
+def wf_filter_attend_cached(p, Q, approx, K, V, Kg, Vg, O, tok_idx, seg_idx,
+                            workspace, stream=None):
+    ws, nb = _ws(workspace)
+    _check(_lib.wf_filter_attend_cached(
+        ctypes.byref(p), _ptr(Q), _ptr(approx), _ptr(K), _ptr(V), _ptr(Kg),
+        _ptr(Vg), _ptr(O), _ptr(tok_idx), _ptr(seg_idx), ws, nb,
+        _stream(stream)))
+
+
+def wf_filter_attend_cached_timed(p, Q, approx, K, V, Kg, Vg, O, tok_idx,
+                                  seg_idx, workspace, events, stream=None):
+    ws, nb = _ws(workspace)
+    arr = (ctypes.c_void_p * len(events))(*events)
+    _check(_lib.wf_filter_attend_cached_timed(
+        ctypes.byref(p), _ptr(Q), _ptr(approx), _ptr(K), _ptr(V), _ptr(Kg),
+        _ptr(Vg), _ptr(O), _ptr(tok_idx), _ptr(seg_idx), ws, nb,
+        _stream(stream), arr, len(events)))
+
+
+def dwt_approx(p: WfParams, K, stream=None) -> torch.Tensor:
+    """A_J of K (fp32 [batch, heads, ctx_len >> levels, d])."""
+    approx = torch.empty((p.batch, p.heads, p.ctx_len >> p.levels,
+                          p.head_dim), dtype=torch.float32, device=K.device)
+    wf_dwt_keys(p, K, approx, None, stream)
+    return approx
+
+
+def filter_attend_cached(p: WfParams, Q, approx, K, V, Kg=None, Vg=None,
+                         workspace=None, want_indices: bool = False,
+                         stream=None):
+    """Allocates O (and the index outputs) and runs wf_filter_attend_cached.
+    Returns O, or (O, tok_idx, seg_idx) when want_indices."""
+    O = torch.empty_like(Q)
+    tok = seg = None
+    if want_indices:
+        tok = torch.empty((p.batch, p.heads, effective_budget(p)),
+                          dtype=torch.int32, device=Q.device)
+        seg = torch.empty((p.batch, p.heads, p.segments), dtype=torch.int32,
+                          device=Q.device)
+    if workspace is None:
+        workspace = alloc_workspace(p, OP_CACHED, Q.device)
+    wf_filter_attend_cached(p, Q, approx, K, V, Kg, Vg, O, tok, seg,
+                            workspace, stream)
+    return (O, tok, seg) if want_indices else O
 
 
 # ------------------------------------------------------------ recursion

@@ -163,19 +163,20 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     return at;
   };
   const bool fast = op == WF_OP_FUSED && fast_path(p);
-  const bool skim = op == WF_OP_SKIM || op == WF_OP_FUSED;
-  const bool scan = op == WF_OP_SCAN || op == WF_OP_FUSED;
-  const bool attn = op == WF_OP_ATTN || op == WF_OP_FUSED;
+  const bool whole = op == WF_OP_FUSED || op == WF_OP_CACHED;  // a whole step
+  const bool skim = op == WF_OP_SKIM || whole;
+  const bool scan = op == WF_OP_SCAN || whole;
+  const bool attn = op == WF_OP_ATTN || whole;
   if (fast) {
     const FastPlan fp = plan_fast(p);
     l.logits = take(U * nJ * 2 * B * sizeof(float));  // block rows: logits, log-sum-exps
     l.sstats = take(U * fp.R * 2 * B * sizeof(float));
   } else if (skim) {
-    const SkimPlan sp = plan_skim(p, op == WF_OP_FUSED);
+    const SkimPlan sp = plan_skim(p, op == WF_OP_FUSED);  // from A_J otherwise
     l.logits = take(U * B * nJ * sizeof(float));
     l.sstats = take(U * sp.ntiles * 2 * B * sizeof(float));
   }
-  if (op == WF_OP_FUSED) {
+  if (whole) {
     l.W = take(U * nJ * sizeof(float));
     l.seg = take(U * p.segments * sizeof(int32_t));
   }
@@ -184,7 +185,7 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     l.cstats = take(U * (fast ? 1 : cp.chunks) * 2 * B * sizeof(float));
     l.wpool = take(U * P * sizeof(float));
   }
-  if (op == WF_OP_FUSED) l.tok = take(U * keff_of(p) * sizeof(int32_t));
+  if (whole) l.tok = take(U * keff_of(p) * sizeof(int32_t));
   if (attn) {
     const AttnPlan ap = plan_attn(p, attn_rows);
     l.part = take(U * ap.splits * B * p.head_dim * sizeof(float));
@@ -289,6 +290,72 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
   WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
   WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
                           part, pstat, s)));
+  WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
+  return ok();
+}
+
+// ------------------------------------------------------------ cached A_J
+
+static const char* const kCachedNames[] = {
+    "skim_tile", "skim_select", "scan_stats", "scan_weights",
+    "scan_select", "sparse_attn", "attn_combine"};
+constexpr int kCachedKernels = 7;
+
+static wf_status cached_impl(const wf_params* p, const void* Q, const float* approx,
+                             const void* K, const void* V, const void* Kg, const void* Vg,
+                             void* O, int32_t* tok_idx, int32_t* seg_idx, void* ws,
+                             size_t ws_bytes, void* stream, void** events, int n_events) {
+  WF_TRY(check_params(p));
+  WF_TRY(check_ptr(Q, "Q", false));
+  WF_TRY(check_ptr(approx, "approx", false));
+  WF_TRY(check_ptr(K, "K", false));
+  WF_TRY(check_ptr(V, "V", false));
+  WF_TRY(check_ptr(O, "O", false));
+  WF_TRY(check_ptr(tok_idx, "tok_idx", true));
+  WF_TRY(check_ptr(seg_idx, "seg_idx", true));
+  if (p->gen_len > 0) {
+    WF_TRY(check_ptr(Kg, "Kg", false));
+    WF_TRY(check_ptr(Vg, "Vg", false));
+  }
+  if (events && n_events < kCachedKernels + 1)
+    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, kCachedKernels + 1);
+  const long keff = keff_of(*p);
+  const long nrows = keff + p->gen_len;
+  const Layout l = layout_for(*p, WF_OP_CACHED, nrows);
+  WF_TRY(check_workspace(ws, ws_bytes, l.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  float* logits = reinterpret_cast<float*>(at(ws, l.logits));
+  float* sstats = reinterpret_cast<float*>(at(ws, l.sstats));
+  float* W = reinterpret_cast<float*>(at(ws, l.W));
+  int32_t* seg = seg_idx ? seg_idx : reinterpret_cast<int32_t*>(at(ws, l.seg));
+  float* cstats = reinterpret_cast<float*>(at(ws, l.cstats));
+  float* wpool = reinterpret_cast<float*>(at(ws, l.wpool));
+  int32_t* tok = tok_idx ? tok_idx : reinterpret_cast<int32_t*>(at(ws, l.tok));
+  float* part = reinterpret_cast<float*>(at(ws, l.part));
+  float* pstat = reinterpret_cast<float*>(at(ws, l.pstat));
+  int k = 0;
+  auto mark = [&]() -> hipError_t {
+    if (!events) return hipSuccess;
+    return hipEventRecord(static_cast<hipEvent_t>(events[k]), s);
+  };
+  auto step = [&](hipError_t launched) -> wf_status {
+    if (launched != hipSuccess)
+      return fail(WF_ERR_HIP, "%s: %s", kCachedNames[k], hipGetErrorString(launched));
+    ++k;
+    hipError_t e = mark();
+    if (e != hipSuccess) return fail(WF_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    return WF_OK;
+  };
+  WF_HIP(mark(), "hipEventRecord");
+  const SkimPlan sp = plan_skim(*p, false);
+  WF_TRY(step(launch_skim_tiles(*p, false, Q, nullptr, approx, logits, sstats, s)));
+  WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
+  WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
+  WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s)));
+  WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
+  WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows, part,
+                          pstat, s)));
   WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
   return ok();
 }
@@ -435,7 +502,7 @@ extern "C" {
 
 size_t wf_workspace_bytes(const wf_params* p, int32_t op) {
   if (check_params(p) != WF_OK) return 0;
-  if (op < WF_OP_SKIM || op > WF_OP_FUSED) return 0;
+  if (op < WF_OP_SKIM || op > WF_OP_CACHED) return 0;
   return layout_for(*p, op, keff_of(*p) + p->gen_len).total;
 }
 
@@ -573,6 +640,38 @@ int32_t wf_filter_attend_kernels(const wf_params* p) {
 const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i) {
   if (check_params(p) != WF_OK || i < 0 || i >= fused_kernels(*p)) return nullptr;
   return fused_names(*p)[i];
+}
+
+wf_status wf_filter_attend_cached(const wf_params* p, const void* Q, const float* approx,
+                                  const void* K, const void* V, const void* Kg,
+                                  const void* Vg, void* O, int32_t* tok_idx,
+                                  int32_t* seg_idx, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  return cached_impl(p, Q, approx, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
+                     workspace_bytes, stream, nullptr, 0);
+}
+
+wf_status wf_filter_attend_cached_timed(const wf_params* p, const void* Q,
+                                        const float* approx, const void* K, const void* V,
+                                        const void* Kg, const void* Vg, void* O,
+                                        int32_t* tok_idx, int32_t* seg_idx, void* workspace,
+                                        size_t workspace_bytes, void* stream, void** events,
+                                        int32_t n_events) {
+  if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
+  for (int i = 0; i < n_events && i <= kCachedKernels; ++i)
+    if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
+  return cached_impl(p, Q, approx, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
+                     workspace_bytes, stream, events, n_events);
+}
+
+int32_t wf_filter_attend_cached_kernels(const wf_params* p) {
+  if (check_params(p) != WF_OK) return -1;
+  return kCachedKernels;
+}
+
+const char* wf_filter_attend_cached_kernel_name(const wf_params* p, int32_t i) {
+  if (check_params(p) != WF_OK || i < 0 || i >= kCachedKernels) return nullptr;
+  return kCachedNames[i];
 }
 
 wf_status wf_recursion_counts(const wf_params* p, const float* proportions,

@@ -68,6 +68,8 @@ class Workload:
     gen_len: int = 0      # G, always-kept generation tail (K_g, V_g)
     # multi-scale recursion: m_b at index b - 1 (empty: the two-stage path)
     proportions: tuple = ()
+    # the prompt's A_J is computed once and reused by every step
+    cached: bool = False
     description: str = field(default="", compare=False)
 
     @property
@@ -145,6 +147,16 @@ _add(Workload("recursion32k", batch=4, heads=32, ctx_len=32768, head_dim=128,
                           "paper's scale B=2: batch 4, 32 heads, d=128, "
                           "L=32768, B=64, bf16, Haar, m_2=0.25, m_1=0.5 "
                           "(4096 positions kept)"))
+
+
+_add(Workload("cached32k", batch=4, heads=32, ctx_len=32768, head_dim=128,
+              q_len=64, dtype="bf16", rho=0.98, needles=8, wavelet="haar",
+              boundary="symmetric", levels=5,
+              segments=_pool_segments(32768, 5, 2048), budget=2048, seed=3,
+              cached=True,
+              description="32K context, one step with the prompt's A_J "
+                          "cached from an earlier step: batch 4, 32 heads, "
+                          "d=128, L=32768, B=64, bf16, Haar J=5, budget 2048"))
 
 
 def needle_starts(w: Workload, layer: int, batch: int) -> np.ndarray:

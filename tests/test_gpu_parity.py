@@ -283,3 +283,53 @@ def test_fused_matches_staged_indices(wf):
     assert torch.equal(st["seg"], seg)
     assert torch.equal(st["tok"], tok)
     assert (st["O"].float() - O.float()).abs().max() <= O_TOL[w.dtype]
+
+
+# ------------------------------------------------------------ cached A_J
+
+def run_cached(wf, w, Q, K, V, Kg, Vg):
+    p = wf.params_for(w)
+    dev = "cuda"
+    Kd = K.to(dev)
+    say(f"[gpu] {w.name}: wf_dwt_keys + wf_filter_attend_cached")
+    approx = wf.dwt_approx(p, Kd)
+    O, tok, seg = wf.filter_attend_cached(
+        p, Q.to(dev), approx, Kd, V.to(dev),
+        Kg.to(dev) if Kg is not None else None,
+        Vg.to(dev) if Vg is not None else None, want_indices=True)
+    torch.cuda.synchronize()
+    say(f"[gpu] {w.name}: cached done")
+    return O.cpu(), tok.cpu(), seg.cpu(), approx
+
+
+@pytest.mark.parametrize("name", ["tiny_scan", "gen_tail", "db2_sym_j3",
+                                  "b256_d128", "layer8b", "cached32k"])
+def test_cached_step(wf, name):
+    """A step from the cached A_J gives the oracle's selection and output."""
+    w = EDGE.get(name) or synth.WORKLOADS[name]
+    Q, K, V, Kg, Vg = inputs(w)
+    O, tok, seg, _ = run_cached(wf, w, Q, K, V, Kg, Vg)
+    for u in sample_units(w, 6 if w.units > 32 else 8):
+        check_unit(Q=unit(Q, w, u), K=unit(K, w, u), V=unit(V, w, u),
+                   Kg=unit(Kg, w, u), Vg=unit(Vg, w, u), levels=w.levels,
+                   segments=w.segments, budget=w.budget, wavelet=w.wavelet,
+                   boundary=w.boundary, dtype=w.dtype, seg_gpu=unit(seg, w, u),
+                   tok_gpu=unit(tok, w, u), O_gpu=unit(O, w, u),
+                   what=f"{w.name} cached unit {u}")
+
+
+def test_cached_steps_reuse_one_approximation(wf):
+    """Two steps from one A_J are bit-identical (nothing in the step writes
+    A_J or depends on state left by an earlier step)."""
+    w = synth.WORKLOADS["layer8b"]
+    Q, K, V, _, _ = inputs(w)
+    p = wf.params_for(w)
+    Qd, Kd, Vd = Q.cuda(), K.cuda(), V.cuda()
+    approx = wf.dwt_approx(p, Kd)
+    a = wf.filter_attend_cached(p, Qd, approx, Kd, Vd, want_indices=True)
+    snap = approx.clone()
+    b = wf.filter_attend_cached(p, Qd, approx, Kd, Vd, want_indices=True)
+    torch.cuda.synchronize()
+    assert torch.equal(approx, snap)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
