@@ -315,6 +315,14 @@ int32_t wf_filter_attend_recursive_kernels(const wf_params* p);
 const char* wf_filter_attend_recursive_kernel_name(const wf_params* p,
                                                    int32_t i);
 
+/* Grouped-query attention (g query heads per KV head) needs no entry point
+ * of its own: the selection shared by a KV head's g query heads uses W
+ * summed over their query rows, which is the selection of the stacked block
+ * of g * q_len rows (W is a column sum of row-wise softmaxes), and attention
+ * is row-wise.  With the heads of a group adjacent, Q [batch][g * heads_kv]
+ * [q_len][d] is already [batch][heads_kv][g * q_len][d]: pass heads =
+ * heads_kv and q_len = g * q_len (at most WF_MAX_Q_LEN). */
+
 /* Static description of a status code. */
 const char* wf_status_str(wf_status s);
 

@@ -248,6 +248,38 @@ def wf_filter_attend_timed(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
                                        _stream(stream), arr, len(events)))
 
 
+# ------------------------------------------------------------ grouped heads
+# Grouped-query attention: g query heads share one KV head.  Their selection
+# is one selection per KV head with W summed over the g heads' query rows;
+# since W is a column sum of row-wise softmaxes, that is the selection of the
+# stacked block of g * B rows, and attention is row-wise, so the stacked call
+# also returns every head's own output.  Heads of a group are adjacent
+# (query head h uses KV head h // g), which makes the stacking a view.
+
+def grouped_view(Q: torch.Tensor, group: int) -> torch.Tensor:
+    """[batch, heads_q, B, d] -> [batch, heads_q // group, group * B, d]."""
+    b, hq, B, d = Q.shape
+    if hq % group:
+        raise ValueError(f"{hq} query heads are not groups of {group}")
+    return Q.reshape(b, hq // group, group * B, d)
+
+
+def filter_attend_grouped(p_kv: WfParams, group: int, Q, K, V, Kg=None,
+                          Vg=None, want_indices: bool = False, stream=None):
+    """One selection per KV head for its `group` query heads.  p_kv: the
+    parameters with heads = KV heads and q_len = group * B.  Returns O
+    [batch, heads_q, B, d] (and the per-KV-head tok, seg)."""
+    Qs = grouped_view(Q, group)
+    if p_kv.heads != Qs.shape[1] or p_kv.q_len != Qs.shape[2]:
+        raise ValueError("p_kv must describe the stacked query blocks")
+    out = filter_attend(p_kv, Qs, K, V, Kg, Vg, want_indices=want_indices,
+                        stream=stream)
+    if want_indices:
+        O, tok, seg = out
+        return O.reshape(Q.shape), tok, seg
+    return out.reshape(Q.shape)
+
+
 # ------------------------------------------------------------ cached A_J
 # A_J of the prompt keys (wf_dwt_keys) reused by every later step.
 

@@ -333,3 +333,42 @@ def test_cached_steps_reuse_one_approximation(wf):
     assert torch.equal(approx, snap)
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+# ------------------------------------------------ grouped query heads (GQA)
+
+@pytest.mark.parametrize("group,B", [(4, 16), (2, 32), (8, 32)])
+def test_grouped_heads(wf, group, B):
+    """g query heads per KV head: one selection per KV head from the summed
+    weights of its query heads (the oracle sums per-head skim weights), every
+    query head attends over it."""
+    w = synth.WORKLOADS["layer8b"]          # 32 KV heads, L 4096, d 128
+    Q, K, V, _, _ = inputs(w)
+    hq = w.heads * group
+    rng = torch.Generator().manual_seed(1000 + group)
+    Qh = (torch.randn((w.batch, hq, B, w.head_dim), generator=rng,
+                      dtype=torch.float64) / np.sqrt(w.head_dim)).to(Q.dtype)
+    p = wf.make_params(batch=w.batch, heads=w.heads, ctx_len=w.ctx_len,
+                       head_dim=w.head_dim, q_len=group * B, levels=w.levels,
+                       segments=w.segments, budget=w.budget, dtype=w.dtype)
+    say(f"[gpu] grouped heads g={group} B={B}")
+    O, tok, seg = wf.filter_attend_grouped(p, group, Qh.cuda(), K.cuda(),
+                                           V.cuda(), want_indices=True)
+    torch.cuda.synchronize()
+    O, tok, seg = O.cpu(), tok.cpu(), seg.cpu()
+    for kv in sample_units(w, 6):
+        k, v = unit(K, w, kv), unit(V, w, kv)
+        heads = [Qh[0, kv * group + i] for i in range(group)]
+        A = oracle.dwt(k, w.levels, w.wavelet)
+        W = sum(oracle.skim(q, A) for q in heads)      # summed per head
+        check_selection(seg[0, kv], W, w.segments, f"g{group} kv {kv} seg")
+        Wp = sum(oracle.scan(q, k, seg[0, kv], w.levels, w.budget)[0]
+                 for q in heads)
+        keff = min(w.budget, w.segments << w.levels)
+        pool = pool_tokens(seg[0, kv], w.levels)
+        t = i64(tok[0, kv])
+        check_selection(np.searchsorted(pool, t), Wp, keff, f"g{group} kv {kv} tok")
+        for i, q in enumerate(heads):
+            ref = oracle.attend(q, k, v, t)
+            err = np.abs(f64(O[0, kv * group + i]) - ref).max()
+            assert err <= O_TOL[w.dtype], f"g{group} kv {kv} head {i}: {err:.2e}"

@@ -596,3 +596,19 @@ def test_recursion_db2_gathers_before_transforming(ref):
     kept = mu1.reshape(-1, 2)[:, 0] // 2
     J1_pyr = np.sort(np.argsort(-(q @ A1[kept].T)[0], kind="stable")[:c1])
     assert not np.array_equal(J1_pyr, J1)
+
+
+# --------------------------------------------- grouped query heads (GQA)
+
+def test_grouped_heads_sum_of_weights_is_the_stacked_skim(ref):
+    """W summed over the query heads that share a KV head equals the skim of
+    the stacked query rows (eq. 8 is a column sum of row-wise softmaxes), so
+    one selection per KV head is the selection of the stacked block."""
+    rng = _rng(31)
+    g, B, d, n = 4, 6, 8, 64
+    A = rng.standard_normal((n, d))
+    Qh = [rng.standard_normal((B, d)) for _ in range(g)]
+    per_head = sum(ref.skim(q, A) for q in Qh)
+    stacked = ref.skim(np.concatenate(Qh), A)
+    np.testing.assert_allclose(stacked, per_head, rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(stacked.sum(), g * B, rtol=1e-12)
