@@ -446,7 +446,7 @@ __global__ __launch_bounds__(kBlock) void attn_ring_kernel(AttnArgs a) {
     // ring of nbuf slots, nbuf - 1 chunks in flight ahead of the one consumed
     for (int k = 0; k < nch && k < nbuf - 1; ++k) {
       kp.r0 = vp.r0 = rb0 + (long)k * CR;
-      issue_chunk<CR, G, NW, true>(ring_lds + (uint32_t)(k * 2 * CHB), kp);
+      issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(k * 2 * CHB), kp);
       issue_chunk<CR, G, NW, true>(ring_lds + (uint32_t)(k * 2 * CHB + CHB), vp);
     }
     for (int ch = 0; ch < nch; ++ch) {
@@ -456,7 +456,7 @@ __global__ __launch_bounds__(kBlock) void attn_ring_kernel(AttnArgs a) {
       if (ch + nbuf - 1 < nch) {
         kp.r0 = vp.r0 = rb0 + (long)(ch + nbuf - 1) * CR;
         const uint32_t slot = ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * 2 * CHB);
-        issue_chunk<CR, G, NW, true>(slot, kp);
+        issue_chunk<CR, G, NW>(slot, kp);
         issue_chunk<CR, G, NW, true>(slot + CHB, vp);
       }
       const unsigned char* Kb = ring + (ch % nbuf) * 2 * CHB;

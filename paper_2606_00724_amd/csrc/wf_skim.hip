@@ -496,6 +496,33 @@ __global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
   }
 }
 
+// Haar A_J alone (no details): block sums of 2^J rows in coefficient tiles
+// (the same tiles the skim builds), then copied to approx [U][nJ][D].
+// Persistent grid over (unit, tile) items.
+template <typename T, int D>
+__global__ __launch_bounds__(kBlock) void haar_approx_kernel(DwtArgs a, float inv_norm,
+                                                             int cpt) {
+  extern __shared__ float coef[];  // [cpt][D + kCoefPad]
+  constexpr int STRIDE = D + kCoefPad;
+  const int total = a.U * a.ntiles;
+  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    const int u = item / a.ntiles;
+    const int tile = item % a.ntiles;
+    const long n0 = (long)tile * cpt;
+    const int ncoef = (int)min((long)cpt, (long)a.nJ - n0);
+    const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
+    haar_sum_tile<T, D>(Kunit, n0, ncoef, a.J, inv_norm, coef, [](long n) { return n; });
+    __syncthreads();
+    float* dst = a.approx + ((long)u * a.nJ + n0) * D;
+    for (int v = threadIdx.x; v < ncoef * (D / 4); v += kBlock) {
+      const int c = v / (D / 4), k = v % (D / 4);
+      *reinterpret_cast<f32x4*>(dst + (long)c * D + 4 * k) =
+          *reinterpret_cast<const f32x4*>(coef + c * STRIDE + 4 * k);
+    }
+    __syncthreads();
+  }
+}
+
 // One workgroup per unit: merge the tiles' row statistics, form W (eq. 8) and
 // select the top-S regions (eq. 9).
 constexpr int kSelectBlock = 1024;
@@ -627,6 +654,9 @@ static hipError_t dwt_dispatch(const DwtArgs& a, const Taps& taps, dim3 grid,
   return hipGetLastError();
 }
 
+// Haar coefficient tile size at level J.
+static int haar_cpt(int J) { return std::min(kMaxCoefTile, std::max(16, 2048 >> J)); }
+
 DwtPlan plan_dwt(const wf_params& p) {
   DwtPlan d;
   const int spw = kWave / (p.head_dim / 2);
@@ -655,6 +685,28 @@ hipError_t launch_dwt(const wf_params& p, const void* K, float* approx,
   a.ntiles = pl.ntiles;
   a.boundary = p.boundary;
   const Taps taps = make_taps(p.wavelet, p.levels);
+  if (p.wavelet == WF_HAAR && !details) {
+    // A_J is the scaled block sum: coefficient tiles at streaming rate
+    const int cpt = haar_cpt(p.levels);
+    a.ntiles = (int)((a.nJ + cpt - 1) / cpt);
+    const size_t lds = (size_t)cpt * (p.head_dim + kCoefPad) * sizeof(float);
+    auto run = [&](auto kern) -> hipError_t {
+      int per_cu = 0;
+      hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per_cu, reinterpret_cast<const void*>(kern), kBlock, lds);
+      if (e != hipSuccess) return e;
+      const long total = (long)a.U * a.ntiles;
+      const long cap = (long)std::max(1, per_cu) * device_cu_count();
+      hipLaunchKernelGGL(kern, dim3((unsigned)std::min(total, cap)), dim3(kBlock), lds, s, a,
+                         taps.inv_norm, cpt);
+      return hipGetLastError();
+    };
+    if (p.dtype == WF_BF16)
+      return p.head_dim == 128 ? run(haar_approx_kernel<bf16_t, 128>)
+                               : run(haar_approx_kernel<bf16_t, 64>);
+    return p.head_dim == 128 ? run(haar_approx_kernel<float, 128>)
+                             : run(haar_approx_kernel<float, 64>);
+  }
   dim3 grid((unsigned)(a.U * a.ntiles));
   const bool haar = p.wavelet == WF_HAAR;
   if (p.dtype == WF_BF16)
@@ -715,9 +767,6 @@ static hipError_t skim_dispatch(int source, const SkimTileArgs& a,
       return hipErrorInvalidValue;
   }
 }
-
-// Haar coefficient tile size at level J.
-static int haar_cpt(int J) { return std::min(kMaxCoefTile, std::max(16, 2048 >> J)); }
 
 static hipError_t skim_tiles_common(const wf_params& p, int source, int cpt, int J,
                                     long nJ, const int32_t* parent, int npar,

@@ -372,3 +372,23 @@ def test_grouped_heads(wf, group, B):
             ref = oracle.attend(q, k, v, t)
             err = np.abs(f64(O[0, kv * group + i]) - ref).max()
             assert err <= O_TOL[w.dtype], f"g{group} kv {kv} head {i}: {err:.2e}"
+
+
+@pytest.mark.parametrize("name", ["tiny", "j1_bf16_d64_b17", "j10_d128_b8",
+                                  "ragged_tiles", "b48_f32_d128", "layer8b"])
+def test_dwt_approximation_only(wf, name):
+    """wf_dwt_keys without details (Haar: coefficient tiles of block sums)
+    against the oracle's A_J."""
+    w = EDGE.get(name) or synth.WORKLOADS[name]
+    if w.wavelet != "haar":
+        pytest.skip("approximation-only tiles are the Haar route")
+    _, K, _, _, _ = inputs(w)
+    p = wf.params_for(w)
+    say(f"[gpu] {w.name}: wf_dwt_keys (A_J only)")
+    A = wf.dwt_approx(p, K.cuda())
+    torch.cuda.synchronize()
+    A = A.cpu()
+    for u in sample_units(w, 8):
+        check_coefficients(unit(A, w, u), oracle.dwt(unit(K, w, u), w.levels,
+                                                     w.wavelet, w.boundary),
+                           f"{w.name} unit {u} A_J")
