@@ -299,7 +299,10 @@ int wf_ref_attn(const double* Q, const double* K, const double* V,
 /*
  * The whole path O1..O8 for one unit.  Every output pointer but O is
  * nullable: approx [L>>J][d], W [L>>J], seg [S], pool_score [S 2^J],
- * tok [k_eff].
+ * tok [k_eff].  When L is not a multiple of 2^J the first Lf = 2^J floor(L /
+ * 2^J) positions are filtered and the last L - Lf are always kept: the
+ * attention runs over [K[tok]; K[Lf..L); K_g] (tok itself holds the k_eff
+ * selected positions).
  */
 int wf_ref_filter_attend_unit(const double* Q, const double* K, const double* V,
                               const double* Kg, const double* Vg, int L, int d,
@@ -308,22 +311,28 @@ int wf_ref_filter_attend_unit(const double* Q, const double* K, const double* V,
                               double* O, double* approx_out, double* W_out,
                               long* seg_out, double* pool_score_out,
                               long* tok_out) {
-    long n = L >> levels;
-    long P = (long)S * (1L << levels);
+    /* a length that is not a multiple of 2^J: the first Lf positions are
+       filtered, the last L - Lf are always kept after the selection */
+    long run = 1L << levels;
+    long Lf = (L / run) * run;
+    long R = L - Lf;
+    long n = Lf >> levels;
+    long P = (long)S * run;
     long keff = budget < P ? budget : P;
-    if (S < 1 || S > n || budget < 1) return -1;
+    if (n < 1 || S < 1 || S > n || budget < 1) return -1;
     double* A = (double*)malloc(sizeof(double) * (size_t)n * d);
     double* W = (double*)malloc(sizeof(double) * (size_t)n);
     long* seg = (long*)malloc(sizeof(long) * (size_t)S);
-    long* tok = (long*)malloc(sizeof(long) * (size_t)keff);
+    long* tok = (long*)malloc(sizeof(long) * (size_t)(keff + R));
     int rc = -1;
     if (!A || !W || !seg || !tok) goto done;
-    if (wf_ref_dwt(K, L, d, levels, wavelet, boundary, A, NULL) != 0) goto done;
+    if (wf_ref_dwt(K, (int)Lf, d, levels, wavelet, boundary, A, NULL) != 0) goto done;
     if (wf_ref_skim(Q, A, B, (int)n, d, scale, W) != 0) goto done;
     if (wf_ref_topk(W, n, S, seg) != 0) goto done;
-    if (wf_ref_scan(Q, K, B, L, d, levels, seg, S, budget, scale,
+    if (wf_ref_scan(Q, K, B, (int)Lf, d, levels, seg, S, budget, scale,
                     pool_score_out, tok) != 0) goto done;
-    if (wf_ref_attn(Q, K, V, tok, keff, Kg, Vg, G, B, d, scale, O) != 0) goto done;
+    for (long r = 0; r < R; ++r) tok[keff + r] = Lf + r;
+    if (wf_ref_attn(Q, K, V, tok, keff + R, Kg, Vg, G, B, d, scale, O) != 0) goto done;
     if (approx_out) memcpy(approx_out, A, sizeof(double) * (size_t)n * d);
     if (W_out) memcpy(W_out, W, sizeof(double) * (size_t)n);
     if (seg_out) memcpy(seg_out, seg, sizeof(long) * (size_t)S);
@@ -356,7 +365,7 @@ int wf_ref_filter_attend(const double* Q, const double* K, const double* V,
             Q + (size_t)u * B * d, K + (size_t)u * L * d, V + (size_t)u * L * d,
             kg, vg, L, d, B, G, levels, wavelet, boundary, S, budget, scale,
             O + (size_t)u * B * d, NULL, NULL, NULL, NULL,
-            tok ? tok + (size_t)u * keff : NULL);
+            tok ? tok + (size_t)u * keff : NULL);  /* selected positions only */
         failures += (rc != 0);
     }
     return failures == 0 ? 0 : -1;
@@ -378,7 +387,8 @@ int wf_ref_filter_attend(const double* Q, const double* K, const double* V,
  *     mu^{b-1} = { mu^b[2^b j + r] : j in J_b ascending, r < 2^b }
  *            (eq. 10, composed with mu^b so that indices stay prompt
  *            positions)
- *   tok = mu^0, ascending, 2 c_1 positions.
+ *   tok = mu^0, ascending, 2 c_1 positions, followed by the last L mod 2^B
+ *   positions when L is not a multiple of 2^B (always kept).
  *
  * counts [levels] (nullable) receives c_b at index b - 1; tok must hold
  * L entries (the largest possible mu^0); *n_tok receives |mu^0|.
@@ -394,7 +404,11 @@ int wf_ref_recursive_select(const double* Q, const double* K, int B, int L,
                             int d, int levels, int wavelet, int boundary,
                             const double* prop, double scale, long* counts,
                             long* tok, long* n_tok) {
-    if (levels < 1 || L < 2 || (L % (1 << levels)) != 0) return -1;
+    /* a length that is not a multiple of 2^B: the recursion runs over the
+       first Lf positions; the last L - Lf are always kept after mu^0 */
+    long Lr = L % (1L << levels);
+    L -= (int)Lr;
+    if (levels < 1 || L < (1 << levels)) return -1;
     for (int b = 1; b <= levels; ++b)
         if (!(prop[b - 1] > 0.0 && prop[b - 1] <= 1.0)) return -1;
     long* mu = (long*)malloc(sizeof(long) * (size_t)L);
@@ -428,7 +442,8 @@ int wf_ref_recursive_select(const double* Q, const double* K, int B, int L,
         memcpy(mu, next, sizeof(long) * (size_t)m);
     }
     memcpy(tok, mu, sizeof(long) * (size_t)m);
-    *n_tok = m;
+    for (long r = 0; r < Lr; ++r) tok[m + r] = L + r;
+    *n_tok = m + Lr;
     rc = 0;
 done:
     free(mu); free(next); free(X); free(C); free(W); free(logit); free(pick);

@@ -612,3 +612,37 @@ def test_grouped_heads_sum_of_weights_is_the_stacked_skim(ref):
     stacked = ref.skim(np.concatenate(Qh), A)
     np.testing.assert_allclose(stacked, per_head, rtol=1e-13, atol=1e-15)
     np.testing.assert_allclose(stacked.sum(), g * B, rtol=1e-12)
+
+
+# ----------------------------------------- lengths not a multiple of 2^J
+
+@pytest.mark.parametrize("levels,rem", [(3, 5), (4, 1), (2, 3)])
+def test_remainder_is_kept_like_a_tail(ref, levels, rem):
+    """A prompt of L = Lf + r positions (Lf a multiple of 2^J, 0 < r < 2^J):
+    the first Lf are filtered and the last r always kept, which is the
+    filtered path on the first Lf positions with those r rows placed in
+    front of the generation tail (the tail path is pinned to SDPA above)."""
+    rng = _rng(40 + levels)
+    Lf, d, B, G = 256, 8, 5, 3
+    L = Lf + rem
+    Q = rng.standard_normal((B, d))
+    K, V = rng.standard_normal((L, d)), rng.standard_normal((L, d))
+    Kg, Vg = rng.standard_normal((G, d)), rng.standard_normal((G, d))
+    S, k = 6, 20
+    got = ref.filter_attend_unit(Q, K, V, levels, S, k, Kg=Kg, Vg=Vg)
+    want = ref.filter_attend_unit(Q, K[:Lf], V[:Lf], levels, S, k,
+                                  Kg=np.concatenate([K[Lf:], Kg]),
+                                  Vg=np.concatenate([V[Lf:], Vg]))
+    np.testing.assert_array_equal(got["tok"], want["tok"])
+    np.testing.assert_array_equal(got["seg"], want["seg"])
+    np.testing.assert_allclose(got["O"], want["O"], rtol=0, atol=1e-13)
+
+
+def test_recursion_remainder_follows_mu0(ref):
+    rng = _rng(77)
+    Lf, rem, d = 256, 3, 6
+    K = rng.standard_normal((Lf + rem, d))
+    Q = rng.standard_normal((4, d))
+    got, _ = ref.recursive_select(Q, K, 3, [0.5, 0.5, 0.25])
+    base, _ = ref.recursive_select(Q, K[:Lf], 3, [0.5, 0.5, 0.25])
+    np.testing.assert_array_equal(got, np.concatenate([base, np.arange(Lf, Lf + rem)]))
