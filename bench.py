@@ -50,10 +50,13 @@ def algorithmic_bytes(w, keff: int, counts=None) -> dict:
         pool = sum(counts[b] << (b + 1) for b in range(len(counts) - 1))
     else:
         pool = w.segments << w.levels
+    # rows always attended: the remainder of a non-dyadic length, the tail
+    kept = (w.ctx_len - ((w.ctx_len >> w.levels) << w.levels)) + w.gen_len
     per_unit = {
         "keys": w.ctx_len * d * e,
         "pool": pool * d * e,
         "values": keff * d * e,
+        "kept": 2 * kept * d * e,
         "q_and_o": 2 * w.q_len * d * e,
     }
     if getattr(w, "cached", False):  # A_J (fp32) is read instead of the keys
@@ -126,7 +129,7 @@ def measured_traffic(kernel: str, workload: str):
     return int(fields["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(w, Q, K, V, min_seconds: float = 10.0) -> dict:
+def cpu_baseline(w, Q, K, V, Kg=None, Vg=None, min_seconds: float = 10.0) -> dict:
     """The oracle as it stands, on every unit of the layer, in chunks of 16
     units, repeated until about min_seconds of oracle time have passed (at
     most 50 passes; only the oracle calls are timed)."""
@@ -138,22 +141,26 @@ def cpu_baseline(w, Q, K, V, min_seconds: float = 10.0) -> dict:
     q = Q.reshape(U, w.q_len, w.head_dim)
     k = K.reshape(U, w.ctx_len, w.head_dim)
     v = V.reshape(U, w.ctx_len, w.head_dim)
+    kg = Kg.reshape(U, w.gen_len, w.head_dim) if Kg is not None else None
+    vg = Vg.reshape(U, w.gen_len, w.head_dim) if Vg is not None else None
     chunk = 16
     elapsed = 0.0
     passes = 0
     while passes < 50 and (passes == 0 or elapsed < min_seconds):
         for u0 in range(0, U, chunk):
             qa, ka, va = (oracle._f64(x[u0:u0 + chunk]) for x in (q, k, v))
+            kga = oracle._f64(kg[u0:u0 + chunk]) if kg is not None else None
+            vga = oracle._f64(vg[u0:u0 + chunk]) if vg is not None else None
             t0 = time.perf_counter()
             if w.proportions:
                 oracle.filter_attend_recursive(
                     qa, ka, va, w.levels,
                     [float(np.float32(m)) for m in w.proportions],
-                    wavelet=w.wavelet, boundary=w.boundary)
+                    wavelet=w.wavelet, boundary=w.boundary, Kg=kga, Vg=vga)
             else:
                 oracle.filter_attend(qa, ka, va, w.levels, w.segments,
                                      w.budget, wavelet=w.wavelet,
-                                     boundary=w.boundary)
+                                     boundary=w.boundary, Kg=kga, Vg=vga)
             elapsed += time.perf_counter() - t0
             del qa, ka, va
         passes += 1
@@ -197,13 +204,18 @@ def main() -> int:
     w = synth.WORKLOADS[args.workload]
     print(f"[bench] generating {w.name} inputs", file=sys.stderr, flush=True)
     Q, K, V = synth.make_inputs(w)
+    Kg = Vg = None
+    if w.gen_len:
+        Kg, Vg = synth.make_tail(w, w.gen_len)
     dev = torch.device("cuda:0")
-    p = wf.params_for(w, gen_len=0)
+    p = wf.params_for(w)
     recursive = bool(w.proportions)
     cached = bool(w.cached)
     counts = wf.recursion_counts(p, w.proportions) if recursive else None
     keff = 2 * counts[0] if recursive else wf.effective_budget(p)
     Qd, Kd, Vd = Q.to(dev), K.to(dev), V.to(dev)
+    Kgd = Kg.to(dev) if Kg is not None else None
+    Vgd = Vg.to(dev) if Vg is not None else None
     O = torch.empty_like(Qd)
     tok = torch.empty((w.batch, w.heads, keff), dtype=torch.int32, device=dev)
     approx = None
@@ -225,13 +237,13 @@ def main() -> int:
 
     def step_plain():
         if recursive:
-            wf.wf_filter_attend_recursive(p, w.proportions, Qd, Kd, Vd, None,
-                                          None, O, tok, ws, stream)
+            wf.wf_filter_attend_recursive(p, w.proportions, Qd, Kd, Vd, Kgd,
+                                          Vgd, O, tok, ws, stream)
         elif cached:
-            wf.wf_filter_attend_cached(p, Qd, approx, Kd, Vd, None, None, O,
+            wf.wf_filter_attend_cached(p, Qd, approx, Kd, Vd, Kgd, Vgd, O,
                                        tok, None, ws, stream)
         else:
-            wf.wf_filter_attend(p, Qd, Kd, Vd, None, None, O, tok, None, ws,
+            wf.wf_filter_attend(p, Qd, Kd, Vd, Kgd, Vgd, O, tok, None, ws,
                                 stream)
 
     def step_timed(i):
@@ -239,14 +251,14 @@ def main() -> int:
         evs = ev.ev[base:base + len(names) + 1]
         if recursive:
             wf.wf_filter_attend_recursive_timed(p, w.proportions, Qd, Kd, Vd,
-                                                None, None, O, tok, ws, evs,
+                                                Kgd, Vgd, O, tok, ws, evs,
                                                 stream)
         elif cached:
-            wf.wf_filter_attend_cached_timed(p, Qd, approx, Kd, Vd, None,
-                                             None, O, tok, None, ws, evs,
+            wf.wf_filter_attend_cached_timed(p, Qd, approx, Kd, Vd, Kgd,
+                                             Vgd, O, tok, None, ws, evs,
                                              stream)
         else:
-            wf.wf_filter_attend_timed(p, Qd, Kd, Vd, None, None, O, tok,
+            wf.wf_filter_attend_timed(p, Qd, Kd, Vd, Kgd, Vgd, O, tok,
                                       None, ws, evs, stream)
 
     if args.copy_calibration:
@@ -321,7 +333,7 @@ def main() -> int:
             "workload": w.description,
             "batch": w.batch, "heads": w.heads, "ctx_len": w.ctx_len,
             "head_dim": w.head_dim, "q_len": w.q_len, "levels": w.levels,
-            "wavelet": w.wavelet, "gen_len": 0,
+            "wavelet": w.wavelet, "gen_len": w.gen_len,
             **({"proportions": list(w.proportions), "counts": counts,
                 "kept_positions": keff} if recursive else
                {"segments": w.segments, "budget": w.budget, "k_eff": keff}),
@@ -345,7 +357,7 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(w, Q, K, V)
+        result["cpu_baseline"] = cpu_baseline(w, Q, K, V, Kg, Vg)
     print(json.dumps(result), flush=True)
     return 0
 

@@ -83,6 +83,11 @@ enum { WF_OP_SKIM = 0, WF_OP_SCAN = 1, WF_OP_ATTN = 2, WF_OP_FUSED = 3,
        WF_OP_CACHED = 4 };
 
 /* Limits of this build. */
+/* Remainder.  When L is not a multiple of 2^J, the first
+ * Lf = 2^J floor(L / 2^J) positions are filtered (transformed, scored,
+ * selected) and the last R = L - Lf positions are always kept: the sparse
+ * cache is [K[tok]; K[Lf .. L); K_g] (values likewise), R = 0 for a multiple
+ * of 2^J.  The recursion does the same with 2^B. */
 enum {
     WF_MAX_LEVELS = 10,  /* J                                   */
     WF_MAX_Q_LEN = 256   /* B, rows of the query block          */
@@ -91,7 +96,7 @@ enum {
 typedef struct wf_params {
     int32_t batch;    /* >= 1                                                 */
     int32_t heads;    /* >= 1; K/V heads equal query heads                    */
-    int32_t ctx_len;  /* L = |I_p|, prompt positions filtered; L % 2^J == 0  */
+    int32_t ctx_len;  /* L = |I_p|, prompt positions; see the remainder note */
     int32_t head_dim; /* d: 64 or 128                                         */
     int32_t q_len;    /* B = |I~|, query rows: 1 .. WF_MAX_Q_LEN              */
     int32_t gen_len;  /* G = |I_g| >= 0, tail rows always kept (never scored) */
@@ -113,11 +118,11 @@ size_t wf_workspace_bytes(const wf_params* p, int32_t op);
 int32_t wf_effective_budget(const wf_params* p);
 
 /*
- * Step 1 (eqs. 5-6): J-level DWT of the keys along the sequence.
+ * Step 1 (eqs. 5-6): J-level DWT of the first Lf keys along the sequence.
  *   K        [batch][heads][L][d]                 dtype
  *   approx   [batch][heads][L >> J][d]            fp32 out: A_J
  *   details  nullable; per unit the rows of D_1, then D_2, ... D_J,
- *            [batch][heads][sum_{j=1..J} L >> j][d] fp32 out
+ *            [batch][heads][sum_{j=1..J} Lf >> j][d] fp32 out
  */
 wf_status wf_dwt_keys(const wf_params* p, const void* K, float* approx,
                       float* details, void* stream);
@@ -159,8 +164,9 @@ wf_status wf_scan_select(const wf_params* p, const void* Q, const void* K,
  *   K, V       [batch][heads][L][d]               dtype
  *   tok_idx    [batch][heads][k_eff]              int32, each in [0, L)
  *   Kg, Vg     [batch][heads][G][d]               dtype; NULL iff G == 0
- *   Ks, Vs     [batch][heads][k_eff + G][d]       dtype out:
- *              rows r < k_eff: K[tok_idx[r]]; then the G tail rows
+ *   Ks, Vs     [batch][heads][k_eff + R + G][d]   dtype out:
+ *              rows r < k_eff: K[tok_idx[r]]; then K[Lf .. L) (the R
+ *              remainder rows); then the G tail rows
  */
 wf_status wf_gather_kv(const wf_params* p, const void* K, const void* V,
                        const int32_t* tok_idx, const void* Kg, const void* Vg,
@@ -173,7 +179,7 @@ wf_status wf_gather_kv(const wf_params* p, const void* K, const void* V,
  *   Ks, Vs     [batch][heads][n_kv][d]            dtype, n_kv >= 1
  *   O          [batch][heads][B][d]               dtype out (RNE for bf16)
  *   workspace  >= wf_workspace_bytes(p, WF_OP_ATTN) (sized for n_kv up to
- *              k_eff + G; a larger n_kv needs the workspace of a params copy
+ *              k_eff + R + G; a larger n_kv needs the workspace of a params copy
  *              whose budget/segments/gen_len give that many rows)
  */
 wf_status wf_sparse_attn(const wf_params* p, const void* Q, const void* Ks,

@@ -78,10 +78,6 @@ static wf_status check_shape(const wf_params* p) {
                 p->ctx_len, 1 << p->levels);
   if (p->ctx_len > (1 << 30))
     return fail(WF_ERR_UNSUPPORTED, "ctx_len %d exceeds 2^30", p->ctx_len);
-  if (p->ctx_len % (1 << p->levels) != 0)
-    return fail(WF_ERR_UNSUPPORTED,
-                "ctx_len %d is not a multiple of 2^levels = %d", p->ctx_len,
-                1 << p->levels);
   if (p->wavelet != WF_HAAR && p->wavelet != WF_DB2)
     return fail(WF_ERR_INVALID_ARG, "unknown wavelet %d", p->wavelet);
   if (p->boundary != WF_EXT_SYMMETRIC && p->boundary != WF_EXT_PERIODIC)
@@ -105,7 +101,7 @@ static wf_status check_params(const wf_params* p) {
           (((long)p->budget < ((long)p->segments << p->levels)
                 ? (long)p->budget
                 : ((long)p->segments << p->levels)) +
-           (long)p->gen_len) > (1L << 31))
+           remainder_len(*p) + (long)p->gen_len) > (1L << 31))
     return fail(WF_ERR_UNSUPPORTED, "sparse cache too large");
   return WF_OK;
 }
@@ -247,7 +243,7 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
   if (events && n_events < nk + 1)
     return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, nk + 1);
   const long keff = keff_of(*p);
-  const long nrows = keff + p->gen_len;
+  const long nrows = keff + remainder_len(*p) + p->gen_len;
   const Layout l = layout_for(*p, WF_OP_FUSED, nrows);
   WF_TRY(check_workspace(ws, ws_bytes, l.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -320,7 +316,7 @@ static wf_status cached_impl(const wf_params* p, const void* Q, const float* app
   if (events && n_events < kCachedKernels + 1)
     return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, kCachedKernels + 1);
   const long keff = keff_of(*p);
-  const long nrows = keff + p->gen_len;
+  const long nrows = keff + remainder_len(*p) + p->gen_len;
   const Layout l = layout_for(*p, WF_OP_CACHED, nrows);
   WF_TRY(check_workspace(ws, ws_bytes, l.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -376,7 +372,8 @@ static wf_status check_recursion(const wf_params* p, const float* prop, int32_t*
     counts[b - 1] = (int32_t)c;
     n = 2 * c;
   }
-  if ((long)p->batch * p->heads * (2L * counts[0] + p->gen_len) > (1L << 31))
+  if ((long)p->batch * p->heads * (2L * counts[0] + remainder_len(*p) + p->gen_len) >
+      (1L << 31))
     return fail(WF_ERR_UNSUPPORTED, "sparse cache too large");
   return WF_OK;
 }
@@ -390,7 +387,7 @@ static RecLayout rec_layout(const wf_params& p, const int32_t* counts) {
   RecLayout l;
   const RecPlan rp = plan_recursion(p, counts);
   const size_t U = (size_t)p.batch * p.heads, B = p.q_len;
-  const long nrows = 2L * counts[0] + p.gen_len;
+  const long nrows = 2L * counts[0] + remainder_len(p) + p.gen_len;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -487,7 +484,7 @@ static wf_status recursive_impl(const wf_params* p, const float* prop, const voi
     n = 2L * counts[b - 1];
   }
   const int nsel = 2 * counts[0];
-  const long nrows = (long)nsel + p->gen_len;
+  const long nrows = (long)nsel + remainder_len(*p) + p->gen_len;
   WF_TRY(step(launch_attn(*p, Q, K, V, tok, nsel, Kg, Vg, p->gen_len, nrows, part, pstat,
                           s)));
   WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
@@ -503,7 +500,7 @@ extern "C" {
 size_t wf_workspace_bytes(const wf_params* p, int32_t op) {
   if (check_params(p) != WF_OK) return 0;
   if (op < WF_OP_SKIM || op > WF_OP_CACHED) return 0;
-  return layout_for(*p, op, keff_of(*p) + p->gen_len).total;
+  return layout_for(*p, op, keff_of(*p) + remainder_len(*p) + p->gen_len).total;
 }
 
 int32_t wf_effective_budget(const wf_params* p) {

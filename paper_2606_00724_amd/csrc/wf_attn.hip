@@ -31,7 +31,8 @@ struct CacheRows {
   const T* tail;
   const int32_t* tok;   // unit's token list or null
   long unit_rows;       // rows per unit in `base` (L, or nrows when contiguous)
-  int u, nsel, G;
+  long Lf;              // rows Lf .. Lf + R - 1 of `base` follow the token list
+  int u, nsel, G, R;
   long r0;
   int nr;
   __device__ __forceinline__ const T* operator()(int r) const {
@@ -40,7 +41,8 @@ struct CacheRows {
     if (tok) {
       if (rr < nsel)
         return base + ((long)u * unit_rows + min(max((long)tok[rr], 0L), unit_rows - 1)) * D;
-      return tail + ((long)u * G + (rr - nsel)) * D;
+      if (rr < nsel + R) return base + ((long)u * unit_rows + Lf + (rr - nsel)) * D;
+      return tail + ((long)u * G + (rr - nsel - R)) * D;
     }
     return base + ((long)u * unit_rows + rr) * D;
   }
@@ -130,6 +132,8 @@ __global__ __launch_bounds__(kBlock) void attn_kernel(AttnArgs a) {
   ksrc.u = vsrc.u = u;
   ksrc.nsel = vsrc.nsel = a.nsel;
   ksrc.G = vsrc.G = a.G;
+  ksrc.R = vsrc.R = a.R;
+  ksrc.Lf = vsrc.Lf = a.Lf;
 
   const int nqb = (a.B + 15) / 16;
   const int tsplit = nqb == 1 ? 4 : (nqb == 2 ? 2 : 1);
@@ -362,7 +366,8 @@ struct RingRowPtr {
   long unit_rows;       // rows per unit in `base`
   long r0, rlast;       // absolute first row of the chunk, last valid row
   long split_r0;        // first row of the split (toks[0])
-  int u, nsel, G;
+  long Lf;              // rows Lf .. Lf + R - 1 of `base` follow the token list
+  int u, nsel, G, R;
   __device__ __forceinline__ const bf16_t* operator()(int r) const {
     const long rr = min(r0 + r, rlast);
     if (toks) {
@@ -370,7 +375,8 @@ struct RingRowPtr {
       if (rr < nsel)
         return base + ((long)u * unit_rows +
                        min(max((long)toks[rr - split_r0], 0L), unit_rows - 1)) * D;
-      return tail + ((long)u * G + (rr - nsel)) * D;
+      if (rr < nsel + R) return base + ((long)u * unit_rows + Lf + (rr - nsel)) * D;
+      return tail + ((long)u * G + (rr - nsel - R)) * D;
     }
     return base + ((long)u * unit_rows + rr) * D;
   }
@@ -414,6 +420,8 @@ __global__ __launch_bounds__(kBlock) void attn_ring_kernel(AttnArgs a) {
   kp.u = vp.u = u;
   kp.nsel = vp.nsel = a.nsel;
   kp.G = vp.G = a.G;
+  kp.R = vp.R = a.R;
+  kp.Lf = vp.Lf = a.Lf;
 
   const int nqb = (a.B + 15) / 16;
   const int tsplit = nqb <= 2 ? 2 : 1;       // row halves per query block
@@ -611,7 +619,7 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, int D) {
 // Sparse cache rows: [K[tok]; Kg] and [V[tok]; Vg], 16 bytes per thread.
 __global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a) {
   const int vpr = a.D * a.elem / 16;
-  const long rows = (long)a.keff + a.G;
+  const long rows = (long)a.keff + a.R + a.G;
   const long total = (long)a.U * rows * vpr;
   for (long v = (long)blockIdx.x * kBlock + threadIdx.x; v < total;
        v += (long)gridDim.x * kBlock) {
@@ -626,9 +634,12 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a) {
       const long t = min(max((long)a.tok[(long)u * a.keff + r], 0L), (long)a.L - 1);
       ks = (const unsigned char*)a.K + ((long)u * a.L + t) * row_bytes;
       vs = (const unsigned char*)a.V + ((long)u * a.L + t) * row_bytes;
+    } else if (r < a.keff + a.R) {
+      ks = (const unsigned char*)a.K + ((long)u * a.L + a.Lf + (r - a.keff)) * row_bytes;
+      vs = (const unsigned char*)a.V + ((long)u * a.L + a.Lf + (r - a.keff)) * row_bytes;
     } else {
-      ks = (const unsigned char*)a.Kg + ((long)u * a.G + (r - a.keff)) * row_bytes;
-      vs = (const unsigned char*)a.Vg + ((long)u * a.G + (r - a.keff)) * row_bytes;
+      ks = (const unsigned char*)a.Kg + ((long)u * a.G + (r - a.keff - a.R)) * row_bytes;
+      vs = (const unsigned char*)a.Vg + ((long)u * a.G + (r - a.keff - a.R)) * row_bytes;
     }
     const long dst = ur * row_bytes + (long)k * 16;
     *reinterpret_cast<u32x4*>((unsigned char*)a.Ks + dst) =
@@ -711,6 +722,9 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
   a.B = p.q_len;
   a.nsel = nsel;
   a.G = G;
+  // indexed rows: the selection, then the always-kept remainder, then the tail
+  a.Lf = filtered_len(p);
+  a.R = tok ? (int)remainder_len(p) : 0;
   a.nrows = (int)nrows;
   a.NS = pl.splits;
   a.rps = pl.rps;
@@ -760,8 +774,10 @@ hipError_t launch_gather(const wf_params& p, const void* K, const void* V,
   a.D = p.head_dim;
   a.keff = wf_effective_budget(&p);
   a.G = p.gen_len;
+  a.Lf = filtered_len(p);
+  a.R = (int)remainder_len(p);
   a.elem = p.dtype == WF_BF16 ? 2 : 4;
-  const long total = (long)a.U * (a.keff + a.G) * (a.D * a.elem / 16);
+  const long total = (long)a.U * (a.keff + a.R + a.G) * (a.D * a.elem / 16);
   const long blocks = std::min((total + kBlock - 1) / kBlock,
                                (long)device_cu_count() * 16);
   hipLaunchKernelGGL(gather_kernel, dim3((unsigned)std::max(1L, blocks)),

@@ -127,7 +127,7 @@ __global__ __launch_bounds__(kTokBlock) void token_skim_kernel(TokenSkimArgs a) 
     __device__ __forceinline__ const bf16_t* operator()(int r) const {
       return Kunit + min(c0 + r, tlast) * D;
     }
-  } rows{reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.L * D, tb, te - 1};
+  } rows{reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D, tb, te - 1};
   const uint32_t ring_lds = lds_offset(ring);
   const int nbuf = a.nbuf;
   if (loader) {
@@ -349,12 +349,13 @@ bool fast_path(const wf_params& p) {
 FastPlan plan_fast(const wf_params& p) {
   FastPlan f{};
   const long U = (long)p.batch * p.heads;
-  const long chunks = ((long)p.ctx_len + kScanChunk - 1) / kScanChunk;
+  const long Lf = filtered_len(p);
+  const long chunks = (Lf + kScanChunk - 1) / kScanChunk;
   const long want = std::max(1L, (long)(device_cu_count() + U - 1) / U);
   const long R = std::min(chunks, want);
   const long cpr = (chunks + R - 1) / R;
   f.span = (int)(cpr * kScanChunk);
-  f.R = (int)(((long)p.ctx_len + f.span - 1) / f.span);
+  f.R = (int)((Lf + f.span - 1) / f.span);
   const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
   // wave reduction pairs, then two batch slots of block results
   const size_t bb = p.levels == 3 ? token_batch_bytes<3>(p.q_len)
@@ -399,7 +400,8 @@ hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, f
   a.blocks = blocks;
   a.wstats = wstats;
   a.U = p.batch * p.heads;
-  a.L = p.ctx_len;
+  a.L = (int)filtered_len(p);
+  a.Ls = p.ctx_len;
   a.B = p.q_len;
   a.nJ = p.ctx_len >> p.levels;
   a.R = f.R;

@@ -16,9 +16,10 @@ constexpr int kCoefPad = 4;        // fp32 pad per LDS coefficient row
 enum CoefSource { kHaarSum = 0, kCascade = 1, kFromApprox = 2 };
 
 struct DwtArgs {
-  const void* K;       // [U][L][D]
+  const void* K;       // [U][Ls][D]
   float* approx;       // [U][nJ][D]
   float* details;      // nullable, [U][L - nJ][D]
+  long Ls;             // rows per unit in K (L: the transformed rows)
   int U, L, D, J, nJ;
   int cps;             // coefficients per stream
   int streams;         // streams per workgroup tile
@@ -35,6 +36,7 @@ struct SkimTileArgs {
   const int32_t* parent;  // nullable: coefficient n is block 2 parent[n/2] + n%2
                           // of level J ([U][npar], ascending block ids at J + 1)
   int npar;
+  long Ls;              // rows per unit in K (L: the filtered rows)
   int U, L, B, J, nJ;
   int cpt;              // coefficients per tile
   int ntiles;           // tiles per unit
@@ -59,6 +61,7 @@ struct ScanArgs {
   const int32_t* seg;   // [U][S]
   float* stats;         // [U][C][2][B]
   float* wpool;         // [U][P]  (weights mode)
+  long Ls;              // rows per unit in K
   int U, L, B, J, S, P, C;
   int Cs;               // (max, sum) slices in `stats`: C, or 1 when precomputed
   int span;             // pool positions per workgroup (multiple of the chunk)
@@ -80,9 +83,10 @@ struct GatherArgs {
   const int32_t* tok;   // [U][keff]
   const void* Kg;       // [U][G][D]
   const void* Vg;
-  void* Ks;             // [U][keff + G][D]
+  void* Ks;             // [U][keff + R + G][D]
   void* Vs;
-  int U, L, D, keff, G, elem;
+  long Lf;              // first always-kept row: rows Lf .. L-1 follow tok
+  int U, L, D, keff, R, G, elem;
 };
 
 struct AttnArgs {
@@ -95,6 +99,8 @@ struct AttnArgs {
   float* part;          // [U][NS][B][D] unnormalised partial outputs
   float* pstat;         // [U][NS][2][B] partial row max, row sum
   void* O;              // [U][B][D]
+  long Lf;              // indexed mode: rows Lf .. Lf + R - 1 of K/V follow tok
+  int R;
   int U, L, B, nsel, G, nrows, NS;
   int rps;              // cache rows per split (multiple of the chunk)
   int nbuf;             // LDS ring depth (bf16 path)
@@ -109,6 +115,7 @@ struct TokenSkimArgs {
   float* blocks;        // [U][nJ][2][B]: coarse logits, then log-sum-exps of
                         // the block's token logits
   float* wstats;        // [U][R][2][B] coarse-logit max and sum of exp per range
+  long Ls;              // rows per unit in K (L: the filtered rows)
   int U, L, B, nJ, R;
   int span;             // tokens per range (multiple of the chunk)
   int nbuf;             // LDS ring depth

@@ -58,6 +58,13 @@ struct RecPlan {
 };
 
 float effective_scale(const wf_params& p);
+
+// Filtered prompt rows: ctx_len rounded down to a multiple of 2^levels; the
+// remaining ctx_len - filtered_len rows are always kept after the selection.
+inline long filtered_len(const wf_params& p) {
+  return ((long)p.ctx_len >> p.levels) << p.levels;
+}
+inline long remainder_len(const wf_params& p) { return (long)p.ctx_len - filtered_len(p); }
 int device_cu_count();
 
 DwtPlan plan_dwt(const wf_params& p);

@@ -65,11 +65,11 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
   const T* Qunit = reinterpret_cast<const T*>(a.Q) + (long)u * a.B * D;
 
   PoolRows<T, D> src;
-  src.Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
+  src.Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * D;
   src.seg = a.seg + (long)u * a.S;
   src.J = a.J;
   src.mask = (1 << a.J) - 1;
-  src.last = (long)a.L - 1;
+  src.last = a.Ls - 1;
   src.p0 = pb;
   src.np = (int)min((long)kScanChunk, pe - pb);
   Stager st;
@@ -274,10 +274,10 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
   __syncthreads();  // every regular load above has been consumed
 
   PoolRowPtr<D> rp;
-  rp.Kunit = reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.L * D;
+  rp.Kunit = reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D;
   rp.segs = segs;
   rp.plast = pe - 1;
-  rp.last = (long)a.L - 1;
+  rp.last = a.Ls - 1;
   rp.J = a.J;
   rp.mask = (1 << a.J) - 1;
   rp.s_lo = s_lo;
@@ -493,7 +493,8 @@ hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
   a.stats = stats;
   a.wpool = wpool;
   a.U = p.batch * p.heads;
-  a.L = p.ctx_len;
+  a.L = (int)filtered_len(p);
+  a.Ls = p.ctx_len;
   a.B = p.q_len;
   a.J = p.levels;
   a.S = p.segments;

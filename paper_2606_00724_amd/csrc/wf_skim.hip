@@ -205,7 +205,7 @@ __global__ __launch_bounds__(kBlock) void dwt_kernel(DwtArgs a, Taps taps) {
   const long n0 = ((long)tile * a.streams + sid) * a.cps;
   if (u >= a.U || n0 >= a.nJ) return;  // no barrier in this kernel
   const long n1 = min(n0 + (long)a.cps, (long)a.nJ);
-  const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * a.D;
+  const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * a.D;
   GlobalSink sink;
   sink.aout = a.approx + (long)u * a.nJ * a.D + 2 * cp;
   sink.dout = a.details ? a.details + (long)u * (a.L - a.nJ) * a.D + 2 * cp
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
     const long n0 = (long)tile * a.cpt;
     const int ncoef = (int)min((long)a.cpt, (long)a.nJ - n0);
     if constexpr (SRC == kHaarSum) {
-      const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
+      const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * D;
       if (a.parent) {
         // block ids are clamped into the unit: a bad id cannot leave K
         const int32_t* par = a.parent + (long)u * a.npar;
@@ -479,7 +479,7 @@ __global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
                             [](long n) { return n; });
       }
     } else if constexpr (SRC == kCascade) {
-      const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
+      const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * D;
       cascade_tile<M, J, T, D>(Kunit, a.L, n0, ncoef, a.cpt,
                                M == 4 && a.boundary == 0, taps, coef);
     } else {
@@ -510,7 +510,7 @@ __global__ __launch_bounds__(kBlock) void haar_approx_kernel(DwtArgs a, float in
     const int tile = item % a.ntiles;
     const long n0 = (long)tile * cpt;
     const int ncoef = (int)min((long)cpt, (long)a.nJ - n0);
-    const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.L * D;
+    const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * D;
     haar_sum_tile<T, D>(Kunit, n0, ncoef, a.J, inv_norm, coef, [](long n) { return n; });
     __syncthreads();
     float* dst = a.approx + ((long)u * a.nJ + n0) * D;
@@ -676,7 +676,8 @@ hipError_t launch_dwt(const wf_params& p, const void* K, float* approx,
   a.approx = approx;
   a.details = details;
   a.U = p.batch * p.heads;
-  a.L = p.ctx_len;
+  a.L = (int)filtered_len(p);
+  a.Ls = p.ctx_len;
   a.D = p.head_dim;
   a.J = p.levels;
   a.nJ = p.ctx_len >> p.levels;
@@ -781,7 +782,8 @@ static hipError_t skim_tiles_common(const wf_params& p, int source, int cpt, int
   a.parent = parent;
   a.npar = npar;
   a.U = p.batch * p.heads;
-  a.L = p.ctx_len;
+  a.L = (int)filtered_len(p);
+  a.Ls = p.ctx_len;
   a.B = p.q_len;
   a.J = J;
   a.nJ = (int)nJ;

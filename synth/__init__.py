@@ -149,6 +149,15 @@ _add(Workload("recursion32k", batch=4, heads=32, ctx_len=32768, head_dim=128,
                           "(4096 positions kept)"))
 
 
+_add(Workload("tail32k", batch=4, heads=32, ctx_len=32768 + 20, head_dim=128,
+              q_len=64, dtype="bf16", rho=0.98, needles=8, wavelet="haar",
+              boundary="symmetric", levels=5,
+              segments=_pool_segments(32768, 5, 2048), budget=2048, seed=5,
+              gen_len=64,
+              description="32K context that is not a multiple of 2^J, with a "
+                          "generation tail: batch 4, 32 heads, d=128, "
+                          "L=32788 (20 positions always kept), G=64, B=64, "
+                          "bf16, Haar J=5, budget 2048"))
 _add(Workload("cached32k", batch=4, heads=32, ctx_len=32768, head_dim=128,
               q_len=64, dtype="bf16", rho=0.98, needles=8, wavelet="haar",
               boundary="symmetric", levels=5,

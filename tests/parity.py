@@ -98,8 +98,12 @@ def pool_tokens(seg, levels: int) -> np.ndarray:
 def check_unit(*, Q, K, V, levels, segments, budget, wavelet, boundary,
                dtype, seg_gpu, tok_gpu, O_gpu, Kg=None, Vg=None, W_gpu=None,
                Wp_gpu=None, what=""):
-    """Full conditional check of one unit's GPU outputs."""
-    A_ref = oracle.dwt(K, levels, wavelet, boundary)
+    """Full conditional check of one unit's GPU outputs.  A length that is
+    not a multiple of 2^J is filtered on its first Lf positions; the rest is
+    always attended, after the selected positions."""
+    L = K.shape[0]
+    Lf = (L >> levels) << levels
+    A_ref = oracle.dwt(K[:Lf], levels, wavelet, boundary)
     W_ref = oracle.skim(Q, A_ref)
     if W_gpu is not None:
         check_scores(W_gpu, W_ref, f"{what} W")
@@ -114,7 +118,7 @@ def check_unit(*, Q, K, V, levels, segments, budget, wavelet, boundary,
     assert np.all(pos < pool.size) and np.all(pool[np.minimum(pos, pool.size - 1)] == tok), \
         f"{what}: tokens outside the pool of the GPU's regions"
     n_tok_diff = check_selection(pos, Wp_ref, keff, f"{what} tok")
-    O_ref = oracle.attend(Q, K, V, tok, Kg, Vg)
+    O_ref = oracle.attend(Q, K, V, np.concatenate([tok, np.arange(Lf, L)]), Kg, Vg)
     err = np.max(np.abs(f64(O_gpu) - O_ref))
     assert err <= O_TOL[dtype], f"{what}: O max abs err {err:.3e} > {O_TOL[dtype]}"
     return dict(seg_diff=n_seg_diff, tok_diff=n_tok_diff, o_err=float(err))

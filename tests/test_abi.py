@@ -65,7 +65,6 @@ def _params(wfpkg, **kw):
     (dict(q_len=257), 2),
     (dict(levels=0), 1),
     (dict(levels=11), 2),
-    (dict(ctx_len=1004), 2),
     (dict(ctx_len=4, levels=3), 1),
     (dict(segments=0), 1),
     (dict(segments=129), 1),

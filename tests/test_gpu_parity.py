@@ -71,12 +71,24 @@ EDGE = {
                           levels=4, segments=30, budget=200, q_len=48, **_BF),
     "tok_j5_b1_d64": V_("tj5", ctx_len=32 * 70, levels=5, segments=12,
                         budget=100, q_len=1, **_BF),
+    # lengths that are not a multiple of 2^J: the last L mod 2^J positions
+    # are always kept after the selection
+    "rem_tok_j5_b64": V_("rj5", ctx_len=32 * 70 + 13, head_dim=128, levels=5,
+                         segments=20, budget=300, q_len=64, **_BF),
+    "rem_tok_j3_tail": V_("rj3", ctx_len=2048 + 5, levels=3, segments=30,
+                          budget=150, q_len=17, gen_len=16, **_BF),
+    "rem_f32_j4": V_("rf4", ctx_len=1024 + 9, levels=4, segments=12,
+                     budget=100),
+    "rem_db2_j3": V_("rdb", ctx_len=2048 + 3, head_dim=128, levels=3,
+                     segments=16, budget=64, wavelet="db2", **_BF),
+    "rem_j10": V_("rj10", ctx_len=1024 * 12 + 700, head_dim=128, levels=10,
+                  segments=3, budget=2000, q_len=8, **_BF),
     "tok_j5_b64_long": V_("tj5l", batch=2, heads=8, ctx_len=32 * 1001,
                           head_dim=128, levels=5, segments=64, budget=700,
                           q_len=64, **_BF),
 }
 
-FULL = ["tiny", "layer8b", "long16k", "headline32k", "stress128k"]
+FULL = ["tiny", "layer8b", "long16k", "headline32k", "stress128k", "tail32k"]
 
 _cache: dict = {}
 
@@ -121,7 +133,8 @@ def run_staged(wf, w, Q, K, V, Kg, Vg):
     Kgd = Kg.to(dev) if G else None
     Vgd = Vg.to(dev) if G else None
     approx = torch.empty((b, h, nJ, d), dtype=torch.float32, device=dev)
-    details = torch.empty((b, h, L - nJ, d), dtype=torch.float32, device=dev)
+    Lf = (L >> w.levels) << w.levels         # the transformed rows
+    details = torch.empty((b, h, Lf - nJ, d), dtype=torch.float32, device=dev)
     say(f"[gpu] {w.name}: wf_dwt_keys")
     wf.wf_dwt_keys(p, Kd, approx, details)
     W = torch.empty((b, h, nJ), dtype=torch.float32, device=dev)
@@ -133,13 +146,14 @@ def run_staged(wf, w, Q, K, V, Kg, Vg):
     say(f"[gpu] {w.name}: wf_scan_select")
     wf.wf_scan_select(p, Qd, Kd, seg, Wp, tok,
                       wf.alloc_workspace(p, wf.OP_SCAN, dev))
-    Ks = torch.empty((b, h, keff + G, d), dtype=K.dtype, device=dev)
+    R = L - ((L >> w.levels) << w.levels)    # always-kept remainder rows
+    Ks = torch.empty((b, h, keff + R + G, d), dtype=K.dtype, device=dev)
     Vs = torch.empty_like(Ks)
     say(f"[gpu] {w.name}: wf_gather_kv")
     wf.wf_gather_kv(p, Kd, Vd, tok, Kgd, Vgd, Ks, Vs)
     O = torch.empty_like(Qd)
     say(f"[gpu] {w.name}: wf_sparse_attn")
-    wf.wf_sparse_attn(p, Qd, Ks, Vs, keff + G, O,
+    wf.wf_sparse_attn(p, Qd, Ks, Vs, keff + R + G, O,
                       wf.alloc_workspace(p, wf.OP_ATTN, dev))
     torch.cuda.synchronize()
     say(f"[gpu] {w.name}: staged done")
@@ -173,7 +187,8 @@ def test_staged_path(wf, name):
         what = f"{name} unit {u}"
         q, k, v = unit(Q, w, u), unit(K, w, u), unit(V, w, u)
         kg, vg = unit(Kg, w, u), unit(Vg, w, u)
-        A_ref, D_ref = oracle.dwt(k, w.levels, w.wavelet, w.boundary,
+        Lf = (w.ctx_len >> w.levels) << w.levels
+        A_ref, D_ref = oracle.dwt(k[:Lf], w.levels, w.wavelet, w.boundary,
                                   details=True)
         check_coefficients(unit(out["approx"], w, u), A_ref, f"{what} A_J")
         det = unit(out["details"], w, u)
@@ -194,10 +209,12 @@ def test_staged_path(wf, name):
         # gather is byte work: bit-exact
         ks, vs = unit(out["Ks"], w, u), unit(out["Vs"], w, u)
         want_k, want_v = k[torch.from_numpy(tok)], v[torch.from_numpy(tok)]
+        want_k, want_v = torch.cat([want_k, k[Lf:]]), torch.cat([want_v, v[Lf:]])
         if kg is not None:
             want_k, want_v = torch.cat([want_k, kg]), torch.cat([want_v, vg])
         assert torch.equal(ks, want_k) and torch.equal(vs, want_v), what
-        O_ref = oracle.attend(q, k, v, tok, kg, vg)
+        O_ref = oracle.attend(q, k, v, np.concatenate([tok, np.arange(Lf, w.ctx_len)]),
+                              kg, vg)
         err = np.abs(f64(unit(out["O"], w, u)) - O_ref).max()
         assert err <= O_TOL[w.dtype], f"{what}: O err {err:.3e}"
 
@@ -230,7 +247,7 @@ def test_fused_edge_shapes(wf, name):
 @pytest.mark.parametrize("name", FULL)
 def test_fused_workloads(wf, name):
     w = synth.WORKLOADS[name]
-    n = {"headline32k": 6, "stress128k": 3}.get(name, 8)
+    n = {"headline32k": 6, "stress128k": 3, "tail32k": 4}.get(name, 8)
     layers = [0, w.layers - 1] if w.layers > 1 else [0]
     for layer in layers:
         _check_fused(wf, w, layer=layer, n_units=n)
@@ -303,7 +320,8 @@ def run_cached(wf, w, Q, K, V, Kg, Vg):
 
 
 @pytest.mark.parametrize("name", ["tiny_scan", "gen_tail", "db2_sym_j3",
-                                  "b256_d128", "layer8b", "cached32k"])
+                                  "b256_d128", "rem_tok_j3_tail", "layer8b",
+                                  "cached32k"])
 def test_cached_step(wf, name):
     """A step from the cached A_J gives the oracle's selection and output."""
     w = EDGE.get(name) or synth.WORKLOADS[name]

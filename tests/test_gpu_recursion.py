@@ -50,6 +50,9 @@ CASES = {
                              proportions=(0.5, 0.5, 0.5, 0.5, 0.5, 0.25)),
     "rec_f32_keep_all": V_("rka", ctx_len=256, levels=3, q_len=16,
                            proportions=(1.0, 1.0, 1.0)),
+    # a length that is not a multiple of 2^B: the remainder follows mu^0
+    "rec_bf16_b3_rem": V_("rrm", ctx_len=1024 + 6, levels=3, dtype="bf16",
+                          gen_len=8, proportions=(0.5, 0.5, 0.25)),
 }
 
 _cache: dict = {}
@@ -103,6 +106,7 @@ def check(wf, w, n_units=8):
     O, tok = run(wf, w, Q, K, V, Kg, Vg)
     counts = wf.recursion_counts(wf.params_for(w), w.proportions)
     assert tok.shape[-1] == 2 * counts[0]
+    Lf = (w.ctx_len >> w.levels) << w.levels
     errs = []
     for u in sample_units(w, n_units):
         q, k, v = unit(Q, w, u), unit(K, w, u), unit(V, w, u)
@@ -110,7 +114,7 @@ def check(wf, w, n_units=8):
         want, want_counts = oracle.recursive_select(q, k, w.levels, props32(w),
                                                     w.wavelet, w.boundary)
         assert list(want_counts) == counts, f"{w.name} unit {u}: counts"
-        got = i64(unit(tok, w, u))
+        got = np.concatenate([i64(unit(tok, w, u)), np.arange(Lf, w.ctx_len)])
         if not np.array_equal(got, want):
             bad = int(np.argmax(got != want)) if got.size == want.size else -1
             raise AssertionError(
@@ -120,7 +124,8 @@ def check(wf, w, n_units=8):
         err = float(np.abs(f64(unit(O, w, u)) - ref).max())
         assert err <= O_TOL[w.dtype], f"{w.name} unit {u}: O err {err:.3e}"
         errs.append(err)
-    say(f"[parity] {w.name}: {len(errs)} units, |mu^0| = {2 * counts[0]}, "
+    say(f"[parity] {w.name}: {len(errs)} units, |mu^0| = {2 * counts[0]} "
+        f"(+{w.ctx_len - Lf} kept), "
         f"max O err {max(errs):.1e}")
 
 
