@@ -5,7 +5,9 @@
 A step is one wf_filter_attend call: DWT + skim, coarse top-S, token scan,
 top-k and sparse attention for every (batch, head) unit of one layer of one
 denoising step.  Inputs are seeded synthetic tensors (synth.WORKLOADS),
-resident in HBM before timing starts.  Prints one JSON line:
+resident in HBM before timing starts; consecutive steps use distinct device
+copies of them (--copies, 3 by default) so that no step finds the rows the
+previous one read in the 256 MB Infinity Cache.  Prints one JSON line:
 
   value       context tokens filtered+attended per second per layer
               (batch * ctx_len / step time)
@@ -182,6 +184,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="headline32k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copies", type=int, default=3,
+                    help="distinct device copies of the inputs, used in turn "
+                         "by consecutive steps so that no step finds the "
+                         "previous step's rows in the 256 MB Infinity Cache")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before timing, run one plain 1 GiB device-to-device "
                          "copy (a known-size kernel for scaling HBM counters)")
@@ -213,9 +219,14 @@ def main() -> int:
     cached = bool(w.cached)
     counts = wf.recursion_counts(p, w.proportions) if recursive else None
     keff = 2 * counts[0] if recursive else wf.effective_budget(p)
-    Qd, Kd, Vd = Q.to(dev), K.to(dev), V.to(dev)
-    Kgd = Kg.to(dev) if Kg is not None else None
-    Vgd = Vg.to(dev) if Vg is not None else None
+    ncopy = max(1, args.copies)
+    copies = []
+    for _ in range(ncopy):
+        copies.append(dict(
+            Q=Q.to(dev), K=K.to(dev), V=V.to(dev),
+            Kg=Kg.to(dev) if Kg is not None else None,
+            Vg=Vg.to(dev) if Vg is not None else None))
+    Qd = copies[0]["Q"]
     O = torch.empty_like(Qd)
     tok = torch.empty((w.batch, w.heads, keff), dtype=torch.int32, device=dev)
     approx = None
@@ -225,7 +236,8 @@ def main() -> int:
         names = wf.recursive_kernel_names(p)
     elif cached:
         # A_J of the prompt keys, computed once as at an earlier step
-        approx = wf.dwt_approx(p, Kd)
+        for c in copies:
+            c["A"] = wf.dwt_approx(p, c["K"])
         torch.cuda.synchronize()
         ws = wf.alloc_workspace(p, wf.OP_CACHED, dev)
         names = wf.cached_kernel_names(p)
@@ -235,31 +247,36 @@ def main() -> int:
     ev = HipEvents((len(names) + 1) * args.steps)
     stream = torch.cuda.current_stream()
 
-    def step_plain():
+    def step_plain(i):
+        c = copies[i % ncopy]
         if recursive:
-            wf.wf_filter_attend_recursive(p, w.proportions, Qd, Kd, Vd, Kgd,
-                                          Vgd, O, tok, ws, stream)
+            wf.wf_filter_attend_recursive(p, w.proportions, c["Q"], c["K"],
+                                          c["V"], c["Kg"], c["Vg"], O, tok,
+                                          ws, stream)
         elif cached:
-            wf.wf_filter_attend_cached(p, Qd, approx, Kd, Vd, Kgd, Vgd, O,
-                                       tok, None, ws, stream)
+            wf.wf_filter_attend_cached(p, c["Q"], c["A"], c["K"], c["V"],
+                                       c["Kg"], c["Vg"], O, tok, None, ws,
+                                       stream)
         else:
-            wf.wf_filter_attend(p, Qd, Kd, Vd, Kgd, Vgd, O, tok, None, ws,
-                                stream)
+            wf.wf_filter_attend(p, c["Q"], c["K"], c["V"], c["Kg"], c["Vg"],
+                                O, tok, None, ws, stream)
 
     def step_timed(i):
+        c = copies[i % ncopy]
         base = i * (len(names) + 1)
         evs = ev.ev[base:base + len(names) + 1]
         if recursive:
-            wf.wf_filter_attend_recursive_timed(p, w.proportions, Qd, Kd, Vd,
-                                                Kgd, Vgd, O, tok, ws, evs,
+            wf.wf_filter_attend_recursive_timed(p, w.proportions, c["Q"],
+                                                c["K"], c["V"], c["Kg"],
+                                                c["Vg"], O, tok, ws, evs,
                                                 stream)
         elif cached:
-            wf.wf_filter_attend_cached_timed(p, Qd, approx, Kd, Vd, Kgd,
-                                             Vgd, O, tok, None, ws, evs,
-                                             stream)
+            wf.wf_filter_attend_cached_timed(p, c["Q"], c["A"], c["K"],
+                                             c["V"], c["Kg"], c["Vg"], O, tok,
+                                             None, ws, evs, stream)
         else:
-            wf.wf_filter_attend_timed(p, Qd, Kd, Vd, Kgd, Vgd, O, tok,
-                                      None, ws, evs, stream)
+            wf.wf_filter_attend_timed(p, c["Q"], c["K"], c["V"], c["Kg"],
+                                      c["Vg"], O, tok, None, ws, evs, stream)
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -268,8 +285,8 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        step_plain()
+    for i in range(args.warmup):
+        step_plain(i)
     torch.cuda.synchronize()
 
     # timed region 1: K plain steps -> value
@@ -279,8 +296,8 @@ def main() -> int:
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record(stream)
-    for _ in range(args.steps):
-        step_plain()
+    for i in range(args.steps):
+        step_plain(i)
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -298,11 +315,17 @@ def main() -> int:
     torch.cuda.synchronize()
     ms_step_events = t_start.elapsed_time(t_end) / args.steps
     per_kernel = {n: 0.0 for n in names}
+    step_ms = []
     for i in range(args.steps):
         base = i * (len(names) + 1)
         for j, n in enumerate(names):
             per_kernel[n] += ev.elapsed_ms(base + j, base + j + 1)
+        step_ms.append(ev.elapsed_ms(base, base + len(names)))
     per_kernel = {n: t / args.steps for n, t in per_kernel.items()}
+    step_ms.sort()
+
+    def pct(q):
+        return step_ms[min(len(step_ms) - 1, int(round(q * (len(step_ms) - 1))))]
     ev.close()
 
     alg = algorithmic_bytes(w, keff, counts)
@@ -353,6 +376,8 @@ def main() -> int:
         "path_algorithmic_bytes": alg["total"] * U,
         "kernel_ms": per_kernel,
         "ms_per_step_with_events": ms_step_events,
+        "step_ms_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
+        "input_copies": ncopy,
         "host_wall_s": wall,
     }
     if not args.no_cpu_baseline:
