@@ -69,7 +69,7 @@ struct SliceBlocks {
   static constexpr int VPB = 16 / NBLK;        // lane values per block
   static constexpr int NST = J == 3 ? 2 : 1;   // blocks kept per lane
   static constexpr int BPC = 128 >> J;         // blocks per 128-token chunk
-  static constexpr int BATCH = 1 << (J - 2);   // chunks per LDS batch (16 KiB at 64 queries)
+  static constexpr int BATCH = J == 5 ? 2 : 1;  // chunks per LDS batch (4 or 8 KiB at 64 queries)
   __device__ static int block(int n, int hi) { return J == 5 ? 0 : J == 4 ? hi : 2 * hi + n; }
   __device__ static bool keeps(int hi) { return J != 5 || hi == 0; }
 };
@@ -80,8 +80,14 @@ constexpr size_t token_batch_bytes(int B) {
   return (size_t)SliceBlocks<J>::BATCH * SliceBlocks<J>::BPC * 2 * B * sizeof(float);
 }
 
+// Waves per SIMD the token skim is compiled to allow: four lets two
+// workgroups share a CU; the 8-token blocks of 128-wide keys need more
+// registers than that leaves, and run one workgroup per CU.
+constexpr int token_skim_waves_per_simd(int D, int J) { return D == 128 && J == 3 ? 2 : 4; }
+
 template <int D, int J>
-__global__ __launch_bounds__(kTokBlock) void token_skim_kernel(TokenSkimArgs a) {
+__global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void token_skim_kernel(
+    TokenSkimArgs a) {
   constexpr int NW = kTokBlock / kWave;  // 8
   constexpr int NIW = NW / 2;            // loading waves
   constexpr int CR = kScanChunk;         // tokens per chunk
@@ -95,9 +101,12 @@ __global__ __launch_bounds__(kTokBlock) void token_skim_kernel(TokenSkimArgs a) 
   static_assert(CR == 32 * NIW, "four 32-token slices per chunk");
   const int B = a.B;
   extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* ring = smem;                                            // [nbuf][CHB]
-  float* red = reinterpret_cast<float*>(smem + (size_t)a.nbuf * CHB);  // [NW][32][2]
-  float* batch = red + NW * 64;  // [2][BATCH * BPC][2][B]: coarse logits, then log-sum-exps
+  unsigned char* ring = smem;  // [nbuf][CHB]
+  // [2][BATCH * BPC][2][B]: coarse logits, then log-sum-exps
+  float* batch = reinterpret_cast<float*>(smem + (size_t)a.nbuf * CHB);
+  // [NW][32][2] running pairs, merged after the last ring load has landed:
+  // they reuse the ring's first bytes
+  float* red = reinterpret_cast<float*>(smem);
   const int slot_floats = BATCH * BPC * 2 * B;
 
   const int item = xcd_swizzle(blockIdx.x, gridDim.x);
@@ -351,20 +360,24 @@ FastPlan plan_fast(const wf_params& p) {
   const long U = (long)p.batch * p.heads;
   const long Lf = filtered_len(p);
   const long chunks = (Lf + kScanChunk - 1) / kScanChunk;
-  const long want = std::max(1L, (long)(device_cu_count() + U - 1) / U);
+  const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
+  // two batch slots of block results; the wave reduction pairs reuse the ring
+  const size_t bb = 2 * (p.levels == 3   ? token_batch_bytes<3>(p.q_len)
+                         : p.levels == 4 ? token_batch_bytes<4>(p.q_len)
+                                         : token_batch_bytes<5>(p.q_len));
+  // Two resident workgroups per CU, each two chunks deep, stream faster than
+  // one three deep (the barrier of one overlaps the other's loads); that
+  // shape is taken whenever two fit in the CU's LDS.
+  constexpr size_t kLdsPerCu = 160 * 1024;
+  const size_t fit2 = kLdsPerCu / 2 > bb ? (kLdsPerCu / 2 - bb) / chb : 0;
+  const int per_cu = fit2 >= 2 && token_skim_waves_per_simd(p.head_dim, p.levels) >= 4 ? 2 : 1;
+  f.nbuf = (int)std::min<size_t>(3, per_cu == 2 ? fit2 : (kLdsPerCu - bb) / chb);
+  f.lds_bytes = f.nbuf * chb + bb;
+  const long want = std::max(1L, ((long)per_cu * device_cu_count() + U - 1) / U);
   const long R = std::min(chunks, want);
   const long cpr = (chunks + R - 1) / R;
   f.span = (int)(cpr * kScanChunk);
   f.R = (int)((Lf + f.span - 1) / f.span);
-  const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
-  // wave reduction pairs, then two batch slots of block results
-  const size_t bb = p.levels == 3 ? token_batch_bytes<3>(p.q_len)
-                    : p.levels == 4 ? token_batch_bytes<4>(p.q_len)
-                                    : token_batch_bytes<5>(p.q_len);
-  const size_t red = (size_t)(kTokBlock / kWave) * 32 * 2 * sizeof(float) + 2 * bb;
-  // three chunks in flight measured best with the per-chunk compute
-  f.nbuf = (int)std::min<size_t>(3, (160 * 1024 - 1024 - red) / chb);
-  f.lds_bytes = f.nbuf * chb + red;
   return f;
 }
 
