@@ -226,15 +226,23 @@ __device__ __forceinline__ void stat_merge(float& m, float& z, float m2, float z
   m = mn;
 }
 
+// 8 waves: two per SIMD, so that one wave's MFMA, exp and LDS latencies
+// overlap the other's work (with one wave per SIMD the ring kernel ran at
+// well under the gather rate of its memory pattern).
+constexpr int kPoolBlock = 512;
+constexpr int kPoolWaves = kPoolBlock / kWave;
+constexpr float kLog2e = 1.44269504088896341f;
+
 template <int WEIGHTS, int D>
-__global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
-  constexpr int NW = kBlock / kWave;
+__global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
+  constexpr int NW = kPoolWaves;
   constexpr int CR = kScanChunk;
   constexpr int G = D / 8;             // 16-byte granules per row
   constexpr int CHB = CR * 2 * D;      // bytes per chunk buffer
   constexpr int IPW = CR * G / (64 * NW);
   constexpr int QSTR = D + 8;
   constexpr int TBW = CR / 16 / NW;    // token blocks per wave
+  static_assert(TBW >= 1 && TBW * 16 * NW == CR, "whole 16-row blocks per wave");
   constexpr int QPG = 4;               // query blocks held in registers
   constexpr int S32 = D / 32;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -244,9 +252,8 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
   float* red = reinterpret_cast<float*>(segs + a.seg_cap);
   const int nqb = (a.B + 15) / 16;
   float* part = red;                   // [nqb][NW][16][2]
-  float* rowa = red + nqb * NW * 32;   // weights: M_q
-  float* rowb = rowa + a.B;            // weights: 1/Z_q
-  float* wsum = rowb + a.B;            // weights: W' of the range
+  float* lse2 = red + nqb * NW * 32;   // weights: log2 of the pool's sum of exp, per query
+  float* wsum = lse2 + a.B;            // weights: W' of the range
 
   const int item = xcd_swizzle(blockIdx.x, gridDim.x);
   const int u = item / a.C, c = item % a.C;
@@ -258,17 +265,17 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
 
   const int s_lo = (int)(pb >> a.J);
   const int ns = (int)((pe - 1) >> a.J) - s_lo + 1;
-  for (int i = threadIdx.x; i < ns; i += kBlock) segs[i] = a.seg[(long)u * a.S + s_lo + i];
+  for (int i = threadIdx.x; i < ns; i += kPoolBlock) segs[i] = a.seg[(long)u * a.S + s_lo + i];
   const bf16_t* Qunit = reinterpret_cast<const bf16_t*>(a.Q) + (long)u * a.B * D;
-  stage_rows_any<bf16_t, D, kBlock>(Qs, a.B, [&](int r) { return Qunit + (long)r * D; });
+  stage_rows_any<bf16_t, D, kPoolBlock>(Qs, a.B, [&](int r) { return Qunit + (long)r * D; });
   if constexpr (WEIGHTS) {
     const float* stt = a.stats + (long)u * a.Cs * 2 * a.B;
-    for (int q = threadIdx.x; q < a.B; q += kBlock) {
+    for (int q = threadIdx.x; q < a.B; q += kPoolBlock) {
       float mx = -INFINITY, z = 0.f;
       for (int k = 0; k < a.Cs; ++k)
         stat_merge(mx, z, stt[(long)k * 2 * a.B + q], stt[(long)k * 2 * a.B + a.B + q]);
-      rowa[q] = mx;
-      rowb[q] = 1.f / z;
+      // exp(s - M) / Z = 2^(s log2(e) - (M log2(e) + log2(Z)))
+      lse2[q] = fmaf(mx, kLog2e, __log2f(z));
     }
   }
   __syncthreads();  // every regular load above has been consumed
@@ -284,6 +291,7 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
   const uint32_t ring_lds = lds_offset(ring);
   const int nbuf = a.nbuf;
 
+  const float s2 = a.scale * kLog2e;
   for (int qg = 0; qg < nqb; qg += QPG) {
     // query operands of this group, in registers for the whole range
     u32x4 qreg[QPG][S32];
@@ -294,6 +302,16 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
       for (int s = 0; s < S32; ++s)
         qreg[j][s] = *reinterpret_cast<const u32x4*>(arow + 32 * s + 8 * g);
     }
+    // weights: the log2-domain normalisers of the lane's query rows (rows
+    // past B contribute 2^-inf = 0)
+    float c2[QPG][4];
+#pragma unroll
+    for (int j = 0; j < QPG; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = (qg + j) * 16 + 4 * g + i;
+        c2[j][i] = WEIGHTS && q < a.B ? lse2[q] : INFINITY;
+      }
     float sm[QPG][4], sz[QPG][4];  // per-lane running row max / sum of exp
 #pragma unroll
     for (int j = 0; j < QPG; ++j)
@@ -338,8 +356,8 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
           // lane holds logit[q = 16 (qg + j) + 4 g + i][p = p0 + row]
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float v = acc[i] * a.scale;
             if constexpr (!WEIGHTS) {
+              const float v = acc[i] * a.scale;
               if (ok) {
                 if (v > sm[j][i]) {
                   sz[j][i] = sz[j][i] * __expf(sm[j][i] - v) + 1.f;
@@ -349,8 +367,7 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
                 }
               }
             } else {
-              const int q = (qg + j) * 16 + 4 * g + i;
-              if (q < a.B) wk += __expf(v - rowa[q]) * rowb[q];
+              wk += __builtin_amdgcn_exp2f(fmaf(acc[i], s2, -c2[j][i]));
             }
           }
         }
@@ -385,7 +402,7 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
   }
   if constexpr (!WEIGHTS) {
     float* stt = a.stats + ((long)u * a.Cs + c) * 2 * a.B;
-    for (int q = threadIdx.x; q < a.B; q += kBlock) {
+    for (int q = threadIdx.x; q < a.B; q += kPoolBlock) {
       const int qb = q >> 4, r = q & 15;
       float mx = -INFINITY, z = 0.f;
 #pragma unroll
@@ -396,7 +413,7 @@ __global__ __launch_bounds__(kBlock) void scan_ring_kernel(ScanArgs a) {
     }
   } else {
     float* dst = a.wpool + (long)u * a.P + pb;
-    for (int i = threadIdx.x; i < (int)(pe - pb); i += kBlock) dst[i] = wsum[i];
+    for (int i = threadIdx.x; i < (int)(pe - pb); i += kPoolBlock) dst[i] = wsum[i];
   }
 }
 
@@ -432,7 +449,6 @@ ScanPlan plan_scan(const wf_params& p) {
   const long U = (long)p.batch * p.heads;
   const long chunks = (P + kScanChunk - 1) / kScanChunk;
   const int nqb = (p.q_len + 15) / 16;
-  const size_t red_base = ((size_t)nqb * 4 * 16 * 2 + (size_t)2 * p.q_len) * sizeof(float);
   if (p.dtype == WF_BF16) {
     // one workgroup per CU, each streaming a long range through the ring
     const long want = std::max(1L, (long)(device_cu_count() + U - 1) / U);
@@ -443,10 +459,12 @@ ScanPlan plan_scan(const wf_params& p) {
     s.chunks = (int)((P + s.span - 1) / s.span);
     s.seg_cap = (s.span >> p.levels) + 2;
     const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
-    const size_t other = (size_t)p.q_len * (p.head_dim + 8) * 2 +
-                         (size_t)s.seg_cap * 4 + red_base +
-                         (size_t)s.span * sizeof(float);
-    s.nbuf = (int)std::min<size_t>(4, (kLdsBudget - std::min(other, kLdsBudget)) / chb);
+    // wave partials, the per-query normalisers, then W' of the range
+    const size_t red_ring =
+        ((size_t)nqb * kPoolWaves * 16 * 2 + (size_t)p.q_len + (size_t)s.span) * sizeof(float);
+    const size_t other = (size_t)p.q_len * (p.head_dim + 8) * 2 + (size_t)s.seg_cap * 4 + red_ring;
+    // three slots (two chunks in flight) measured slightly faster than four
+    s.nbuf = (int)std::min<size_t>(3, (kLdsBudget - std::min(other, kLdsBudget)) / chb);
     s.lds_bytes = s.nbuf * chb + other;
     if (s.nbuf < 2) s.nbuf = 0;  // rejected by the caller
     return s;
@@ -456,12 +474,13 @@ ScanPlan plan_scan(const wf_params& p) {
   s.span = (int)(cpw * kScanChunk);
   s.chunks = (int)((P + s.span - 1) / s.span);
   const size_t stride = (size_t)p.head_dim * 4 + 16;
+  const size_t red_base = ((size_t)nqb * 4 * 16 * 2 + (size_t)2 * p.q_len) * sizeof(float);
   s.lds_bytes = (size_t)(p.q_len + kScanChunk) * stride + red_base;
   return s;
 }
 
 template <class Kernel>
-static hipError_t launch_with_lds(Kernel kern, dim3 grid, size_t lds, hipStream_t s,
+static hipError_t launch_with_lds(Kernel kern, dim3 grid, int block, size_t lds, hipStream_t s,
                                   const ScanArgs& a) {
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -469,7 +488,7 @@ static hipError_t launch_with_lds(Kernel kern, dim3 grid, size_t lds, hipStream_
                                        (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(kern, grid, dim3(kBlock), lds, s, a);
+  hipLaunchKernelGGL(kern, grid, dim3(block), lds, s, a);
   return hipGetLastError();
 }
 
@@ -477,9 +496,9 @@ template <int WEIGHTS, typename T, int D>
 static hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t s) {
   const dim3 grid((unsigned)(a.U * a.C));
   if constexpr (sizeof(T) == 2)
-    return launch_with_lds(scan_ring_kernel<WEIGHTS, D>, grid, lds, s, a);
+    return launch_with_lds(scan_ring_kernel<WEIGHTS, D>, grid, kPoolBlock, lds, s, a);
   else
-    return launch_with_lds(scan_chunk_kernel<WEIGHTS, T, D>, grid, lds, s, a);
+    return launch_with_lds(scan_chunk_kernel<WEIGHTS, T, D>, grid, kBlock, lds, s, a);
 }
 
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
