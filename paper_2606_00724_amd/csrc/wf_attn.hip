@@ -382,9 +382,14 @@ struct RingRowPtr {
   }
 };
 
+// 8 waves, two per SIMD, so that one wave's MFMA, exp and LDS latencies
+// overlap the other's work; with up to four query blocks each block's rows
+// are split over two waves.
+constexpr int kAttnRingBlock = 512;
+
 template <int D>
-__global__ __launch_bounds__(kBlock) void attn_ring_kernel(AttnArgs a) {
-  constexpr int NW = kBlock / kWave;
+__global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
+  constexpr int NW = kAttnRingBlock / kWave;
   constexpr int CR = kRingRows;
   constexpr int G = D / 8;
   constexpr int CHB = CR * 2 * D;            // bytes of one K (or V) chunk
@@ -403,7 +408,7 @@ __global__ __launch_bounds__(kBlock) void attn_ring_kernel(AttnArgs a) {
 
   if (a.tok) {
     const long hi = min(re0, (long)a.nsel);
-    for (long i = rb0 + threadIdx.x; i < hi; i += kBlock)
+    for (long i = rb0 + threadIdx.x; i < hi; i += kAttnRingBlock)
       toks[i - rb0] = a.tok[(long)u * a.nsel + i];
   }
   __syncthreads();
@@ -424,7 +429,7 @@ __global__ __launch_bounds__(kBlock) void attn_ring_kernel(AttnArgs a) {
   kp.Lf = vp.Lf = a.Lf;
 
   const int nqb = (a.B + 15) / 16;
-  const int tsplit = nqb <= 2 ? 2 : 1;       // row halves per query block
+  const int tsplit = 2 * nqb <= NW ? 2 : 1;  // row halves per query block
   const int qpg = NW / tsplit;
   const int ngroups = (nqb + qpg - 1) / qpg;
   const int part = wave % tsplit;
@@ -669,7 +674,8 @@ AttnPlan plan_attn(const wf_params& p, long nrows) {
     const size_t budget = 160 * 1024 - 1024;
     a.nbuf = (int)std::min<size_t>(4, (budget - toks) / stage);
     if (a.nbuf < 2) a.nbuf = 0;  // rejected by the caller
-    const size_t comb = (size_t)4 * 16 * D * 4 + (size_t)2 * 4 * 16 * 4;
+    constexpr int nw = kAttnRingBlock / kWave;  // row-half merge: [nw][16][D] + 2 [nw][16]
+    const size_t comb = (size_t)nw * 16 * D * 4 + (size_t)2 * nw * 16 * 4;
     a.lds_bytes = std::max((size_t)a.nbuf * stage, comb) + toks;
     return a;
   }
@@ -698,7 +704,8 @@ static hipError_t attn_launch(const AttnArgs& a, size_t lds, hipStream_t s) {
                                        (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)(a.U * a.NS)), dim3(kBlock), lds, s, a);
+  const int block = sizeof(T) == 2 ? kAttnRingBlock : kBlock;
+  hipLaunchKernelGGL(kern, dim3((unsigned)(a.U * a.NS)), dim3(block), lds, s, a);
   return hipGetLastError();
 }
 
