@@ -439,6 +439,57 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
   float* ps_base = a.pstat + ((long)u * a.NS + sp) * 2 * a.B;
   const uint32_t ring_lds = lds_offset(ring);
   const int nbuf = a.nbuf;
+  const float c2 = a.scale * kLog2e;  // scores in log2 units
+
+  // K and V rows of chunk c into the ring slot at `slot`.  A chunk whose
+  // rows are all selected tokens (rows past the split repeat its last row)
+  // takes one token id and one address per row for both loads; any other
+  // chunk goes through the general row map.
+  const bf16_t* kunit = kp.base + (long)u * kp.unit_rows * D;
+  const bf16_t* vunit = vp.base + (long)u * vp.unit_rows * D;
+  const int split_last = (int)(re0 - 1 - rb0);
+  auto issue_kv = [&](int c, uint32_t slot) {
+    const long r0 = rb0 + (long)c * CR;
+    if (a.tok && min(r0 + CR, re0) <= (long)a.nsel) {
+      constexpr int RPI = 64 / G;
+#pragma unroll
+      for (int i = 0; i < IPW; ++i) {
+        const int inst = wave * IPW + i;
+        const int r = inst * RPI + lane / G;
+        const int k = (lane % G) ^ granule_swz<G>(r);
+        // token ids are clamped into the unit: a bad id cannot leave K / V
+        const int t = min(max(toks[min((int)(r0 - rb0) + r, split_last)], 0), a.L - 1);
+        const long off = (long)t * D + 8 * k;
+        async_load16<false>(kunit + off, __builtin_amdgcn_readfirstlane(slot + 1024u * inst));
+        async_load16<true>(vunit + off, __builtin_amdgcn_readfirstlane(slot + CHB + 1024u * inst));
+      }
+    } else {
+      kp.r0 = vp.r0 = r0;
+      issue_chunk<CR, G, NW>(slot, kp);
+      issue_chunk<CR, G, NW, true>(slot + CHB, vp);
+    }
+  };
+
+  // LDS byte offsets of the lane's operands inside a 32-row block: the
+  // granule swizzle depends only on the row mod 32 and every block starts at
+  // a multiple of 32 rows, so one set serves all blocks
+  int koff[D / 32], kyoff[D / 32], vlo[D / 16], vhi[D / 16];
+  {
+    const int rx0 = 8 * (col >> 2) + (col & 3);  // QK rows rx0 and rx0 + 4
+    const int t00 = 8 * g + (col >> 2);          // PV rows t00 and t00 + 4
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s) {
+      koff[s] = granule_offset<G>(rx0, 4 * s + g);
+      kyoff[s] = granule_offset<G>(rx0 + 4, 4 * s + g);
+    }
+#pragma unroll
+    for (int cb = 0; cb < D / 16; ++cb) {
+      const int gran = 2 * cb + ((col & 3) >> 1);
+      const int byte = 8 * (col & 1);
+      vlo[cb] = granule_offset<G>(t00, gran) + byte;
+      vhi[cb] = granule_offset<G>(t00 + 4, gran) + byte;
+    }
+  }
 
   for (int grp = 0; grp < ngroups; ++grp) {
     const int qb = grp * qpg + wave / tsplit;
@@ -457,84 +508,94 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
 #pragma unroll
     for (int s = 0; s < D / 32; ++s) asm volatile("" ::"v"(qreg[s]));
     // ring of nbuf slots, nbuf - 1 chunks in flight ahead of the one consumed
-    for (int k = 0; k < nch && k < nbuf - 1; ++k) {
-      kp.r0 = vp.r0 = rb0 + (long)k * CR;
-      issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(k * 2 * CHB), kp);
-      issue_chunk<CR, G, NW, true>(ring_lds + (uint32_t)(k * 2 * CHB + CHB), vp);
-    }
+    for (int k = 0; k < nch && k < nbuf - 1; ++k)
+      issue_kv(k, ring_lds + (uint32_t)(k * 2 * CHB));
     for (int ch = 0; ch < nch; ++ch) {
       const int nr = (int)min((long)CR, re0 - (rb0 + (long)ch * CR));
       wait_vmcnt_chunks<2 * IPW>(min(nch - 1 - ch, nbuf - 2));
       lds_barrier();  // chunk ch visible; everyone is past chunk ch - 1
-      if (ch + nbuf - 1 < nch) {
-        kp.r0 = vp.r0 = rb0 + (long)(ch + nbuf - 1) * CR;
-        const uint32_t slot = ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * 2 * CHB);
-        issue_chunk<CR, G, NW>(slot, kp);
-        issue_chunk<CR, G, NW, true>(slot + CHB, vp);
-      }
+      if (ch + nbuf - 1 < nch)
+        issue_kv(ch + nbuf - 1, ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * 2 * CHB));
       const unsigned char* Kb = ring + (ch % nbuf) * 2 * CHB;
       const unsigned char* Vb = Kb + CHB;
       if (active) {
         const int rb = part * R;
         const int re = min(rb + R, nr);
         for (int sb = rb; sb < re; sb += 32) {
-          const int rx = sb + 8 * (col >> 2) + (col & 3);
+          // every LDS operand of the block is read first: the V reads'
+          // latency then overlaps the QK products and the softmax
+          const unsigned char* kblk = Kb + sb * (16 * G);
+          const uint32_t vblk = lds_offset(Vb) + (uint32_t)(sb * (16 * G));
+          u32x4 kx[D / 32], ky[D / 32], vb[D / 16];
+#pragma unroll
+          for (int s = 0; s < D / 32; ++s) {
+            kx[s] = *reinterpret_cast<const u32x4*>(kblk + koff[s]);
+            ky[s] = *reinterpret_cast<const u32x4*>(kblk + kyoff[s]);
+          }
+#pragma unroll
+          for (int cb = 0; cb < D / 16; ++cb) {
+            const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4i16*)(size_t)(vblk + vlo[cb]));
+            const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4i16*)(size_t)(vblk + vhi[cb]));
+            const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
+            const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
+            vb[cb] = u32x4{l2[0], l2[1], h2[0], h2[1]};
+          }
           f32x4 ax = {0.f, 0.f, 0.f, 0.f}, ay = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int s = 0; s < D / 32; ++s) {
-            const u32x4 kx = *reinterpret_cast<const u32x4*>(Kb + granule_offset<G>(rx, 4 * s + g));
-            const u32x4 ky = *reinterpret_cast<const u32x4*>(Kb + granule_offset<G>(rx + 4, 4 * s + g));
             ax = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, kx), __builtin_bit_cast(bf16x8, qreg[s]), ax, 0, 0, 0);
+                __builtin_bit_cast(bf16x8, kx[s]), __builtin_bit_cast(bf16x8, qreg[s]), ax, 0, 0, 0);
             ay = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, ky), __builtin_bit_cast(bf16x8, qreg[s]), ay, 0, 0, 0);
+                __builtin_bit_cast(bf16x8, ky[s]), __builtin_bit_cast(bf16x8, qreg[s]), ay, 0, 0, 0);
           }
-          // lane holds scores of rows sb + 8g + e (e < 8) for query col
-          float sv[8];
+          // lane holds the scores of rows sb + 8g + e (e < 8) for query col,
+          // here in log2 units; rows past the range (only in a last partial
+          // block) are -inf
+          float t[8];
+          const bool full = sb + 32 <= re;  // uniform
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            sv[i] = (sb + 8 * g + i < re) ? ax[i] * a.scale : -INFINITY;
-            sv[4 + i] = (sb + 8 * g + 4 + i < re) ? ay[i] * a.scale : -INFINITY;
+            t[i] = ax[i] * c2;
+            t[4 + i] = ay[i] * c2;
           }
-          float mb = sv[0];
+          if (!full) {
 #pragma unroll
-          for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
-          mb = fmaxf(mb, __shfl_xor(mb, 16));
-          mb = fmaxf(mb, __shfl_xor(mb, 32));
-          const float m_new = fmaxf(m_run, mb);
-          const float alpha = __expf(m_run - m_new);
+            for (int e = 0; e < 8; ++e)
+              if (sb + 8 * g + e >= re) t[e] = -INFINITY;
+          }
+          float mb = fmaxf(fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3])),
+                           fmaxf(fmaxf(t[4], t[5]), fmaxf(t[6], t[7])));
+          mb = max_xor32(max_xor16(mb));
+          const float m_new = fmaxf(m_run, mb);  // finite: row sb is in range
           float pv[8], ps = 0.f;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            pv[e] = sv[e] > -INFINITY ? __expf(sv[e] - m_new) : 0.f;
+            pv[e] = __builtin_amdgcn_exp2f(t[e] - m_new);  // 2^-inf = 0
             ps += pv[e];
           }
-          ps += __shfl_xor(ps, 16);
-          ps += __shfl_xor(ps, 32);
-          l_run = l_run * alpha + ps;
+          ps = add_xor32(add_xor16(ps));
+          // rescale only when some row maximum grew: otherwise the factor
+          // is exactly 1 and the update is the same without it
+          if (__builtin_amdgcn_ballot_w64(m_new != m_run) != 0) {
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            l_run = l_run * alpha + ps;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float ai = __shfl(alpha, 4 * g + i);
+            for (int i = 0; i < 4; ++i) {
+              const float ai = __shfl(alpha, 4 * g + i);
 #pragma unroll
-            for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
+              for (int cb = 0; cb < D / 16; ++cb) O[cb][i] *= ai;
+            }
+          } else {
+            l_run += ps;
           }
           const u32x4 pp = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
                             pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
-          const int t0 = sb + 8 * g + (col >> 2);
 #pragma unroll
-          for (int cb = 0; cb < D / 16; ++cb) {
-            const int gran = 2 * cb + ((col & 3) >> 1);
-            const int byte = 8 * (col & 1);
-            const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) v4i16*)(size_t)(lds_offset(Vb + granule_offset<G>(t0, gran) + byte)));
-            const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) v4i16*)(size_t)(lds_offset(Vb + granule_offset<G>(t0 + 4, gran) + byte)));
-            const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
-            const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
-            const u32x4 vb = {l2[0], l2[1], h2[0], h2[1]};
+          for (int cb = 0; cb < D / 16; ++cb)
             O[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, pp), __builtin_bit_cast(bf16x8, vb), O[cb], 0, 0, 0);
-          }
+                __builtin_bit_cast(bf16x8, pp), __builtin_bit_cast(bf16x8, vb[cb]), O[cb], 0, 0, 0);
           m_run = m_new;
         }
       }
@@ -553,7 +614,7 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
         }
         const int q = qb * 16 + col;
         if (g == 0 && q < a.B) {
-          ps_base[q] = m_run;
+          ps_base[q] = m_run * kLn2;  // back to natural-log units
           ps_base[a.B + q] = l_run;
         }
       }
@@ -581,8 +642,8 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
           const int q = qb * 16 + rr;
           const float m0 = cm[wave * 16 + rr], m1 = cm[(wave + 1) * 16 + rr];
           const float M = fmaxf(m0, m1);
-          const float w0 = m0 > -INFINITY ? __expf(m0 - M) : 0.f;
-          const float w1 = m1 > -INFINITY ? __expf(m1 - M) : 0.f;
+          const float w0 = m0 > -INFINITY ? __builtin_amdgcn_exp2f(m0 - M) : 0.f;
+          const float w1 = m1 > -INFINITY ? __builtin_amdgcn_exp2f(m1 - M) : 0.f;
           const float lsum = w0 * cl[wave * 16 + rr] + w1 * cl[(wave + 1) * 16 + rr];
           if (q < a.B) {
 #pragma unroll
@@ -591,7 +652,7 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
                   w0 * cO[(wave * 16 + rr) * D + cb * 16 + col] +
                   w1 * cO[((wave + 1) * 16 + rr) * D + cb * 16 + col];
             if (col == 0) {
-              ps_base[q] = M;
+              ps_base[q] = M * kLn2;  // back to natural-log units
               ps_base[a.B + q] = lsum;
             }
           }

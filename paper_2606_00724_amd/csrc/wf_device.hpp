@@ -37,8 +37,13 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
   return u >> 16;
 }
 
+// Two floats to packed bf16 with one v_cvt_pk_bf16_f32: round to nearest
+// even, bit-identical to f32_to_bf16_bits for every finite input (NaNs stay
+// NaNs, possibly with another payload).
+typedef __bf16 hw_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float hw_f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((hw_f32x2{lo, hi}), hw_bf16x2));
 }
 
 template <typename T>
@@ -136,6 +141,9 @@ __device__ __forceinline__ f32x4 tile_dot<float, 128>(const float* a,
   return tile_dot_f32<128>(a, b, c);
 }
 
+constexpr float kLog2e = 1.44269504088896341f;  // log2(e)
+constexpr float kLn2 = 0.69314718055994531f;     // ln(2)
+
 // ------------------------------------------------------------ reductions
 
 __device__ __forceinline__ float wave_max16(float v) {
@@ -143,6 +151,28 @@ __device__ __forceinline__ float wave_max16(float v) {
 #pragma unroll
   for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;
+}
+
+// Reductions over the lane pairs (l, l ^ 16) and (l, l ^ 32) on the VALU:
+// v_permlane16_swap / v_permlane32_swap of a value with itself leave the
+// two partners' values in the two results (lane l gets {v[l], v[l ^ 16]} and
+// {v[l % 32], v[l % 32 + 32]}), so no LDS round trip is needed. Every lane of
+// the wave must be active.
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float add_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float add_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // Order-preserving map of a float to uint32 (larger float -> larger key).

@@ -148,7 +148,7 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
 
   float* out = a.blocks + (long)u * a.nJ * 2 * B;  // [nJ][2][B]
   const long jend = te >> J;                        // blocks of this range end here
-  const float c2 = a.scale * 1.44269504088896341f;  // scale * log2(e)
+  const float c2 = a.scale * kLog2e;
   const float cl = a.scale * a.norm;
   const bool keeps = SB::keeps(hi);
   const bool vec = (B & 1) == 0;  // block rows are 16-byte multiples

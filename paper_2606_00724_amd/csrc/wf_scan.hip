@@ -231,7 +231,6 @@ __device__ __forceinline__ void stat_merge(float& m, float& z, float m2, float z
 // well under the gather rate of its memory pattern).
 constexpr int kPoolBlock = 512;
 constexpr int kPoolWaves = kPoolBlock / kWave;
-constexpr float kLog2e = 1.44269504088896341f;
 
 template <int WEIGHTS, int D>
 __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
