@@ -265,12 +265,26 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
   int tile = 0;
   for (int base = 0; base < n; base += NT * ITEMS, ++tile) {
     const int start = base + tid * ITEMS;
+    // the thread's ITEMS consecutive scores, as 16-byte loads when aligned
+    float v[ITEMS];
+    if (start + ITEMS <= n && (reinterpret_cast<uintptr_t>(score + start) & 15) == 0) {
+#pragma unroll
+      for (int q = 0; q < ITEMS / 4; ++q) {
+        const float4 f = reinterpret_cast<const float4*>(score + start)[q];
+        v[4 * q] = f.x;
+        v[4 * q + 1] = f.y;
+        v[4 * q + 2] = f.z;
+        v[4 * q + 3] = f.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < ITEMS; ++j) v[j] = start + j < n ? score[start + j] : 0.f;
+    }
     uint32_t gt_bits = 0, eq_bits = 0;
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j) {
-      const int i = start + j;
-      if (i < n) {
-        const uint32_t key = order_key(score[i]);
+      if (start + j < n) {
+        const uint32_t key = order_key(v[j]);
         gt_bits |= (key > prefix ? 1u : 0u) << j;
         eq_bits |= (key == prefix ? 1u : 0u) << j;
       }

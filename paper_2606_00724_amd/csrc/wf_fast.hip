@@ -268,13 +268,13 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
 constexpr int kFastSelectBlock = 1024;
 
 __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelectArgs a,
-                                                                       int w_in_lds) {
+                                                                       int w_in_lds,
+                                                                       int seg_in_lds) {
   constexpr int NT = kFastSelectBlock;
-  __shared__ float row_max[16 * kFastMaxQBlocks];
-  __shared__ float row_inv[16 * kFastMaxQBlocks];
+  __shared__ float row_c[16 * kFastMaxQBlocks];
   __shared__ float part_m[NT], part_z[NT];
   __shared__ SelectShared<NT> sh;
-  extern __shared__ float wsh[];
+  extern __shared__ float wsh[];  // W (when it fits), then the picked block ids
   const int u = blockIdx.x;
   const int B = a.B, nJ = a.nJ;
   const float* ws = a.wstats + (long)u * a.R * 2 * B;
@@ -282,56 +282,87 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
     float mx = -INFINITY, z = 0.f;
     for (int r = 0; r < a.R; ++r)
       stat_absorb(mx, z, ws[(long)r * 2 * B + q], ws[(long)r * 2 * B + B + q]);
-    row_max[q] = mx;
-    row_inv[q] = 1.f / z;
+    // exp(l - M_q) / Z_q = 2^(l log2(e) - c_q)
+    row_c[q] = fmaf(mx, kLog2e, __log2f(z));
   }
   __syncthreads();
-  // W_j = sum_q softmax_j(l_q.): four threads per block j, 16 queries each
+  // W_j = sum_q softmax_j(l_q.): four threads per block j, queries
+  // q0 .. q0 + 15 each; a thread's q0 is the same for all its blocks, so its
+  // normalisers stay in registers (2^-inf = 0 for queries past B)
   const float* lg = a.blocks + (long)u * nJ * 2 * B;  // row j: logits at 2 j B
   float* W = a.W + (long)u * nJ;
   const bool vec = (B & 3) == 0;
-  for (int base = 0; base < 4 * nJ; base += NT) {
-    const int t = base + threadIdx.x;
-    const int j = t >> 2, q0 = 16 * (t & 3);
-    float w = 0.f;
-    if (t < 4 * nJ && q0 < B) {
-      const float* row = lg + (long)j * 2 * B + q0;
-      const int nq = min(16, B - q0);
+  const int q0 = 16 * (threadIdx.x & 3);
+  const int nq = min(16, B - q0);
+  float cq[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) cq[k] = k < nq ? row_c[q0 + k] : INFINITY;
+  constexpr int UNR = 4;  // rows of blocks whose loads are in flight together
+  for (int base = 0; base < 4 * nJ; base += UNR * NT) {
+    float x[UNR][16];
+#pragma unroll
+    for (int r = 0; r < UNR; ++r) {
+      const int t = base + r * NT + threadIdx.x;
+      const bool ok = t < 4 * nJ && nq > 0;
+      const float* row = lg + (long)(t >> 2) * 2 * B + q0;
       if (vec) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          if (4 * k < nq) {
-            const float4 v = *reinterpret_cast<const float4*>(row + 4 * k);
-            const int q = q0 + 4 * k;
-            w += __expf(v.x - row_max[q]) * row_inv[q] +
-                 __expf(v.y - row_max[q + 1]) * row_inv[q + 1] +
-                 __expf(v.z - row_max[q + 2]) * row_inv[q + 2] +
-                 __expf(v.w - row_max[q + 3]) * row_inv[q + 3];
-          }
+        for (int k4 = 0; k4 < 4; ++k4) {
+          const float4 f = ok && 4 * k4 < nq ? reinterpret_cast<const float4*>(row)[k4]
+                                              : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+          x[r][4 * k4] = f.x;
+          x[r][4 * k4 + 1] = f.y;
+          x[r][4 * k4 + 2] = f.z;
+          x[r][4 * k4 + 3] = f.w;
         }
       } else {
-        for (int k = 0; k < nq; ++k) w += __expf(row[k] - row_max[q0 + k]) * row_inv[q0 + k];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) x[r][k] = ok && k < nq ? row[k] : -INFINITY;
       }
     }
-    w += __shfl_xor(w, 1);
-    w += __shfl_xor(w, 2);
-    if (t < 4 * nJ && (t & 3) == 0) {
-      W[j] = w;
-      if (w_in_lds) wsh[j] = w;
+#pragma unroll
+    for (int r = 0; r < UNR; ++r) {
+      const int t = base + r * NT + threadIdx.x;
+      float w = 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) w += __builtin_amdgcn_exp2f(fmaf(x[r][k], kLog2e, -cq[k]));
+      w += __shfl_xor(w, 1);
+      w += __shfl_xor(w, 2);
+      if (t < 4 * nJ && (t & 3) == 0) {
+        W[t >> 2] = w;
+        if (w_in_lds) wsh[t >> 2] = w;
+      }
     }
   }
   __syncthreads();
   int32_t* seg = a.seg + (long)u * a.S;
+  int32_t* seg_sh = reinterpret_cast<int32_t*>(wsh + (w_in_lds ? nJ : 0));
   block_select_topk<NT>(w_in_lds ? wsh : W, nJ, a.S,
-                        [&](uint32_t pos, int i) { seg[pos] = i; }, sh);
+                        [&](uint32_t pos, int i) {
+                          seg[pos] = i;
+                          if (seg_in_lds) seg_sh[pos] = i;
+                        },
+                        sh);
   __syncthreads();
   // pool normalisers: thread (q, part) folds selected blocks part, part + parts, ...
+  const int32_t* segx = seg_in_lds ? seg_sh : seg;
   const int parts = NT / B;
   const int q = threadIdx.x % B, part = threadIdx.x / B;
   float mx = -INFINITY, z = 0.f;
   if (part < parts) {
     const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
-    for (int s = part; s < a.S; s += parts) stat_absorb(mx, z, lse[(long)seg[s] * 2 * B + q], 1.f);
+    constexpr int BATCH = 8;  // loads in flight together
+    for (int s0 = part; s0 < a.S; s0 += BATCH * parts) {
+      float v[BATCH];
+#pragma unroll
+      for (int k = 0; k < BATCH; ++k) {
+        const int s_ = s0 + k * parts;
+        v[k] = s_ < a.S ? lse[(long)segx[s_] * 2 * B + q] : -INFINITY;
+      }
+#pragma unroll
+      for (int k = 0; k < BATCH; ++k)
+        if (s0 + k * parts < a.S) stat_absorb(mx, z, v[k], 1.f);
+    }
   }
   part_m[threadIdx.x] = mx;
   part_z[threadIdx.x] = z;
@@ -442,14 +473,17 @@ hipError_t launch_fast_select(const wf_params& p, const float* blocks, const flo
   a.R = f.R;
   a.S = p.segments;
   const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
-  const size_t lds = in_lds ? (size_t)a.nJ * sizeof(float) : 0;
+  const int seg_in_lds = a.S <= kSelectLdsSegs ? 1 : 0;
+  // W when it fits, then the picked block ids when they fit
+  const size_t lds =
+      ((in_lds ? (size_t)a.nJ : 0) + (seg_in_lds ? (size_t)a.S : 0)) * sizeof(float);
   if (lds > 32768) {  // with the static arrays, past the default 64 KiB
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fast_select_kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(fast_select_kernel, dim3((unsigned)a.U), dim3(kFastSelectBlock), lds, s, a,
-                     in_lds);
+                     in_lds, seg_in_lds);
   return hipGetLastError();
 }
 

@@ -14,6 +14,8 @@ namespace wf {
 
 // Scores up to this many floats are staged in LDS by the select kernels.
 constexpr int kSelectLdsFloats = 16384;
+// region ids a select kernel keeps in LDS (more are read from global memory)
+constexpr int kSelectLdsSegs = 8192;
 
 struct DwtPlan {
   int streams;  // streams per workgroup

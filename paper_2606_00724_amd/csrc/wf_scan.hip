@@ -212,9 +212,10 @@ struct PoolRowPtr {
   long last;            // the unit's last row (region ids are clamped to it)
   int J, mask, s_lo;
   __device__ __forceinline__ const bf16_t* operator()(int r) const {
-    const long p = min(p0 + r, plast);
-    const long sg = segs[(int)(p >> J) - s_lo];
-    return Kunit + min(max((sg << J) | (p & mask), 0L), last) * D;
+    // row numbers fit in 32 bits (ctx_len <= 2^30)
+    const int p = (int)min(p0 + r, plast);
+    const int t = (segs[(p >> J) - s_lo] << J) | (p & mask);
+    return Kunit + (long)min(max(t, 0), (int)last) * D;
   }
 };
 
@@ -291,6 +292,12 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
   const int nbuf = a.nbuf;
 
   const float s2 = a.scale * kLog2e;
+  // LDS byte offsets of the lane's key operands: the same rows of every chunk
+  int boff[TBW][S32];
+#pragma unroll
+  for (int k = 0; k < TBW; ++k)
+#pragma unroll
+    for (int s = 0; s < S32; ++s) boff[k][s] = granule_offset<G>((wave * TBW + k) * 16 + col, 4 * s + g);
   for (int qg = 0; qg < nqb; qg += QPG) {
     // query operands of this group, in registers for the whole range
     u32x4 qreg[QPG][S32];
@@ -340,23 +347,28 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
         const bool ok = row < np;
         u32x4 bv[S32];
 #pragma unroll
+        for (int s = 0; s < S32; ++s) bv[s] = *reinterpret_cast<const u32x4*>(buf + boff[k][s]);
+        // the query blocks' products interleaved: independent accumulators
+        // (blocks past B use clamped query rows; their results are unused)
+        f32x4 acc[QPG];
+#pragma unroll
+        for (int j = 0; j < QPG; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
         for (int s = 0; s < S32; ++s)
-          bv[s] = *reinterpret_cast<const u32x4*>(buf + granule_offset<G>(row, 4 * s + g));
+#pragma unroll
+          for (int j = 0; j < QPG; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, qreg[j][s]), __builtin_bit_cast(bf16x8, bv[s]),
+                acc[j], 0, 0, 0);
         float wk = 0.f;
 #pragma unroll
         for (int j = 0; j < QPG; ++j) {
           if (qg + j >= nqb) break;
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s = 0; s < S32; ++s)
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, qreg[j][s]), __builtin_bit_cast(bf16x8, bv[s]),
-                acc, 0, 0, 0);
           // lane holds logit[q = 16 (qg + j) + 4 g + i][p = p0 + row]
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             if constexpr (!WEIGHTS) {
-              const float v = acc[i] * a.scale;
+              const float v = acc[j][i] * a.scale;
               if (ok) {
                 if (v > sm[j][i]) {
                   sz[j][i] = sz[j][i] * __expf(sm[j][i] - v) + 1.f;
@@ -366,13 +378,12 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
                 }
               }
             } else {
-              wk += __builtin_amdgcn_exp2f(fmaf(acc[i], s2, -c2[j][i]));
+              wk += __builtin_amdgcn_exp2f(fmaf(acc[j][i], s2, -c2[j][i]));
             }
           }
         }
         if constexpr (WEIGHTS) {
-          wk += __shfl_xor(wk, 16);
-          wk += __shfl_xor(wk, 32);
+          wk = add_xor32(add_xor16(wk));
           // query groups add up in place: the same lane owns this position
           // in every group
           if (g == 0 && ok) wsum[p0 - pb + row] = (qg == 0 ? 0.f : wsum[p0 - pb + row]) + wk;
@@ -419,16 +430,21 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
 constexpr int kScanSelectBlock = 1024;
 
 __global__ __launch_bounds__(kScanSelectBlock) void scan_select_kernel(
-    ScanSelectArgs a, int w_in_lds) {
+    ScanSelectArgs a, int w_in_lds, int seg_in_lds) {
   __shared__ SelectShared<kScanSelectBlock> sh;
   extern __shared__ float wsh[];
   const int u = blockIdx.x;
   const float* W = a.wpool + (long)u * a.P;
-  if (w_in_lds) {
-    for (int i = threadIdx.x; i < a.P; i += kScanSelectBlock) wsh[i] = W[i];
-    __syncthreads();
-  }
+  // the unit's region ids, read by the emits (from LDS when they fit)
   const int32_t* seg = a.seg + (long)u * a.S;
+  if (seg_in_lds) {
+    int32_t* seg_sh = reinterpret_cast<int32_t*>(wsh + (w_in_lds ? a.P : 0));
+    for (int i = threadIdx.x; i < a.S; i += kScanSelectBlock) seg_sh[i] = seg[i];
+    seg = seg_sh;
+  }
+  if (w_in_lds)
+    for (int i = threadIdx.x; i < a.P; i += kScanSelectBlock) wsh[i] = W[i];
+  __syncthreads();
   const int J = a.J;
   const int mask = (1 << J) - 1;
   int32_t* tok = a.tok + (long)u * a.keff;
@@ -549,9 +565,17 @@ hipError_t launch_scan_select(const wf_params& p, const float* wpool,
   a.P = p.segments << p.levels;
   a.keff = wf_effective_budget(&p);
   const int in_lds = a.P <= kSelectLdsFloats ? 1 : 0;
-  const size_t lds = in_lds ? (size_t)a.P * sizeof(float) : 0;
+  const int seg_in_lds = a.S <= kSelectLdsSegs ? 1 : 0;
+  // W' when it fits, then the region ids when they fit
+  const size_t lds =
+      ((in_lds ? (size_t)a.P : 0) + (seg_in_lds ? (size_t)a.S : 0)) * sizeof(float);
+  if (lds > 32768) {  // with the static arrays, past the default 64 KiB
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(scan_select_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(scan_select_kernel, dim3((unsigned)a.U),
-                     dim3(kScanSelectBlock), lds, s, a, in_lds);
+                     dim3(kScanSelectBlock), lds, s, a, in_lds, seg_in_lds);
   return hipGetLastError();
 }
 
