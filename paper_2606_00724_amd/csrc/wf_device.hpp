@@ -183,8 +183,8 @@ __device__ __forceinline__ uint32_t order_key(float x) {
 
 template <int NT>
 struct SelectShared {
-  uint32_t hist[3][256];       // digit histograms, used in turn by the passes
-  uint32_t wsum[2][NT / 64];   // per-wave packed counts, used in turn by tiles
+  uint32_t hist[3][256];          // digit histograms, used in turn by the passes
+  uint32_t cnt[2][8 * (NT / 64)]; // per-(round, wave) packed counts, used in turn by tiles
 };
 
 // Inclusive prefix sum over the 64 lanes of a wave.
@@ -210,8 +210,8 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
 // largest candidate, so a pass costs one barrier (three histograms rotate so
 // that the next one is cleared while the current one fills).  The last pass
 // leaves the k-th largest key and the number of its copies to take.  The
-// output positions then follow from one block scan of packed (greater,
-// equal) counts over the positions in index order:
+// output positions then follow from a scan of packed (greater, equal)
+// counts over the positions in index order:
 //   pos = #greater before + min(#equal before, copies to take).
 template <int NT, typename Emit>
 __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
@@ -260,63 +260,70 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
     need -= above;
   }
   // prefix is now the k-th largest key; `need` copies of it are taken.
-  constexpr int ITEMS = 16;  // per-tile counts stay below 2^16
+  // Ordered compaction in tiles of ROUNDS x NT positions: position
+  // base + j NT + tid is round j of the thread.  Each wave ballots its
+  // (greater, equal) flags per round; one scan over the packed per-(round,
+  // wave) counts, in index order, gives every wave its offsets, and a lane's
+  // place inside its wave is the popcount of the ballot below it.
+  constexpr int NW = NT / 64;
+  constexpr int ROUNDS = 8;              // per-tile counts stay below 2^16
+  constexpr int NE = ROUNDS * NW;        // entries of the count scan (<= 128)
+  static_assert(NE <= 256, "count scan: at most four entries per lane");
   uint32_t gt_base = 0, eq_base = 0;
   int tile = 0;
-  for (int base = 0; base < n; base += NT * ITEMS, ++tile) {
-    const int start = base + tid * ITEMS;
-    // the thread's ITEMS consecutive scores, as 16-byte loads when aligned
-    float v[ITEMS];
-    if (start + ITEMS <= n && (reinterpret_cast<uintptr_t>(score + start) & 15) == 0) {
+  for (int base = 0; base < n; base += ROUNDS * NT, ++tile) {
+    uint64_t gtm[ROUNDS], eqm[ROUNDS];
+    uint32_t mine = 0;  // lane j < ROUNDS: the wave's packed counts of round j
 #pragma unroll
-      for (int q = 0; q < ITEMS / 4; ++q) {
-        const float4 f = reinterpret_cast<const float4*>(score + start)[q];
-        v[4 * q] = f.x;
-        v[4 * q + 1] = f.y;
-        v[4 * q + 2] = f.z;
-        v[4 * q + 3] = f.w;
+    for (int j = 0; j < ROUNDS; ++j) {
+      const int i = base + j * NT + tid;
+      bool gt = false, eq = false;
+      if (i < n) {
+        const uint32_t key = order_key(score[i]);
+        gt = key > prefix;
+        eq = key == prefix;
       }
-    } else {
-#pragma unroll
-      for (int j = 0; j < ITEMS; ++j) v[j] = start + j < n ? score[start + j] : 0.f;
+      gtm[j] = __ballot(gt);
+      eqm[j] = __ballot(eq);
+      if (lane == j) mine = ((uint32_t)__popcll(gtm[j]) << 16) | (uint32_t)__popcll(eqm[j]);
     }
-    uint32_t gt_bits = 0, eq_bits = 0;
-#pragma unroll
-    for (int j = 0; j < ITEMS; ++j) {
-      if (start + j < n) {
-        const uint32_t key = order_key(v[j]);
-        gt_bits |= (key > prefix ? 1u : 0u) << j;
-        eq_bits |= (key == prefix ? 1u : 0u) << j;
-      }
-    }
-    const uint32_t packed = ((uint32_t)__popc(gt_bits) << 16) | (uint32_t)__popc(eq_bits);
-    const uint32_t incl = wave_inclusive_scan(packed);
-    uint32_t* ws = sh.wsum[tile & 1];
-    if (lane == 63) ws[wid] = incl;
+    uint32_t* cnt = sh.cnt[tile & 1];  // [ROUNDS][NW]
+    if (lane < ROUNDS) cnt[lane * NW + wid] = mine;
     __syncthreads();
-    uint32_t wbefore = 0, wtot = 0;
+    // exclusive scan of the NE entries (entry e = j NW + w), four per lane
+    uint32_t c[4], sum = 0;
 #pragma unroll
-    for (int w = 0; w < NT / 64; ++w) {
-      const uint32_t v = ws[w];
-      wbefore += (w < wid) ? v : 0u;
-      wtot += v;
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * lane + q;
+      c[q] = e < NE ? cnt[e] : 0u;
+      sum += c[q];
     }
-    const uint32_t ex = wbefore + incl - packed;
-    const uint32_t eq_before = eq_base + (ex & 0xffffu);
-    uint32_t pos = gt_base + (ex >> 16) + min(eq_before, need);
-    uint32_t eq_seen = eq_before;
+    const uint32_t incl = wave_inclusive_scan(sum);
+    const uint32_t total = (uint32_t)__shfl((int)incl, 63);
+    uint32_t ex[4];
+    ex[0] = incl - sum;
 #pragma unroll
-    for (int j = 0; j < ITEMS; ++j) {
-      const bool gt = (gt_bits >> j) & 1u;
-      const bool eq = (eq_bits >> j) & 1u;
-      if (gt || (eq && eq_seen < need)) {
-        if (pos < (uint32_t)k) emit(pos, start + j);
-        ++pos;
+    for (int q = 1; q < 4; ++q) ex[q] = ex[q - 1] + c[q - 1];
+#pragma unroll
+    for (int j = 0; j < ROUNDS; ++j) {
+      if (base + j * NT >= n) break;  // uniform
+      const int e = j * NW + wid;   // uniform
+      const int q = e & 3;
+      const uint32_t pick = q == 0 ? ex[0] : q == 1 ? ex[1] : q == 2 ? ex[2] : ex[3];
+      const uint32_t off = (uint32_t)__shfl((int)pick, e >> 2);
+      const uint64_t gm = gtm[j], em = eqm[j];
+      const bool gt = (gm >> lane) & 1ull, eq = (em >> lane) & 1ull;
+      const uint32_t gt_before = gt_base + (off >> 16) +
+          __builtin_amdgcn_mbcnt_hi((uint32_t)(gm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)gm, 0u));
+      const uint32_t eq_before = eq_base + (off & 0xffffu) +
+          __builtin_amdgcn_mbcnt_hi((uint32_t)(em >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)em, 0u));
+      if (gt || (eq && eq_before < need)) {
+        const uint32_t pos = gt_before + min(eq_before, need);
+        if (pos < (uint32_t)k) emit(pos, base + j * NT + tid);
       }
-      eq_seen += eq ? 1u : 0u;
     }
-    gt_base += wtot >> 16;
-    eq_base += wtot & 0xffffu;
+    gt_base += total >> 16;
+    eq_base += total & 0xffffu;
   }
 }
 
