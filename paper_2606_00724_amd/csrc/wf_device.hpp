@@ -187,14 +187,17 @@ struct SelectShared {
   uint32_t cnt[2][8 * (NT / 64)]; // per-(round, wave) packed counts, used in turn by tiles
 };
 
-// Inclusive prefix sum over the 64 lanes of a wave.
+// Inclusive prefix sum over the 64 lanes of a wave, on DPP (no LDS round
+// trips): shifts by 1, 2, 4, 8 inside each 16-lane row, then row 0's total
+// into row 1 and row 2's into row 3 (row_bcast:15), then the first two
+// rows' total into rows 2 and 3 (row_bcast:31).  Every lane must be active.
 __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
   return x;
 }
 
@@ -253,8 +256,9 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
       before += c[j];
     }
     const int src = __ffsll((unsigned long long)__ballot(found)) - 1;
-    const uint32_t digit = (uint32_t)__shfl(255 - 4 * lane - hit, src);
-    const uint32_t above = (uint32_t)__shfl((int)hit_above, src);
+    // src is uniform: read the lane's values without an LDS round trip
+    const uint32_t digit = (uint32_t)__builtin_amdgcn_readlane(255 - 4 * lane - hit, src);
+    const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)hit_above, src);
     prefix |= digit << shift;
     mask |= 255u << shift;
     need -= above;
@@ -299,7 +303,7 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
       sum += c[q];
     }
     const uint32_t incl = wave_inclusive_scan(sum);
-    const uint32_t total = (uint32_t)__shfl((int)incl, 63);
+    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
     uint32_t ex[4];
     ex[0] = incl - sum;
 #pragma unroll
@@ -310,7 +314,7 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
       const int e = j * NW + wid;   // uniform
       const int q = e & 3;
       const uint32_t pick = q == 0 ? ex[0] : q == 1 ? ex[1] : q == 2 ? ex[2] : ex[3];
-      const uint32_t off = (uint32_t)__shfl((int)pick, e >> 2);
+      const uint32_t off = (uint32_t)__builtin_amdgcn_readlane((int)pick, e >> 2);
       const uint64_t gm = gtm[j], em = eqm[j];
       const bool gt = (gm >> lane) & 1ull, eq = (em >> lane) & 1ull;
       const uint32_t gt_before = gt_base + (off >> 16) +

@@ -267,12 +267,24 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
 // normalisers from the selected blocks' token statistics.
 constexpr int kFastSelectBlock = 1024;
 
+// Merges into the lane's (max, sum of exp) pair the pair R lanes away (mod 16) in its
+// 16-lane row (DPP row_ror:R; every lane must be active).
+template <int R>
+__device__ __forceinline__ void row16_merge(float& m, float& z) {
+  const float m2 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(m), 0x120 + R, 0xf, 0xf, false));
+  const float z2 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(z), 0x120 + R, 0xf, 0xf, false));
+  const float mn = fmaxf(m, m2);
+  if (mn > -INFINITY) {
+    z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
+    m = mn;
+  }
+}
+
 __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelectArgs a,
                                                                        int w_in_lds,
                                                                        int seg_in_lds) {
   constexpr int NT = kFastSelectBlock;
   __shared__ float row_c[16 * kFastMaxQBlocks];
-  __shared__ float part_m[NT], part_z[NT];
   __shared__ SelectShared<NT> sh;
   extern __shared__ float wsh[];  // W (when it fits), then the picked block ids
   const int u = blockIdx.x;
@@ -344,36 +356,42 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
                         },
                         sh);
   __syncthreads();
-  // pool normalisers: thread (q, part) folds selected blocks part, part + parts, ...
+  // pool normalisers from the selected blocks' log-sum-exps: the 16 lanes of
+  // a row share query q = tid / 16 and take blocks part, part + 16, ...; each
+  // folds its blocks into a (max, sum of exp) pair, then the row merges its
+  // 16 pairs with rotations (every lane ends with the row's pair)
   const int32_t* segx = seg_in_lds ? seg_sh : seg;
-  const int parts = NT / B;
-  const int q = threadIdx.x % B, part = threadIdx.x / B;
+  const int q = threadIdx.x >> 4, part = threadIdx.x & 15;
+  const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
   float mx = -INFINITY, z = 0.f;
-  if (part < parts) {
-    const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
-    constexpr int BATCH = 8;  // loads in flight together
-    for (int s0 = part; s0 < a.S; s0 += BATCH * parts) {
-      float v[BATCH];
+  constexpr int BATCH = 8;  // loads in flight together
+  for (int s0 = part; s0 < a.S; s0 += BATCH * 16) {
+    float v[BATCH];
 #pragma unroll
-      for (int k = 0; k < BATCH; ++k) {
-        const int s_ = s0 + k * parts;
-        v[k] = s_ < a.S ? lse[(long)segx[s_] * 2 * B + q] : -INFINITY;
-      }
+    for (int k = 0; k < BATCH; ++k) {
+      const int s_ = s0 + 16 * k;
+      v[k] = q < B && s_ < a.S ? lse[(long)segx[s_] * 2 * B + q] : -INFINITY;
+    }
+    float bm = v[0];
 #pragma unroll
-      for (int k = 0; k < BATCH; ++k)
-        if (s0 + k * parts < a.S) stat_absorb(mx, z, v[k], 1.f);
+    for (int k = 1; k < BATCH; ++k) bm = fmaxf(bm, v[k]);
+    const float mn = fmaxf(mx, bm);
+    if (mn > -INFINITY) {
+      float zb = 0.f;
+#pragma unroll
+      for (int k = 0; k < BATCH; ++k) zb += __expf(v[k] - mn);  // e^-inf = 0
+      z = (mx > -INFINITY ? z * __expf(mx - mn) : 0.f) + zb;
+      mx = mn;
     }
   }
-  part_m[threadIdx.x] = mx;
-  part_z[threadIdx.x] = z;
-  __syncthreads();
-  if (threadIdx.x < B) {
-    float m2 = -INFINITY, z2 = 0.f;
-    for (int k = 0; k < parts; ++k)
-      stat_absorb(m2, z2, part_m[k * B + threadIdx.x], part_z[k * B + threadIdx.x]);
+  row16_merge<8>(mx, z);
+  row16_merge<4>(mx, z);
+  row16_merge<2>(mx, z);
+  row16_merge<1>(mx, z);
+  if (part == 0 && q < B) {
     float* ps = a.pstats + (long)u * 2 * B;
-    ps[threadIdx.x] = m2;
-    ps[B + threadIdx.x] = z2;
+    ps[q] = mx;
+    ps[B + q] = z;
   }
 }
 
