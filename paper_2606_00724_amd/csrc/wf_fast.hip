@@ -285,6 +285,7 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
                                                                        int seg_in_lds) {
   constexpr int NT = kFastSelectBlock;
   __shared__ float row_c[16 * kFastMaxQBlocks];
+  __shared__ float pool_m[16 * (16 * kFastMaxQBlocks + 1)], pool_z[16 * (16 * kFastMaxQBlocks + 1)];
   __shared__ SelectShared<NT> sh;
   extern __shared__ float wsh[];  // W (when it fits), then the picked block ids
   const int u = blockIdx.x;
@@ -356,42 +357,58 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
                         },
                         sh);
   __syncthreads();
-  // pool normalisers from the selected blocks' log-sum-exps: the 16 lanes of
-  // a row share query q = tid / 16 and take blocks part, part + 16, ...; each
-  // folds its blocks into a (max, sum of exp) pair, then the row merges its
-  // 16 pairs with rotations (every lane ends with the row's pair)
+  // pool normalisers from the selected blocks' log-sum-exps.  Thread
+  // (part, q) = (tid / B, tid % B) folds blocks part, part + parts, ... into
+  // a (max, sum of exp) pair (the loads of a wave cover whole rows); the
+  // pairs go through LDS to rows of 16 lanes per query, merged by rotations.
   const int32_t* segx = seg_in_lds ? seg_sh : seg;
-  const int q = threadIdx.x >> 4, part = threadIdx.x & 15;
-  const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
-  float mx = -INFINITY, z = 0.f;
-  constexpr int BATCH = 8;  // loads in flight together
-  for (int s0 = part; s0 < a.S; s0 += BATCH * 16) {
-    float v[BATCH];
+  const int parts = min(NT / B, 16);
+  {
+    const int q = threadIdx.x % B, part = threadIdx.x / B;
+    const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
+    float mx = -INFINITY, z = 0.f;
+    constexpr int BATCH = 8;  // loads in flight together
+    if (part < parts) {
+      for (int s0 = part; s0 < a.S; s0 += BATCH * parts) {
+        float v[BATCH];
 #pragma unroll
-    for (int k = 0; k < BATCH; ++k) {
-      const int s_ = s0 + 16 * k;
-      v[k] = q < B && s_ < a.S ? lse[(long)segx[s_] * 2 * B + q] : -INFINITY;
-    }
-    float bm = v[0];
+        for (int k = 0; k < BATCH; ++k) {
+          const int s_ = s0 + parts * k;
+          v[k] = s_ < a.S ? lse[(long)segx[s_] * 2 * B + q] : -INFINITY;
+        }
+        float bm = v[0];
 #pragma unroll
-    for (int k = 1; k < BATCH; ++k) bm = fmaxf(bm, v[k]);
-    const float mn = fmaxf(mx, bm);
-    if (mn > -INFINITY) {
-      float zb = 0.f;
+        for (int k = 1; k < BATCH; ++k) bm = fmaxf(bm, v[k]);
+        const float mn = fmaxf(mx, bm);
+        if (mn > -INFINITY) {
+          float zb = 0.f;
 #pragma unroll
-      for (int k = 0; k < BATCH; ++k) zb += __expf(v[k] - mn);  // e^-inf = 0
-      z = (mx > -INFINITY ? z * __expf(mx - mn) : 0.f) + zb;
-      mx = mn;
+          for (int k = 0; k < BATCH; ++k) zb += __expf(v[k] - mn);  // e^-inf = 0
+          z = (mx > -INFINITY ? z * __expf(mx - mn) : 0.f) + zb;
+          mx = mn;
+        }
+      }
+      pool_m[part * (B + 1) + q] = mx;  // rows padded by one: no bank conflicts below
+      pool_z[part * (B + 1) + q] = z;
     }
   }
-  row16_merge<8>(mx, z);
-  row16_merge<4>(mx, z);
-  row16_merge<2>(mx, z);
-  row16_merge<1>(mx, z);
-  if (part == 0 && q < B) {
-    float* ps = a.pstats + (long)u * 2 * B;
-    ps[q] = mx;
-    ps[B + q] = z;
+  __syncthreads();
+  {
+    const int q = threadIdx.x >> 4, part = threadIdx.x & 15;
+    float mx = -INFINITY, z = 0.f;
+    if (q < B && part < parts) {
+      mx = pool_m[part * (B + 1) + q];
+      z = pool_z[part * (B + 1) + q];
+    }
+    row16_merge<8>(mx, z);
+    row16_merge<4>(mx, z);
+    row16_merge<2>(mx, z);
+    row16_merge<1>(mx, z);
+    if (part == 0 && q < B) {
+      float* ps = a.pstats + (long)u * 2 * B;
+      ps[q] = mx;
+      ps[B + q] = z;
+    }
   }
 }
 
