@@ -662,24 +662,59 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
   }
 }
 
+// Merges the splits of each query row: O = sum_s e^(M_s - M) O_s / sum_s
+// e^(M_s - M) l_s.  A workgroup takes 2048 / D rows of one unit, a thread 8
+// consecutive channels of one row (two 16-byte loads per split, one 16-byte
+// store for bf16).
+constexpr int kCombineBlock = 256;
+
 template <typename T>
-__global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a, int D) {
-  const int u = blockIdx.x / a.B, q = blockIdx.x % a.B;
+__device__ __forceinline__ void store8(T* dst, const float* v);
+template <>
+__device__ __forceinline__ void store8<bf16_t>(bf16_t* dst, const float* v) {
+  *reinterpret_cast<u32x4*>(dst) = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                         pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+}
+template <>
+__device__ __forceinline__ void store8<float>(float* dst, const float* v) {
+  reinterpret_cast<float4*>(dst)[0] = float4{v[0], v[1], v[2], v[3]};
+  reinterpret_cast<float4*>(dst)[1] = float4{v[4], v[5], v[6], v[7]};
+}
+
+template <typename T>
+__global__ __launch_bounds__(kCombineBlock) void attn_combine_kernel(AttnArgs a, int D) {
+  const int tpr = D / 8;                  // threads per row
+  const int rpb = kCombineBlock / tpr;    // rows per workgroup
+  const int nqb = (a.B + rpb - 1) / rpb;
+  const int u = blockIdx.x / nqb;
+  const int q = (blockIdx.x % nqb) * rpb + threadIdx.x / tpr;
+  const int c0 = (threadIdx.x % tpr) * 8;
+  if (q >= a.B) return;  // no barrier follows
   const float* ps = a.pstat + (long)u * a.NS * 2 * a.B;
   float M = -INFINITY;
   for (int s = 0; s < a.NS; ++s) M = fmaxf(M, ps[(long)s * 2 * a.B + q]);
+  float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float lsum = 0.f;
-  for (int s = 0; s < a.NS; ++s)
-    lsum += ps[(long)s * 2 * a.B + a.B + q] * __expf(ps[(long)s * 2 * a.B + q] - M);
-  const float inv = 1.f / lsum;
-  T* O = reinterpret_cast<T*>(a.O) + ((long)u * a.B + q) * D;
-  for (int ch = threadIdx.x; ch < D; ch += blockDim.x) {
-    float o = 0.f;
-    for (int s = 0; s < a.NS; ++s)
-      o += a.part[(((long)u * a.NS + s) * a.B + q) * D + ch] *
-           __expf(ps[(long)s * 2 * a.B + q] - M);
-    store_elem<T>(O, ch, o * inv);
+  for (int s = 0; s < a.NS; ++s) {
+    const float ms = ps[(long)s * 2 * a.B + q];
+    const float w = ms > -INFINITY ? __expf(ms - M) : 0.f;
+    lsum += ps[(long)s * 2 * a.B + a.B + q] * w;
+    const float4* src =
+        reinterpret_cast<const float4*>(a.part + (((long)u * a.NS + s) * a.B + q) * D + c0);
+    const float4 x0 = src[0], x1 = src[1];
+    o[0] += w * x0.x;
+    o[1] += w * x0.y;
+    o[2] += w * x0.z;
+    o[3] += w * x0.w;
+    o[4] += w * x1.x;
+    o[5] += w * x1.y;
+    o[6] += w * x1.z;
+    o[7] += w * x1.w;
   }
+  const float inv = 1.f / lsum;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] *= inv;
+  store8<T>(reinterpret_cast<T*>(a.O) + ((long)u * a.B + q) * D + c0, o);
 }
 
 // Sparse cache rows: [K[tok]; Kg] and [V[tok]; Vg], 16 bytes per thread.
@@ -816,12 +851,13 @@ hipError_t launch_attn_combine(const wf_params& p, long nrows,
   a.U = p.batch * p.heads;
   a.B = p.q_len;
   a.NS = plan_attn(p, nrows).splits;
-  const dim3 grid((unsigned)(a.U * a.B));
+  const int rpb = kCombineBlock / (p.head_dim / 8);
+  const dim3 grid((unsigned)(a.U * ((a.B + rpb - 1) / rpb)));
   if (p.dtype == WF_BF16)
-    hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, grid, dim3(128), 0, s, a,
+    hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, grid, dim3(kCombineBlock), 0, s, a,
                        p.head_dim);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<float>, grid, dim3(128), 0, s, a,
+    hipLaunchKernelGGL(attn_combine_kernel<float>, grid, dim3(kCombineBlock), 0, s, a,
                        p.head_dim);
   return hipGetLastError();
 }
