@@ -18,6 +18,9 @@
 //    the query block on fp32 MFMA (v_mfma_f32_16x16x4_f32), then writes the
 //    logits and per-tile row max / row sum of exponentials.  A per-unit
 //    kernel merges the tiles' row statistics, forms W and selects.
+#include <mutex>
+#include <vector>
+
 #include "wf_device.hpp"
 #include "wf_kernels.hpp"
 #include "wf_launch.hpp"
@@ -351,6 +354,209 @@ __device__ void cascade_tile(const T* Kunit, long L, long n0, int ncoef,
   run_stream<M, J, false, T>(cas, Kunit, D, cp, t0, t_stop, L, sink);
 }
 
+// ------------------------------------------------------------ banded filter
+
+// Away from the end of the sequence the level-J approximation of a 4-tap
+// bank is one banded filter: A_J[n] = sum_m f_J[m] y0[2^J n + m] with
+// f_1 = g and f_{j+1}[s] = sum_k g_k f_j[s - 2^j k] (length 3 (2^J - 1) + 1).
+// With the symmetric extension the per-level extensions do not compose, so
+// the filter is exact only while 2^J n + 3 (2^J - 1) < L; the periodic
+// extension composes (even lengths), with rows read modulo L.
+__host__ __device__ constexpr int band_len(int J) { return 3 * ((1 << J) - 1) + 1; }
+
+// Rows a 16-byte wave load covers and whether the banded fill applies: every
+// load must lie inside one 2^J-row block.
+template <typename T, int D, int J>
+struct BandShape {
+  static constexpr int CPL = 16 / (int)sizeof(T);  // channels per lane
+  static constexpr int LPR = D / CPL;              // lanes per row
+  static constexpr int RPI = kWave / LPR;          // rows per load
+  static constexpr bool ok = (1 << J) >= RPI;
+};
+
+// f_J into taps[0 .. 3 2^J) (zero past its length), built in LDS by the
+// whole workgroup from the 4 low-pass taps; tmp is scratch of the same size.
+template <int J>
+__device__ void build_band_taps(const Taps& t, float* taps, float* tmp) {
+  constexpr int N = 3 << J;
+  float* cur = (J % 2 == 1) ? taps : tmp;  // f_1 lands where f_J ends up
+  for (int i = threadIdx.x; i < N; i += kBlock) cur[i] = i < 4 ? t.g[i] : 0.f;
+  __syncthreads();
+  for (int j = 1; j < J; ++j) {
+    float* nxt = cur == taps ? tmp : taps;
+    const int step = 1 << j;
+    for (int i = threadIdx.x; i < N; i += kBlock) {
+      float v = 0.f;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int src = i - step * k;
+        if (src >= 0) v += t.g[k] * cur[src];
+      }
+      nxt[i] = v;
+    }
+    __syncthreads();
+    cur = nxt;
+  }
+}
+
+// Sum of v over the lanes l ^ sh, sh = LPR .. 32 (the RPI rows of a load).
+template <int LPR>
+__device__ __forceinline__ float sum_rows(float v) {
+  if constexpr (LPR <= 8)
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
+  if constexpr (LPR <= 16) v = add_xor16(v);
+  v = add_xor32(v);
+  return v;
+}
+
+// Level-J approximation of coefficients [n0, n0 + ncoef) ∩ [0, n_end) into
+// the LDS tile by the banded filter.  Wave w takes a contiguous run of the
+// tile's coefficients and streams their rows once: at block b a lane adds
+// its row's contribution to coefficients b, b - 1, b - 2 (taps o, o + 2^J,
+// o + 2^(J+1) at offset o in the block); when block b + 1 starts,
+// coefficient b - 2 is complete and its RPI row lanes are summed.
+template <typename T, int D, int J>
+__device__ void band_tile(const T* Kunit, long L, long n0, int ncoef, long n_end,
+                          bool periodic, const float* taps, float* coef) {
+  using BS = BandShape<T, D, J>;
+  constexpr int CPL = BS::CPL, LPR = BS::LPR, RPI = BS::RPI;
+  constexpr int BLK = 1 << J;
+  constexpr int GPB = BLK / RPI;  // loads per block
+  constexpr int BATCH = GPB < 8 ? GPB : 8;
+  constexpr int STRIDE = D + kCoefPad;
+  constexpr int NW = kBlock / kWave;
+  static_assert(BS::ok, "a load must stay inside one block");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rsub = lane / LPR, csub = lane % LPR;
+  const int per = (ncoef + NW - 1) / NW;
+  const long c0 = n0 + (long)wave * per;
+  const long c1 = min(min(c0 + (long)per, n0 + (long)ncoef), n_end);
+  if (c0 >= c1) return;  // uniform per wave; no barrier follows inside
+  float a0[CPL], a1[CPL], a2[CPL];  // coefficients b, b - 1, b - 2
+#pragma unroll
+  for (int e = 0; e < CPL; ++e) a0[e] = a1[e] = a2[e] = 0.f;
+  auto flush = [&](long n) {
+    float r[CPL];
+#pragma unroll
+    for (int e = 0; e < CPL; ++e) r[e] = sum_rows<LPR>(a2[e]);
+    if (rsub == 0 && n >= c0 && n < c1) {
+      float* dst = coef + (n - n0) * STRIDE + csub * CPL;
+#pragma unroll
+      for (int e = 0; e < CPL; e += 4)
+        *reinterpret_cast<f32x4*>(dst + e) = f32x4{r[e], r[e + 1], r[e + 2], r[e + 3]};
+    }
+  };
+  // batches of BATCH loads over blocks c0 .. c1 + 1; the next batch's loads
+  // are issued before the current one is used
+  constexpr int NBB = GPB / BATCH;  // batches per block
+  const long nbt = (c1 + 2 - c0) * NBB;
+  auto load_batch = [&](long bi, u32x4* v) {
+    const long b = c0 + bi / NBB;
+    const int g0 = (int)(bi % NBB) * BATCH;
+#pragma unroll
+    for (int gi = 0; gi < BATCH; ++gi) {
+      const long r = b * BLK + (g0 + gi) * RPI + rsub;
+      // past L: wrapped (periodic) or the last row with a zero tap
+      const long row = r < L ? r : (periodic ? r % L : L - 1);
+      v[gi] = *reinterpret_cast<const u32x4*>(Kunit + row * D + csub * CPL);
+    }
+  };
+  u32x4 vn[BATCH];
+  load_batch(0, vn);
+  for (long bi = 0; bi < nbt; ++bi) {
+    u32x4 v[BATCH];
+#pragma unroll
+    for (int gi = 0; gi < BATCH; ++gi) v[gi] = vn[gi];
+    if (bi + 1 < nbt) load_batch(bi + 1, vn);
+    const long b = c0 + bi / NBB;
+    const int g0 = (int)(bi % NBB) * BATCH;
+    if (g0 == 0 && b > c0) {
+      flush(b - 3);
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) {
+        a2[e] = a1[e];
+        a1[e] = a0[e];
+        a0[e] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int gi = 0; gi < BATCH; ++gi) {
+      const int o = (g0 + gi) * RPI + rsub;
+      const float t0 = taps[o], t1 = taps[o + BLK], t2 = taps[o + 2 * BLK];
+      float x[CPL];
+      if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x[2 * e] = bf16_lo(v[gi][e]);
+          x[2 * e + 1] = bf16_hi(v[gi][e]);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = __uint_as_float(v[gi][e]);
+      }
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) {
+        a0[e] = fmaf(t0, x[e], a0[e]);
+        a1[e] = fmaf(t1, x[e], a1[e]);
+        a2[e] = fmaf(t2, x[e], a2[e]);
+      }
+    }
+  }
+  flush(c1 - 1);
+}
+
+// The coefficients next to a symmetric end: coefficient nJ - 1 - m (m < 3)
+// is sum_r E_m[r] y0[(nJ - 1 - m) 2^J + r], r < 2^J (m + 1).  The per-level
+// extensions make E_m differ from f_J, but E_m depends only on m (lengths
+// are multiples of 2^J), so the host builds the three filters once per J by
+// pushing impulses through the extended cascade.  Filter m starts at
+// 2^J m (m + 1) / 2.  The banded path with edges covers J <= kBandMaxJ.
+constexpr int kBandMaxJ = 7;
+struct EdgeTaps {
+  float e[6 << kBandMaxJ];
+};
+
+// Edge coefficient n of the tile into LDS by the calling wave.
+template <typename T, int D, int J>
+__device__ void edge_coef(const T* Kunit, long n0, long n, long nJ, const float* edge,
+                          float* coef) {
+  using BS = BandShape<T, D, J>;
+  constexpr int CPL = BS::CPL, LPR = BS::LPR, RPI = BS::RPI;
+  constexpr int BLK = 1 << J;
+  constexpr int STRIDE = D + kCoefPad;
+  const int lane = threadIdx.x & 63;
+  const int rsub = lane / LPR, csub = lane % LPR;
+  const int m = (int)(nJ - 1 - n);
+  const float* e = edge + BLK * (m * (m + 1) / 2);
+  const int len = BLK * (m + 1);  // rows n 2^J .. L - 1
+  float acc[CPL];
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) acc[k] = 0.f;
+  for (int r0 = 0; r0 < len; r0 += RPI) {
+    const int rr = r0 + rsub;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(Kunit + (n * BLK + rr) * D + csub * CPL);
+    const float t = e[rr];
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        acc[2 * k] = fmaf(t, bf16_lo(v[k]), acc[2 * k]);
+        acc[2 * k + 1] = fmaf(t, bf16_hi(v[k]), acc[2 * k + 1]);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[k] = fmaf(t, __uint_as_float(v[k]), acc[k]);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) acc[k] = sum_rows<LPR>(acc[k]);
+  if (rsub == 0) {
+    float* dst = coef + (n - n0) * STRIDE + csub * CPL;
+#pragma unroll
+    for (int k = 0; k < CPL; k += 4)
+      *reinterpret_cast<f32x4*>(dst + k) = f32x4{acc[k], acc[k + 1], acc[k + 2], acc[k + 3]};
+  }
+}
+
 // logits[q][n0 + c] = scale * <Q_q, coef_c> for the tile, plus per-row max
 // and sum of exp over the tile's columns.
 template <typename T, int D>
@@ -456,9 +662,16 @@ __device__ void skim_epilogue(const SkimTileArgs& a, int u, int tile, long n0,
 }
 
 template <int SRC, int M, int J, typename T, int D>
-__global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
-                                                           Taps taps) {
-  extern __shared__ float coef[];  // [cpt][D + kCoefPad]
+__global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a, Taps taps,
+                                                           EdgeTaps edge) {
+  extern __shared__ float coef[];  // [cpt][D + kCoefPad], then the banded taps
+  constexpr bool kBand = SRC == kCascade && M == 4 && BandShape<T, D, J>::ok && J <= kBandMaxJ;
+  float* band = coef + a.cpt * (D + kCoefPad);  // [2][3 << J], then [6 << J] edge filters
+  float* edge_lds = band + 2 * (3 << J);
+  if constexpr (kBand) {
+    for (int i = threadIdx.x; i < (6 << J); i += kBlock) edge_lds[i] = edge.e[i];
+    build_band_taps<J>(taps, band, band + (3 << J));  // ends with a barrier
+  }
   const int total = a.U * a.ntiles;
   for (int item = blockIdx.x; item < total; item += gridDim.x) {
     const int u = item / a.ntiles;
@@ -480,8 +693,20 @@ __global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a,
       }
     } else if constexpr (SRC == kCascade) {
       const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * D;
-      cascade_tile<M, J, T, D>(Kunit, a.L, n0, ncoef, a.cpt,
-                               M == 4 && a.boundary == 0, taps, coef);
+      const bool sym = M == 4 && a.boundary == 0;
+      if constexpr (kBand) {
+        // interior coefficients by the banded filter, those whose window
+        // reaches a symmetric end by the cascade (on the last wave)
+        const long nJf = (long)a.L >> J;
+        const long n_end = sym ? (a.L >= band_len(J) ? min((a.L - band_len(J)) / (1L << J) + 1, nJf) : 0L)
+                               : nJf;
+        band_tile<T, D, J>(Kunit, a.L, n0, ncoef, n_end, !sym, band, coef);
+        // at most three edge coefficients: wave w takes the w-th of the tile
+        const long n = max(n0, n_end) + (threadIdx.x >> 6);
+        if (n < n0 + ncoef) edge_coef<T, D, J>(Kunit, n0, n, nJf, edge_lds, coef);
+      } else {
+        cascade_tile<M, J, T, D>(Kunit, a.L, n0, ncoef, a.cpt, sym, taps, coef);
+      }
     } else {
       const float* src = a.approx + ((long)u * a.nJ + n0) * D;
       for (int v = threadIdx.x; v < ncoef * (D / 4); v += kBlock) {
@@ -635,6 +860,44 @@ static Taps make_taps(int wavelet, int J) {
   return t;
 }
 
+// The three symmetric-end filters of the level-J Daubechies-2 approximation
+// (see EdgeTaps), in double, once per J: impulses at each of the last 3 2^J
+// rows of a sequence of 6 2^J rows, through the cascade with the
+// half-sample symmetric extension at every level.
+static const EdgeTaps& symmetric_edge_filters(int J) {
+  static EdgeTaps table[kBandMaxJ + 1];
+  static std::once_flag once[kBandMaxJ + 1];
+  std::call_once(once[J], [J] {
+    const double r2 = std::sqrt(2.0), r3 = std::sqrt(3.0), den = 4.0 * r2;
+    const double g[4] = {(1 + r3) / den, (3 + r3) / den, (3 - r3) / den, (1 - r3) / den};
+    const int blk = 1 << J, len = 6 * blk, nJ = 6;
+    EdgeTaps& t = table[J];
+    for (int i = 0; i < (6 << kBandMaxJ); ++i) t.e[i] = 0.f;
+    for (int r = len - 3 * blk; r < len; ++r) {
+      std::vector<double> y(len, 0.0);
+      y[r] = 1.0;
+      for (int j = 1; j <= J; ++j) {
+        const int N = (int)y.size();
+        std::vector<double> a(N / 2);
+        for (int n = 0; n < N / 2; ++n) {
+          double v = 0.0;
+          for (int m = 0; m < 4; ++m) {
+            const int i = 2 * n + m;
+            v += g[m] * (i < N ? y[i] : y[2 * N - 1 - i]);
+          }
+          a[n] = v;
+        }
+        y.swap(a);
+      }
+      for (int m = 0; m < 3; ++m) {
+        const int start = len - blk * (m + 1);  // first row of coefficient nJ - 1 - m
+        if (r >= start) t.e[blk * (m * (m + 1) / 2) + (r - start)] = (float)y[nJ - 1 - m];
+      }
+    }
+  });
+  return table[J];
+}
+
 template <int M, typename T>
 static hipError_t dwt_dispatch(const DwtArgs& a, const Taps& taps, dim3 grid,
                                hipStream_t s) {
@@ -732,12 +995,13 @@ SkimPlan plan_skim(const wf_params& p, bool fused) {
   }
   const long nJ = (long)p.ctx_len >> J;
   k.ntiles = (int)((nJ + k.cpt - 1) / k.cpt);
-  k.lds_bytes = (size_t)k.cpt * (p.head_dim + kCoefPad) * sizeof(float);
+  k.lds_bytes = ((size_t)k.cpt * (p.head_dim + kCoefPad) +
+                 (k.source == kCascade ? (size_t)12 << J : 0)) * sizeof(float);
   return k;
 }
 
 template <int SRC, int M, int J, typename T, int D>
-static hipError_t skim_launch_one(const SkimTileArgs& a, const Taps& taps,
+static hipError_t skim_launch_one(const SkimTileArgs& a, const Taps& taps, const EdgeTaps& edge,
                                   size_t lds, hipStream_t s) {
   auto kern = skim_tile_kernel<SRC, M, J, T, D>;
   int per_cu = 0;
@@ -747,19 +1011,20 @@ static hipError_t skim_launch_one(const SkimTileArgs& a, const Taps& taps,
   const long total = (long)a.U * a.ntiles;
   const long cap = (long)std::max(1, per_cu) * device_cu_count();
   dim3 grid((unsigned)std::min(total, cap));
-  hipLaunchKernelGGL(kern, grid, dim3(kBlock), lds, s, a, taps);
+  hipLaunchKernelGGL(kern, grid, dim3(kBlock), lds, s, a, taps, edge);
   return hipGetLastError();
 }
 
 template <typename T, int D>
-static hipError_t skim_dispatch(int source, const SkimTileArgs& a,
-                                const Taps& taps, size_t lds, hipStream_t s) {
-  if (source == kHaarSum) return skim_launch_one<kHaarSum, 2, 1, T, D>(a, taps, lds, s);
-  if (source == kFromApprox) return skim_launch_one<kFromApprox, 2, 1, T, D>(a, taps, lds, s);
+static hipError_t skim_dispatch(int source, const SkimTileArgs& a, const Taps& taps,
+                                const EdgeTaps& edge, size_t lds, hipStream_t s) {
+  if (source == kHaarSum) return skim_launch_one<kHaarSum, 2, 1, T, D>(a, taps, edge, lds, s);
+  if (source == kFromApprox)
+    return skim_launch_one<kFromApprox, 2, 1, T, D>(a, taps, edge, lds, s);
   switch (a.J) {
 #define WF_SKIM_CASE(JJ) \
   case JJ:               \
-    return skim_launch_one<kCascade, 4, JJ, T, D>(a, taps, lds, s);
+    return skim_launch_one<kCascade, 4, JJ, T, D>(a, taps, edge, lds, s);
     WF_SKIM_CASE(1) WF_SKIM_CASE(2) WF_SKIM_CASE(3) WF_SKIM_CASE(4)
     WF_SKIM_CASE(5) WF_SKIM_CASE(6) WF_SKIM_CASE(7) WF_SKIM_CASE(8)
     WF_SKIM_CASE(9) WF_SKIM_CASE(10)
@@ -791,13 +1056,22 @@ static hipError_t skim_tiles_common(const wf_params& p, int source, int cpt, int
   a.ntiles = (int)((nJ + cpt - 1) / cpt);
   a.boundary = p.boundary;
   a.scale = effective_scale(p);
-  const size_t lds = (size_t)cpt * (p.head_dim + kCoefPad) * sizeof(float);
+  // the coefficient tile, then (cascade source) the banded filter's taps
+  // and the symmetric-end filters
+  const size_t lds = ((size_t)cpt * (p.head_dim + kCoefPad) +
+                      (source == kCascade ? (size_t)12 << J : 0)) *
+                     sizeof(float);
   const Taps taps = make_taps(p.wavelet, J);
+  static const EdgeTaps no_edge{};
+  const EdgeTaps& edge = source == kCascade && p.wavelet == WF_DB2 &&
+                                 p.boundary == WF_EXT_SYMMETRIC && J <= kBandMaxJ
+                             ? symmetric_edge_filters(J)
+                             : no_edge;
   if (p.dtype == WF_BF16)
-    return p.head_dim == 128 ? skim_dispatch<bf16_t, 128>(source, a, taps, lds, s)
-                             : skim_dispatch<bf16_t, 64>(source, a, taps, lds, s);
-  return p.head_dim == 128 ? skim_dispatch<float, 128>(source, a, taps, lds, s)
-                           : skim_dispatch<float, 64>(source, a, taps, lds, s);
+    return p.head_dim == 128 ? skim_dispatch<bf16_t, 128>(source, a, taps, edge, lds, s)
+                             : skim_dispatch<bf16_t, 64>(source, a, taps, edge, lds, s);
+  return p.head_dim == 128 ? skim_dispatch<float, 128>(source, a, taps, edge, lds, s)
+                           : skim_dispatch<float, 64>(source, a, taps, edge, lds, s);
 }
 
 hipError_t launch_skim_tiles(const wf_params& p, bool fused, const void* Q,

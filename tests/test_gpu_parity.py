@@ -52,6 +52,19 @@ EDGE = {
                      budget=64, wavelet="db2", boundary="periodic", **_BF),
     "db2_sym_j6_f32": V_("db2f", ctx_len=4096, levels=6, segments=5,
                          budget=200, wavelet="db2"),
+    # the banded db2 fill: every coefficient an edge one (L shorter than the
+    # filter), a single periodic coefficient, 8 rows per bf16 load (d=64),
+    # the largest J with edge filters, and the cascade past it
+    "db2_sym_j6_short": V_("db2e", ctx_len=128, head_dim=128, levels=6, segments=2,
+                           budget=40, wavelet="db2", **_BF),
+    "db2_per_j5_one": V_("db2o", ctx_len=32, head_dim=128, levels=5, segments=1,
+                         budget=8, wavelet="db2", boundary="periodic", **_BF),
+    "db2_sym_j4_d64": V_("db2d", ctx_len=16 * 70, levels=4, segments=9, budget=60,
+                         wavelet="db2", **_BF),
+    "db2_sym_j7": V_("db2m", ctx_len=128 * 20, head_dim=128, levels=7, segments=4,
+                     budget=300, wavelet="db2", **_BF),
+    "db2_sym_j8_cascade": V_("db2c", ctx_len=256 * 6, head_dim=128, levels=8,
+                             segments=2, budget=300, wavelet="db2", **_BF),
     "keep_all": V_("all", ctx_len=256, levels=3, segments=32, budget=4096,
                    q_len=16),
     "s1_k1": V_("s1k1", segments=1, budget=1, q_len=1),
