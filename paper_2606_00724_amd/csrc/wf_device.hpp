@@ -175,6 +175,25 @@ __device__ __forceinline__ float add_xor32(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Merges the (max, sum of exp) pair (m2, z2) into (m, z); empty pairs have
+// m = -inf.
+__device__ __forceinline__ void pair_merge(float& m, float& z, float m2, float z2) {
+  const float mn = fmaxf(m, m2);
+  if (mn > -INFINITY) {
+    z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
+    m = mn;
+  }
+}
+
+// Merges into the lane's (max, sum of exp) pair the pair R lanes away (mod 16) in its
+// 16-lane row (DPP row_ror:R; every lane must be active).
+template <int R>
+__device__ __forceinline__ void row16_merge(float& m, float& z) {
+  const float m2 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(m), 0x120 + R, 0xf, 0xf, false));
+  const float z2 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(z), 0x120 + R, 0xf, 0xf, false));
+  pair_merge(m, z, m2, z2);
+}
+
 // Order-preserving map of a float to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t order_key(float x) {
   uint32_t u = __float_as_uint(x);

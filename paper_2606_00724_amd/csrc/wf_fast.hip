@@ -267,19 +267,6 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
 // normalisers from the selected blocks' token statistics.
 constexpr int kFastSelectBlock = 1024;
 
-// Merges into the lane's (max, sum of exp) pair the pair R lanes away (mod 16) in its
-// 16-lane row (DPP row_ror:R; every lane must be active).
-template <int R>
-__device__ __forceinline__ void row16_merge(float& m, float& z) {
-  const float m2 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(m), 0x120 + R, 0xf, 0xf, false));
-  const float z2 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(z), 0x120 + R, 0xf, 0xf, false));
-  const float mn = fmaxf(m, m2);
-  if (mn > -INFINITY) {
-    z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
-    m = mn;
-  }
-}
-
 __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelectArgs a,
                                                                        int w_in_lds,
                                                                        int seg_in_lds) {

@@ -754,28 +754,56 @@ constexpr int kSelectBlock = 1024;
 
 __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArgs a,
                                                                    int w_in_lds) {
-  __shared__ float row_max[WF_MAX_Q_LEN];
-  __shared__ float row_inv[WF_MAX_Q_LEN];
-  __shared__ SelectShared<kSelectBlock> sh;
+  constexpr int NT = kSelectBlock;
+  __shared__ float row_c[WF_MAX_Q_LEN];  // per query: M log2(e) + log2(Z)
+  __shared__ float pm[16][65], pz[16][65];
+  __shared__ SelectShared<NT> sh;
   extern __shared__ float wsh[];
   const int u = blockIdx.x;
   const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
-  for (int q = threadIdx.x; q < a.B; q += kSelectBlock) {
-    float mx = -INFINITY;
-    for (int t = 0; t < a.ntiles; ++t) mx = fmaxf(mx, st[(long)t * 2 * a.B + q]);
-    float z = 0.f;
-    for (int t = 0; t < a.ntiles; ++t)
-      z += st[(long)t * 2 * a.B + a.B + q] * __expf(st[(long)t * 2 * a.B + q] - mx);
-    row_max[q] = mx;
-    row_inv[q] = 1.f / z;
+  // merge the tiles' (max, sum of exp) pairs, 64 queries at a time: thread
+  // (part, q) = (tid / 64, tid % 64) folds tiles part, part + 16, ...; the 16
+  // pairs of a query meet in a 16-lane row and are merged by rotations
+  for (int qc = 0; qc < a.B; qc += 64) {
+    {
+      const int q = qc + (threadIdx.x & 63), part = threadIdx.x >> 6;
+      float m = -INFINITY, z = 0.f;
+      if (q < a.B) {
+        constexpr int BATCH = 8;
+        for (int t0 = part; t0 < a.ntiles; t0 += 16 * BATCH) {
+          float tm[BATCH], tz[BATCH];
+#pragma unroll
+          for (int k = 0; k < BATCH; ++k) {
+            const int t = t0 + 16 * k;
+            tm[k] = t < a.ntiles ? st[(long)t * 2 * a.B + q] : -INFINITY;
+            tz[k] = t < a.ntiles ? st[(long)t * 2 * a.B + a.B + q] : 0.f;
+          }
+#pragma unroll
+          for (int k = 0; k < BATCH; ++k) pair_merge(m, z, tm[k], tz[k]);
+        }
+      }
+      pm[part][threadIdx.x & 63] = m;
+      pz[part][threadIdx.x & 63] = z;
+    }
+    __syncthreads();
+    {
+      const int ql = threadIdx.x >> 4, part = threadIdx.x & 15;
+      float m = pm[part][ql], z = pz[part][ql];
+      row16_merge<8>(m, z);
+      row16_merge<4>(m, z);
+      row16_merge<2>(m, z);
+      row16_merge<1>(m, z);
+      // exp(l - M) / Z = 2^(l log2(e) - c)
+      if (part == 0 && qc + ql < a.B) row_c[qc + ql] = fmaf(m, kLog2e, __log2f(z));
+    }
+    __syncthreads();
   }
-  __syncthreads();
   const float* lg = a.logits + (long)u * a.B * a.nJ;
   float* W = a.W + (long)u * a.nJ;
   if ((a.nJ & 3) == 0) {
-    // four adjacent columns per thread, 8 query rows of loads in flight
-    constexpr int QB = 8;
-    for (int j4 = threadIdx.x; j4 < a.nJ / 4; j4 += kSelectBlock) {
+    // four adjacent columns per thread, 16 query rows of loads in flight
+    constexpr int QB = 16;
+    for (int j4 = threadIdx.x; j4 < a.nJ / 4; j4 += NT) {
       float w[4] = {0.f, 0.f, 0.f, 0.f};
       for (int q0 = 0; q0 < a.B; q0 += QB) {
         float4 v[QB];
@@ -786,11 +814,11 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
 #pragma unroll
         for (int i = 0; i < QB; ++i) {
           if (q0 + i < a.B) {
-            const float m = row_max[q0 + i], r = row_inv[q0 + i];
-            w[0] += __expf(v[i].x - m) * r;
-            w[1] += __expf(v[i].y - m) * r;
-            w[2] += __expf(v[i].z - m) * r;
-            w[3] += __expf(v[i].w - m) * r;
+            const float c = row_c[q0 + i];
+            w[0] += __builtin_amdgcn_exp2f(fmaf(v[i].x, kLog2e, -c));
+            w[1] += __builtin_amdgcn_exp2f(fmaf(v[i].y, kLog2e, -c));
+            w[2] += __builtin_amdgcn_exp2f(fmaf(v[i].z, kLog2e, -c));
+            w[3] += __builtin_amdgcn_exp2f(fmaf(v[i].w, kLog2e, -c));
           }
         }
       }
@@ -800,25 +828,23 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
         for (int e = 0; e < 4; ++e) wsh[4 * j4 + e] = w[e];
       }
     }
-    __syncthreads();
   } else {
-  constexpr int RB = 8;  // rows in flight per thread
-  for (int j = threadIdx.x; j < a.nJ; j += kSelectBlock) {
-    float w = 0.f;
-    for (int q0 = 0; q0 < a.B; q0 += RB) {
-      float v[RB];
+    constexpr int RB = 16;  // rows in flight per thread
+    for (int j = threadIdx.x; j < a.nJ; j += NT) {
+      float w = 0.f;
+      for (int q0 = 0; q0 < a.B; q0 += RB) {
+        float v[RB];
 #pragma unroll
-      for (int i = 0; i < RB; ++i)
-        v[i] = q0 + i < a.B ? lg[(long)(q0 + i) * a.nJ + j] : 0.f;
+        for (int i = 0; i < RB; ++i) v[i] = q0 + i < a.B ? lg[(long)(q0 + i) * a.nJ + j] : 0.f;
 #pragma unroll
-      for (int i = 0; i < RB; ++i)
-        if (q0 + i < a.B) w += __expf(v[i] - row_max[q0 + i]) * row_inv[q0 + i];
+        for (int i = 0; i < RB; ++i)
+          if (q0 + i < a.B) w += __builtin_amdgcn_exp2f(fmaf(v[i], kLog2e, -row_c[q0 + i]));
+      }
+      W[j] = w;
+      if (w_in_lds) wsh[j] = w;
     }
-    W[j] = w;
-    if (w_in_lds) wsh[j] = w;
   }
   __syncthreads();
-  }
   const float* src = w_in_lds ? wsh : W;
   // candidate n is block n, or on a refinement scale child n % 2 of kept
   // block parent[n / 2]; the last scale emits the two tokens of each block
