@@ -146,11 +146,35 @@ constexpr float kLn2 = 0.69314718055994531f;     // ln(2)
 
 // ------------------------------------------------------------ reductions
 
+// The value of the lane R lanes away (mod 16) in the same 16-lane row (DPP
+// row_ror:R).
+template <int R>
+__device__ __forceinline__ float dpp_row_ror(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + R, 0xf, 0xf, false));
+}
+
+// Max / sum over the 16 lanes of the lane's row, on DPP rotations (every
+// lane ends with the row's result; every lane of the wave must be active).
+// The sum's association order differs between the lanes of a row.
 __device__ __forceinline__ float wave_max16(float v) {
-  // max over the 16 lanes that share l / 16
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = fmaxf(v, dpp_row_ror<8>(v));
+  v = fmaxf(v, dpp_row_ror<4>(v));
+  v = fmaxf(v, dpp_row_ror<2>(v));
+  return fmaxf(v, dpp_row_ror<1>(v));
+}
+__device__ __forceinline__ float wave_sum16(float v) {
+  v += dpp_row_ror<8>(v);
+  v += dpp_row_ror<4>(v);
+  v += dpp_row_ror<2>(v);
+  return v + dpp_row_ror<1>(v);
+}
+
+// Sums of v over lane pairs (l, l ^ 1) and (l, l ^ 2), DPP quad_perm.
+__device__ __forceinline__ float add_xor1(float v) {
+  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float add_xor2(float v) {
+  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xf, 0xf, false));
 }
 
 // Reductions over the lane pairs (l, l ^ 16) and (l, l ^ 32) on the VALU:
@@ -173,6 +197,11 @@ __device__ __forceinline__ float add_xor16(float v) {
 __device__ __forceinline__ float add_xor32(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// The value of lane l ^ 32.
+__device__ __forceinline__ float partner32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
 }
 
 // Merges the (max, sum of exp) pair (m2, z2) into (m, z); empty pairs have

@@ -204,13 +204,13 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
         bs[b] += acc[v];
         bm[b] = fmaxf(bm[b], acc[v]);
       }
-      bs[b] += __shfl_xor(bs[b], 32);
-      bm[b] = fmaxf(bm[b], __shfl_xor(bm[b], 32));
+      bs[b] = add_xor32(bs[b]);
+      bm[b] = max_xor32(bm[b]);
       const float off = -bm[b] * c2;
       be[b] = 0.f;
 #pragma unroll
       for (int v = b * VPB; v < (b + 1) * VPB; ++v) be[b] += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, off));
-      be[b] += __shfl_xor(be[b], 32);
+      be[b] = add_xor32(be[b]);
     }
     float* slot = batch + ((ch / BATCH) & 1) * slot_floats;
     const int bl0 = (ch % BATCH) * BPC + ((32 * ts) >> J);  // slice's first block in the batch
@@ -240,7 +240,7 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
   // merge the running coarse statistics: partner lanes, then the four
   // slices of the query tile
   {
-    const float m2 = __shfl_xor(cm, 32), z2 = __shfl_xor(cz, 32);
+    const float m2 = partner32(cm), z2 = partner32(cz);
     stat_absorb(cm, cz, m2, z2);
   }
   if (hi == 0) {
@@ -326,8 +326,7 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
       float w = 0.f;
 #pragma unroll
       for (int k = 0; k < 16; ++k) w += __builtin_amdgcn_exp2f(fmaf(x[r][k], kLog2e, -cq[k]));
-      w += __shfl_xor(w, 1);
-      w += __shfl_xor(w, 2);
+      w = add_xor2(add_xor1(w));
       if (t < 4 * nJ && (t & 3) == 0) {
         W[t >> 2] = w;
         if (w_in_lds) wsh[t >> 2] = w;

@@ -141,8 +141,7 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
             for (int k = 0; k < TBW; ++k)
               if ((wave * TBW + k) * 16 + col < np) z += __expf(sacc[k][i] - mx);
           }
-#pragma unroll
-          for (int o = 1; o < 16; o <<= 1) z += __shfl_xor(z, o);
+          z = wave_sum16(z);
           if (col == 0) {
             rq[(4 * g + i) * 2] = mx;
             rq[(4 * g + i) * 2 + 1] = z;
@@ -183,9 +182,7 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
       // column sums over the 4 lane groups (rows 4g + i)
 #pragma unroll
       for (int k = 0; k < TBW; ++k) {
-        float w = wacc[k];
-        w += __shfl_xor(w, 16);
-        w += __shfl_xor(w, 32);
+        const float w = add_xor32(add_xor16(wacc[k]));
         const int pl = (wave * TBW + k) * 16 + col;
         if (g == 0 && pl < np) a.wpool[(long)u * a.P + p0 + pl] = w;
       }
@@ -396,11 +393,10 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
       for (int j = 0; j < QPG; ++j) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-#pragma unroll
-          for (int o = 1; o < 16; o <<= 1) {
-            const float m2 = __shfl_xor(sm[j][i], o), z2 = __shfl_xor(sz[j][i], o);
-            stat_merge(sm[j][i], sz[j][i], m2, z2);
-          }
+          row16_merge<8>(sm[j][i], sz[j][i]);
+          row16_merge<4>(sm[j][i], sz[j][i]);
+          row16_merge<2>(sm[j][i], sz[j][i]);
+          row16_merge<1>(sm[j][i], sz[j][i]);
           if (col == 0 && qg + j < nqb) {
             part[(((qg + j) * NW + wave) * 16 + 4 * g + i) * 2] = sm[j][i];
             part[(((qg + j) * NW + wave) * 16 + 4 * g + i) * 2 + 1] = sz[j][i];

@@ -293,6 +293,10 @@ __device__ void haar_sum_tile_groups(const T* Kunit, long n0, int ncoef, int J,
     }
 #pragma unroll
     for (int gi = 0; gi < GPI; ++gi) {
+      // the red rows of a coefficient sit LPR, 2 LPR, ... lanes apart (LDS
+      // permutes: with many waves resident their latency hides, where the
+      // VALU lane swaps would take issue slots)
+#pragma unroll
       for (int sh = 1; sh < red; sh <<= 1) {
 #pragma unroll
         for (int e = 0; e < CPL; ++e) acc[gi][e] += __shfl_xor(acc[gi][e], LPR * sh);
@@ -631,8 +635,7 @@ __device__ void skim_epilogue(const SkimTileArgs& a, int u, int tile, long n0,
         const int c = cb * 16 + col;
         if (cb < ncb && c < ncoef) s += __expf(acc[cb][i] - m[i]);
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o);
+      s = wave_sum16(s);
       z[i] = s;
     }
     float* lg = a.logits + (long)u * a.B * a.nJ + n0;
