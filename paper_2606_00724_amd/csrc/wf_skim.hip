@@ -561,6 +561,44 @@ __device__ void edge_coef(const T* Kunit, long n0, long n, long nJ, const float*
   }
 }
 
+// In place, every fp32 coefficient row of the tile becomes [hi x D][lo x D]
+// bf16 in the same bytes: hi = bf16(c), lo = bf16(c - hi) (round to nearest
+// even), so |c - hi - lo| <= 2^-17 |c|.  The whole workgroup reads, then
+// writes (the halves overlap other threads' sources); it ends with a barrier.
+template <int D>
+__device__ void split_tile_bf16(float* coef, int ncoef) {
+  constexpr int STRIDE = D + kCoefPad;
+  constexpr int GPR = D / 8;  // 8-channel groups per row
+  constexpr int MAXI = kMaxCoefTile * GPR / kBlock;
+  uint32_t hi[MAXI][4], lo[MAXI][4];
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int it = threadIdx.x + k * kBlock, row = it / GPR, grp = it % GPR;
+    if (row < ncoef) {
+      const float* src = coef + row * STRIDE + 8 * grp;
+      const f32x4 v0 = *reinterpret_cast<const f32x4*>(src);
+      const f32x4 v1 = *reinterpret_cast<const f32x4*>(src + 4);
+      const float v[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        hi[k][e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+        lo[k][e] = pack_bf16x2(v[2 * e] - bf16_lo(hi[k][e]), v[2 * e + 1] - bf16_hi(hi[k][e]));
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int it = threadIdx.x + k * kBlock, row = it / GPR, grp = it % GPR;
+    if (row < ncoef) {
+      unsigned char* dst = reinterpret_cast<unsigned char*>(coef + row * STRIDE);
+      *reinterpret_cast<u32x4*>(dst + 16 * grp) = u32x4{hi[k][0], hi[k][1], hi[k][2], hi[k][3]};
+      *reinterpret_cast<u32x4*>(dst + 2 * D + 16 * grp) = u32x4{lo[k][0], lo[k][1], lo[k][2], lo[k][3]};
+    }
+  }
+  __syncthreads();
+}
+
 // logits[q][n0 + c] = scale * <Q_q, coef_c> for the tile, plus per-row max
 // and sum of exp over the tile's columns.
 template <typename T, int D>
@@ -573,42 +611,57 @@ __device__ void skim_epilogue(const SkimTileArgs& a, int u, int tile, long n0,
   const int ncb = (ncoef + 15) / 16;
   const T* Qunit = reinterpret_cast<const T*>(a.Q) + (long)u * a.B * D;
   for (int qb = wave; qb < nqb; qb += kBlock / kWave) {
-    // A operand: query row (clamped), channels [g D/4, (g+1) D/4)
-    const int qrow = min(qb * 16 + col, a.B - 1);
-    float qv[D / 4];
-    const T* qsrc = Qunit + (long)qrow * D + g * (D / 4);
+    const int qrow = min(qb * 16 + col, a.B - 1);  // clamped query row
+    f32x4 acc[kMaxCoefTile / 16];
     if constexpr (sizeof(T) == 2) {
+      // bf16 queries are exact; the tile holds each coefficient row as
+      // [hi x D][lo x D] bf16 (split_tile_bf16), so two bf16 products give
+      // the fp32 dot product to within 2^-17 of each term.  A operand: query
+      // row, channels 32 s + 8 g ..; B operand: the same channels of
+      // coefficient 16 cb + col.
+      u32x4 qa[D / 32];
 #pragma unroll
-      for (int v = 0; v < D / 32; ++v) {
-        u32x4 w = *reinterpret_cast<const u32x4*>(qsrc + 8 * v);
+      for (int s32 = 0; s32 < D / 32; ++s32)
+        qa[s32] = *reinterpret_cast<const u32x4*>(Qunit + (long)qrow * D + 32 * s32 + 8 * g);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          qv[8 * v + 2 * e] = bf16_lo(w[e]);
-          qv[8 * v + 2 * e + 1] = bf16_hi(w[e]);
+      for (int cb = 0; cb < kMaxCoefTile / 16; ++cb) {
+        acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (cb < ncb) {
+          const unsigned char* crow =
+              reinterpret_cast<const unsigned char*>(coef + (cb * 16 + col) * STRIDE);
+#pragma unroll
+          for (int s32 = 0; s32 < D / 32; ++s32) {
+            const u32x4 hi = *reinterpret_cast<const u32x4*>(crow + 2 * (32 * s32 + 8 * g));
+            const u32x4 lo = *reinterpret_cast<const u32x4*>(crow + 2 * D + 2 * (32 * s32 + 8 * g));
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, qa[s32]), __builtin_bit_cast(bf16x8, hi), acc[cb], 0, 0, 0);
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, qa[s32]), __builtin_bit_cast(bf16x8, lo), acc[cb], 0, 0, 0);
+          }
         }
       }
     } else {
+      // A operand: query row, channels [g D/4, (g+1) D/4) (fp32 products)
+      float qv[D / 4];
+      const T* qsrc = Qunit + (long)qrow * D + g * (D / 4);
 #pragma unroll
       for (int v = 0; v < D / 16; ++v) {
         f32x4 w = *reinterpret_cast<const f32x4*>(qsrc + 4 * v);
 #pragma unroll
         for (int e = 0; e < 4; ++e) qv[4 * v + e] = w[e];
       }
-    }
-    f32x4 acc[kMaxCoefTile / 16];
 #pragma unroll
-    for (int cb = 0; cb < kMaxCoefTile / 16; ++cb) {
-      acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (cb < ncb) {
-        const float* crow = coef + (cb * 16 + col) * STRIDE + g * (D / 4);
+      for (int cb = 0; cb < kMaxCoefTile / 16; ++cb) {
+        acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (cb < ncb) {
+          const float* crow = coef + (cb * 16 + col) * STRIDE + g * (D / 4);
 #pragma unroll
-        for (int s4 = 0; s4 < D / 16; ++s4) {
-          f32x4 cv = *reinterpret_cast<const f32x4*>(crow + 4 * s4);
+          for (int s4 = 0; s4 < D / 16; ++s4) {
+            f32x4 cv = *reinterpret_cast<const f32x4*>(crow + 4 * s4);
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[4 * s4 + e],
-                                                           cv[e], acc[cb], 0,
-                                                           0, 0);
+            for (int e = 0; e < 4; ++e)
+              acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[4 * s4 + e], cv[e], acc[cb], 0, 0, 0);
+          }
         }
       }
     }
@@ -719,6 +772,7 @@ __global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a, Taps 
       }
     }
     __syncthreads();
+    if constexpr (sizeof(T) == 2) split_tile_bf16<D>(coef, ncoef);
     skim_epilogue<T, D>(a, u, tile, n0, ncoef, coef);
     __syncthreads();
   }
