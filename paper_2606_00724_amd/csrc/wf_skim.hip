@@ -450,13 +450,13 @@ __device__ void band_tile(const T* Kunit, long L, long n0, int ncoef, long n_end
         *reinterpret_cast<f32x4*>(dst + e) = f32x4{r[e], r[e + 1], r[e + 2], r[e + 3]};
     }
   };
-  // batches of BATCH loads over blocks c0 .. c1 + 1; the next batch's loads
-  // are issued before the current one is used
+  // batches of BATCH loads over blocks c0 .. c1 + 1
   constexpr int NBB = GPB / BATCH;  // batches per block
   const long nbt = (c1 + 2 - c0) * NBB;
-  auto load_batch = [&](long bi, u32x4* v) {
+  for (long bi = 0; bi < nbt; ++bi) {
     const long b = c0 + bi / NBB;
     const int g0 = (int)(bi % NBB) * BATCH;
+    u32x4 v[BATCH];
 #pragma unroll
     for (int gi = 0; gi < BATCH; ++gi) {
       const long r = b * BLK + (g0 + gi) * RPI + rsub;
@@ -464,16 +464,6 @@ __device__ void band_tile(const T* Kunit, long L, long n0, int ncoef, long n_end
       const long row = r < L ? r : (periodic ? r % L : L - 1);
       v[gi] = *reinterpret_cast<const u32x4*>(Kunit + row * D + csub * CPL);
     }
-  };
-  u32x4 vn[BATCH];
-  load_batch(0, vn);
-  for (long bi = 0; bi < nbt; ++bi) {
-    u32x4 v[BATCH];
-#pragma unroll
-    for (int gi = 0; gi < BATCH; ++gi) v[gi] = vn[gi];
-    if (bi + 1 < nbt) load_batch(bi + 1, vn);
-    const long b = c0 + bi / NBB;
-    const int g0 = (int)(bi % NBB) * BATCH;
     if (g0 == 0 && b > c0) {
       flush(b - 3);
 #pragma unroll
@@ -717,9 +707,18 @@ __device__ void skim_epilogue(const SkimTileArgs& a, int u, int tile, long n0,
   }
 }
 
+// Waves per SIMD a skim tile instance is compiled for.  The banded db2
+// tiles at J = 6, 7 (d = 128, bf16) fit four workgroups per CU in 128 VGPRs
+// without spills, so one round of workgroups covers the 32 tiles per unit of
+// the 128K shape instead of a round and a third; other instances would
+// spill under that bound and keep the default.
+constexpr int skim_tile_waves(int src, int M, int J, int elem, int D) {
+  return src == kCascade && M == 4 && elem == 2 && D == 128 && (J == 6 || J == 7) ? 4 : 1;
+}
+
 template <int SRC, int M, int J, typename T, int D>
-__global__ __launch_bounds__(kBlock) void skim_tile_kernel(SkimTileArgs a, Taps taps,
-                                                           EdgeTaps edge) {
+__global__ __launch_bounds__(kBlock, skim_tile_waves(SRC, M, J, (int)sizeof(T), D)) void
+skim_tile_kernel(SkimTileArgs a, Taps taps, EdgeTaps edge) {
   extern __shared__ float coef[];  // [cpt][D + kCoefPad], then the banded taps
   constexpr bool kBand = SRC == kCascade && M == 4 && BandShape<T, D, J>::ok && J <= kBandMaxJ;
   float* band = coef + a.cpt * (D + kCoefPad);  // [2][3 << J], then [6 << J] edge filters
