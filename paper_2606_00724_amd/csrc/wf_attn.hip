@@ -768,7 +768,8 @@ AttnPlan plan_attn(const wf_params& p, long nrows) {
     const size_t stage = (size_t)2 * kRingRows * 2 * D;      // K + V chunk
     const size_t toks = (size_t)a.rps * sizeof(int32_t);
     const size_t budget = 160 * 1024 - 1024;
-    a.nbuf = (int)std::min<size_t>(4, (budget - toks) / stage);
+    // three slots (two chunks in flight) measured slightly faster than four
+    a.nbuf = (int)std::min<size_t>(3, (budget - toks) / stage);
     if (a.nbuf < 2) a.nbuf = 0;  // rejected by the caller
     constexpr int nw = kAttnRingBlock / kWave;  // row-half merge: [nw][16][D] + 2 [nw][16]
     const size_t comb = (size_t)nw * 16 * D * 4 + (size_t)2 * nw * 16 * 4;
