@@ -691,25 +691,53 @@ __global__ __launch_bounds__(kCombineBlock) void attn_combine_kernel(AttnArgs a,
   const int c0 = (threadIdx.x % tpr) * 8;
   if (q >= a.B) return;  // no barrier follows
   const float* ps = a.pstat + (long)u * a.NS * 2 * a.B;
-  float M = -INFINITY;
-  for (int s = 0; s < a.NS; ++s) M = fmaxf(M, ps[(long)s * 2 * a.B + q]);
+  // splits in groups of SB whose loads are all in flight together; each
+  // group is merged into the running (max, sum, output) in one step, so up
+  // to SB splits the arithmetic is the plain max-then-sum
+  constexpr int SB = 8;
+  float M = -INFINITY, lsum = 0.f;
   float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  float lsum = 0.f;
-  for (int s = 0; s < a.NS; ++s) {
-    const float ms = ps[(long)s * 2 * a.B + q];
-    const float w = ms > -INFINITY ? __expf(ms - M) : 0.f;
-    lsum += ps[(long)s * 2 * a.B + a.B + q] * w;
-    const float4* src =
-        reinterpret_cast<const float4*>(a.part + (((long)u * a.NS + s) * a.B + q) * D + c0);
-    const float4 x0 = src[0], x1 = src[1];
-    o[0] += w * x0.x;
-    o[1] += w * x0.y;
-    o[2] += w * x0.z;
-    o[3] += w * x0.w;
-    o[4] += w * x1.x;
-    o[5] += w * x1.y;
-    o[6] += w * x1.z;
-    o[7] += w * x1.w;
+  for (int s0 = 0; s0 < a.NS; s0 += SB) {
+    float ms[SB], zs[SB];
+    float4 x[SB][2];
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int s = s0 + k;
+      if (s < a.NS) {
+        ms[k] = ps[(long)s * 2 * a.B + q];
+        zs[k] = ps[(long)s * 2 * a.B + a.B + q];
+        const float4* src =
+            reinterpret_cast<const float4*>(a.part + (((long)u * a.NS + s) * a.B + q) * D + c0);
+        x[k][0] = src[0];
+        x[k][1] = src[1];
+      } else {
+        ms[k] = -INFINITY;
+        zs[k] = 0.f;
+        x[k][0] = x[k][1] = float4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    float mn = M;
+#pragma unroll
+    for (int k = 0; k < SB; ++k) mn = fmaxf(mn, ms[k]);
+    if (mn == -INFINITY) continue;
+    const float r = M > -INFINITY ? __expf(M - mn) : 0.f;
+    lsum *= r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] *= r;
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const float w = ms[k] > -INFINITY ? __expf(ms[k] - mn) : 0.f;
+      lsum += zs[k] * w;
+      o[0] += w * x[k][0].x;
+      o[1] += w * x[k][0].y;
+      o[2] += w * x[k][0].z;
+      o[3] += w * x[k][0].w;
+      o[4] += w * x[k][1].x;
+      o[5] += w * x[k][1].y;
+      o[6] += w * x[k][1].z;
+      o[7] += w * x[k][1].w;
+    }
+    M = mn;
   }
   const float inv = 1.f / lsum;
 #pragma unroll

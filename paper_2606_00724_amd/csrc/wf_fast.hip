@@ -277,13 +277,35 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
   extern __shared__ float wsh[];  // W (when it fits), then the picked block ids
   const int u = blockIdx.x;
   const int B = a.B, nJ = a.nJ;
-  const float* ws = a.wstats + (long)u * a.R * 2 * B;
-  for (int q = threadIdx.x; q < B; q += NT) {
+  // the ranges' (max, sum of exp) pairs: thread (part, q) = (tid / B, tid % B)
+  // folds ranges part, part + parts, ..., then rows of 16 lanes per query
+  // merge the parts by rotations
+  const int parts = min(NT / B, 16);
+  {
+    const float* ws = a.wstats + (long)u * a.R * 2 * B;
+    const int q = threadIdx.x % B, part = threadIdx.x / B;
+    if (part < parts) {
+      float mx = -INFINITY, z = 0.f;
+      for (int r = part; r < a.R; r += parts)
+        stat_absorb(mx, z, ws[(long)r * 2 * B + q], ws[(long)r * 2 * B + B + q]);
+      pool_m[part * (B + 1) + q] = mx;
+      pool_z[part * (B + 1) + q] = z;
+    }
+  }
+  __syncthreads();
+  {
+    const int q = threadIdx.x >> 4, part = threadIdx.x & 15;
     float mx = -INFINITY, z = 0.f;
-    for (int r = 0; r < a.R; ++r)
-      stat_absorb(mx, z, ws[(long)r * 2 * B + q], ws[(long)r * 2 * B + B + q]);
+    if (q < B && part < parts) {
+      mx = pool_m[part * (B + 1) + q];
+      z = pool_z[part * (B + 1) + q];
+    }
+    row16_merge<8>(mx, z);
+    row16_merge<4>(mx, z);
+    row16_merge<2>(mx, z);
+    row16_merge<1>(mx, z);
     // exp(l - M_q) / Z_q = 2^(l log2(e) - c_q)
-    row_c[q] = fmaf(mx, kLog2e, __log2f(z));
+    if (part == 0 && q < B) row_c[q] = fmaf(mx, kLog2e, __log2f(z));
   }
   __syncthreads();
   // W_j = sum_q softmax_j(l_q.): four threads per block j, queries
@@ -348,7 +370,6 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
   // a (max, sum of exp) pair (the loads of a wave cover whole rows); the
   // pairs go through LDS to rows of 16 lanes per query, merged by rotations.
   const int32_t* segx = seg_in_lds ? seg_sh : seg;
-  const int parts = min(NT / B, 16);
   {
     const int q = threadIdx.x % B, part = threadIdx.x / B;
     const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
