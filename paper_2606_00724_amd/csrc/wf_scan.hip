@@ -269,8 +269,18 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     const float* stt = a.stats + (long)u * a.Cs * 2 * a.B;
     for (int q = threadIdx.x; q < a.B; q += kPoolBlock) {
       float mx = -INFINITY, z = 0.f;
-      for (int k = 0; k < a.Cs; ++k)
-        stat_merge(mx, z, stt[(long)k * 2 * a.B + q], stt[(long)k * 2 * a.B + a.B + q]);
+      constexpr int SB = 8;  // slices whose loads are in flight together
+      for (int k0 = 0; k0 < a.Cs; k0 += SB) {
+        float mk[SB], zk[SB];
+#pragma unroll
+        for (int k = 0; k < SB; ++k) {
+          const bool ok = k0 + k < a.Cs;
+          mk[k] = ok ? stt[(long)(k0 + k) * 2 * a.B + q] : -INFINITY;
+          zk[k] = ok ? stt[(long)(k0 + k) * 2 * a.B + a.B + q] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < SB; ++k) stat_merge(mx, z, mk[k], zk[k]);
+      }
       // exp(s - M) / Z = 2^(s log2(e) - (M log2(e) + log2(Z)))
       lse2[q] = fmaf(mx, kLog2e, __log2f(z));
     }
