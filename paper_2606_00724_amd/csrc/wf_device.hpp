@@ -249,6 +249,27 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   return x;
 }
 
+// One count into bin d of the LDS histogram h for every active lane with m
+// set.  When at least 8 of the wave's counting lanes share the digit of its
+// first counting lane, they add as one atomic carrying the group's size and
+// the rest add one each; otherwise every lane adds one.  Clustered keys
+// (equal or nearly equal scores) would otherwise queue most of a wave's
+// atomics on one LDS address.
+__device__ __forceinline__ void hist_add(uint32_t* h, bool m, uint32_t d, int lane) {
+  const uint64_t act = __builtin_amdgcn_ballot_w64(m);
+  if (act == 0) return;  // uniform
+  const int lead = __ffsll((unsigned long long)act) - 1;
+  const uint32_t ld = (uint32_t)__builtin_amdgcn_readlane((int)d, lead);
+  const bool mine = m && d == ld;
+  const uint32_t group = (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(mine));
+  if (group >= 8) {  // uniform
+    if (lane == lead) atomicAdd(&h[ld], group);
+    if (m && !mine) atomicAdd(&h[d], 1u);
+  } else if (m) {
+    atomicAdd(&h[d], 1u);
+  }
+}
+
 // Picks the k largest of score[0..n) (ties: lower index first) and calls
 // emit(pos, i) for each picked position i, pos = its rank in ascending order
 // of i (0..k-1).  Requires 1 <= k <= n and 64 <= NT <= 1024.  score may live in LDS or
@@ -280,7 +301,7 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
       for (int i = tid; i < 256; i += NT) sh.hist[(pass + 1) % 3][i] = 0;
     for (int i = tid; i < n; i += NT) {
       const uint32_t key = order_key(score[i]);
-      if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
+      hist_add(h, (key & mask) == prefix, (key >> shift) & 255u, lane);
     }
     __syncthreads();
     // lane l looks at digits 255 - 4l - j, j < 4 (descending)
