@@ -476,9 +476,16 @@ static wf_status recursive_impl(const wf_params* p, const float* prop, const voi
   int npar = 0;
   for (int b = p->levels; b >= 1; --b) {
     int32_t* out = b == 1 ? tok : sel[b & 1];
-    WF_TRY(step(launch_rec_tiles(*p, b, n, parent, npar, Q, K, logits, stats, s)));
-    WF_TRY(step(launch_rec_select(*p, b, n, counts[b - 1], parent, npar, logits, stats, W,
-                                  out, s)));
+    if (b == p->levels && rec_token_path(*p)) {
+      // the first scale's coarse logits as sums of token logits
+      WF_TRY(step(launch_rec_token_skim(*p, Q, K, logits, stats, s)));
+      WF_TRY(step(launch_rec_select_slices(*p, b, n, counts[b - 1], parent, npar,
+                                           plan_rec_token(*p).R, logits, stats, W, out, s)));
+    } else {
+      WF_TRY(step(launch_rec_tiles(*p, b, n, parent, npar, Q, K, logits, stats, s)));
+      WF_TRY(step(launch_rec_select(*p, b, n, counts[b - 1], parent, npar, logits, stats, W,
+                                    out, s)));
+    }
     parent = out;
     npar = counts[b - 1];
     n = 2L * counts[b - 1];

@@ -16,6 +16,11 @@
 //   M_q = max_{j in seg} e_qj,   Z_q = sum_{j in seg} exp(e_qj - M_q),
 // with M_q at or above every pool logit of query q.
 //
+// The same kernel without the log-sum-exps serves the first scale of the
+// multi-scale recursion (Alg. 1 at b = B, 1..5 levels): it writes only the
+// coarse logits, query-major ([U][B][nJ], the layout of the coefficient
+// tiles), and the per-range statistics.
+//
 // The keys stream through an LDS ring filled by direct global->LDS loads;
 // see token_skim_kernel for the roles of its waves.
 #include "wf_device.hpp"
@@ -74,19 +79,37 @@ struct SliceBlocks {
   __device__ static bool keeps(int hi) { return J != 5 || hi == 0; }
 };
 
-// LDS bytes of one token-skim batch slot (block rows of 2 * B floats)
-template <int J>
+// Blocks of 2 or 4 tokens (J = 1, 2) lie inside one lane: its values
+// v in [i 2^J, (i + 1) 2^J) are the block (8 (v / 4) + 4 (l / 32) + v % 4) >> J
+// of the slice, 16 / 2^J of them per lane.
+//
+// Chunks per LDS batch.  With the log-sum-exps a batch holds block rows of
+// 2 B floats; without them it holds NBB = 32 or 64 blocks of every query row
+// (a run of 128 bytes or more per row), block e of row q at column
+// e ^ (q mod NBB), so that the 32 query rows a wave writes at once fall in
+// distinct banks.
+template <int J, bool LSE>
+constexpr int token_batch_chunks() {
+  return LSE ? SliceBlocks<J>::BATCH : ((128 >> J) >= 32 ? 1 : 32 / (128 >> J));
+}
+
+// LDS bytes of one token-skim batch slot
+template <int J, bool LSE>
 constexpr size_t token_batch_bytes(int B) {
-  return (size_t)SliceBlocks<J>::BATCH * SliceBlocks<J>::BPC * 2 * B * sizeof(float);
+  constexpr int nbb = token_batch_chunks<J, LSE>() * (128 >> J);
+  return (size_t)nbb * (LSE ? 2 * B : B) * sizeof(float);
 }
 
 // Waves per SIMD the token skim is compiled to allow: four lets two
-// workgroups share a CU; the 8-token blocks of 128-wide keys need more
-// registers than that leaves, and run one workgroup per CU.
-constexpr int token_skim_waves_per_simd(int D, int J) { return D == 128 && J == 3 ? 2 : 4; }
+// workgroups share a CU; with 128-wide keys, the 8-token blocks with their
+// log-sum-exps and the 2-token blocks need more registers than that leaves,
+// and run one workgroup per CU.
+constexpr int token_skim_waves_per_simd(int D, int J, bool lse) {
+  return D == 128 && ((lse && J == 3) || (!lse && J == 1)) ? 2 : 4;
+}
 
-template <int D, int J>
-__global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void token_skim_kernel(
+template <int D, int J, bool LSE>
+__global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) void token_skim_kernel(
     TokenSkimArgs a) {
   constexpr int NW = kTokBlock / kWave;  // 8
   constexpr int NIW = NW / 2;            // loading waves
@@ -96,18 +119,22 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
   constexpr int IPW = CR * G / (64 * NIW);
   constexpr int KS = D / 16;             // k-steps of the 32x32x16 product
   using SB = SliceBlocks<J>;
-  constexpr int NBLK = SB::NBLK, VPB = SB::VPB, NST = SB::NST, BPC = SB::BPC, BATCH = SB::BATCH;
-  static_assert(J >= 3 && J <= 5, "blocks of 8, 16 or 32 tokens");
+  constexpr int BPC = 128 >> J;                           // blocks per chunk
+  constexpr int BATCH = token_batch_chunks<J, LSE>();
+  constexpr int NBB = BATCH * BPC;                        // blocks per batch
+  static_assert(J >= 1 && J <= 5, "blocks of 2 .. 32 tokens");
+  static_assert(!LSE || J >= 3, "log-sum-exps for blocks of 8, 16 or 32 tokens");
   static_assert(CR == 32 * NIW, "four 32-token slices per chunk");
   const int B = a.B;
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* ring = smem;  // [nbuf][CHB]
-  // [2][BATCH * BPC][2][B]: coarse logits, then log-sum-exps
+  // two slots: [NBB][2][B] coarse logits, then log-sum-exps (LSE), or
+  // [B][NBB] coarse logits (columns swizzled)
   float* batch = reinterpret_cast<float*>(smem + (size_t)a.nbuf * CHB);
   // [NW][32][2] running pairs, merged after the last ring load has landed:
   // they reuse the ring's first bytes
   float* red = reinterpret_cast<float*>(smem);
-  const int slot_floats = BATCH * BPC * 2 * B;
+  const int slot_floats = LSE ? NBB * 2 * B : B * NBB;
 
   const int item = xcd_swizzle(blockIdx.x, gridDim.x);
   const int u = item / a.R, r = item % a.R;
@@ -146,26 +173,32 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
     }
   }
 
-  float* out = a.blocks + (long)u * a.nJ * 2 * B;  // [nJ][2][B]
   const long jend = te >> J;                        // blocks of this range end here
-  const float c2 = a.scale * kLog2e;
   const float cl = a.scale * a.norm;
-  const bool keeps = SB::keeps(hi);
-  const bool vec = (B & 1) == 0;  // block rows are 16-byte multiples
 
   // waves 4..7: copy batch k (its blocks inside the range) to global memory
   auto copy_batch = [&](int k) {
-    const long jb0 = (tb >> J) + (long)k * BATCH * BPC;
-    const int nb = (int)min((long)(BATCH * BPC), jend - jb0);
-    const int nf = nb * 2 * B;
+    const long jb0 = (tb >> J) + (long)k * NBB;
+    const int nb = (int)min((long)NBB, jend - jb0);
     const float* src = batch + (k & 1) * slot_floats;
-    float* dst = out + jb0 * 2 * B;
     const int t = (wave - NIW) * 64 + lane;
-    if (vec) {
-      for (int i = t; i < nf / 4; i += NIW * 64)
-        reinterpret_cast<float4*>(dst)[i] = reinterpret_cast<const float4*>(src)[i];
+    if constexpr (LSE) {
+      // one contiguous run of nb block rows ([nJ][2][B])
+      const int nf = nb * 2 * B;
+      float* dst = a.blocks + ((long)u * a.nJ + jb0) * 2 * B;
+      if ((B & 1) == 0) {  // block rows are 16-byte multiples
+        for (int i = t; i < nf / 4; i += NIW * 64)
+          reinterpret_cast<float4*>(dst)[i] = reinterpret_cast<const float4*>(src)[i];
+      } else {
+        for (int i = t; i < nf; i += NIW * 64) dst[i] = src[i];
+      }
     } else {
-      for (int i = t; i < nf; i += NIW * 64) dst[i] = src[i];
+      // one run of nb logits per query row ([B][nJ])
+      float* dst = a.blocks + (long)u * B * a.nJ + jb0;
+      for (int i = t; i < nb * B; i += NIW * 64) {
+        const int qq = i / nb, e = i - qq * nb;
+        dst[(long)qq * a.nJ + e] = src[qq * NBB + (e ^ (qq & (NBB - 1)))];
+      }
     }
   };
 
@@ -193,44 +226,70 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J)) void to
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
                                                     __builtin_bit_cast(bf16x8, qreg[s]), acc, 0, 0, 0);
     }
-    // raw block sums and maxima, completed with the partner lane l ^ 32
-    float bs[NBLK], bm[NBLK], be[NBLK];
-#pragma unroll
-    for (int b = 0; b < NBLK; ++b) {
-      bs[b] = 0.f;
-      bm[b] = -INFINITY;
-#pragma unroll
-      for (int v = b * VPB; v < (b + 1) * VPB; ++v) {
-        bs[b] += acc[v];
-        bm[b] = fmaxf(bm[b], acc[v]);
-      }
-      bs[b] = add_xor32(bs[b]);
-      bm[b] = max_xor32(bm[b]);
-      const float off = -bm[b] * c2;
-      be[b] = 0.f;
-#pragma unroll
-      for (int v = b * VPB; v < (b + 1) * VPB; ++v) be[b] += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, off));
-      be[b] = add_xor32(be[b]);
-    }
     float* slot = batch + ((ch / BATCH) & 1) * slot_floats;
     const int bl0 = (ch % BATCH) * BPC + ((32 * ts) >> J);  // slice's first block in the batch
+    if constexpr (J <= 2) {
+      // every block lies in one lane
+      constexpr int VPB = 1 << J, NL = 16 / VPB;
 #pragma unroll
-    for (int n = 0; n < NST; ++n) {
-      const int b = SB::block(n, hi);
-      // b takes at most two values across the wave: select, do not index
-      float s_ = bs[0], m_ = bm[0], e_ = be[0];
+      for (int i = 0; i < NL; ++i) {
+        float s_ = 0.f;
 #pragma unroll
-      for (int k = 1; k < NBLK; ++k)
-        if (b == k) {
-          s_ = bs[k];
-          m_ = bm[k];
-          e_ = be[k];
+        for (int v = i * VPB; v < (i + 1) * VPB; ++v) s_ += acc[v];
+        const int b = (8 * ((i * VPB) / 4) + 4 * hi + (i * VPB) % 4) >> J;
+        const float l = s_ * cl;
+        if (q < B && (slice0 >> J) + b < jend) {
+          stat_add(cm, cz, l);
+          slot[q * NBB + ((bl0 + b) ^ (q & (NBB - 1)))] = l;
         }
-      const float l = s_ * cl;
-      if (keeps && q < B && (slice0 >> J) + b < jend) {
-        stat_add(cm, cz, l);
-        slot[(bl0 + b) * 2 * B + q] = l;
-        slot[((bl0 + b) * 2 + 1) * B + q] = fmaf(m_, a.scale, __logf(e_));
+      }
+    } else {
+      constexpr int NBLK = SB::NBLK, VPB = SB::VPB, NST = SB::NST;
+      const float c2 = a.scale * kLog2e;
+      // raw block sums (and maxima), completed with the partner lane l ^ 32
+      float bs[NBLK], bm[NBLK], be[NBLK];
+#pragma unroll
+      for (int b = 0; b < NBLK; ++b) {
+        bs[b] = 0.f;
+        bm[b] = -INFINITY;
+#pragma unroll
+        for (int v = b * VPB; v < (b + 1) * VPB; ++v) {
+          bs[b] += acc[v];
+          if constexpr (LSE) bm[b] = fmaxf(bm[b], acc[v]);
+        }
+        bs[b] = add_xor32(bs[b]);
+        be[b] = 0.f;
+        if constexpr (LSE) {
+          bm[b] = max_xor32(bm[b]);
+          const float off = -bm[b] * c2;
+#pragma unroll
+          for (int v = b * VPB; v < (b + 1) * VPB; ++v) be[b] += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, off));
+          be[b] = add_xor32(be[b]);
+        }
+      }
+      const bool keeps = SB::keeps(hi);
+#pragma unroll
+      for (int n = 0; n < NST; ++n) {
+        const int b = SB::block(n, hi);
+        // b takes at most two values across the wave: select, do not index
+        float s_ = bs[0], m_ = bm[0], e_ = be[0];
+#pragma unroll
+        for (int k = 1; k < NBLK; ++k)
+          if (b == k) {
+            s_ = bs[k];
+            m_ = bm[k];
+            e_ = be[k];
+          }
+        const float l = s_ * cl;
+        if (keeps && q < B && (slice0 >> J) + b < jend) {
+          stat_add(cm, cz, l);
+          if constexpr (LSE) {
+            slot[(bl0 + b) * 2 * B + q] = l;
+            slot[((bl0 + b) * 2 + 1) * B + q] = fmaf(m_, a.scale, __logf(e_));
+          } else {
+            slot[q * NBB + ((bl0 + b) ^ (q & (NBB - 1)))] = l;
+          }
+        }
       }
     }
   }
@@ -428,22 +487,34 @@ bool fast_path(const wf_params& p) {
          p.q_len <= 16 * kFastMaxQBlocks && effective_scale(p) > 0.f;
 }
 
-FastPlan plan_fast(const wf_params& p) {
+template <bool LSE>
+static size_t token_batch_bytes_at(int J, int B) {
+  switch (J) {
+    case 1: return LSE ? 0 : token_batch_bytes<1, false>(B);
+    case 2: return LSE ? 0 : token_batch_bytes<2, false>(B);
+    case 3: return token_batch_bytes<3, LSE>(B);
+    case 4: return token_batch_bytes<4, LSE>(B);
+    default: return token_batch_bytes<5, LSE>(B);
+  }
+}
+
+// Ranges and ring of the token-level skim at J = p.levels.
+static FastPlan plan_token(const wf_params& p, bool lse) {
   FastPlan f{};
   const long U = (long)p.batch * p.heads;
   const long Lf = filtered_len(p);
   const long chunks = (Lf + kScanChunk - 1) / kScanChunk;
   const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
   // two batch slots of block results; the wave reduction pairs reuse the ring
-  const size_t bb = 2 * (p.levels == 3   ? token_batch_bytes<3>(p.q_len)
-                         : p.levels == 4 ? token_batch_bytes<4>(p.q_len)
-                                         : token_batch_bytes<5>(p.q_len));
+  const size_t bb = 2 * (lse ? token_batch_bytes_at<true>(p.levels, p.q_len)
+                             : token_batch_bytes_at<false>(p.levels, p.q_len));
   // Two resident workgroups per CU, each two chunks deep, stream faster than
   // one three deep (the barrier of one overlaps the other's loads); that
   // shape is taken whenever two fit in the CU's LDS.
   constexpr size_t kLdsPerCu = 160 * 1024;
   const size_t fit2 = kLdsPerCu / 2 > bb ? (kLdsPerCu / 2 - bb) / chb : 0;
-  const int per_cu = fit2 >= 2 && token_skim_waves_per_simd(p.head_dim, p.levels) >= 4 ? 2 : 1;
+  const int per_cu =
+      fit2 >= 2 && token_skim_waves_per_simd(p.head_dim, p.levels, lse) >= 4 ? 2 : 1;
   f.nbuf = (int)std::min<size_t>(3, per_cu == 2 ? fit2 : (kLdsPerCu - bb) / chb);
   f.lds_bytes = f.nbuf * chb + bb;
   const long want = std::max(1L, ((long)per_cu * device_cu_count() + U - 1) / U);
@@ -454,9 +525,18 @@ FastPlan plan_fast(const wf_params& p) {
   return f;
 }
 
-template <int D, int J>
+FastPlan plan_fast(const wf_params& p) { return plan_token(p, true); }
+
+bool rec_token_path(const wf_params& p) {
+  return p.dtype == WF_BF16 && p.wavelet == WF_HAAR && p.levels >= 1 && p.levels <= 5 &&
+         p.q_len <= 16 * kFastMaxQBlocks;
+}
+
+FastPlan plan_rec_token(const wf_params& p) { return plan_token(p, false); }
+
+template <int D, int J, bool LSE>
 static hipError_t token_skim_launch(const TokenSkimArgs& a, size_t lds, hipStream_t s) {
-  auto kern = token_skim_kernel<D, J>;
+  auto kern = token_skim_kernel<D, J, LSE>;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -466,24 +546,33 @@ static hipError_t token_skim_launch(const TokenSkimArgs& a, size_t lds, hipStrea
   return hipGetLastError();
 }
 
-template <int D>
+template <int D, bool LSE>
 static hipError_t token_skim_dispatch(int J, const TokenSkimArgs& a, size_t lds, hipStream_t s) {
-  switch (J) {
-    case 3: return token_skim_launch<D, 3>(a, lds, s);
-    case 4: return token_skim_launch<D, 4>(a, lds, s);
-    case 5: return token_skim_launch<D, 5>(a, lds, s);
-    default: return hipErrorInvalidValue;
+  if constexpr (LSE) {
+    switch (J) {
+      case 3: return token_skim_launch<D, 3, true>(a, lds, s);
+      case 4: return token_skim_launch<D, 4, true>(a, lds, s);
+      case 5: return token_skim_launch<D, 5, true>(a, lds, s);
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (J) {
+      case 1: return token_skim_launch<D, 1, false>(a, lds, s);
+      case 2: return token_skim_launch<D, 2, false>(a, lds, s);
+      case 3: return token_skim_launch<D, 3, false>(a, lds, s);
+      case 4: return token_skim_launch<D, 4, false>(a, lds, s);
+      case 5: return token_skim_launch<D, 5, false>(a, lds, s);
+      default: return hipErrorInvalidValue;
+    }
   }
 }
 
-hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, float* blocks,
-                             float* wstats, hipStream_t s) {
-  if (!fast_path(p)) return hipErrorInvalidValue;
-  const FastPlan f = plan_fast(p);
+static TokenSkimArgs token_args(const wf_params& p, const FastPlan& f, const void* Q,
+                                const void* K, float* out, float* wstats) {
   TokenSkimArgs a;
   a.K = K;
   a.Q = Q;
-  a.blocks = blocks;
+  a.blocks = out;
   a.wstats = wstats;
   a.U = p.batch * p.heads;
   a.L = (int)filtered_len(p);
@@ -495,8 +584,25 @@ hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, f
   a.nbuf = f.nbuf;
   a.scale = effective_scale(p);
   a.norm = (float)std::pow(2.0, -0.5 * p.levels);
-  return p.head_dim == 128 ? token_skim_dispatch<128>(p.levels, a, f.lds_bytes, s)
-                           : token_skim_dispatch<64>(p.levels, a, f.lds_bytes, s);
+  return a;
+}
+
+hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, float* blocks,
+                             float* wstats, hipStream_t s) {
+  if (!fast_path(p)) return hipErrorInvalidValue;
+  const FastPlan f = plan_fast(p);
+  const TokenSkimArgs a = token_args(p, f, Q, K, blocks, wstats);
+  return p.head_dim == 128 ? token_skim_dispatch<128, true>(p.levels, a, f.lds_bytes, s)
+                           : token_skim_dispatch<64, true>(p.levels, a, f.lds_bytes, s);
+}
+
+hipError_t launch_rec_token_skim(const wf_params& p, const void* Q, const void* K,
+                                 float* logits, float* stats, hipStream_t s) {
+  if (!rec_token_path(p)) return hipErrorInvalidValue;
+  const FastPlan f = plan_rec_token(p);
+  const TokenSkimArgs a = token_args(p, f, Q, K, logits, stats);
+  return p.head_dim == 128 ? token_skim_dispatch<128, false>(p.levels, a, f.lds_bytes, s)
+                           : token_skim_dispatch<64, false>(p.levels, a, f.lds_bytes, s);
 }
 
 hipError_t launch_fast_select(const wf_params& p, const float* blocks, const float* wstats,

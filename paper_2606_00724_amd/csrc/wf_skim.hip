@@ -1205,7 +1205,9 @@ RecPlan plan_recursion(const wf_params& p, const int32_t* counts) {
   long n = (long)p.ctx_len >> p.levels;
   for (int b = p.levels; b >= 1; --b) {
     const int cpt = haar_cpt(b);
-    const int ntiles = (int)((n + cpt - 1) / cpt);
+    // the first scale's statistics come from the token skim's ranges
+    const int ntiles = b == p.levels && rec_token_path(p) ? plan_rec_token(p).R
+                                                          : (int)((n + cpt - 1) / cpt);
     r.max_n = std::max(r.max_n, n);
     r.max_tiles = std::max(r.max_tiles, ntiles);
     r.max_keep = std::max(r.max_keep, (long)counts[b - 1]);
@@ -1227,6 +1229,13 @@ hipError_t launch_rec_select(const wf_params& p, int b, long n, int keep,
   const int cpt = haar_cpt(b);
   const int ntiles = (int)((n + cpt - 1) / cpt);
   return skim_select_common(p, n, ntiles, keep, parent, npar, b == 1 ? 1 : 0, logits,
+                            stats, W, out, s);
+}
+hipError_t launch_rec_select_slices(const wf_params& p, int b, long n, int keep,
+                                    const int32_t* parent, int npar, int nslices,
+                                    const float* logits, const float* stats, float* W,
+                                    int32_t* out, hipStream_t s) {
+  return skim_select_common(p, n, nslices, keep, parent, npar, b == 1 ? 1 : 0, logits,
                             stats, W, out, s);
 }
 
