@@ -476,11 +476,14 @@ static wf_status recursive_impl(const wf_params* p, const float* prop, const voi
   int npar = 0;
   for (int b = p->levels; b >= 1; --b) {
     int32_t* out = b == 1 ? tok : sel[b & 1];
-    if (b == p->levels && rec_token_path(*p)) {
-      // the first scale's coarse logits as sums of token logits
-      WF_TRY(step(launch_rec_token_skim(*p, Q, K, logits, stats, s)));
+    if (rec_token_path(*p) && b <= 5) {
+      // the scale's coarse logits as sums of token logits (of the kept
+      // blocks' tokens below the first scale)
+      const long rows = parent ? (long)npar << (b + 1) : filtered_len(*p);
+      WF_TRY(step(launch_rec_token_skim(*p, b, n, parent, npar, Q, K, logits, stats, s)));
       WF_TRY(step(launch_rec_select_slices(*p, b, n, counts[b - 1], parent, npar,
-                                           plan_rec_token(*p).R, logits, stats, W, out, s)));
+                                           plan_rec_token(*p, b, rows, parent != nullptr).R,
+                                           logits, stats, W, out, s)));
     } else {
       WF_TRY(step(launch_rec_tiles(*p, b, n, parent, npar, Q, K, logits, stats, s)));
       WF_TRY(step(launch_rec_select(*p, b, n, counts[b - 1], parent, npar, logits, stats, W,

@@ -108,7 +108,7 @@ constexpr int token_skim_waves_per_simd(int D, int J, bool lse) {
   return D == 128 && ((lse && J == 3) || (!lse && J == 1)) ? 2 : 4;
 }
 
-template <int D, int J, bool LSE>
+template <int D, int J, bool LSE, bool GATHER = false>
 __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) void token_skim_kernel(
     TokenSkimArgs a) {
   constexpr int NW = kTokBlock / kWave;  // 8
@@ -124,6 +124,7 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
   constexpr int NBB = BATCH * BPC;                        // blocks per batch
   static_assert(J >= 1 && J <= 5, "blocks of 2 .. 32 tokens");
   static_assert(!LSE || J >= 3, "log-sum-exps for blocks of 8, 16 or 32 tokens");
+  static_assert(!(LSE && GATHER), "gathered rows only without the log-sum-exps");
   static_assert(CR == 32 * NIW, "four 32-token slices per chunk");
   const int B = a.B;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -157,19 +158,42 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
 #pragma unroll
   for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qreg[s]));
 
+  // row r of the chunk at c0: key row c0 + r, or on a refinement scale
+  // gathered row p = c0 + r, token par[p >> pshift] 2^pshift + p mod 2^pshift
+  // (rows past the range repeat its last row; ids are clamped into the unit)
   struct Rows {
     const bf16_t* Kunit;
+    const int32_t* par;  // LDS: the range's parent ids from p_lo on, or null
     long c0, tlast;
+    int pshift, p_lo, last;
     __device__ __forceinline__ const bf16_t* operator()(int r) const {
-      return Kunit + min(c0 + r, tlast) * D;
+      const long p = min(c0 + r, tlast);
+      if (!par) return Kunit + p * D;
+      const int t = (par[(int)(p >> pshift) - p_lo] << pshift) | (int)(p & ((1 << pshift) - 1));
+      return Kunit + (long)min(max(t, 0), last) * D;
     }
-  } rows{reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D, tb, te - 1};
+  } rows{reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D, nullptr, tb, te - 1,
+         a.pshift, (int)(tb >> a.pshift), (int)a.Ls - 1};
+  if constexpr (GATHER) {
+    {
+      // stage the range's parent ids (every thread reads them back below)
+      int32_t* par_sh = reinterpret_cast<int32_t*>(batch + 2 * slot_floats);
+      const int n_ids = (int)((te - 1) >> a.pshift) - rows.p_lo + 1;
+      const int32_t* src = a.parent + (long)u * a.npar + rows.p_lo;
+      for (int i = threadIdx.x; i < n_ids && i < a.par_cap; i += kTokBlock) par_sh[i] = src[i];
+      __syncthreads();
+      rows.par = par_sh;
+    }
+  }
   const uint32_t ring_lds = lds_offset(ring);
   const int nbuf = a.nbuf;
+  // the keys stream past the caches; the gathered rows of a refinement scale
+  // are loaded normally, since the attention reads many of them again
+  auto issue_rows = [&](uint32_t slot) { issue_chunk<CR, G, NIW, !GATHER>(slot, rows); };
   if (loader) {
     for (int k = 0; k < nch && k < nbuf - 1; ++k) {
       rows.c0 = tb + (long)k * CR;
-      issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(k * CHB), rows);
+      issue_rows(ring_lds + (uint32_t)(k * CHB));
     }
   }
 
@@ -210,7 +234,7 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
     if (loader) {
       if (ch + nbuf - 1 < nch) {
         rows.c0 = tb + (long)(ch + nbuf - 1) * CR;
-        issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rows);
+        issue_rows(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB));
       }
     } else if (ch > 0 && ch % BATCH == 0) {
       copy_batch(ch / BATCH - 1);
@@ -498,45 +522,57 @@ static size_t token_batch_bytes_at(int J, int B) {
   }
 }
 
-// Ranges and ring of the token-level skim at J = p.levels.
-static FastPlan plan_token(const wf_params& p, bool lse) {
+// Ranges and ring of the token-level skim with blocks of 2^J tokens over Lf
+// rows; `gather`: the rows are a gathered sequence of blocks of 2^(J+1)
+// tokens, whose ids each range stages in LDS.
+static FastPlan plan_token(const wf_params& p, int J, long Lf, bool lse, bool gather) {
   FastPlan f{};
   const long U = (long)p.batch * p.heads;
-  const long Lf = filtered_len(p);
   const long chunks = (Lf + kScanChunk - 1) / kScanChunk;
   const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
   // two batch slots of block results; the wave reduction pairs reuse the ring
-  const size_t bb = 2 * (lse ? token_batch_bytes_at<true>(p.levels, p.q_len)
-                             : token_batch_bytes_at<false>(p.levels, p.q_len));
+  const size_t bb = 2 * (lse ? token_batch_bytes_at<true>(J, p.q_len)
+                             : token_batch_bytes_at<false>(J, p.q_len));
   // Two resident workgroups per CU, each two chunks deep, stream faster than
   // one three deep (the barrier of one overlaps the other's loads); that
   // shape is taken whenever two fit in the CU's LDS.
   constexpr size_t kLdsPerCu = 160 * 1024;
-  const size_t fit2 = kLdsPerCu / 2 > bb ? (kLdsPerCu / 2 - bb) / chb : 0;
-  const int per_cu =
-      fit2 >= 2 && token_skim_waves_per_simd(p.head_dim, p.levels, lse) >= 4 ? 2 : 1;
-  f.nbuf = (int)std::min<size_t>(3, per_cu == 2 ? fit2 : (kLdsPerCu - bb) / chb);
-  f.lds_bytes = f.nbuf * chb + bb;
+  const long want0 = std::max(1L, (2L * device_cu_count() + U - 1) / U);
+  const long cpr0 = (chunks + std::min(chunks, want0) - 1) / std::min(chunks, want0);
+  const size_t ids = gather ? (size_t)(((cpr0 * kScanChunk) >> (J + 1)) + 2) * 4 : 0;
+  const size_t fixed = bb + ((ids + 15) & ~(size_t)15);
+  const size_t fit2 = kLdsPerCu / 2 > fixed ? (kLdsPerCu / 2 - fixed) / chb : 0;
+  const int per_cu = fit2 >= 2 && token_skim_waves_per_simd(p.head_dim, J, lse) >= 4 ? 2 : 1;
   const long want = std::max(1L, ((long)per_cu * device_cu_count() + U - 1) / U);
   const long R = std::min(chunks, want);
   const long cpr = (chunks + R - 1) / R;
   f.span = (int)(cpr * kScanChunk);
   f.R = (int)((Lf + f.span - 1) / f.span);
+  // the parent ids of one range (at most span / 2^(J+1) + 2 of them)
+  f.par_cap = gather ? (int)((f.span >> (J + 1)) + 2) : 0;
+  const size_t fixed2 = bb + (((size_t)f.par_cap * 4 + 15) & ~(size_t)15);
+  f.nbuf = (int)std::min<size_t>(3, per_cu == 2 ? (kLdsPerCu / 2 - fixed2) / chb
+                                                : (kLdsPerCu - fixed2) / chb);
+  f.lds_bytes = f.nbuf * chb + fixed2;
   return f;
 }
 
-FastPlan plan_fast(const wf_params& p) { return plan_token(p, true); }
+FastPlan plan_fast(const wf_params& p) {
+  return plan_token(p, p.levels, filtered_len(p), true, false);
+}
 
 bool rec_token_path(const wf_params& p) {
   return p.dtype == WF_BF16 && p.wavelet == WF_HAAR && p.levels >= 1 && p.levels <= 5 &&
          p.q_len <= 16 * kFastMaxQBlocks;
 }
 
-FastPlan plan_rec_token(const wf_params& p) { return plan_token(p, false); }
+FastPlan plan_rec_token(const wf_params& p, int b, long rows, bool gather) {
+  return plan_token(p, b, rows, false, gather);
+}
 
-template <int D, int J, bool LSE>
+template <int D, int J, bool LSE, bool GATHER = false>
 static hipError_t token_skim_launch(const TokenSkimArgs& a, size_t lds, hipStream_t s) {
-  auto kern = token_skim_kernel<D, J, LSE>;
+  auto kern = token_skim_kernel<D, J, LSE, GATHER>;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -555,6 +591,14 @@ static hipError_t token_skim_dispatch(int J, const TokenSkimArgs& a, size_t lds,
       case 5: return token_skim_launch<D, 5, true>(a, lds, s);
       default: return hipErrorInvalidValue;
     }
+  } else if (a.parent) {
+    switch (J) {
+      case 1: return token_skim_launch<D, 1, false, true>(a, lds, s);
+      case 2: return token_skim_launch<D, 2, false, true>(a, lds, s);
+      case 3: return token_skim_launch<D, 3, false, true>(a, lds, s);
+      case 4: return token_skim_launch<D, 4, false, true>(a, lds, s);
+      default: return hipErrorInvalidValue;
+    }
   } else {
     switch (J) {
       case 1: return token_skim_launch<D, 1, false>(a, lds, s);
@@ -567,23 +611,28 @@ static hipError_t token_skim_dispatch(int J, const TokenSkimArgs& a, size_t lds,
   }
 }
 
-static TokenSkimArgs token_args(const wf_params& p, const FastPlan& f, const void* Q,
-                                const void* K, float* out, float* wstats) {
-  TokenSkimArgs a;
+static TokenSkimArgs token_args(const wf_params& p, const FastPlan& f, int J, long rows,
+                                long nJ, const void* Q, const void* K, float* out,
+                                float* wstats) {
+  TokenSkimArgs a{};
   a.K = K;
   a.Q = Q;
   a.blocks = out;
   a.wstats = wstats;
   a.U = p.batch * p.heads;
-  a.L = (int)filtered_len(p);
+  a.L = (int)rows;
   a.Ls = p.ctx_len;
   a.B = p.q_len;
-  a.nJ = p.ctx_len >> p.levels;
+  a.nJ = (int)nJ;
   a.R = f.R;
   a.span = f.span;
   a.nbuf = f.nbuf;
   a.scale = effective_scale(p);
-  a.norm = (float)std::pow(2.0, -0.5 * p.levels);
+  a.norm = (float)std::pow(2.0, -0.5 * J);
+  a.parent = nullptr;
+  a.npar = 0;
+  a.pshift = J + 1;
+  a.par_cap = f.par_cap;
   return a;
 }
 
@@ -591,18 +640,24 @@ hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, f
                              float* wstats, hipStream_t s) {
   if (!fast_path(p)) return hipErrorInvalidValue;
   const FastPlan f = plan_fast(p);
-  const TokenSkimArgs a = token_args(p, f, Q, K, blocks, wstats);
+  const TokenSkimArgs a = token_args(p, f, p.levels, filtered_len(p), p.ctx_len >> p.levels, Q,
+                                     K, blocks, wstats);
   return p.head_dim == 128 ? token_skim_dispatch<128, true>(p.levels, a, f.lds_bytes, s)
                            : token_skim_dispatch<64, true>(p.levels, a, f.lds_bytes, s);
 }
 
-hipError_t launch_rec_token_skim(const wf_params& p, const void* Q, const void* K,
-                                 float* logits, float* stats, hipStream_t s) {
-  if (!rec_token_path(p)) return hipErrorInvalidValue;
-  const FastPlan f = plan_rec_token(p);
-  const TokenSkimArgs a = token_args(p, f, Q, K, logits, stats);
-  return p.head_dim == 128 ? token_skim_dispatch<128, false>(p.levels, a, f.lds_bytes, s)
-                           : token_skim_dispatch<64, false>(p.levels, a, f.lds_bytes, s);
+hipError_t launch_rec_token_skim(const wf_params& p, int b, long n, const int32_t* parent,
+                                 int npar, const void* Q, const void* K, float* logits,
+                                 float* stats, hipStream_t s) {
+  if (!rec_token_path(p) || b < 1 || b > 5) return hipErrorInvalidValue;
+  // rows: the filtered keys at the first scale, else the gathered kept blocks
+  const long rows = parent ? (long)npar << (b + 1) : filtered_len(p);
+  const FastPlan f = plan_rec_token(p, b, rows, parent != nullptr);
+  TokenSkimArgs a = token_args(p, f, b, rows, n, Q, K, logits, stats);
+  a.parent = parent;
+  a.npar = npar;
+  return p.head_dim == 128 ? token_skim_dispatch<128, false>(b, a, f.lds_bytes, s)
+                           : token_skim_dispatch<64, false>(b, a, f.lds_bytes, s);
 }
 
 hipError_t launch_fast_select(const wf_params& p, const float* blocks, const float* wstats,

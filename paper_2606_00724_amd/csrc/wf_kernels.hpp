@@ -113,7 +113,8 @@ struct TokenSkimArgs {
   const void* K;        // [U][L][D] bf16
   const void* Q;        // [U][B][D] bf16
   float* blocks;        // [U][nJ][2][B]: coarse logits, then log-sum-exps of
-                        // the block's token logits
+                        // the block's token logits; without the log-sum-exps
+                        // [U][B][nJ] coarse logits
   float* wstats;        // [U][R][2][B] coarse-logit max and sum of exp per range
   long Ls;              // rows per unit in K (L: the filtered rows)
   int U, L, B, nJ, R;
@@ -121,6 +122,12 @@ struct TokenSkimArgs {
   int nbuf;             // LDS ring depth
   float scale;          // logit scale
   float norm;           // 2^{-J/2}
+  // nullable: the rows are the gathered sequence of the kept blocks
+  // parent [U][npar] of 2^pshift tokens each (a refinement scale of the
+  // recursion); L then counts gathered rows
+  const int32_t* parent;
+  int npar, pshift;
+  int par_cap;          // parent ids staged in LDS per range
 };
 
 struct FastSelectArgs {

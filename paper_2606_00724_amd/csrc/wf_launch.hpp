@@ -49,6 +49,7 @@ struct FastPlan {
   int R;             // ranges (workgroups) per unit
   int span;          // tokens per range
   int nbuf;          // LDS ring depth
+  int par_cap;       // parent ids staged per range (gathered rows), else 0
   size_t lds_bytes;
 };
 
@@ -102,14 +103,17 @@ hipError_t launch_rec_tiles(const wf_params& p, int b, long n, const int32_t* pa
 hipError_t launch_rec_select(const wf_params& p, int b, long n, int keep,
                              const int32_t* parent, int npar, const float* logits,
                              const float* stats, float* W, int32_t* out, hipStream_t s);
-// The recursion's first scale (b = levels) from token logits: bf16 keys,
-// Haar, 1..5 levels, at most 64 query rows.  Writes the same coarse logits
-// as the tiles ([U][B][n]) and one (max, sum) slice per range; the select
-// then merges plan_rec_token(p).R slices.
+// A scale b <= 5 of the recursion from token logits (bf16 keys, Haar, at
+// most 64 query rows): over all filtered keys when parent is null (b =
+// levels), else over the gathered kept blocks parent [U][npar] of 2^(b+1)
+// tokens.  Writes the same n coarse logits per query row as the tiles
+// ([U][B][n]) and one (max, sum) slice per range; the select then merges
+// plan_rec_token(..).R slices.
 bool rec_token_path(const wf_params& p);
-FastPlan plan_rec_token(const wf_params& p);
-hipError_t launch_rec_token_skim(const wf_params& p, const void* Q, const void* K,
-                                 float* logits, float* stats, hipStream_t s);
+FastPlan plan_rec_token(const wf_params& p, int b, long rows, bool gather);
+hipError_t launch_rec_token_skim(const wf_params& p, int b, long n, const int32_t* parent,
+                                 int npar, const void* Q, const void* K, float* logits,
+                                 float* stats, hipStream_t s);
 hipError_t launch_rec_select_slices(const wf_params& p, int b, long n, int keep,
                                     const int32_t* parent, int npar, int nslices,
                                     const float* logits, const float* stats, float* W,

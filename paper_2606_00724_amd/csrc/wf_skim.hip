@@ -1205,9 +1205,11 @@ RecPlan plan_recursion(const wf_params& p, const int32_t* counts) {
   long n = (long)p.ctx_len >> p.levels;
   for (int b = p.levels; b >= 1; --b) {
     const int cpt = haar_cpt(b);
-    // the first scale's statistics come from the token skim's ranges
-    const int ntiles = b == p.levels && rec_token_path(p) ? plan_rec_token(p).R
-                                                          : (int)((n + cpt - 1) / cpt);
+    // with token logits the statistics come from the token skim's ranges
+    const int ntiles =
+        rec_token_path(p) && b <= 5
+            ? plan_rec_token(p, b, b == p.levels ? filtered_len(p) : n << b, b != p.levels).R
+            : (int)((n + cpt - 1) / cpt);
     r.max_n = std::max(r.max_n, n);
     r.max_tiles = std::max(r.max_tiles, ntiles);
     r.max_keep = std::max(r.max_keep, (long)counts[b - 1]);
