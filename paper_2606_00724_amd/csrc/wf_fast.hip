@@ -27,6 +27,8 @@
 #include "wf_kernels.hpp"
 #include "wf_launch.hpp"
 
+#include <mutex>
+
 namespace wf {
 
 // one running (max, sum of exp) pair absorbs another
@@ -345,6 +347,227 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
   }
 }
 
+// Daubechies-2 at J = 6 from token logits.  The level-6 approximation is one
+// banded filter of the keys (A[n] = sum_m f[m] K[64 n + m], 190 taps), so
+// the coarse logit is the same filter over token logits:
+//   l_n = P_0(n) + P_1(n + 1) + P_2(n + 2),  P_k(c) = sum_{o < 64} f[64 k + o] s_(64 c + o),
+// with s the raw products times the logit scale.  Every slice (32 tokens,
+// half a block) forms its three partials and its (max, sum of exp) on the
+// lanes of the 32x32 product; they wait in a three-chunk LDS ring until the
+// two blocks after theirs are in, and waves 4..7 then add the six partials of
+// a coefficient in a fixed order and store its block row (coarse logit, then
+// the block's log-sum-exp, as the Haar path).  A range reads one chunk past
+// its end (its last coefficients need the next two blocks), wrapped around
+// the unit for the periodic extension.  With the symmetric extension the
+// last three coefficients of the unit use the end filters E_m instead, from
+// their own partials of the last three blocks, which the range owning them
+// reads (its reads stop at the unit's end).
+template <int D>
+__global__ __launch_bounds__(kTokBlock, 2) void token_db2_kernel(TokenSkimArgs a, Db2TokenTaps tp,
+                                                                 int periodic) {
+  constexpr int NW = kTokBlock / kWave;  // 8
+  constexpr int NIW = NW / 2;            // loading waves
+  constexpr int CR = kScanChunk;         // tokens per chunk: two blocks
+  constexpr int G = D / 8;
+  constexpr int CHB = CR * 2 * D;
+  constexpr int IPW = CR * G / (64 * NIW);
+  constexpr int KS = D / 16;
+  static_assert(CR == 128, "two 64-token blocks per chunk");
+  const int B = a.B;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ring = smem;                                           // [nbuf][CHB]
+  float* part = reinterpret_cast<float*>(smem + (size_t)a.nbuf * CHB);  // [3][4][3][B]
+  float* sst = part + 36 * B;                                           // [3][4][2][B]
+  float* edg = sst + 24 * B;                                            // [6][2][B]
+  float* etap = edg + 12 * B;                                           // [6 << 6]
+  float* btap = etap + (6 << 6);                                        // [3 << 6]
+  float* red = reinterpret_cast<float*>(smem);  // [2B][2] once the ring is idle
+
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / a.R, r = item % a.R;
+  const long tb = (long)r * a.span;
+  const long te = min(tb + (long)a.span, (long)a.L);
+  const long L = a.L, nJ = a.nJ;
+  const long nb0 = tb >> 6, jend = te >> 6;  // coefficients of this range
+  // it owns some of the unit's last three coefficients (symmetric extension)
+  const bool sym_end = !periodic && jend > nJ - 3;
+  const int nch = (int)((te - tb + CR - 1) / CR);
+  // chunks through two blocks past the range (not past the unit with the
+  // symmetric extension, whose end coefficients take no rows beyond it)
+  const long xe = periodic ? te + CR : min(te + CR, L);
+  const int nch_ext = (int)((xe - tb + CR - 1) / CR);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ts = wave & 3, qt = wave >> 2, h = ts & 1;
+  const bool loader = qt == 0;
+  const int hi = lane >> 5, col = lane & 31;
+  const int q = 32 * qt + col;
+  const bool live = 32 * qt < B;
+
+  const bf16_t* qrow = reinterpret_cast<const bf16_t*>(a.Q) + ((long)u * B + min(q, B - 1)) * D;
+  u32x4 qreg[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) qreg[s] = *reinterpret_cast<const u32x4*>(qrow + 16 * s + 8 * hi);
+  for (int i = threadIdx.x; i < (6 << 6); i += kTokBlock) etap[i] = tp.edge[i];
+  for (int i = threadIdx.x; i < (3 << 6); i += kTokBlock) btap[i] = tp.band[i];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qreg[s]));
+  // the lane's 16 tokens sit at offsets 32 h + 8 g + 4 hi + i (g, i < 4) of
+  // their block: taps k of group g are one 16-byte LDS read
+  const float* lane_taps = btap + 32 * h + 4 * hi;
+
+  // row r of the chunk at c0: token c0 + r, past the unit wrapped (periodic)
+  // or the last row (symmetric: those rows feed no kept coefficient)
+  struct Rows {
+    const bf16_t* Kunit;
+    long c0, L;
+    int periodic;
+    __device__ __forceinline__ const bf16_t* operator()(int r) const {
+      const long p = c0 + r;
+      return Kunit + (p < L ? p : (periodic ? p - L : L - 1)) * D;
+    }
+  } rows{reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D, tb, L, periodic};
+  const uint32_t ring_lds = lds_offset(ring);
+  const int nbuf = a.nbuf;
+  if (loader) {
+    for (int k = 0; k < nch_ext && k < nbuf - 1; ++k) {
+      rows.c0 = tb + (long)k * CR;
+      issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(k * CHB), rows);
+    }
+  }
+  const float c2 = a.scale * kLog2e;
+  float* out = a.blocks + (long)u * nJ * 2 * B;  // [nJ][2][B]
+  // waves 4..7: thread (ci, cq) completes coefficient 2 c + ci of chunk c
+  const int t2 = threadIdx.x - NIW * 64;
+  const int ci = t2 / B, cq = t2 - ci * B;
+  const bool comb = t2 >= 0 && t2 < 2 * B;
+  float cm = -INFINITY, cz = 0.f;  // running max / sum of exp of the coarse logits
+  auto combine = [&](int c) {
+    const long n = nb0 + 2L * c + ci;
+    if (n >= jend) return;
+    float s;
+    if (sym_end && n >= nJ - 3) {
+      const int m = (int)(nJ - 1 - n);
+      const float* ep = edg + (m * (m + 1)) * B + cq;  // (m (m + 1) / 2) * 2 B
+      s = 0.f;
+      for (int k = 0; k <= m; ++k) s += ep[2 * k * B] + ep[(2 * k + 1) * B];
+    } else {
+      // slots of chunks c and c + 1: [4 slices][3 partials][B]
+      const float* p0 = part + (c % 3) * 12 * B + cq;
+      const float* p1 = part + ((c + 1) % 3) * 12 * B + cq;
+      const float* pb = ci == 0 ? p0 + 6 * B : p1;  // block n + 1: slices 2, 3 of c or 0, 1 of c + 1
+      s = p0[(6 * ci) * B] + p0[(6 * ci + 3) * B];
+      s += pb[B] + pb[4 * B];
+      s += p1[(6 * ci + 2) * B] + p1[(6 * ci + 5) * B];
+    }
+    const float l = s * a.scale;
+    // the block's log-sum-exp from its two slices (raw maxima: positive scale)
+    const float* st = sst + ((c % 3) * 8 + 4 * ci) * B + cq;
+    const float m0 = st[0], e0 = st[B], m1 = st[2 * B], e1 = st[3 * B];
+    const float mx = fmaxf(m0, m1);
+    const float e = e0 * __builtin_amdgcn_exp2f((m0 - mx) * c2) + e1 * __builtin_amdgcn_exp2f((m1 - mx) * c2);
+    float* o = out + n * 2 * B + cq;
+    o[0] = l;
+    o[B] = fmaf(mx, a.scale, __logf(e));
+    stat_add(cm, cz, l);
+  };
+
+  // one wave's slice of chunk ch: its partials and statistics into LDS
+  auto slice_step = [&](int ch) {
+    const unsigned char* buf = ring + (ch % nbuf) * CHB;
+    const int row = 32 * ts + col;
+    f32x16 acc = {};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const u32x4 ka = *reinterpret_cast<const u32x4*>(buf + granule_offset<G>(row, 2 * s + hi));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
+                                                    __builtin_bit_cast(bf16x8, qreg[s]), acc, 0, 0, 0);
+    }
+    float mx = acc[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, acc[v]);
+    mx = max_xor32(mx);
+    const float off = -mx * c2;
+    float e = 0.f, p0 = 0.f, p1 = 0.f, p2 = 0.f;
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const f32x4 t0 = *reinterpret_cast<const f32x4*>(lane_taps + 8 * g4);
+      const f32x4 t1 = *reinterpret_cast<const f32x4*>(lane_taps + 64 + 8 * g4);
+      const f32x4 t2 = *reinterpret_cast<const f32x4*>(lane_taps + 128 + 8 * g4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float x = acc[4 * g4 + i];
+        e += __builtin_amdgcn_exp2f(fmaf(x, c2, off));
+        p0 = fmaf(t0[i], x, p0);
+        p1 = fmaf(t1[i], x, p1);
+        p2 = fmaf(t2[i], x, p2);
+      }
+    }
+    e = add_xor32(e);
+    p0 = add_xor32(p0);
+    p1 = add_xor32(p1);
+    p2 = add_xor32(p2);
+    const int slot = ch % 3;
+    if (hi == 0 && q < B) {
+      float* pp = part + ((slot * 4 + ts) * 3) * B + q;
+      pp[0] = p0;
+      pp[B] = p1;
+      pp[2 * B] = p2;
+      float* sp = sst + ((slot * 4 + ts) * 2) * B + q;
+      sp[0] = mx;
+      sp[B] = e;
+    }
+    if (sym_end) {
+      // end-filter partials of the unit's last three blocks
+      const long cg = (tb + (long)ch * CR + 32 * ts) >> 6;
+      if (cg >= nJ - 3 && cg < nJ) {
+#pragma unroll 1
+        for (int m = 0; m < 3; ++m) {
+          const int k = (int)(cg - (nJ - 1 - m));
+          if (k < 0 || k > m) continue;  // uniform
+          const float* et = etap + 64 * (m * (m + 1) / 2 + k) + 32 * h + 4 * hi;
+          float x = 0.f;
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const f32x4 t = *reinterpret_cast<const f32x4*>(et + 8 * g4);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x = fmaf(t[i], acc[4 * g4 + i], x);
+          }
+          x = add_xor32(x);
+          if (hi == 0 && q < B) edg[((m * (m + 1) / 2 + k) * 2 + h) * B + q] = x;
+        }
+      }
+    }
+  };
+
+  for (int ch = 0; ch < nch_ext + 2; ++ch) {
+    if (loader && ch < nch_ext) wait_vmcnt_chunks<IPW>(min(nch_ext - 1 - ch, nbuf - 2));
+    lds_barrier();  // chunk ch in the ring; chunk ch - 1's partials in LDS
+    if (loader) {
+      if (ch + nbuf - 1 < nch_ext) {
+        rows.c0 = tb + (long)(ch + nbuf - 1) * CR;
+        issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rows);
+      }
+    }
+    if (ch < nch_ext && live) slice_step(ch);
+    if (comb && ch >= 2) combine(ch - 2);
+  }
+
+  // the range's (max, sum of exp) per query from the combining threads
+  __syncthreads();
+  if (comb) {
+    red[2 * t2] = cm;
+    red[2 * t2 + 1] = cz;
+  }
+  __syncthreads();
+  float* ws = a.wstats + ((long)u * a.R + r) * 2 * B;
+  for (int qq = threadIdx.x; qq < B; qq += kTokBlock) {
+    float m_ = red[2 * qq], z_ = red[2 * qq + 1];
+    stat_absorb(m_, z_, red[2 * (B + qq)], red[2 * (B + qq) + 1]);
+    ws[qq] = m_;
+    ws[B + qq] = z_;
+  }
+}
+
 // One workgroup per unit: the coarse softmax normalisers (merged over the
 // ranges), W (eq. 8), the top-S regions (eq. 9), then the scan's pool
 // normalisers from the selected blocks' token statistics.
@@ -504,12 +727,22 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
 
 // ------------------------------------------------------------ host side
 
+bool db2_token_path(const wf_params& p) {
+  return p.dtype == WF_BF16 && p.wavelet == WF_DB2 && p.levels == 6 &&
+         (p.ctx_len >> 6) >= 4 && p.q_len <= 16 * kFastMaxQBlocks && effective_scale(p) > 0.f;
+}
+
 bool fast_path(const wf_params& p) {
   // a positive scale keeps the block maximum of the raw products the maximum
   // of the scaled logits
-  return p.dtype == WF_BF16 && p.wavelet == WF_HAAR && p.levels >= 3 && p.levels <= 5 &&
-         p.q_len <= 16 * kFastMaxQBlocks && effective_scale(p) > 0.f;
+  return (p.dtype == WF_BF16 && p.wavelet == WF_HAAR && p.levels >= 3 && p.levels <= 5 &&
+          p.q_len <= 16 * kFastMaxQBlocks && effective_scale(p) > 0.f) ||
+         db2_token_path(p);
 }
+
+// LDS of the db2 token skim besides its ring: the partial and statistic
+// rings, the end-filter partials and taps
+static size_t db2_fixed_lds(int B) { return ((size_t)72 * B + (9 << 6)) * sizeof(float); }
 
 template <bool LSE>
 static size_t token_batch_bytes_at(int J, int B) {
@@ -530,9 +763,11 @@ static FastPlan plan_token(const wf_params& p, int J, long Lf, bool lse, bool ga
   const long U = (long)p.batch * p.heads;
   const long chunks = (Lf + kScanChunk - 1) / kScanChunk;
   const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
-  // two batch slots of block results; the wave reduction pairs reuse the ring
-  const size_t bb = 2 * (lse ? token_batch_bytes_at<true>(J, p.q_len)
-                             : token_batch_bytes_at<false>(J, p.q_len));
+  // two batch slots of block results (the db2 skim: its partial rings); the
+  // wave reduction pairs reuse the ring
+  const size_t bb = db2_token_path(p) ? db2_fixed_lds(p.q_len)
+                    : 2 * (lse ? token_batch_bytes_at<true>(J, p.q_len)
+                               : token_batch_bytes_at<false>(J, p.q_len));
   // Two resident workgroups per CU, each two chunks deep, stream faster than
   // one three deep (the barrier of one overlaps the other's loads); that
   // shape is taken whenever two fit in the CU's LDS.
@@ -542,7 +777,9 @@ static FastPlan plan_token(const wf_params& p, int J, long Lf, bool lse, bool ga
   const size_t ids = gather ? (size_t)(((cpr0 * kScanChunk) >> (J + 1)) + 2) * 4 : 0;
   const size_t fixed = bb + ((ids + 15) & ~(size_t)15);
   const size_t fit2 = kLdsPerCu / 2 > fixed ? (kLdsPerCu / 2 - fixed) / chb : 0;
-  const int per_cu = fit2 >= 2 && token_skim_waves_per_simd(p.head_dim, J, lse) >= 4 ? 2 : 1;
+  // (the db2 skim needs more than 128 registers a lane: one workgroup per CU)
+  const int per_cu = fit2 >= 2 && !db2_token_path(p) &&
+                     token_skim_waves_per_simd(p.head_dim, J, lse) >= 4 ? 2 : 1;
   const long want = std::max(1L, ((long)per_cu * device_cu_count() + U - 1) / U);
   const long R = std::min(chunks, want);
   const long cpr = (chunks + R - 1) / R;
@@ -636,10 +873,37 @@ static TokenSkimArgs token_args(const wf_params& p, const FastPlan& f, int J, lo
   return a;
 }
 
+template <int D>
+static hipError_t token_db2_launch(const TokenSkimArgs& a, const Db2TokenTaps& t, int periodic,
+                                   size_t lds, hipStream_t s) {
+  auto kern = token_db2_kernel<D>;
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)(a.U * a.R)), dim3(kTokBlock), lds, s, a, t, periodic);
+  return hipGetLastError();
+}
+
+static const Db2TokenTaps& db2_taps6() {
+  static Db2TokenTaps t;
+  static std::once_flag once;
+  std::call_once(once, [] { db2_token_taps(6, &t); });
+  return t;
+}
+
 hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, float* blocks,
                              float* wstats, hipStream_t s) {
   if (!fast_path(p)) return hipErrorInvalidValue;
   const FastPlan f = plan_fast(p);
+  if (db2_token_path(p)) {
+    const TokenSkimArgs a = token_args(p, f, 6, filtered_len(p), p.ctx_len >> 6, Q, K, blocks,
+                                       wstats);
+    const int periodic = p.boundary == WF_EXT_PERIODIC ? 1 : 0;
+    return p.head_dim == 128 ? token_db2_launch<128>(a, db2_taps6(), periodic, f.lds_bytes, s)
+                             : token_db2_launch<64>(a, db2_taps6(), periodic, f.lds_bytes, s);
+  }
   const TokenSkimArgs a = token_args(p, f, p.levels, filtered_len(p), p.ctx_len >> p.levels, Q,
                                      K, blocks, wstats);
   return p.head_dim == 128 ? token_skim_dispatch<128, true>(p.levels, a, f.lds_bytes, s)

@@ -130,6 +130,14 @@ struct TokenSkimArgs {
   int par_cap;          // parent ids staged in LDS per range
 };
 
+// Daubechies-2 at J = 6 for the token-level skim: the level-6 low-pass filter
+// f_6 (190 taps, zero-padded) and the three symmetric-end filters E_0 | E_1
+// | E_2 (64, 128 and 192 taps).
+struct Db2TokenTaps {
+  float band[3 << 6];
+  float edge[6 << 6];
+};
+
 struct FastSelectArgs {
   const float* blocks;  // [U][nJ][2][B]
   const float* wstats;  // [U][R][2][B]

@@ -79,6 +79,10 @@ AttnPlan plan_attn(const wf_params& p, long nrows);
 // are bf16, the wavelet is Haar with 3..5 levels and the query block has at
 // most 64 rows; the scan then needs only its weights pass.
 bool fast_path(const wf_params& p);
+// The Daubechies-2 form of that path (J = 6, at least 4 coefficients).
+bool db2_token_path(const wf_params& p);
+// f_J (J <= 6) and the symmetric-end filters, computed in double.
+void db2_token_taps(int J, Db2TokenTaps* out);
 FastPlan plan_fast(const wf_params& p);
 hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K,
                              float* blocks, float* wstats, hipStream_t s);

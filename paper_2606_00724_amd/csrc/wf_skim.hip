@@ -980,6 +980,25 @@ static const EdgeTaps& symmetric_edge_filters(int J) {
   return table[J];
 }
 
+void db2_token_taps(int J, Db2TokenTaps* out) {
+  const double r2 = std::sqrt(2.0), r3 = std::sqrt(3.0), den = 4.0 * r2;
+  const double g[4] = {(1 + r3) / den, (3 + r3) / den, (3 - r3) / den, (1 - r3) / den};
+  // f_1 = g, f_{j+1}[s] = sum_k g_k f_j[s - 2^j k]
+  std::vector<double> f(g, g + 4);
+  for (int j = 1; j < J; ++j) {
+    std::vector<double> nf(f.size() + 3 * ((size_t)1 << j), 0.0);
+    for (size_t s = 0; s < nf.size(); ++s)
+      for (int k = 0; k < 4; ++k) {
+        const long i = (long)s - ((long)k << j);
+        if (i >= 0 && i < (long)f.size()) nf[s] += g[k] * f[i];
+      }
+    f.swap(nf);
+  }
+  for (int i = 0; i < (3 << 6); ++i) out->band[i] = i < (int)f.size() ? (float)f[i] : 0.f;
+  const EdgeTaps& e = symmetric_edge_filters(J);
+  for (int i = 0; i < (6 << 6); ++i) out->edge[i] = e.e[i];
+}
+
 template <int M, typename T>
 static hipError_t dwt_dispatch(const DwtArgs& a, const Taps& taps, dim3 grid,
                                hipStream_t s) {

@@ -132,6 +132,9 @@ def test_budget_and_workspace_arithmetic(wfpkg):
     (dict(dtype="bf16", levels=6), "general"),             # blocks > 32 tokens
     (dict(dtype="bf16", q_len=65), "general"),             # > 64 query rows
     (dict(dtype="bf16", wavelet="db2"), "general"),
+    (dict(dtype="bf16", wavelet="db2", levels=6, segments=4), "token"),   # db2 band over token logits
+    (dict(dtype="bf16", wavelet="db2", levels=6, segments=2, ctx_len=192), "general"),  # 3 coefficients
+    (dict(dtype="bf16", wavelet="db2", levels=7, segments=2), "general"),
 ])
 def test_fused_kernel_sequence_follows_the_path(wfpkg, change, path):
     p = _params(wfpkg, **change)

@@ -99,6 +99,23 @@ EDGE = {
     "tok_j5_b64_long": V_("tj5l", batch=2, heads=8, ctx_len=32 * 1001,
                           head_dim=128, levels=5, segments=64, budget=700,
                           q_len=64, **_BF),
+    # db2 at J = 6 from token logits: ranges of one chunk (two blocks), an
+    # odd coefficient count (the last range holds one block), the fewest
+    # coefficients the path takes (4), both extensions, 64 query rows,
+    # d = 64 with a non-dyadic length
+    "db2tok_sym_odd": V_("d2so", ctx_len=64 * 13, head_dim=128, levels=6,
+                         segments=4, budget=100, wavelet="db2", **_BF),
+    "db2tok_per_b64": V_("d2pb", ctx_len=64 * 40, head_dim=128, levels=6,
+                         segments=6, budget=200, q_len=64, wavelet="db2",
+                         boundary="periodic", **_BF),
+    "db2tok_sym_four": V_("d2s4", ctx_len=256, head_dim=128, levels=6,
+                          segments=2, budget=64, wavelet="db2", **_BF),
+    "db2tok_per_four": V_("d2p4", ctx_len=256, head_dim=128, levels=6,
+                          segments=2, budget=64, wavelet="db2",
+                          boundary="periodic", **_BF),
+    "db2tok_sym_d64_rem": V_("d2sr", ctx_len=64 * 37 + 5, levels=6, segments=5,
+                             budget=150, q_len=48, wavelet="db2", gen_len=8,
+                             **_BF),
 }
 
 FULL = ["tiny", "layer8b", "long16k", "headline32k", "stress128k", "tail32k"]
