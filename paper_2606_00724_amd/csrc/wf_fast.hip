@@ -1,5 +1,6 @@
-// Token-level skim for bf16 keys with the Haar wavelet at 3..5 levels and a
-// query block of at most 64 rows.
+// Token-level skim for bf16 keys and a query block of at most 64 rows: the
+// Haar wavelet at 3..5 levels (token_skim_kernel) and Daubechies-2 at 6
+// levels (token_db2_kernel, further below).
 //
 // The Haar approximation of block j at level J is 2^{-J/2} times the sum of
 // its 2^J keys (eq. 5 with the Haar filter, applied J times), and the skim
@@ -16,10 +17,11 @@
 //   M_q = max_{j in seg} e_qj,   Z_q = sum_{j in seg} exp(e_qj - M_q),
 // with M_q at or above every pool logit of query q.
 //
-// The same kernel without the log-sum-exps serves the first scale of the
-// multi-scale recursion (Alg. 1 at b = B, 1..5 levels): it writes only the
-// coarse logits, query-major ([U][B][nJ], the layout of the coefficient
-// tiles), and the per-range statistics.
+// The same kernel without the log-sum-exps serves the scales b <= 5 of the
+// multi-scale recursion (Alg. 1): it writes only the coarse logits,
+// query-major ([U][B][nJ], the layout of the coefficient tiles), and the
+// per-range statistics, over all keys at the first scale and over the
+// gathered kept blocks below it.
 //
 // The keys stream through an LDS ring filled by direct global->LDS loads;
 // see token_skim_kernel for the roles of its waves.
