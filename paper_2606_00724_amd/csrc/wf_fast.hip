@@ -616,50 +616,85 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
     if (part == 0 && q < B) row_c[q] = fmaf(mx, kLog2e, __log2f(z));
   }
   __syncthreads();
-  // W_j = sum_q softmax_j(l_q.): four threads per block j, queries
-  // q0 .. q0 + 15 each; a thread's q0 is the same for all its blocks, so its
-  // normalisers stay in registers (2^-inf = 0 for queries past B)
   const float* lg = a.blocks + (long)u * nJ * 2 * B;  // row j: logits at 2 j B
   float* W = a.W + (long)u * nJ;
-  const bool vec = (B & 3) == 0;
-  const int q0 = 16 * (threadIdx.x & 3);
-  const int nq = min(16, B - q0);
-  float cq[16];
+  if (B > 32 && (B & 3) == 0) {
+    // W_j = sum_q softmax_j(l_q.): a 16-lane row per block j, lane i holding
+    // queries 4 i .. 4 i + 3, so that a wave's loads cover whole rows; the
+    // lanes' sums meet by DPP rotations (2^-inf = 0 for queries past B)
+    const int l16 = threadIdx.x & 15, grp = threadIdx.x >> 4;
+    const bool qok = 4 * l16 < B;
+    float cq[4];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) cq[k] = k < nq ? row_c[q0 + k] : INFINITY;
-  constexpr int UNR = 4;  // rows of blocks whose loads are in flight together
-  for (int base = 0; base < 4 * nJ; base += UNR * NT) {
-    float x[UNR][16];
+    for (int e = 0; e < 4; ++e) cq[e] = qok ? row_c[4 * l16 + e] : INFINITY;
+    constexpr int G16 = NT / 16;  // blocks per round
+    constexpr int RPT = 8;        // rounds whose loads are in flight together
+    for (int j0 = 0; j0 < nJ; j0 += RPT * G16) {
+      float4 x[RPT];
 #pragma unroll
-    for (int r = 0; r < UNR; ++r) {
-      const int t = base + r * NT + threadIdx.x;
-      const bool ok = t < 4 * nJ && nq > 0;
-      const float* row = lg + (long)(t >> 2) * 2 * B + q0;
-      if (vec) {
+      for (int r = 0; r < RPT; ++r) {
+        const int j = j0 + r * G16 + grp;
+        x[r] = qok && j < nJ ? *reinterpret_cast<const float4*>(lg + (long)j * 2 * B + 4 * l16)
+                             : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      }
 #pragma unroll
-        for (int k4 = 0; k4 < 4; ++k4) {
-          const float4 f = ok && 4 * k4 < nq ? reinterpret_cast<const float4*>(row)[k4]
-                                              : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-          x[r][4 * k4] = f.x;
-          x[r][4 * k4 + 1] = f.y;
-          x[r][4 * k4 + 2] = f.z;
-          x[r][4 * k4 + 3] = f.w;
+      for (int r = 0; r < RPT; ++r) {
+        const int j = j0 + r * G16 + grp;
+        float w = __builtin_amdgcn_exp2f(fmaf(x[r].x, kLog2e, -cq[0])) +
+                  __builtin_amdgcn_exp2f(fmaf(x[r].y, kLog2e, -cq[1])) +
+                  __builtin_amdgcn_exp2f(fmaf(x[r].z, kLog2e, -cq[2])) +
+                  __builtin_amdgcn_exp2f(fmaf(x[r].w, kLog2e, -cq[3]));
+        w = wave_sum16(w);
+        if (l16 == 0 && j < nJ) {
+          W[j] = w;
+          if (w_in_lds) wsh[j] = w;
         }
-      } else {
-#pragma unroll
-        for (int k = 0; k < 16; ++k) x[r][k] = ok && k < nq ? row[k] : -INFINITY;
       }
     }
+  } else {
+    // W_j = sum_q softmax_j(l_q.): four threads per block j, queries
+    // q0 .. q0 + 15 each; a thread's q0 is the same for all its blocks, so its
+    // normalisers stay in registers (2^-inf = 0 for queries past B)
+    const bool vec = (B & 3) == 0;
+    const int q0 = 16 * (threadIdx.x & 3);
+    const int nq = min(16, B - q0);
+    float cq[16];
 #pragma unroll
-    for (int r = 0; r < UNR; ++r) {
-      const int t = base + r * NT + threadIdx.x;
-      float w = 0.f;
+    for (int k = 0; k < 16; ++k) cq[k] = k < nq ? row_c[q0 + k] : INFINITY;
+    constexpr int UNR = 4;  // rows of blocks whose loads are in flight together
+    for (int base = 0; base < 4 * nJ; base += UNR * NT) {
+      float x[UNR][16];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) w += __builtin_amdgcn_exp2f(fmaf(x[r][k], kLog2e, -cq[k]));
-      w = add_xor2(add_xor1(w));
-      if (t < 4 * nJ && (t & 3) == 0) {
-        W[t >> 2] = w;
-        if (w_in_lds) wsh[t >> 2] = w;
+      for (int r = 0; r < UNR; ++r) {
+        const int t = base + r * NT + threadIdx.x;
+        const bool ok = t < 4 * nJ && nq > 0;
+        const float* row = lg + (long)(t >> 2) * 2 * B + q0;
+        if (vec) {
+#pragma unroll
+          for (int k4 = 0; k4 < 4; ++k4) {
+            const float4 f = ok && 4 * k4 < nq ? reinterpret_cast<const float4*>(row)[k4]
+                                                : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+            x[r][4 * k4] = f.x;
+            x[r][4 * k4 + 1] = f.y;
+            x[r][4 * k4 + 2] = f.z;
+            x[r][4 * k4 + 3] = f.w;
+          }
+        } else {
+#pragma unroll
+          for (int k = 0; k < 16; ++k) x[r][k] = ok && k < nq ? row[k] : -INFINITY;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < UNR; ++r) {
+        const int t = base + r * NT + threadIdx.x;
+        float w = 0.f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) w += __builtin_amdgcn_exp2f(fmaf(x[r][k], kLog2e, -cq[k]));
+        w = add_xor2(add_xor1(w));
+        if (t < 4 * nJ && (t & 3) == 0) {
+          W[t >> 2] = w;
+          if (w_in_lds) wsh[t >> 2] = w;
+        }
       }
     }
   }
