@@ -297,16 +297,22 @@ def test_keep_all_equals_dense_attention(wf):
         assert np.abs(f64(unit(O, w, u)) - dense).max() <= O_TOL[w.dtype]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_constant_keys_pick_lowest_indices(wf, dtype):
+@pytest.mark.parametrize("dtype,shape", [
+    ("f32", dict(ctx_len=512, levels=3, segments=6, budget=20)),
+    ("bf16", dict(ctx_len=512, levels=3, segments=6, budget=20)),
+    # many tied scores per wave and several compaction rounds
+    ("bf16", dict(ctx_len=16384, levels=5, segments=100, budget=1500, head_dim=128)),
+])
+def test_constant_keys_pick_lowest_indices(wf, dtype, shape):
     """Every score ties: regions 0..S-1 and the first k_eff pool tokens, exactly."""
-    w = V_("const", ctx_len=512, levels=3, segments=6, budget=20, dtype=dtype)
+    w = V_("const", dtype=dtype, **shape)
     Q, K, V, _, _ = inputs(w)
     K = torch.full_like(K, 0.375)
     O, tok, seg = run_fused(wf, w, Q, K, V, None, None)
+    S, k = shape["segments"], shape["budget"]
     for u in range(w.units):
-        assert unit(seg, w, u).tolist() == list(range(6))
-        assert unit(tok, w, u).tolist() == list(range(20))
+        assert unit(seg, w, u).tolist() == list(range(S))
+        assert unit(tok, w, u).tolist() == list(range(k))
     out = run_staged(wf, w, Q, K, V, None, None)
     assert torch.equal(out["seg"], seg) and torch.equal(out["tok"], tok)
 
