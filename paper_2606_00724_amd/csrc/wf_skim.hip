@@ -806,10 +806,88 @@ __global__ __launch_bounds__(kBlock) void haar_approx_kernel(DwtArgs a, float in
 
 // One workgroup per unit: merge the tiles' row statistics, form W (eq. 8) and
 // select the top-S regions (eq. 9).
+// W_j (eq. 8) of unit u for the columns 4 j4 .. 4 j4 + 3, j4 in [j4_lo,
+// j4_hi) (nJ a multiple of 4), from the query-major logits and the row
+// normalisers c_q = M_q log2(e) + log2(Z_q); also into wsh when given.
+template <int NT>
+__device__ void skim_w_columns(const SkimSelectArgs& a, int u, const float* row_c, int j4_lo,
+                               int j4_hi, float* wsh) {
+  const float* lg = a.logits + (long)u * a.B * a.nJ;
+  float* W = a.W + (long)u * a.nJ;
+  // four adjacent columns per thread, 16 query rows of loads in flight
+  constexpr int QB = 16;
+  for (int j4 = j4_lo + (int)threadIdx.x; j4 < j4_hi; j4 += NT) {
+    float w[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int q0 = 0; q0 < a.B; q0 += QB) {
+      float4 v[QB];
+#pragma unroll
+      for (int i = 0; i < QB; ++i)
+        v[i] = q0 + i < a.B ? *reinterpret_cast<const float4*>(lg + (long)(q0 + i) * a.nJ + 4 * j4)
+                            : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int i = 0; i < QB; ++i) {
+        if (q0 + i < a.B) {
+          const float c = row_c[q0 + i];
+          w[0] += __builtin_amdgcn_exp2f(fmaf(v[i].x, kLog2e, -c));
+          w[1] += __builtin_amdgcn_exp2f(fmaf(v[i].y, kLog2e, -c));
+          w[2] += __builtin_amdgcn_exp2f(fmaf(v[i].z, kLog2e, -c));
+          w[3] += __builtin_amdgcn_exp2f(fmaf(v[i].w, kLog2e, -c));
+        }
+      }
+    }
+    *reinterpret_cast<float4*>(W + 4 * j4) = make_float4(w[0], w[1], w[2], w[3]);
+    if (wsh) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) wsh[4 * j4 + e] = w[e];
+    }
+  }
+}
+
+// W of a wide candidate set spread over `parts` workgroups per unit (the
+// loads of one workgroup per unit would leave most CUs idle): every
+// workgroup merges the unit's (max, sum) slices itself, four parts of 64
+// query rows folded in sequence, then forms W for its share of the columns.
+__global__ __launch_bounds__(kBlock) void skim_weights_kernel(SkimSelectArgs a, int parts) {
+  __shared__ float row_c[WF_MAX_Q_LEN];
+  __shared__ float pm[4][64], pz[4][64];
+  const int u = blockIdx.x / parts, part = blockIdx.x % parts;
+  const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
+  for (int qc = 0; qc < a.B; qc += 64) {
+    const int q = qc + (threadIdx.x & 63), pp = threadIdx.x >> 6;
+    float m = -INFINITY, z = 0.f;
+    if (q < a.B) {
+      constexpr int BATCH = 8;
+      for (int t0 = pp; t0 < a.ntiles; t0 += 4 * BATCH) {
+        float tm[BATCH], tz[BATCH];
+#pragma unroll
+        for (int k = 0; k < BATCH; ++k) {
+          const int t = t0 + 4 * k;
+          tm[k] = t < a.ntiles ? st[(long)t * 2 * a.B + q] : -INFINITY;
+          tz[k] = t < a.ntiles ? st[(long)t * 2 * a.B + a.B + q] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < BATCH; ++k) pair_merge(m, z, tm[k], tz[k]);
+      }
+    }
+    pm[pp][threadIdx.x & 63] = m;
+    pz[pp][threadIdx.x & 63] = z;
+    __syncthreads();
+    if (threadIdx.x < 64 && q < a.B) {
+      float mm = pm[0][threadIdx.x], zz = pz[0][threadIdx.x];
+#pragma unroll
+      for (int k = 1; k < 4; ++k) pair_merge(mm, zz, pm[k][threadIdx.x], pz[k][threadIdx.x]);
+      row_c[q] = fmaf(mm, kLog2e, __log2f(zz));
+    }
+    __syncthreads();
+  }
+  const int n4 = a.nJ / 4, per = (n4 + parts - 1) / parts;
+  skim_w_columns<kBlock>(a, u, row_c, part * per, min(n4, (part + 1) * per), nullptr);
+}
+
 constexpr int kSelectBlock = 1024;
 
 __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArgs a,
-                                                                   int w_in_lds) {
+                                                                   int w_in_lds, int w_ready) {
   constexpr int NT = kSelectBlock;
   __shared__ float row_c[WF_MAX_Q_LEN];  // per query: M log2(e) + log2(Z)
   __shared__ float pm[16][65], pz[16][65];
@@ -817,87 +895,67 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
   extern __shared__ float wsh[];
   const int u = blockIdx.x;
   const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
-  // merge the tiles' (max, sum of exp) pairs, 64 queries at a time: thread
-  // (part, q) = (tid / 64, tid % 64) folds tiles part, part + 16, ...; the 16
-  // pairs of a query meet in a 16-lane row and are merged by rotations
-  for (int qc = 0; qc < a.B; qc += 64) {
-    {
-      const int q = qc + (threadIdx.x & 63), part = threadIdx.x >> 6;
-      float m = -INFINITY, z = 0.f;
-      if (q < a.B) {
-        constexpr int BATCH = 8;
-        for (int t0 = part; t0 < a.ntiles; t0 += 16 * BATCH) {
-          float tm[BATCH], tz[BATCH];
-#pragma unroll
-          for (int k = 0; k < BATCH; ++k) {
-            const int t = t0 + 16 * k;
-            tm[k] = t < a.ntiles ? st[(long)t * 2 * a.B + q] : -INFINITY;
-            tz[k] = t < a.ntiles ? st[(long)t * 2 * a.B + a.B + q] : 0.f;
-          }
-#pragma unroll
-          for (int k = 0; k < BATCH; ++k) pair_merge(m, z, tm[k], tz[k]);
-        }
-      }
-      pm[part][threadIdx.x & 63] = m;
-      pz[part][threadIdx.x & 63] = z;
-    }
-    __syncthreads();
-    {
-      const int ql = threadIdx.x >> 4, part = threadIdx.x & 15;
-      float m = pm[part][ql], z = pz[part][ql];
-      row16_merge<8>(m, z);
-      row16_merge<4>(m, z);
-      row16_merge<2>(m, z);
-      row16_merge<1>(m, z);
-      // exp(l - M) / Z = 2^(l log2(e) - c)
-      if (part == 0 && qc + ql < a.B) row_c[qc + ql] = fmaf(m, kLog2e, __log2f(z));
-    }
-    __syncthreads();
-  }
-  const float* lg = a.logits + (long)u * a.B * a.nJ;
   float* W = a.W + (long)u * a.nJ;
-  if ((a.nJ & 3) == 0) {
-    // four adjacent columns per thread, 16 query rows of loads in flight
-    constexpr int QB = 16;
-    for (int j4 = threadIdx.x; j4 < a.nJ / 4; j4 += NT) {
-      float w[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int q0 = 0; q0 < a.B; q0 += QB) {
-        float4 v[QB];
+  if (w_ready) {
+    // W was formed by skim_weights_kernel
+    if (w_in_lds)
+      for (int j = threadIdx.x; j < a.nJ; j += NT) wsh[j] = W[j];
+  } else {
+    // merge the tiles' (max, sum of exp) pairs, 64 queries at a time: thread
+    // (part, q) = (tid / 64, tid % 64) folds tiles part, part + 16, ...; the 16
+    // pairs of a query meet in a 16-lane row and are merged by rotations
+    for (int qc = 0; qc < a.B; qc += 64) {
+      {
+        const int q = qc + (threadIdx.x & 63), part = threadIdx.x >> 6;
+        float m = -INFINITY, z = 0.f;
+        if (q < a.B) {
+          constexpr int BATCH = 8;
+          for (int t0 = part; t0 < a.ntiles; t0 += 16 * BATCH) {
+            float tm[BATCH], tz[BATCH];
 #pragma unroll
-        for (int i = 0; i < QB; ++i)
-          v[i] = q0 + i < a.B ? *reinterpret_cast<const float4*>(lg + (long)(q0 + i) * a.nJ + 4 * j4)
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int k = 0; k < BATCH; ++k) {
+              const int t = t0 + 16 * k;
+              tm[k] = t < a.ntiles ? st[(long)t * 2 * a.B + q] : -INFINITY;
+              tz[k] = t < a.ntiles ? st[(long)t * 2 * a.B + a.B + q] : 0.f;
+            }
 #pragma unroll
-        for (int i = 0; i < QB; ++i) {
-          if (q0 + i < a.B) {
-            const float c = row_c[q0 + i];
-            w[0] += __builtin_amdgcn_exp2f(fmaf(v[i].x, kLog2e, -c));
-            w[1] += __builtin_amdgcn_exp2f(fmaf(v[i].y, kLog2e, -c));
-            w[2] += __builtin_amdgcn_exp2f(fmaf(v[i].z, kLog2e, -c));
-            w[3] += __builtin_amdgcn_exp2f(fmaf(v[i].w, kLog2e, -c));
+            for (int k = 0; k < BATCH; ++k) pair_merge(m, z, tm[k], tz[k]);
           }
         }
+        pm[part][threadIdx.x & 63] = m;
+        pz[part][threadIdx.x & 63] = z;
       }
-      *reinterpret_cast<float4*>(W + 4 * j4) = make_float4(w[0], w[1], w[2], w[3]);
-      if (w_in_lds) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) wsh[4 * j4 + e] = w[e];
+      __syncthreads();
+      {
+        const int ql = threadIdx.x >> 4, part = threadIdx.x & 15;
+        float m = pm[part][ql], z = pz[part][ql];
+        row16_merge<8>(m, z);
+        row16_merge<4>(m, z);
+        row16_merge<2>(m, z);
+        row16_merge<1>(m, z);
+        // exp(l - M) / Z = 2^(l log2(e) - c)
+        if (part == 0 && qc + ql < a.B) row_c[qc + ql] = fmaf(m, kLog2e, __log2f(z));
       }
+      __syncthreads();
     }
-  } else {
-    constexpr int RB = 16;  // rows in flight per thread
-    for (int j = threadIdx.x; j < a.nJ; j += NT) {
-      float w = 0.f;
-      for (int q0 = 0; q0 < a.B; q0 += RB) {
-        float v[RB];
+    const float* lg = a.logits + (long)u * a.B * a.nJ;
+    if ((a.nJ & 3) == 0) {
+      skim_w_columns<NT>(a, u, row_c, 0, a.nJ / 4, w_in_lds ? wsh : nullptr);
+    } else {
+      constexpr int RB = 16;  // rows in flight per thread
+      for (int j = threadIdx.x; j < a.nJ; j += NT) {
+        float w = 0.f;
+        for (int q0 = 0; q0 < a.B; q0 += RB) {
+          float v[RB];
 #pragma unroll
-        for (int i = 0; i < RB; ++i) v[i] = q0 + i < a.B ? lg[(long)(q0 + i) * a.nJ + j] : 0.f;
+          for (int i = 0; i < RB; ++i) v[i] = q0 + i < a.B ? lg[(long)(q0 + i) * a.nJ + j] : 0.f;
 #pragma unroll
-        for (int i = 0; i < RB; ++i)
-          if (q0 + i < a.B) w += __builtin_amdgcn_exp2f(fmaf(v[i], kLog2e, -row_c[q0 + i]));
+          for (int i = 0; i < RB; ++i)
+            if (q0 + i < a.B) w += __builtin_amdgcn_exp2f(fmaf(v[i], kLog2e, -row_c[q0 + i]));
+        }
+        W[j] = w;
+        if (w_in_lds) wsh[j] = w;
       }
-      W[j] = w;
-      if (w_in_lds) wsh[j] = w;
     }
   }
   __syncthreads();
@@ -1207,8 +1265,15 @@ static hipError_t skim_select_common(const wf_params& p, long nJ, int ntiles, in
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
+  // wide candidate sets: W over all CUs first (1024 columns a workgroup)
+  const int w_ready = a.nJ >= 4096 && (a.nJ & 3) == 0 ? 1 : 0;
+  if (w_ready) {
+    const int parts = (a.nJ + 1023) / 1024;
+    hipLaunchKernelGGL(skim_weights_kernel, dim3((unsigned)(a.U * parts)), dim3(kBlock), 0, s,
+                       a, parts);
+  }
   hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kSelectBlock),
-                     lds, s, a, in_lds);
+                     lds, s, a, in_lds, w_ready);
   return hipGetLastError();
 }
 
