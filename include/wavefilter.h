@@ -298,7 +298,9 @@ size_t wf_recursive_workspace_bytes(const wf_params* p,
  * [batch][heads][2 c_1]) receives mu^0.  The workspace is caller-owned
  * device memory, 256-byte aligned, of at least
  * wf_recursive_workspace_bytes(p, proportions) bytes.  Errors as in
- * wf_filter_attend; UNSUPPORTED for a wavelet other than Haar. */
+ * wf_filter_attend.  Haar and Daubechies-2: for db2 the transform of each
+ * gathered sequence reads across the joins of its blocks, with the
+ * boundary rule of p at the sequence's right end (eq. 11). */
 wf_status wf_filter_attend_recursive(const wf_params* p,
                                      const float* proportions, const void* Q,
                                      const void* K, const void* V,

@@ -431,8 +431,6 @@ static wf_status recursive_impl(const wf_params* p, const float* prop, const voi
                                 int n_events) {
   int32_t counts[WF_MAX_LEVELS];
   WF_TRY(check_recursion(p, prop, counts));
-  if (p->wavelet != WF_HAAR)
-    return fail(WF_ERR_UNSUPPORTED, "the recursion is built for the Haar wavelet only");
   WF_TRY(check_ptr(Q, "Q", false));
   WF_TRY(check_ptr(K, "K", false));
   WF_TRY(check_ptr(V, "V", false));

@@ -133,11 +133,28 @@ __host__ __device__ constexpr long cascade_halo(int M, int J) {
   return M == 4 ? (2L << J) - 2 : 0;
 }
 
+// Row t of the sequence a tile transforms: the unit's key row t, or on a
+// refinement scale of the recursion row t of the gathered kept blocks
+// (parent [npar] ids of 2^shift rows each; ids are clamped into the unit).
+struct RowsIdentity {
+  __device__ __forceinline__ long operator()(long t) const { return t; }
+};
+struct RowsGathered {
+  const int32_t* par;
+  int shift;
+  long last;
+  __device__ __forceinline__ long operator()(long t) const {
+    const long r = ((long)par[t >> shift] << shift) | (t & ((1L << shift) - 1));
+    return min(max(r, 0L), last);
+  }
+};
+
 // Streams rows [t0, t_stop) of one unit into the cascade (periodic extension
 // reads row t mod L), 16 loads in flight per lane.
-template <int M, int J, bool DET, typename T, class Sink>
+template <int M, int J, bool DET, typename T, class Sink, class RowMap = RowsIdentity>
 __device__ void run_stream(Cascade<M, J, DET>& cas, const T* Kunit, int D,
-                           int cp, long t0, long t_stop, long L, Sink& sink) {
+                           int cp, long t0, long t_stop, long L, Sink& sink,
+                           const RowMap& map = RowMap{}) {
   constexpr int U = 16;
   for (long t = t0; t < t_stop; t += U) {
     F2 v[U];
@@ -146,7 +163,7 @@ __device__ void run_stream(Cascade<M, J, DET>& cas, const T* Kunit, int D,
       long tt = t + k;
       if (tt < t_stop) {
         long row = tt < L ? tt : tt % L;
-        v[k] = load_pair(Kunit + row * D + 2 * cp);
+        v[k] = load_pair(Kunit + map(row) * D + 2 * cp);
       } else {
         v[k] = F2{0.f, 0.f};
       }
@@ -330,10 +347,10 @@ __device__ void haar_sum_tile(const T* Kunit, long n0, int ncoef, int J, float i
 
 // Cascade level-J approximation of tile rows [n0, n0 + ncoef) into LDS.
 // The tile is split into one stream per half/whole wave.
-template <int M, int J, typename T, int D>
+template <int M, int J, typename T, int D, class RowMap>
 __device__ void cascade_tile(const T* Kunit, long L, long n0, int ncoef,
                              int cpt, bool sym, const Taps& taps,
-                             float* coef) {
+                             float* coef, const RowMap& map) {
   constexpr int LPS = D / 2;
   constexpr int SPW = kWave / LPS;
   constexpr int NSTREAM = (kBlock / kWave) * SPW;
@@ -355,7 +372,7 @@ __device__ void cascade_tile(const T* Kunit, long L, long n0, int ncoef,
   const long t0 = s0 << J;
   long t_stop = (s1 << J) + cascade_halo(M, J);
   if (sym || M == 2) t_stop = min(t_stop, L);
-  run_stream<M, J, false, T>(cas, Kunit, D, cp, t0, t_stop, L, sink);
+  run_stream<M, J, false, T>(cas, Kunit, D, cp, t0, t_stop, L, sink, map);
 }
 
 // ------------------------------------------------------------ banded filter
@@ -419,9 +436,9 @@ __device__ __forceinline__ float sum_rows(float v) {
 // its row's contribution to coefficients b, b - 1, b - 2 (taps o, o + 2^J,
 // o + 2^(J+1) at offset o in the block); when block b + 1 starts,
 // coefficient b - 2 is complete and its RPI row lanes are summed.
-template <typename T, int D, int J>
+template <typename T, int D, int J, class RowMap>
 __device__ void band_tile(const T* Kunit, long L, long n0, int ncoef, long n_end,
-                          bool periodic, const float* taps, float* coef) {
+                          bool periodic, const float* taps, float* coef, const RowMap& map) {
   using BS = BandShape<T, D, J>;
   constexpr int CPL = BS::CPL, LPR = BS::LPR, RPI = BS::RPI;
   constexpr int BLK = 1 << J;
@@ -462,7 +479,7 @@ __device__ void band_tile(const T* Kunit, long L, long n0, int ncoef, long n_end
       const long r = b * BLK + (g0 + gi) * RPI + rsub;
       // past L: wrapped (periodic) or the last row with a zero tap
       const long row = r < L ? r : (periodic ? r % L : L - 1);
-      v[gi] = *reinterpret_cast<const u32x4*>(Kunit + row * D + csub * CPL);
+      v[gi] = *reinterpret_cast<const u32x4*>(Kunit + map(row) * D + csub * CPL);
     }
     if (g0 == 0 && b > c0) {
       flush(b - 3);
@@ -511,9 +528,9 @@ struct EdgeTaps {
 };
 
 // Edge coefficient n of the tile into LDS by the calling wave.
-template <typename T, int D, int J>
+template <typename T, int D, int J, class RowMap>
 __device__ void edge_coef(const T* Kunit, long n0, long n, long nJ, const float* edge,
-                          float* coef) {
+                          float* coef, const RowMap& map) {
   using BS = BandShape<T, D, J>;
   constexpr int CPL = BS::CPL, LPR = BS::LPR, RPI = BS::RPI;
   constexpr int BLK = 1 << J;
@@ -528,7 +545,7 @@ __device__ void edge_coef(const T* Kunit, long n0, long n, long nJ, const float*
   for (int k = 0; k < CPL; ++k) acc[k] = 0.f;
   for (int r0 = 0; r0 < len; r0 += RPI) {
     const int rr = r0 + rsub;
-    const u32x4 v = *reinterpret_cast<const u32x4*>(Kunit + (n * BLK + rr) * D + csub * CPL);
+    const u32x4 v = *reinterpret_cast<const u32x4*>(Kunit + map(n * BLK + rr) * D + csub * CPL);
     const float t = e[rr];
     if constexpr (sizeof(T) == 2) {
 #pragma unroll
@@ -749,19 +766,27 @@ skim_tile_kernel(SkimTileArgs a, Taps taps, EdgeTaps edge) {
     } else if constexpr (SRC == kCascade) {
       const T* Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * D;
       const bool sym = M == 4 && a.boundary == 0;
-      if constexpr (kBand) {
-        // interior coefficients by the banded filter, those whose window
-        // reaches a symmetric end by the cascade (on the last wave)
-        const long nJf = (long)a.L >> J;
-        const long n_end = sym ? (a.L >= band_len(J) ? min((a.L - band_len(J)) / (1L << J) + 1, nJf) : 0L)
-                               : nJf;
-        band_tile<T, D, J>(Kunit, a.L, n0, ncoef, n_end, !sym, band, coef);
-        // at most three edge coefficients: wave w takes the w-th of the tile
-        const long n = max(n0, n_end) + (threadIdx.x >> 6);
-        if (n < n0 + ncoef) edge_coef<T, D, J>(Kunit, n0, n, nJf, edge_lds, coef);
-      } else {
-        cascade_tile<M, J, T, D>(Kunit, a.L, n0, ncoef, a.cpt, sym, taps, coef);
-      }
+      // a.L rows: the filtered keys, or on a refinement scale of the
+      // recursion the gathered kept blocks (eq. 11), read across their joins
+      auto transform = [&](const auto& map) {
+        if constexpr (kBand) {
+          // interior coefficients by the banded filter, those whose window
+          // reaches a symmetric end by the end filters (a wave each)
+          const long nJf = (long)a.L >> J;
+          const long n_end =
+              sym ? (a.L >= band_len(J) ? min((a.L - band_len(J)) / (1L << J) + 1, nJf) : 0L) : nJf;
+          band_tile<T, D, J>(Kunit, a.L, n0, ncoef, n_end, !sym, band, coef, map);
+          // at most three edge coefficients: wave w takes the w-th of the tile
+          const long n = max(n0, n_end) + (threadIdx.x >> 6);
+          if (n < n0 + ncoef) edge_coef<T, D, J>(Kunit, n0, n, nJf, edge_lds, coef, map);
+        } else {
+          cascade_tile<M, J, T, D>(Kunit, a.L, n0, ncoef, a.cpt, sym, taps, coef, map);
+        }
+      };
+      if (a.parent)
+        transform(RowsGathered{a.parent + (long)u * a.npar, J + 1, a.Ls - 1});
+      else
+        transform(RowsIdentity{});
     } else {
       const float* src = a.approx + ((long)u * a.nJ + n0) * D;
       for (int v = threadIdx.x; v < ncoef * (D / 4); v += kBlock) {
@@ -1078,6 +1103,10 @@ static hipError_t dwt_dispatch(const DwtArgs& a, const Taps& taps, dim3 grid,
 
 // Haar coefficient tile size at level J.
 static int haar_cpt(int J) { return std::min(kMaxCoefTile, std::max(16, 2048 >> J)); }
+// coefficients per tile at scale b of the recursion
+static int rec_cpt(const wf_params& p, int b) {
+  return p.wavelet == WF_HAAR ? haar_cpt(b) : kMaxCoefTile;
+}
 
 DwtPlan plan_dwt(const wf_params& p) {
   DwtPlan d;
@@ -1206,7 +1235,10 @@ static hipError_t skim_tiles_common(const wf_params& p, int source, int cpt, int
   a.parent = parent;
   a.npar = npar;
   a.U = p.batch * p.heads;
-  a.L = (int)filtered_len(p);
+  // rows transformed: the filtered keys, or for the db2 filter on a
+  // refinement scale of the recursion the gathered kept blocks of 2^(J+1)
+  // rows each (Haar sums read the kept blocks' halves in place)
+  a.L = parent && source == kCascade ? (int)((long)npar << (J + 1)) : (int)filtered_len(p);
   a.Ls = p.ctx_len;
   a.B = p.q_len;
   a.J = J;
@@ -1288,7 +1320,7 @@ RecPlan plan_recursion(const wf_params& p, const int32_t* counts) {
   RecPlan r{};
   long n = (long)p.ctx_len >> p.levels;
   for (int b = p.levels; b >= 1; --b) {
-    const int cpt = haar_cpt(b);
+    const int cpt = rec_cpt(p, b);
     // with token logits the statistics come from the token skim's ranges
     const int ntiles =
         rec_token_path(p) && b <= 5
@@ -1305,14 +1337,14 @@ RecPlan plan_recursion(const wf_params& p, const int32_t* counts) {
 hipError_t launch_rec_tiles(const wf_params& p, int b, long n, const int32_t* parent,
                             int npar, const void* Q, const void* K, float* logits,
                             float* stats, hipStream_t s) {
-  return skim_tiles_common(p, kHaarSum, haar_cpt(b), b, n, parent, npar, Q, K, nullptr,
-                           logits, stats, s);
+  return skim_tiles_common(p, p.wavelet == WF_HAAR ? kHaarSum : kCascade, rec_cpt(p, b), b, n,
+                           parent, npar, Q, K, nullptr, logits, stats, s);
 }
 
 hipError_t launch_rec_select(const wf_params& p, int b, long n, int keep,
                              const int32_t* parent, int npar, const float* logits,
                              const float* stats, float* W, int32_t* out, hipStream_t s) {
-  const int cpt = haar_cpt(b);
+  const int cpt = rec_cpt(p, b);
   const int ntiles = (int)((n + cpt - 1) / cpt);
   return skim_select_common(p, n, ntiles, keep, parent, npar, b == 1 ? 1 : 0, logits,
                             stats, W, out, s);

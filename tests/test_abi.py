@@ -201,16 +201,14 @@ def test_recursion_rejects_bad_proportions(wfpkg, props):
     assert lib.wf_recursion_counts(ctypes.byref(p), None, out) == 1
 
 
-def test_recursion_db2_is_unsupported(wfpkg):
-    """The GPU recursion is built for Haar; db2 is refused before any
-    pointer is used."""
-    lib = wfpkg.library()
+def test_recursion_db2_kernel_sequence(wfpkg):
+    """The db2 recursion runs coefficient tiles at every scale (the token
+    path is Haar's), two kernels a scale, then the attention."""
     p = _params(wfpkg, levels=2, dtype="bf16", wavelet="db2")
-    arr = (ctypes.c_float * 2)(0.5, 0.5)
-    good = ctypes.c_void_p(256)
-    assert lib.wf_filter_attend_recursive(ctypes.byref(p), arr, good, good,
-                                          good, None, None, good, None, good,
-                                          1 << 30, None) == 2
+    assert wfpkg.recursive_kernel_names(p) == [
+        "rec_tiles_b2", "rec_select_b2", "rec_tiles_b1", "rec_select_b1",
+        "sparse_attn", "attn_combine"]
+    assert wfpkg.recursive_workspace_bytes(p, [0.5, 0.5]) > 0
 
 
 def test_recursion_kernel_sequence(wfpkg):

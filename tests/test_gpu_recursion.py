@@ -1,5 +1,6 @@
 """GPU parity of the multi-scale recursion (wf_filter_attend_recursive)
-against the oracle's R1 (scales B..1, eqs. 9-11) and O7-O8.
+against the oracle's R1 (scales B..1, eqs. 9-11) and O7-O8, for Haar and
+Daubechies-2.
 
 The kept positions mu^0 must equal the oracle's exactly (these seeds put no
 weight within rounding of a selection threshold at any scale; a failure
@@ -53,6 +54,16 @@ CASES = {
     # a length that is not a multiple of 2^B: the remainder follows mu^0
     "rec_bf16_b3_rem": V_("rrm", ctx_len=1024 + 6, levels=3, dtype="bf16",
                           gen_len=8, proportions=(0.5, 0.5, 0.25)),
+    # Daubechies-2: every scale's transform of the gathered blocks reads
+    # across their joins (banded filter from J = 2 at d = 128 bf16, the
+    # cascade below), symmetric or periodic at the gathered sequence's end
+    "rec_db2_sym_b2": V_("rd2s", ctx_len=2048, head_dim=128, levels=2,
+                         dtype="bf16", wavelet="db2", proportions=(0.5, 0.3)),
+    "rec_db2_per_b3_f32": V_("rd2p", ctx_len=1024, levels=3, wavelet="db2",
+                             boundary="periodic", proportions=(0.5, 0.5, 0.25)),
+    "rec_db2_sym_b4_rem": V_("rd2r", ctx_len=4096 + 9, head_dim=128, levels=4,
+                             dtype="bf16", wavelet="db2", gen_len=16,
+                             proportions=(0.6, 0.5, 0.5, 0.25)),
 }
 
 _cache: dict = {}
