@@ -326,6 +326,27 @@ def test_fused_is_deterministic(wf):
         assert torch.equal(x, y)
 
 
+@pytest.mark.parametrize("name", ["layer8b", "rem_tok_j3_tail", "tok_j5_b64_long"])
+def test_fused_output_does_not_depend_on_index_outputs(wf, name):
+    """Without tok_idx and seg_idx the fused call keeps the indices in its
+    workspace and gives the same output bit for bit; the ids it returns when
+    asked are strictly ascending."""
+    w = EDGE.get(name) or synth.WORKLOADS[name]
+    Q, K, V, Kg, Vg = inputs(w)
+    p = wf.params_for(w)
+    dev = "cuda"
+    args = [Q.to(dev), K.to(dev), V.to(dev),
+            Kg.to(dev) if Kg is not None else None,
+            Vg.to(dev) if Vg is not None else None]
+    say(f"[gpu] {w.name}: wf_filter_attend without indices")
+    O0 = wf.filter_attend(p, *args)
+    O1, tok, seg = wf.filter_attend(p, *args, want_indices=True)
+    torch.cuda.synchronize()
+    assert torch.equal(O0, O1)
+    assert torch.all(tok[..., 1:] > tok[..., :-1])
+    assert torch.all(seg[..., 1:] > seg[..., :-1])
+
+
 def test_fused_matches_staged_indices(wf):
     """Both routes select the same regions and tokens on the 8B-layer shape
     (up to the tie band, which this seed does not hit)."""
