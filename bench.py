@@ -7,10 +7,13 @@ top-k and sparse attention for every (batch, head) unit of one layer of one
 denoising step.  Inputs are seeded synthetic tensors (synth.WORKLOADS),
 resident in HBM before timing starts; consecutive steps use distinct device
 copies of them (--copies, 3 by default) so that no step finds the rows the
-previous one read in the 256 MB Infinity Cache.  Prints one JSON line:
+previous one read in the 256 MB Infinity Cache.  A workload of several
+layers (the 16K long-context one: 32) runs every layer once per step, each
+on its own seeded inputs (--layers overrides the count).  Prints one JSON
+line:
 
   value       context tokens filtered+attended per second per layer
-              (batch * ctx_len / step time)
+              (layers * batch * ctx_len / step time)
   roofline    the dominant kernel (the first of the sequence, token_skim
               or skim_tile: it streams every key once) against MI355X's
               8 TB/s HBM peak; durations come from HIP events recorded
@@ -188,6 +191,9 @@ def main() -> int:
                     help="distinct device copies of the inputs, used in turn "
                          "by consecutive steps so that no step finds the "
                          "previous step's rows in the 256 MB Infinity Cache")
+    ap.add_argument("--layers", type=int, default=0,
+                    help="layers per step, each with its own seeded inputs "
+                         "(default: the workload's layer count)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before timing, run one plain 1 GiB device-to-device "
                          "copy (a known-size kernel for scaling HBM counters)")
@@ -219,13 +225,31 @@ def main() -> int:
     cached = bool(w.cached)
     counts = wf.recursion_counts(p, w.proportions) if recursive else None
     keff = 2 * counts[0] if recursive else wf.effective_budget(p)
-    ncopy = max(1, args.copies)
+    nl = max(1, args.layers or getattr(w, "layers", 1))
     copies = []
-    for _ in range(ncopy):
-        copies.append(dict(
-            Q=Q.to(dev), K=K.to(dev), V=V.to(dev),
-            Kg=Kg.to(dev) if Kg is not None else None,
-            Vg=Vg.to(dev) if Vg is not None else None))
+    if nl > 1:
+        # a step runs every layer once, each on its own seeded inputs
+        for l in range(nl):
+            if l:
+                print(f"[bench] generating layer {l}", file=sys.stderr, flush=True)
+                Ql, Kl, Vl = synth.make_inputs(w, layer=l)
+                Kgl, Vgl = (synth.make_tail(w, w.gen_len, layer=l) if w.gen_len
+                            else (None, None))
+            else:
+                Ql, Kl, Vl, Kgl, Vgl = Q, K, V, Kg, Vg
+            copies.append(dict(
+                Q=Ql.to(dev), K=Kl.to(dev), V=Vl.to(dev),
+                Kg=Kgl.to(dev) if Kgl is not None else None,
+                Vg=Vgl.to(dev) if Vgl is not None else None))
+            del Ql, Kl, Vl, Kgl, Vgl
+        ncopy = nl
+    else:
+        ncopy = max(1, args.copies)
+        for _ in range(ncopy):
+            copies.append(dict(
+                Q=Q.to(dev), K=K.to(dev), V=V.to(dev),
+                Kg=Kg.to(dev) if Kg is not None else None,
+                Vg=Vg.to(dev) if Vg is not None else None))
     Qd = copies[0]["Q"]
     O = torch.empty_like(Qd)
     tok = torch.empty((w.batch, w.heads, keff), dtype=torch.int32, device=dev)
@@ -244,11 +268,18 @@ def main() -> int:
     else:
         ws = wf.alloc_workspace(p, wf.OP_FUSED, dev)
         names = wf.fused_kernel_names(p)
-    ev = HipEvents((len(names) + 1) * args.steps)
+    ev = HipEvents((len(names) + 1) * args.steps * nl)
     stream = torch.cuda.current_stream()
 
+    def layer_copies(i):
+        # the layers of step i: every layer in turn, or one rotated copy
+        return copies if nl > 1 else [copies[i % ncopy]]
+
     def step_plain(i):
-        c = copies[i % ncopy]
+        for c in layer_copies(i):
+            call_plain(c)
+
+    def call_plain(c):
         if recursive:
             wf.wf_filter_attend_recursive(p, w.proportions, c["Q"], c["K"],
                                           c["V"], c["Kg"], c["Vg"], O, tok,
@@ -262,8 +293,10 @@ def main() -> int:
                                 O, tok, None, ws, stream)
 
     def step_timed(i):
-        c = copies[i % ncopy]
-        base = i * (len(names) + 1)
+        for l, c in enumerate(layer_copies(i)):
+            call_timed(c, (i * nl + l) * (len(names) + 1))
+
+    def call_timed(c, base):
         evs = ev.ev[base:base + len(names) + 1]
         if recursive:
             wf.wf_filter_attend_recursive_timed(p, w.proportions, c["Q"],
@@ -317,11 +350,15 @@ def main() -> int:
     per_kernel = {n: 0.0 for n in names}
     step_ms = []
     for i in range(args.steps):
-        base = i * (len(names) + 1)
-        for j, n in enumerate(names):
-            per_kernel[n] += ev.elapsed_ms(base + j, base + j + 1)
-        step_ms.append(ev.elapsed_ms(base, base + len(names)))
-    per_kernel = {n: t / args.steps for n, t in per_kernel.items()}
+        t_step = 0.0
+        for l in range(nl):
+            base = (i * nl + l) * (len(names) + 1)
+            for j, n in enumerate(names):
+                per_kernel[n] += ev.elapsed_ms(base + j, base + j + 1)
+            t_step += ev.elapsed_ms(base, base + len(names))
+        step_ms.append(t_step)
+    # per launch
+    per_kernel = {n: t / (args.steps * nl) for n, t in per_kernel.items()}
     step_ms.sort()
 
     def pct(q):
@@ -330,7 +367,7 @@ def main() -> int:
 
     alg = algorithmic_bytes(w, keff, counts)
     U = w.units
-    tokens = w.batch * w.ctx_len
+    tokens = w.batch * w.ctx_len * nl
     value = tokens / (ms_step * 1e-3)
     # the dominant kernel: the longest one with an algorithmic byte count
     dom = max((n for n in names if n in alg["kernel"]),
@@ -356,7 +393,7 @@ def main() -> int:
             "workload": w.description,
             "batch": w.batch, "heads": w.heads, "ctx_len": w.ctx_len,
             "head_dim": w.head_dim, "q_len": w.q_len, "levels": w.levels,
-            "wavelet": w.wavelet, "gen_len": w.gen_len,
+            "wavelet": w.wavelet, "gen_len": w.gen_len, "layers": nl,
             **({"proportions": list(w.proportions), "counts": counts,
                 "kept_positions": keff} if recursive else
                {"segments": w.segments, "budget": w.budget, "k_eff": keff}),
@@ -372,12 +409,12 @@ def main() -> int:
             "algorithmic_bytes_per_launch": dom_bytes,
             "avg_launch_ms": dom_ms,
         },
-        "path_hbm_frac": alg["total"] * U / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
-        "path_algorithmic_bytes": alg["total"] * U,
+        "path_hbm_frac": alg["total"] * U * nl / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "path_algorithmic_bytes": alg["total"] * U * nl,
         "kernel_ms": per_kernel,
         "ms_per_step_with_events": ms_step_events,
         "step_ms_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
-        "input_copies": ncopy,
+        "input_copies": ncopy if nl == 1 else None,
         "host_wall_s": wall,
     }
     if not args.no_cpu_baseline:
