@@ -377,8 +377,8 @@ def run_cached(wf, w, Q, K, V, Kg, Vg):
 
 
 @pytest.mark.parametrize("name", ["tiny_scan", "gen_tail", "db2_sym_j3",
-                                  "b256_d128", "rem_tok_j3_tail", "layer8b",
-                                  "cached32k"])
+                                  "db2_per_j3", "b256_d128", "rem_tok_j3_tail",
+                                  "layer8b", "cached32k"])
 def test_cached_step(wf, name):
     """A step from the cached A_J gives the oracle's selection and output."""
     w = EDGE.get(name) or synth.WORKLOADS[name]

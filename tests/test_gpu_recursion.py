@@ -64,6 +64,12 @@ CASES = {
     "rec_db2_sym_b4_rem": V_("rd2r", ctx_len=4096 + 9, head_dim=128, levels=4,
                              dtype="bf16", wavelet="db2", gen_len=16,
                              proportions=(0.6, 0.5, 0.5, 0.25)),
+    "rec_db2_per_b2_tail": V_("rd2t", ctx_len=2048, head_dim=128, levels=2,
+                              dtype="bf16", wavelet="db2", boundary="periodic",
+                              gen_len=24, proportions=(0.5, 0.4)),
+    # more than 64 query rows: coefficient tiles at every scale
+    "rec_bf16_b3_q100": V_("rq1", ctx_len=2048, levels=3, q_len=100,
+                           dtype="bf16", proportions=(0.5, 0.5, 0.25)),
 }
 
 _cache: dict = {}
