@@ -116,6 +116,14 @@ EDGE = {
     "db2tok_sym_d64_rem": V_("d2sr", ctx_len=64 * 37 + 5, levels=6, segments=5,
                              budget=150, q_len=48, wavelet="db2", gen_len=8,
                              **_BF),
+    # token-level path at its degenerate ends: every block and token kept
+    # (S = n_J, k = P = L), one block and one token, one query row on db2
+    "tok_keep_all": V_("tka", ctx_len=2048, head_dim=128, levels=4,
+                       segments=128, budget=2048, **_BF),
+    "tok_s1_k1": V_("ts1", ctx_len=1024, head_dim=128, levels=5, segments=1,
+                    budget=1, q_len=1, **_BF),
+    "db2tok_q1": V_("d2q1", ctx_len=64 * 20, head_dim=128, levels=6,
+                    segments=3, budget=50, q_len=1, wavelet="db2", **_BF),
 }
 
 FULL = ["tiny", "layer8b", "long16k", "headline32k", "stress128k", "tail32k"]
