@@ -355,6 +355,27 @@ def test_fused_output_does_not_depend_on_index_outputs(wf, name):
     assert torch.all(seg[..., 1:] > seg[..., :-1])
 
 
+def test_fused_on_a_side_stream(wf):
+    """The library launches on the stream it is given: the fused call on a
+    second (default-priority) stream, with its inputs made there, gives the
+    current stream's result bit for bit."""
+    w = EDGE["rem_tok_j3_tail"]
+    Q, K, V, Kg, Vg = inputs(w)
+    p = wf.params_for(w)
+    args = [x.to("cuda") if x is not None else None for x in (Q, K, V, Kg, Vg)]
+    torch.cuda.synchronize()
+    O0 = wf.filter_attend(p, *args)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        ws = wf.alloc_workspace(p, wf.OP_FUSED, torch.device("cuda"))
+        O1 = torch.empty_like(args[0])
+        wf.wf_filter_attend(p, *args, O1, None, None, ws, side)
+    side.synchronize()
+    torch.cuda.synchronize()
+    assert torch.equal(O0, O1)
+
+
 def test_fused_matches_staged_indices(wf):
     """Both routes select the same regions and tokens on the 8B-layer shape
     (up to the tie band, which this seed does not hit)."""
