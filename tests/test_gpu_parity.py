@@ -376,6 +376,62 @@ def test_fused_on_a_side_stream(wf):
     assert torch.equal(O0, O1)
 
 
+def test_fused_in_a_hip_graph(wf):
+    """The fused call records into a HIP graph (it issues kernel launches
+    only: no memsets, copies, synchronisations or allocations).  Every replay,
+    with eager work and synchronisations between them, equals the eager
+    result; a replay after new queries are copied into the captured buffer
+    equals the eager call on those queries."""
+    w = synth.WORKLOADS["layer8b"]
+    Q, K, V, _, _ = inputs(w)
+    Q2 = inputs(w, layer=1)[0]
+    p = wf.params_for(w)
+    dev = torch.device("cuda")
+    Qd, Kd, Vd, Q2d = Q.to(dev), K.to(dev), V.to(dev), Q2.to(dev)
+    keff = wf.effective_budget(p)
+
+    def eager(q):
+        O = torch.empty_like(q)
+        tok = torch.empty((p.batch, p.heads, keff), dtype=torch.int32, device=dev)
+        ws = wf.alloc_workspace(p, wf.OP_FUSED, dev)
+        wf.wf_filter_attend(p, q, Kd, Vd, None, None, O, tok, None, ws)
+        torch.cuda.synchronize()
+        return O, tok
+
+    O_ref, tok_ref = eager(Qd)
+    O2_ref, tok2_ref = eager(Q2d)
+    Qc = Qd.clone()
+    O = torch.empty_like(Qd)
+    tok = torch.empty_like(tok_ref)
+    ws = wf.alloc_workspace(p, wf.OP_FUSED, dev)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up off the capture
+        wf.wf_filter_attend(p, Qc, Kd, Vd, None, None, O, tok, None, ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say("[gpu] layer8b: capturing wf_filter_attend")
+    with torch.cuda.graph(g):
+        wf.wf_filter_attend(p, Qc, Kd, Vd, None, None, O, tok, None, ws)
+    torch.cuda.synchronize()
+    for r in range(3):
+        O.zero_()
+        tok.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(O, O_ref), f"replay {r}"
+        assert torch.equal(tok, tok_ref), f"replay {r}"
+    Qc.copy_(Q2d)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(O, O2_ref)
+    assert torch.equal(tok, tok2_ref)
+    assert not torch.equal(tok2_ref, tok_ref)
+
+
 def test_fused_matches_staged_indices(wf):
     """Both routes select the same regions and tokens on the 8B-layer shape
     (up to the tie band, which this seed does not hit)."""
