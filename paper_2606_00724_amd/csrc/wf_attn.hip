@@ -686,8 +686,10 @@ __global__ __launch_bounds__(kCombineBlock) void attn_combine_kernel(AttnArgs a,
   const int tpr = D / 8;                  // threads per row
   const int rpb = kCombineBlock / tpr;    // rows per workgroup
   const int nqb = (a.B + rpb - 1) / rpb;
-  const int u = blockIdx.x / nqb;
-  const int q = (blockIdx.x % nqb) * rpb + threadIdx.x / tpr;
+  // the unit on the XCD whose L2 took its partials from the attention
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / nqb;
+  const int q = (item % nqb) * rpb + threadIdx.x / tpr;
   const int c0 = (threadIdx.x % tpr) * 8;
   if (q >= a.B) return;  // no barrier follows
   const float* ps = a.pstat + (long)u * a.NS * 2 * a.B;

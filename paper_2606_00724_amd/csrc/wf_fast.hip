@@ -583,7 +583,8 @@ __global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelec
   __shared__ float pool_m[16 * (16 * kFastMaxQBlocks + 1)], pool_z[16 * (16 * kFastMaxQBlocks + 1)];
   __shared__ SelectShared<NT> sh;
   extern __shared__ float wsh[];  // W (when it fits), then the picked block ids
-  const int u = blockIdx.x;
+  // the unit on the XCD whose L2 took its block rows from the token skim
+  const int u = xcd_swizzle(blockIdx.x, gridDim.x);
   const int B = a.B, nJ = a.nJ;
   // the ranges' (max, sum of exp) pairs: thread (part, q) = (tid / B, tid % B)
   // folds ranges part, part + parts, ..., then rows of 16 lanes per query
