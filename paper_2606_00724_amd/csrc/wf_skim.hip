@@ -875,7 +875,9 @@ __device__ void skim_w_columns(const SkimSelectArgs& a, int u, const float* row_
 __global__ __launch_bounds__(kBlock) void skim_weights_kernel(SkimSelectArgs a, int parts) {
   __shared__ float row_c[WF_MAX_Q_LEN];
   __shared__ float pm[4][64], pz[4][64];
-  const int u = blockIdx.x / parts, part = blockIdx.x % parts;
+  // a unit's parts on the XCD of the token skim that wrote its logits
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / parts, part = item % parts;
   const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
   for (int qc = 0; qc < a.B; qc += 64) {
     const int q = qc + (threadIdx.x & 63), pp = threadIdx.x >> 6;
@@ -918,7 +920,8 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
   __shared__ float pm[16][65], pz[16][65];
   __shared__ SelectShared<NT> sh;
   extern __shared__ float wsh[];
-  const int u = blockIdx.x;
+  // the unit on the XCD whose L2 took its W (or its logits)
+  const int u = xcd_swizzle(blockIdx.x, gridDim.x);
   const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
   float* W = a.W + (long)u * a.nJ;
   if (w_ready) {
