@@ -82,12 +82,13 @@ enum { WF_BF16 = 0, WF_F32 = 1 };
 enum { WF_OP_SKIM = 0, WF_OP_SCAN = 1, WF_OP_ATTN = 2, WF_OP_FUSED = 3,
        WF_OP_CACHED = 4 };
 
-/* Limits of this build. */
 /* Remainder.  When L is not a multiple of 2^J, the first
  * Lf = 2^J floor(L / 2^J) positions are filtered (transformed, scored,
  * selected) and the last R = L - Lf positions are always kept: the sparse
  * cache is [K[tok]; K[Lf .. L); K_g] (values likewise), R = 0 for a multiple
  * of 2^J.  The recursion does the same with 2^B. */
+
+/* Limits of this build. */
 enum {
     WF_MAX_LEVELS = 10,  /* J                                   */
     WF_MAX_Q_LEN = 256   /* B, rows of the query block          */
@@ -261,26 +262,30 @@ const char* wf_filter_attend_cached_kernel_name(const wf_params* p, int32_t i);
 
 /* ---------------------------------------------------------------------
  * Multi-scale recursive filtering (Section 3.2, eqs. 9-11; Algorithm 1,
- * the loop over scales).  Scale B = p->levels; selection proportions
- * m_b = proportions[b - 1] for b = 1..B (host array of p->levels floats,
- * each in (0, 1]).  Per unit:
+ * the loop over scales), for the Haar and Daubechies-2 wavelets.  Scale
+ * B = p->levels; selection proportions m_b = proportions[b - 1] for
+ * b = 1..B (host array of p->levels floats, each in (0, 1]).  Per unit:
  *
- *   mu^B = all ctx_len positions
+ *   mu^B = all Lf filtered positions (Lf as in the remainder note)
  *   for b = B .. 1:
- *     candidates: the b-level Haar coefficients of the gathered keys
- *       K[mu^b] -- n_B = ctx_len / 2^B at b = B, n_b = 2 c_{b+1} below
- *       (the two halves of every kept block; for Haar, eq. 11's transform
- *       of the gathered sequence is exactly these block coefficients)
+ *     candidates: the n_b coefficients of the b-level DWT of the gathered
+ *       keys K[mu^b], taken as one sequence (eq. 11; eq. 6 at b = B):
+ *       n_B = Lf / 2^B, n_b = 2 c_{b+1} below.  Coefficient i covers
+ *       positions mu^b[2^b i .. 2^b i + 2^b).  For Haar it is the level-b
+ *       coefficient of the prompt block holding those positions; for db2 the
+ *       filter reads across the joins of the gathered blocks, with the
+ *       boundary rule of p at the gathered sequence's right end.
  *     weights: eqs. 7-8 over the n_b candidates only
  *     keep: the c_b best (eq. 9; ties to the lower index), where
  *       c_b = max(1, ceil(m_b * n_b)) evaluated in double from the float
  *       m_b, at most n_b
- *     mu^{b-1}: the positions of the kept blocks (eq. 10 through mu^b)
- *   then attention over [K[mu^0]; Kg], [V[mu^0]; Vg] as in wf_filter_attend.
+ *     mu^{b-1}: the positions the kept candidates cover (eq. 10 through
+ *       mu^b), ascending
+ *   then attention over [K[mu^0]; K[Lf .. L); Kg], values likewise, as in
+ *   wf_filter_attend.
  *
  * mu^0 has 2 c_1 positions, ascending.  p->segments and p->budget are not
- * used.  This build runs the recursion for the Haar wavelet (the paper's
- * setting); db2 returns WF_ERR_UNSUPPORTED.
+ * used.
  * --------------------------------------------------------------------- */
 
 /* c_b for every scale into counts[b - 1] (host array of p->levels).
@@ -294,27 +299,33 @@ size_t wf_recursive_workspace_bytes(const wf_params* p,
                                     const float* proportions);
 
 /* The recursion and the attention, asynchronous on `stream`.  Q, K, V, Kg,
- * Vg and O as in wf_filter_attend; tok_idx (nullable, device,
- * [batch][heads][2 c_1]) receives mu^0.  The workspace is caller-owned
- * device memory, 256-byte aligned, of at least
- * wf_recursive_workspace_bytes(p, proportions) bytes.  Errors as in
- * wf_filter_attend.  Haar and Daubechies-2: for db2 the transform of each
- * gathered sequence reads across the joins of its blocks, with the
- * boundary rule of p at the sequence's right end (eq. 11). */
+ * Vg and O as in wf_filter_attend.
+ *   tok_idx    nullable [batch][heads][2 c_1]     int32 out: mu^0, ascending
+ *   kept_idx   nullable, int32 out: the kept candidates of the scales
+ *              b = B .. 2 as prompt block ids at level b (block j covers
+ *              positions 2^b j .. 2^b j + 2^b - 1, so mu^{b-1} is the union
+ *              of the kept blocks), ascending per unit.  Scale b's ids are
+ *              [batch][heads][c_b] starting at element
+ *              batch * heads * (c_B + ... + c_{b+1}); the array holds
+ *              batch * heads * (c_B + ... + c_2) elements (none when B = 1).
+ *   workspace  caller-owned device memory, 256-byte aligned, of at least
+ *              wf_recursive_workspace_bytes(p, proportions) bytes.
+ * Errors as in wf_filter_attend. */
 wf_status wf_filter_attend_recursive(const wf_params* p,
                                      const float* proportions, const void* Q,
                                      const void* K, const void* V,
                                      const void* Kg, const void* Vg, void* O,
-                                     int32_t* tok_idx, void* workspace,
-                                     size_t workspace_bytes, void* stream);
+                                     int32_t* tok_idx, int32_t* kept_idx,
+                                     void* workspace, size_t workspace_bytes,
+                                     void* stream);
 
 /* Same, recording events[i] before kernel i and events[n] after the last
  * (n = wf_filter_attend_recursive_kernels(p); n_events >= n + 1). */
 wf_status wf_filter_attend_recursive_timed(
     const wf_params* p, const float* proportions, const void* Q, const void* K,
     const void* V, const void* Kg, const void* Vg, void* O, int32_t* tok_idx,
-    void* workspace, size_t workspace_bytes, void* stream, void** events,
-    int32_t n_events);
+    int32_t* kept_idx, void* workspace, size_t workspace_bytes, void* stream,
+    void** events, int32_t n_events);
 
 /* Kernels one recursive call queues (2 per scale, then the attention and
  * its combine) and the name of the i-th one, or -1 / NULL if p is

@@ -94,10 +94,10 @@ def _load() -> ctypes.CDLL:
         "wf_recursive_workspace_bytes": (sz, [P, fp]),
         "wf_filter_attend_recursive": (ctypes.c_int,
                                        [P, fp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                        sz, vp]),
+                                        vp, sz, vp]),
         "wf_filter_attend_recursive_timed": (ctypes.c_int,
                                              [P, fp, vp, vp, vp, vp, vp, vp,
-                                              vp, vp, sz, vp,
+                                              vp, vp, vp, sz, vp,
                                               ctypes.POINTER(vp), i32]),
         "wf_filter_attend_recursive_kernels": (i32, [P]),
         "wf_filter_attend_recursive_kernel_name": (ctypes.c_char_p, [P, i32]),
@@ -178,6 +178,43 @@ def _ptr(t) -> int | None:
     return t.data_ptr()
 
 
+def _expect(t, name: str, dtype: torch.dtype, numel: int,
+            nullable: bool = False) -> None:
+    """The element type and count a tensor must have for these parameters
+    (the kernels index it by the parameters alone)."""
+    if t is None:
+        if nullable:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if t.numel() != numel:
+        raise ValueError(f"{name}: {t.numel()} elements, expected {numel} "
+                         f"for these parameters")
+
+
+def _units(p) -> int:
+    return p.batch * p.heads
+
+
+def _remainder(p) -> int:
+    return p.ctx_len - ((p.ctx_len >> p.levels) << p.levels)
+
+
+def _expect_qkv(p, Q=None, K=None, V=None, Kg=None, Vg=None, O=None) -> None:
+    dt, U, d = torch_dtype(p), _units(p), p.head_dim
+    for name, t in (("Q", Q), ("O", O)):
+        if t is not None:
+            _expect(t, name, dt, U * p.q_len * d)
+    for name, t in (("K", K), ("V", V)):
+        if t is not None:
+            _expect(t, name, dt, U * p.ctx_len * d)
+    for name, t in (("Kg", Kg), ("Vg", Vg)):
+        _expect(t, name, dt, U * p.gen_len * d, nullable=p.gen_len == 0)
+
+
 def _ws(t) -> tuple[int | None, int]:
     if t is None:
         return None, 0
@@ -192,17 +229,39 @@ def _stream(stream) -> int | None:
     return int(stream)
 
 
+def _torch_stream(stream) -> torch.cuda.Stream:
+    """The stream the library will queue on, as a torch stream, so that the
+    buffers a wrapper allocates belong to it (the caching allocator then
+    reuses them only after the kernels queued there)."""
+    if stream is None:
+        return torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream))
+
+
 def _check(status: int) -> None:
     if status != 0:
         raise WfError(status, _lib.wf_last_error().decode())
 
 
 def wf_dwt_keys(p, K, approx, details=None, stream=None):
+    U, d = _units(p), p.head_dim
+    Lf = (p.ctx_len >> p.levels) << p.levels
+    _expect_qkv(p, K=K)
+    _expect(approx, "approx", torch.float32, U * (p.ctx_len >> p.levels) * d)
+    _expect(details, "details", torch.float32,
+            U * sum(Lf >> j for j in range(1, p.levels + 1)) * d, nullable=True)
     _check(_lib.wf_dwt_keys(ctypes.byref(p), _ptr(K), _ptr(approx),
                             _ptr(details), _stream(stream)))
 
 
 def wf_skim_score(p, Q, approx, seg_score, seg_idx, workspace, stream=None):
+    U, nJ = _units(p), p.ctx_len >> p.levels
+    _expect_qkv(p, Q=Q)
+    _expect(approx, "approx", torch.float32, U * nJ * p.head_dim)
+    _expect(seg_score, "seg_score", torch.float32, U * nJ)
+    _expect(seg_idx, "seg_idx", torch.int32, U * p.segments)
     ws, nb = _ws(workspace)
     _check(_lib.wf_skim_score(ctypes.byref(p), _ptr(Q), _ptr(approx),
                               _ptr(seg_score), _ptr(seg_idx), ws, nb,
@@ -211,6 +270,12 @@ def wf_skim_score(p, Q, approx, seg_score, seg_idx, workspace, stream=None):
 
 def wf_scan_select(p, Q, K, seg_idx, tok_score, tok_idx, workspace,
                    stream=None):
+    U = _units(p)
+    _expect_qkv(p, Q=Q, K=K)
+    _expect(seg_idx, "seg_idx", torch.int32, U * p.segments)
+    _expect(tok_score, "tok_score", torch.float32,
+            U * (p.segments << p.levels), nullable=True)
+    _expect(tok_idx, "tok_idx", torch.int32, U * effective_budget(p))
     ws, nb = _ws(workspace)
     _check(_lib.wf_scan_select(ctypes.byref(p), _ptr(Q), _ptr(K),
                                _ptr(seg_idx), _ptr(tok_score), _ptr(tok_idx),
@@ -218,19 +283,37 @@ def wf_scan_select(p, Q, K, seg_idx, tok_score, tok_idx, workspace,
 
 
 def wf_gather_kv(p, K, V, tok_idx, Kg, Vg, Ks, Vs, stream=None):
+    U, keff = _units(p), effective_budget(p)
+    _expect_qkv(p, K=K, V=V, Kg=Kg, Vg=Vg)
+    _expect(tok_idx, "tok_idx", torch.int32, U * keff)
+    rows = keff + _remainder(p) + p.gen_len
+    for name, t in (("Ks", Ks), ("Vs", Vs)):
+        _expect(t, name, torch_dtype(p), U * rows * p.head_dim)
     _check(_lib.wf_gather_kv(ctypes.byref(p), _ptr(K), _ptr(V), _ptr(tok_idx),
                              _ptr(Kg), _ptr(Vg), _ptr(Ks), _ptr(Vs),
                              _stream(stream)))
 
 
 def wf_sparse_attn(p, Q, Ks, Vs, n_kv, O, workspace, stream=None):
+    _expect_qkv(p, Q=Q, O=O)
+    for name, t in (("Ks", Ks), ("Vs", Vs)):
+        _expect(t, name, torch_dtype(p), _units(p) * int(n_kv) * p.head_dim)
     ws, nb = _ws(workspace)
     _check(_lib.wf_sparse_attn(ctypes.byref(p), _ptr(Q), _ptr(Ks), _ptr(Vs),
                                int(n_kv), _ptr(O), ws, nb, _stream(stream)))
 
 
+def _expect_fused(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx) -> None:
+    _expect_qkv(p, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, O=O)
+    _expect(tok_idx, "tok_idx", torch.int32, _units(p) * effective_budget(p),
+            nullable=True)
+    _expect(seg_idx, "seg_idx", torch.int32, _units(p) * p.segments,
+            nullable=True)
+
+
 def wf_filter_attend(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
                      stream=None):
+    _expect_fused(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx)
     ws, nb = _ws(workspace)
     _check(_lib.wf_filter_attend(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V),
                                  _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx),
@@ -240,6 +323,7 @@ def wf_filter_attend(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
 def wf_filter_attend_timed(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
                            workspace, events, stream=None):
     """``events``: sequence of raw hipEvent_t handles (ints)."""
+    _expect_fused(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx)
     ws, nb = _ws(workspace)
     arr = (ctypes.c_void_p * len(events))(*events)
     _check(_lib.wf_filter_attend_timed(ctypes.byref(p), _ptr(Q), _ptr(K),
@@ -290,8 +374,15 @@ def cached_kernel_names(p: WfParams) -> list[str]:
             for i in range(n)]
 
 
+def _expect_approx(p, approx) -> None:
+    _expect(approx, "approx", torch.float32,
+            _units(p) * (p.ctx_len >> p.levels) * p.head_dim)
+
+
 def wf_filter_attend_cached(p, Q, approx, K, V, Kg, Vg, O, tok_idx, seg_idx,
                             workspace, stream=None):
+    _expect_fused(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx)
+    _expect_approx(p, approx)
     ws, nb = _ws(workspace)
     _check(_lib.wf_filter_attend_cached(
         ctypes.byref(p), _ptr(Q), _ptr(approx), _ptr(K), _ptr(V), _ptr(Kg),
@@ -301,6 +392,8 @@ def wf_filter_attend_cached(p, Q, approx, K, V, Kg, Vg, O, tok_idx, seg_idx,
 
 def wf_filter_attend_cached_timed(p, Q, approx, K, V, Kg, Vg, O, tok_idx,
                                   seg_idx, workspace, events, stream=None):
+    _expect_fused(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx)
+    _expect_approx(p, approx)
     ws, nb = _ws(workspace)
     arr = (ctypes.c_void_p * len(events))(*events)
     _check(_lib.wf_filter_attend_cached_timed(
@@ -311,8 +404,10 @@ def wf_filter_attend_cached_timed(p, Q, approx, K, V, Kg, Vg, O, tok_idx,
 
 def dwt_approx(p: WfParams, K, stream=None) -> torch.Tensor:
     """A_J of K (fp32 [batch, heads, ctx_len >> levels, d])."""
-    approx = torch.empty((p.batch, p.heads, p.ctx_len >> p.levels,
-                          p.head_dim), dtype=torch.float32, device=K.device)
+    with torch.cuda.stream(_torch_stream(stream)):
+        approx = torch.empty((p.batch, p.heads, p.ctx_len >> p.levels,
+                              p.head_dim), dtype=torch.float32,
+                             device=K.device)
     wf_dwt_keys(p, K, approx, None, stream)
     return approx
 
@@ -321,16 +416,18 @@ def filter_attend_cached(p: WfParams, Q, approx, K, V, Kg=None, Vg=None,
                          workspace=None, want_indices: bool = False,
                          stream=None):
     """Allocates O (and the index outputs) and runs wf_filter_attend_cached.
-    Returns O, or (O, tok_idx, seg_idx) when want_indices."""
-    O = torch.empty_like(Q)
-    tok = seg = None
-    if want_indices:
-        tok = torch.empty((p.batch, p.heads, effective_budget(p)),
-                          dtype=torch.int32, device=Q.device)
-        seg = torch.empty((p.batch, p.heads, p.segments), dtype=torch.int32,
-                          device=Q.device)
-    if workspace is None:
-        workspace = alloc_workspace(p, OP_CACHED, Q.device)
+    Returns O, or (O, tok_idx, seg_idx) when want_indices.  What it
+    allocates belongs to the stream the kernels run on."""
+    with torch.cuda.stream(_torch_stream(stream)):
+        O = torch.empty_like(Q)
+        tok = seg = None
+        if want_indices:
+            tok = torch.empty((p.batch, p.heads, effective_budget(p)),
+                              dtype=torch.int32, device=Q.device)
+            seg = torch.empty((p.batch, p.heads, p.segments),
+                              dtype=torch.int32, device=Q.device)
+        if workspace is None:
+            workspace = alloc_workspace(p, OP_CACHED, Q.device)
     wf_filter_attend_cached(p, Q, approx, K, V, Kg, Vg, O, tok, seg,
                             workspace, stream)
     return (O, tok, seg) if want_indices else O
@@ -366,37 +463,64 @@ def recursive_kernel_names(p: WfParams) -> list[str]:
             for i in range(n)]
 
 
+def kept_elements(p: WfParams, proportions) -> int:
+    """Elements of the kept_idx output: batch * heads * (c_B + ... + c_2)."""
+    return _units(p) * sum(recursion_counts(p, proportions)[1:])
+
+
+def _expect_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok_idx,
+                      kept_idx) -> None:
+    _expect_qkv(p, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, O=O)
+    counts = recursion_counts(p, proportions)
+    _expect(tok_idx, "tok_idx", torch.int32, _units(p) * 2 * counts[0],
+            nullable=True)
+    _expect(kept_idx, "kept_idx", torch.int32, _units(p) * sum(counts[1:]),
+            nullable=True)
+
+
 def wf_filter_attend_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok_idx,
-                               workspace, stream=None):
+                               workspace, stream=None, kept_idx=None):
+    _expect_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, kept_idx)
     ws, nb = _ws(workspace)
     _check(_lib.wf_filter_attend_recursive(
         ctypes.byref(p), _props(p, proportions), _ptr(Q), _ptr(K), _ptr(V),
-        _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx), ws, nb, _stream(stream)))
+        _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx), _ptr(kept_idx), ws, nb,
+        _stream(stream)))
 
 
 def wf_filter_attend_recursive_timed(p, proportions, Q, K, V, Kg, Vg, O,
-                                     tok_idx, workspace, events, stream=None):
+                                     tok_idx, workspace, events, stream=None,
+                                     kept_idx=None):
+    _expect_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, kept_idx)
     ws, nb = _ws(workspace)
     arr = (ctypes.c_void_p * len(events))(*events)
     _check(_lib.wf_filter_attend_recursive_timed(
         ctypes.byref(p), _props(p, proportions), _ptr(Q), _ptr(K), _ptr(V),
-        _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx), ws, nb, _stream(stream),
-        arr, len(events)))
+        _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx), _ptr(kept_idx), ws, nb,
+        _stream(stream), arr, len(events)))
 
 
 def filter_attend_recursive(p: WfParams, proportions, Q, K, V, Kg=None,
-                            Vg=None, workspace=None, stream=None):
-    """Allocates O, mu^0 and the workspace; returns (O, tok_idx)."""
+                            Vg=None, workspace=None, stream=None,
+                            want_kept: bool = False):
+    """Allocates O, mu^0 and the workspace (on the stream the kernels run
+    on); returns (O, tok_idx), or (O, tok_idx, kept_idx) when want_kept."""
     counts = recursion_counts(p, proportions)
-    O = torch.empty_like(Q)
-    tok = torch.empty((p.batch, p.heads, 2 * counts[0]), dtype=torch.int32,
-                      device=Q.device)
-    if workspace is None:
-        nb = recursive_workspace_bytes(p, proportions)
-        workspace = torch.empty(nb, dtype=torch.uint8, device=Q.device)
+    with torch.cuda.stream(_torch_stream(stream)):
+        O = torch.empty_like(Q)
+        tok = torch.empty((p.batch, p.heads, 2 * counts[0]),
+                          dtype=torch.int32, device=Q.device)
+        kept = None
+        if want_kept:
+            kept = torch.empty(max(1, _units(p) * sum(counts[1:])),
+                               dtype=torch.int32, device=Q.device)
+            kept = kept[:_units(p) * sum(counts[1:])]
+        if workspace is None:
+            nb = recursive_workspace_bytes(p, proportions)
+            workspace = torch.empty(nb, dtype=torch.uint8, device=Q.device)
     wf_filter_attend_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok,
-                               workspace, stream)
-    return O, tok
+                               workspace, stream, kept_idx=kept)
+    return (O, tok, kept) if want_kept else (O, tok)
 
 
 # ------------------------------------------------------------ allocation
@@ -413,15 +537,17 @@ def alloc_workspace(p: WfParams, op: int, device) -> torch.Tensor | None:
 def filter_attend(p: WfParams, Q, K, V, Kg=None, Vg=None, workspace=None,
                   want_indices: bool = False, stream=None):
     """Allocates O (and the index outputs) and runs wf_filter_attend.
-    Returns O, or (O, tok_idx, seg_idx) when want_indices."""
-    O = torch.empty_like(Q)
-    tok = seg = None
-    if want_indices:
-        tok = torch.empty((p.batch, p.heads, effective_budget(p)),
-                          dtype=torch.int32, device=Q.device)
-        seg = torch.empty((p.batch, p.heads, p.segments), dtype=torch.int32,
-                          device=Q.device)
-    if workspace is None:
-        workspace = alloc_workspace(p, OP_FUSED, Q.device)
+    Returns O, or (O, tok_idx, seg_idx) when want_indices.  What it
+    allocates belongs to the stream the kernels run on."""
+    with torch.cuda.stream(_torch_stream(stream)):
+        O = torch.empty_like(Q)
+        tok = seg = None
+        if want_indices:
+            tok = torch.empty((p.batch, p.heads, effective_budget(p)),
+                              dtype=torch.int32, device=Q.device)
+            seg = torch.empty((p.batch, p.heads, p.segments),
+                              dtype=torch.int32, device=Q.device)
+        if workspace is None:
+            workspace = alloc_workspace(p, OP_FUSED, Q.device)
     wf_filter_attend(p, Q, K, V, Kg, Vg, O, tok, seg, workspace, stream)
     return (O, tok, seg) if want_indices else O

@@ -426,9 +426,9 @@ static const char* rec_kernel_name(const wf_params& p, int i) {
 
 static wf_status recursive_impl(const wf_params* p, const float* prop, const void* Q,
                                 const void* K, const void* V, const void* Kg,
-                                const void* Vg, void* O, int32_t* tok_idx, void* ws,
-                                size_t ws_bytes, void* stream, void** events,
-                                int n_events) {
+                                const void* Vg, void* O, int32_t* tok_idx,
+                                int32_t* kept_idx, void* ws, size_t ws_bytes,
+                                void* stream, void** events, int n_events) {
   int32_t counts[WF_MAX_LEVELS];
   WF_TRY(check_recursion(p, prop, counts));
   WF_TRY(check_ptr(Q, "Q", false));
@@ -436,6 +436,8 @@ static wf_status recursive_impl(const wf_params* p, const float* prop, const voi
   WF_TRY(check_ptr(V, "V", false));
   WF_TRY(check_ptr(O, "O", false));
   WF_TRY(check_ptr(tok_idx, "tok_idx", true));
+  if (kept_idx && ((uintptr_t)kept_idx & 3u) != 0)
+    return fail(WF_ERR_INVALID_ARG, "kept_idx is not 4-byte aligned");
   if (p->gen_len > 0) {
     WF_TRY(check_ptr(Kg, "Kg", false));
     WF_TRY(check_ptr(Vg, "Vg", false));
@@ -472,8 +474,11 @@ static wf_status recursive_impl(const wf_params* p, const float* prop, const voi
   long n = (long)p->ctx_len >> p->levels;
   const int32_t* parent = nullptr;
   int npar = 0;
+  const long U = (long)p->batch * p->heads;
+  long kept_at = 0;  // element offset of this scale's ids in kept_idx
   for (int b = p->levels; b >= 1; --b) {
-    int32_t* out = b == 1 ? tok : sel[b & 1];
+    int32_t* out = b == 1 ? tok : kept_idx ? kept_idx + kept_at : sel[b & 1];
+    kept_at += U * counts[b - 1];
     if (rec_token_path(*p) && b <= 5) {
       // the scale's coarse logits as sums of token logits (of the kept
       // blocks' tokens below the first scale)
@@ -697,23 +702,23 @@ size_t wf_recursive_workspace_bytes(const wf_params* p, const float* proportions
 wf_status wf_filter_attend_recursive(const wf_params* p, const float* proportions,
                                      const void* Q, const void* K, const void* V,
                                      const void* Kg, const void* Vg, void* O,
-                                     int32_t* tok_idx, void* workspace,
+                                     int32_t* tok_idx, int32_t* kept_idx, void* workspace,
                                      size_t workspace_bytes, void* stream) {
-  return recursive_impl(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, workspace,
+  return recursive_impl(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, kept_idx, workspace,
                         workspace_bytes, stream, nullptr, 0);
 }
 
 wf_status wf_filter_attend_recursive_timed(const wf_params* p, const float* proportions,
                                            const void* Q, const void* K, const void* V,
                                            const void* Kg, const void* Vg, void* O,
-                                           int32_t* tok_idx, void* workspace,
-                                           size_t workspace_bytes, void* stream,
-                                           void** events, int32_t n_events) {
+                                           int32_t* tok_idx, int32_t* kept_idx,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream, void** events, int32_t n_events) {
   if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
   WF_TRY(check_shape(p));
   for (int i = 0; i < n_events && i <= rec_kernels(*p); ++i)
     if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
-  return recursive_impl(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, workspace,
+  return recursive_impl(p, proportions, Q, K, V, Kg, Vg, O, tok_idx, kept_idx, workspace,
                         workspace_bytes, stream, events, n_events);
 }
 

@@ -14,7 +14,9 @@ near-tie cannot cascade):
 """
 from __future__ import annotations
 
+import os
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import torch
@@ -122,3 +124,43 @@ def check_unit(*, Q, K, V, levels, segments, budget, wavelet, boundary,
     err = np.max(np.abs(f64(O_gpu) - O_ref))
     assert err <= O_TOL[dtype], f"{what}: O max abs err {err:.3e} > {O_TOL[dtype]}"
     return dict(seg_diff=n_seg_diff, tok_diff=n_tok_diff, o_err=float(err))
+
+
+def oracle_workers() -> int:
+    """Threads for per-unit oracle checks: the host's cores, at most 16
+    (the oracle's C entry points release the GIL while they run)."""
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def check_units(w, *, Q, K, V, seg, tok, O, Kg=None, Vg=None, units=None,
+                what: str = "") -> list[dict]:
+    """check_unit on every unit of a launch (or on `units`), in a thread
+    pool.  Q/K/V/O [batch, heads, ...] as the GPU saw them, seg/tok the GPU's
+    index outputs.  Returns the per-unit summaries in unit order."""
+    U = w.units
+
+    def flat(t):
+        return None if t is None else t.reshape(U, *t.shape[2:])
+
+    q, k, v, kg, vg = (flat(t) for t in (Q, K, V, Kg, Vg))
+    sg, tk, o = flat(seg), flat(tok), flat(O)
+    todo = list(range(U)) if units is None else list(units)
+
+    def one(u):
+        return check_unit(
+            Q=q[u], K=k[u], V=v[u], Kg=None if kg is None else kg[u],
+            Vg=None if vg is None else vg[u], levels=w.levels,
+            segments=w.segments, budget=w.budget, wavelet=w.wavelet,
+            boundary=w.boundary, dtype=w.dtype, seg_gpu=sg[u], tok_gpu=tk[u],
+            O_gpu=o[u], what=f"{what} unit {u}")
+
+    with ThreadPoolExecutor(max_workers=oracle_workers()) as ex:
+        return list(ex.map(one, todo))
+
+
+def summary(stats: list[dict]) -> str:
+    """One line over many unit checks: units, allowed index differences
+    inside the tie band, worst output error."""
+    return (f"{len(stats)} units, seg diffs {sum(s['seg_diff'] for s in stats)}, "
+            f"tok diffs {sum(s['tok_diff'] for s in stats)}, "
+            f"max O err {max(s['o_err'] for s in stats):.2e}")

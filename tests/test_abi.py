@@ -216,3 +216,75 @@ def test_recursion_kernel_sequence(wfpkg):
     assert wfpkg.recursive_kernel_names(p) == [
         "rec_tiles_b3", "rec_select_b3", "rec_tiles_b2", "rec_select_b2",
         "rec_tiles_b1", "rec_select_b1", "sparse_attn", "attn_combine"]
+
+
+# ------------------------------------------------------------ binding checks
+
+def _fused_tensors(wfpkg, p):
+    import torch
+    dt = wfpkg.torch_dtype(p)
+    U, d = p.batch * p.heads, p.head_dim
+    return dict(
+        Q=torch.zeros((p.batch, p.heads, p.q_len, d), dtype=dt),
+        K=torch.zeros((p.batch, p.heads, p.ctx_len, d), dtype=dt),
+        V=torch.zeros((p.batch, p.heads, p.ctx_len, d), dtype=dt),
+        O=torch.zeros((p.batch, p.heads, p.q_len, d), dtype=dt),
+        tok=torch.zeros(U * wfpkg.effective_budget(p), dtype=torch.int32),
+        seg=torch.zeros(U * p.segments, dtype=torch.int32))
+
+
+@pytest.mark.parametrize("field,bad,err,needle", [
+    ("K", lambda t: t.to(__import__("torch").bfloat16), TypeError, "K: dtype"),
+    ("V", lambda t: t[:, :, :-1].contiguous(), ValueError, "V:"),
+    ("Q", lambda t: t.double(), TypeError, "Q: dtype"),
+    ("O", lambda t: t[:, :1].contiguous(), ValueError, "O:"),
+    ("tok", lambda t: t[:-1].contiguous(), ValueError, "tok_idx:"),
+    ("seg", lambda t: t.long(), TypeError, "seg_idx: dtype"),
+])
+def test_binding_checks_types_and_sizes(wfpkg, field, bad, err, needle):
+    """The wrappers compare every tensor's element type and count with the
+    parameters before anything reaches the library (the kernels index the
+    buffers by the parameters alone)."""
+    p = _params(wfpkg)
+    t = _fused_tensors(wfpkg, p)
+    t[field] = bad(t[field])
+    with pytest.raises(err, match=needle):
+        wfpkg.wf_filter_attend(p, t["Q"], t["K"], t["V"], None, None, t["O"],
+                               t["tok"], t["seg"], None)
+
+
+def test_binding_checks_the_tail_and_approximation(wfpkg):
+    import torch
+    pg = _params(wfpkg, gen_len=4)
+    t = _fused_tensors(wfpkg, pg)
+    with pytest.raises(ValueError, match="Kg is required"):
+        wfpkg.wf_filter_attend(pg, t["Q"], t["K"], t["V"], None, None, t["O"],
+                               None, None, None)
+    p = _params(wfpkg)
+    t = _fused_tensors(wfpkg, p)
+    A = torch.zeros((p.batch, p.heads, (p.ctx_len >> p.levels) - 1, p.head_dim))
+    with pytest.raises(ValueError, match="approx:"):
+        wfpkg.wf_filter_attend_cached(p, t["Q"], A, t["K"], t["V"], None, None,
+                                      t["O"], None, None, None)
+    K16 = t["K"].to(torch.bfloat16)
+    with pytest.raises(TypeError, match="K: dtype"):
+        wfpkg.wf_dwt_keys(p, K16, A)
+
+
+def test_binding_checks_recursion_outputs(wfpkg):
+    import torch
+    p = _params(wfpkg, levels=3, dtype="bf16")
+    props = [0.5, 0.5, 0.25]
+    counts = wfpkg.recursion_counts(p, props)
+    t = _fused_tensors(wfpkg, p)
+    U = p.batch * p.heads
+    assert wfpkg.kept_elements(p, props) == U * (counts[1] + counts[2])
+    kept = torch.zeros(wfpkg.kept_elements(p, props) + 1, dtype=torch.int32)
+    tok = torch.zeros(U * 2 * counts[0], dtype=torch.int32)
+    with pytest.raises(ValueError, match="kept_idx:"):
+        wfpkg.wf_filter_attend_recursive(p, props, t["Q"], t["K"], t["V"],
+                                         None, None, t["O"], tok, None,
+                                         kept_idx=kept)
+    with pytest.raises(ValueError, match="tok_idx:"):
+        wfpkg.wf_filter_attend_recursive(p, props, t["Q"], t["K"], t["V"],
+                                         None, None, t["O"], tok[1:], None)

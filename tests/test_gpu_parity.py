@@ -2,9 +2,8 @@
 
 Staged calls (wf_dwt_keys -> wf_skim_score -> wf_scan_select -> wf_gather_kv
 -> wf_sparse_attn) are checked stage by stage; the fused wf_filter_attend is
-checked on its region, token and output results, on all five workloads (large
-ones on a deterministic sample of units, the launch itself always covers every
-unit) and on edge shapes: J = 1 and 10, S = 1 and S = L/2^J, k = 1 and k >=
+checked on its region, token and output results, on every unit of all five
+workloads (every layer of the 32-layer one) and on edge shapes: J = 1 and 10, S = 1 and S = L/2^J, k = 1 and k >=
 pool, a generation tail, ragged tiles, query blocks of 1..256 rows, db2 with
 both extensions, constant keys (all scores tie).  Comparison rules: see
 tests/parity.py.
@@ -18,7 +17,7 @@ import torch
 import oracle
 import synth
 from parity import (O_TOL, check_coefficients, check_scores, check_selection,
-                    check_unit, f64, i64, pool_tokens, say)
+                    check_units, f64, i64, pool_tokens, say, summary)
 
 pytestmark = pytest.mark.gpu
 
@@ -145,14 +144,6 @@ def inputs(w, layer: int = 0):
     return _cache[key]
 
 
-def sample_units(w, n: int):
-    U = w.units
-    if U <= n:
-        return list(range(U))
-    rng = np.random.default_rng(1234)
-    return sorted({0, U - 1, *rng.choice(U, n - 2, replace=False).tolist()})
-
-
 def unit(t, w, u):
     if t is None:
         return None
@@ -221,7 +212,7 @@ def test_staged_path(wf, name):
     Q, K, V, Kg, Vg = inputs(w)
     out = run_staged(wf, w, Q, K, V, Kg, Vg)
     keff = min(w.budget, w.segments << w.levels)
-    for u in sample_units(w, 8):
+    for u in range(w.units):
         what = f"{name} unit {u}"
         q, k, v = unit(Q, w, u), unit(K, w, u), unit(V, w, u)
         kg, vg = unit(Kg, w, u), unit(Vg, w, u)
@@ -259,21 +250,13 @@ def test_staged_path(wf, name):
 
 # ------------------------------------------------------------ fused call
 
-def _check_fused(wf, w, layer=0, n_units=8):
+def _check_fused(wf, w, layer=0):
+    """The fused call on one layer, every unit checked against the oracle."""
     Q, K, V, Kg, Vg = inputs(w, layer)
     O, tok, seg = run_fused(wf, w, Q, K, V, Kg, Vg)
-    stats = []
-    for u in sample_units(w, n_units):
-        stats.append(check_unit(
-            Q=unit(Q, w, u), K=unit(K, w, u), V=unit(V, w, u),
-            Kg=unit(Kg, w, u), Vg=unit(Vg, w, u), levels=w.levels,
-            segments=w.segments, budget=w.budget, wavelet=w.wavelet,
-            boundary=w.boundary, dtype=w.dtype, seg_gpu=unit(seg, w, u),
-            tok_gpu=unit(tok, w, u), O_gpu=unit(O, w, u),
-            what=f"{w.name} L{layer} unit {u}"))
-    say(f"[parity] {w.name} layer {layer}: " + ", ".join(
-        f"u: seg±{s['seg_diff']} tok±{s['tok_diff']} err {s['o_err']:.1e}"
-        for s in stats[:4]))
+    stats = check_units(w, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, seg=seg, tok=tok, O=O,
+                        what=f"{w.name} L{layer}")
+    say(f"[parity] {w.name} layer {layer}: {summary(stats)}")
     return O, tok, seg
 
 
@@ -284,11 +267,10 @@ def test_fused_edge_shapes(wf, name):
 
 @pytest.mark.parametrize("name", FULL)
 def test_fused_workloads(wf, name):
+    """Every unit of every layer of the workload."""
     w = synth.WORKLOADS[name]
-    n = {"headline32k": 6, "stress128k": 3, "tail32k": 4}.get(name, 8)
-    layers = [0, w.layers - 1] if w.layers > 1 else [0]
-    for layer in layers:
-        _check_fused(wf, w, layer=layer, n_units=n)
+    for layer in range(w.layers):
+        _check_fused(wf, w, layer=layer)
 
 
 def test_keep_all_equals_dense_attention(wf):
@@ -326,12 +308,15 @@ def test_constant_keys_pick_lowest_indices(wf, dtype, shape):
 
 
 def test_fused_is_deterministic(wf):
+    """Ten calls on the same inputs give bit-identical outputs and indices
+    (no atomics decide an order anywhere on the path)."""
     w = synth.WORKLOADS["layer8b"]
     Q, K, V, _, _ = inputs(w)
-    a = run_fused(wf, w, Q, K, V, None, None)
-    b = run_fused(wf, w, Q, K, V, None, None)
-    for x, y in zip(a, b):
-        assert torch.equal(x, y)
+    first = run_fused(wf, w, Q, K, V, None, None)
+    for r in range(9):
+        again = run_fused(wf, w, Q, K, V, None, None)
+        for x, y in zip(first, again):
+            assert torch.equal(x, y), f"run {r + 2} differs from run 1"
 
 
 @pytest.mark.parametrize("name", ["layer8b", "rem_tok_j3_tail", "tok_j5_b64_long"])
@@ -469,13 +454,9 @@ def test_cached_step(wf, name):
     w = EDGE.get(name) or synth.WORKLOADS[name]
     Q, K, V, Kg, Vg = inputs(w)
     O, tok, seg, _ = run_cached(wf, w, Q, K, V, Kg, Vg)
-    for u in sample_units(w, 6 if w.units > 32 else 8):
-        check_unit(Q=unit(Q, w, u), K=unit(K, w, u), V=unit(V, w, u),
-                   Kg=unit(Kg, w, u), Vg=unit(Vg, w, u), levels=w.levels,
-                   segments=w.segments, budget=w.budget, wavelet=w.wavelet,
-                   boundary=w.boundary, dtype=w.dtype, seg_gpu=unit(seg, w, u),
-                   tok_gpu=unit(tok, w, u), O_gpu=unit(O, w, u),
-                   what=f"{w.name} cached unit {u}")
+    stats = check_units(w, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, seg=seg, tok=tok, O=O,
+                        what=f"{w.name} cached")
+    say(f"[parity] {w.name} cached: {summary(stats)}")
 
 
 def test_cached_steps_reuse_one_approximation(wf):
@@ -516,7 +497,7 @@ def test_grouped_heads(wf, group, B):
                                            V.cuda(), want_indices=True)
     torch.cuda.synchronize()
     O, tok, seg = O.cpu(), tok.cpu(), seg.cpu()
-    for kv in sample_units(w, 6):
+    for kv in range(w.units):
         k, v = unit(K, w, kv), unit(V, w, kv)
         heads = [Qh[0, kv * group + i] for i in range(group)]
         A = oracle.dwt(k, w.levels, w.wavelet)
@@ -548,7 +529,7 @@ def test_dwt_approximation_only(wf, name):
     A = wf.dwt_approx(p, K.cuda())
     torch.cuda.synchronize()
     A = A.cpu()
-    for u in sample_units(w, 8):
+    for u in range(w.units):
         check_coefficients(unit(A, w, u), oracle.dwt(unit(K, w, u), w.levels,
                                                      w.wavelet, w.boundary),
                            f"{w.name} unit {u} A_J")

@@ -1,15 +1,21 @@
 """GPU parity of the multi-scale recursion (wf_filter_attend_recursive)
 against the oracle's R1 (scales B..1, eqs. 9-11) and O7-O8, for Haar and
-Daubechies-2.
+Daubechies-2, on every unit of every case.
 
-The kept positions mu^0 must equal the oracle's exactly (these seeds put no
-weight within rounding of a selection threshold at any scale; a failure
-reports the sizes and the first differing position).  O is checked on the
-GPU's own positions against the oracle's attention, to the tolerance of the
+Each scale is checked conditionally, as the two-stage path's token
+selection is: the oracle transforms and scores the candidates that follow
+from the GPU's own selection at the scale above (eq. 11 over the gathered
+keys, eqs. 7-8), and the GPU's kept candidates must equal the oracle's top
+c_b there except for candidates whose oracle weight lies within 1e-3
+relative of the c_b-th (the stated tie band).  How many picks differed
+inside the band is reported, never asserted.  O is checked on the GPU's own
+positions against the oracle's attention, to the tolerance of the
 two-stage path.  Proportions reach the oracle as the float32 values the
 library receives.
 """
 from __future__ import annotations
+
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import pytest
@@ -17,7 +23,7 @@ import torch
 
 import oracle
 import synth
-from parity import O_TOL, f64, i64, say
+from parity import O_TOL, check_selection, f64, i64, oracle_workers, say
 
 pytestmark = pytest.mark.gpu
 
@@ -92,17 +98,17 @@ def props32(w):
     return [float(np.float32(m)) for m in w.proportions]
 
 
-def run(wf, w, Q, K, V, Kg, Vg):
+def run(wf, w, Q, K, V, Kg, Vg, want_kept=False):
     p = wf.params_for(w)
     dev = "cuda"
     say(f"[gpu] {w.name}: wf_filter_attend_recursive")
-    O, tok = wf.filter_attend_recursive(
+    out = wf.filter_attend_recursive(
         p, w.proportions, Q.to(dev), K.to(dev), V.to(dev),
         Kg.to(dev) if Kg is not None else None,
-        Vg.to(dev) if Vg is not None else None)
+        Vg.to(dev) if Vg is not None else None, want_kept=want_kept)
     torch.cuda.synchronize()
     say(f"[gpu] {w.name}: done")
-    return O.cpu(), tok.cpu()
+    return tuple(x.cpu() for x in out)
 
 
 def unit(t, w, u):
@@ -111,39 +117,81 @@ def unit(t, w, u):
     return t.reshape(w.units, *t.shape[2:])[u]
 
 
-def sample_units(w, n):
-    if w.units <= n:
-        return list(range(w.units))
-    rng = np.random.default_rng(4321)
-    return sorted({0, w.units - 1, *rng.choice(w.units, n - 2, replace=False).tolist()})
+def kept_of_scale(kept, w, counts, b):
+    """Scale b's kept block ids [units][c_b] from the packed kept_idx."""
+    U = w.units
+    at = U * sum(counts[b:])          # c_B + ... + c_{b+1}, per unit
+    return kept[at:at + U * counts[b - 1]].reshape(U, counts[b - 1])
 
 
-def check(wf, w, n_units=8):
+def check_unit_scales(w, counts, q, k, v, kg, vg, kept_u, tok_u, O_u, what):
+    """Every scale of one unit, conditioned on the GPU's selection above it;
+    returns (picks that differed inside the tie band, O error)."""
+    B = w.levels
+    Lf = (w.ctx_len >> B) << B
+    mu = np.arange(Lf)
+    diffs = 0
+    tok = i64(tok_u)
+    for b in range(B, 0, -1):
+        run_ = 1 << b
+        A = oracle.dwt(k[torch.from_numpy(mu)], b, w.wavelet, w.boundary)
+        W = oracle.skim(q, A)
+        cand = mu[::run_] >> b          # prompt block of each candidate
+        if b >= 2:
+            got = i64(kept_u[b])
+        else:
+            assert np.all(tok[1::2] == tok[0::2] + 1), f"{what}: mu^0 not block pairs"
+            got = tok[0::2] >> 1
+        pos = np.searchsorted(cand, got)
+        assert np.all(pos < cand.size) and np.all(cand[np.minimum(pos, cand.size - 1)] == got), \
+            f"{what}: scale {b} kept a block that was no candidate"
+        diffs += check_selection(pos, W, counts[b - 1], f"{what} scale {b}")
+        mu = (got[:, None] * run_ + np.arange(run_)[None, :]).ravel()
+    assert np.array_equal(mu, tok), f"{what}: mu^0 is not the last scale's blocks"
+    pos_all = np.concatenate([tok, np.arange(Lf, w.ctx_len)])
+    ref = oracle.attend(q, k, v, pos_all, kg, vg)
+    err = float(np.abs(f64(O_u) - ref).max())
+    assert err <= O_TOL[w.dtype], f"{what}: O err {err:.3e}"
+    return diffs, err
+
+
+def check(wf, w):
     Q, K, V, Kg, Vg = inputs(w)
-    O, tok = run(wf, w, Q, K, V, Kg, Vg)
+    O, tok, kept = run(wf, w, Q, K, V, Kg, Vg, want_kept=True)
     counts = wf.recursion_counts(wf.params_for(w), w.proportions)
     assert tok.shape[-1] == 2 * counts[0]
+    scales = {b: kept_of_scale(kept, w, counts, b) for b in range(2, w.levels + 1)}
+    U = w.units
+    Qf, Kf, Vf = (x.reshape(U, *x.shape[2:]) for x in (Q, K, V))
+    Kgf = Kg.reshape(U, *Kg.shape[2:]) if Kg is not None else None
+    Vgf = Vg.reshape(U, *Vg.shape[2:]) if Vg is not None else None
+
+    def one(u):
+        return check_unit_scales(
+            w, counts, Qf[u], Kf[u], Vf[u],
+            None if Kgf is None else Kgf[u], None if Vgf is None else Vgf[u],
+            {b: scales[b][u] for b in scales}, unit(tok, w, u),
+            unit(O, w, u), f"{w.name} unit {u}")
+
+    with ThreadPoolExecutor(max_workers=oracle_workers()) as ex:
+        res = list(ex.map(one, range(U)))
     Lf = (w.ctx_len >> w.levels) << w.levels
-    errs = []
-    for u in sample_units(w, n_units):
-        q, k, v = unit(Q, w, u), unit(K, w, u), unit(V, w, u)
-        kg, vg = unit(Kg, w, u), unit(Vg, w, u)
-        want, want_counts = oracle.recursive_select(q, k, w.levels, props32(w),
-                                                    w.wavelet, w.boundary)
-        assert list(want_counts) == counts, f"{w.name} unit {u}: counts"
-        got = np.concatenate([i64(unit(tok, w, u)), np.arange(Lf, w.ctx_len)])
-        if not np.array_equal(got, want):
-            bad = int(np.argmax(got != want)) if got.size == want.size else -1
-            raise AssertionError(
-                f"{w.name} unit {u}: mu^0 differs (sizes {got.size}/{want.size}, "
-                f"first difference at {bad})")
-        ref = oracle.attend(q, k, v, got, kg, vg)
-        err = float(np.abs(f64(unit(O, w, u)) - ref).max())
-        assert err <= O_TOL[w.dtype], f"{w.name} unit {u}: O err {err:.3e}"
-        errs.append(err)
-    say(f"[parity] {w.name}: {len(errs)} units, |mu^0| = {2 * counts[0]} "
-        f"(+{w.ctx_len - Lf} kept), "
-        f"max O err {max(errs):.1e}")
+    say(f"[parity] {w.name}: {U} units, |mu^0| = {2 * counts[0]} "
+        f"(+{w.ctx_len - Lf} kept), picks differing inside the tie band "
+        f"{sum(r[0] for r in res)}, max O err {max(r[1] for r in res):.1e}")
+
+
+def test_recursion_counts_equal_the_oracle(wf):
+    """The library's c_b are the oracle's (same float32 proportions)."""
+    for w in list(CASES.values()) + [synth.WORKLOADS["recursion8b"],
+                                     synth.WORKLOADS["recursion32k"]]:
+        counts = wf.recursion_counts(wf.params_for(w), w.proportions)
+        Lf = (w.ctx_len >> w.levels) << w.levels
+        n, want = Lf >> w.levels, [0] * w.levels
+        for b in range(w.levels, 0, -1):
+            want[b - 1] = oracle.recursion_count(props32(w)[b - 1], n)
+            n = 2 * want[b - 1]
+        assert counts == want, w.name
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -178,13 +226,15 @@ def test_recursion_constant_keys_keep_the_first_positions(wf, dtype):
 
 @pytest.mark.parametrize("name", ["recursion8b", "recursion32k"])
 def test_recursion_workloads(wf, name):
-    w = synth.WORKLOADS[name]
-    check(wf, w, n_units=8 if name == "recursion8b" else 4)
+    check(wf, synth.WORKLOADS[name])
 
 
 def test_recursion_is_deterministic(wf):
+    """Ten calls give bit-identical outputs and kept sets."""
     w = CASES["rec_bf16_b5_b64"]
     Q, K, V, _, _ = inputs(w)
-    a = run(wf, w, Q, K, V, None, None)
-    b = run(wf, w, Q, K, V, None, None)
-    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    first = run(wf, w, Q, K, V, None, None, want_kept=True)
+    for r in range(9):
+        again = run(wf, w, Q, K, V, None, None, want_kept=True)
+        for x, y in zip(first, again):
+            assert torch.equal(x, y), f"run {r + 2} differs from run 1"
