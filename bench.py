@@ -134,6 +134,57 @@ def measured_traffic(kernel: str, workload: str):
     return int(fields["traffic_bytes_per_launch"])
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or "" if unknown."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
+def measured_bandwidth(torch, dev, nbytes: int = 1 << 30, reps: int = 10) -> dict:
+    """The HBM rate this machine reaches with a plain device copy of nbytes
+    (bytes read + bytes written over the time; best of `reps` launches)."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    best = float("inf")
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        b.synchronize()
+        best = min(best, a.elapsed_time(b))
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"copy_GBs": 2 * nbytes / (best * 1e-3) / 1e9}
+
+
+def needle_recall(w, tok, layer: int = 0) -> dict:
+    """Share of the planted needle tokens (16-token spans) that the selection
+    kept, per unit: reported, never asserted (it depends on the data)."""
+    import numpy as np
+
+    import synth
+    t = tok.reshape(w.batch, w.heads, -1).cpu().numpy()
+    rec = []
+    for b in range(w.batch):
+        span = np.concatenate([np.arange(s, s + synth.NEEDLE_LEN)
+                               for s in synth.needle_starts(w, layer, b)])
+        for h in range(w.heads):
+            rec.append(np.isin(span, t[b, h]).mean())
+    return {"mean": float(np.mean(rec)), "min": float(np.min(rec)),
+            "units": len(rec), "needle_tokens_per_sequence": int(span.size)}
+
+
 def cpu_baseline(w, Q, K, V, Kg=None, Vg=None, min_seconds: float = 10.0) -> dict:
     """The oracle as it stands, on every unit of the layer, in chunks of 16
     units, repeated until about min_seconds of oracle time have passed (at
@@ -173,7 +224,8 @@ def cpu_baseline(w, Q, K, V, Kg=None, Vg=None, min_seconds: float = 10.0) -> dic
     note = ("; the oracle recomputes A_J instead of reusing it"
             if getattr(w, "cached", False) else "")
     return {"value": tokens / elapsed, "unit": "tokens/s",
-            "cores": oracle.max_threads(), "kind": "oracle",
+            "cores": oracle.max_threads(), "cpu_model": cpu_model(),
+            "kind": "oracle",
             "sample": f"all {U} (batch, head) units of one {w.name} layer, "
                       f"{passes} passes, fp64, OpenMP over units, {chunk} "
                       f"units per call; {elapsed:.2f} s{note}",
@@ -365,6 +417,13 @@ def main() -> int:
         return step_ms[min(len(step_ms) - 1, int(round(q * (len(step_ms) - 1))))]
     ev.close()
 
+    # which tokens the selection kept on copy 0 (layer 0): one more plain call
+    call_plain(copies[0])
+    torch.cuda.synchronize()
+    recall = needle_recall(w, tok)
+    print("[bench] measuring the copy rate", file=sys.stderr, flush=True)
+    hbm = measured_bandwidth(torch, dev)
+
     alg = algorithmic_bytes(w, keff, counts)
     U = w.units
     tokens = w.batch * w.ctx_len * nl
@@ -410,6 +469,17 @@ def main() -> int:
             "avg_launch_ms": dom_ms,
         },
         "path_hbm_frac": alg["total"] * U * nl / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        # the same rates against what plain copy / read kernels reach on
+        # this box (the vendor's 8 TB/s is the roofline's peak)
+        "hbm_measured": {
+            **hbm,
+            "kind": "best of 10 timed torch copy_ of 1 GiB on this GPU "
+                    "(read + write bytes over time)",
+            "dominant_frac_of_copy": achieved / hbm["copy_GBs"],
+            "path_frac_of_copy": alg["total"] * U * nl / (ms_step * 1e-3) / 1e9
+                                 / hbm["copy_GBs"],
+        },
+        "needle_recall": recall,
         "path_algorithmic_bytes": alg["total"] * U * nl,
         "kernel_ms": per_kernel,
         "ms_per_step_with_events": ms_step_events,

@@ -203,7 +203,10 @@ def _remainder(p) -> int:
     return p.ctx_len - ((p.ctx_len >> p.levels) << p.levels)
 
 
-def _expect_qkv(p, Q=None, K=None, V=None, Kg=None, Vg=None, O=None) -> None:
+def _expect_qkv(p, Q=None, K=None, V=None, Kg=None, Vg=None, O=None,
+                tail: bool = False) -> None:
+    """Q/O, K/V (when given) and, for calls that read the generation tail,
+    Kg/Vg (required iff gen_len > 0)."""
     dt, U, d = torch_dtype(p), _units(p), p.head_dim
     for name, t in (("Q", Q), ("O", O)):
         if t is not None:
@@ -211,8 +214,9 @@ def _expect_qkv(p, Q=None, K=None, V=None, Kg=None, Vg=None, O=None) -> None:
     for name, t in (("K", K), ("V", V)):
         if t is not None:
             _expect(t, name, dt, U * p.ctx_len * d)
-    for name, t in (("Kg", Kg), ("Vg", Vg)):
-        _expect(t, name, dt, U * p.gen_len * d, nullable=p.gen_len == 0)
+    if tail:
+        for name, t in (("Kg", Kg), ("Vg", Vg)):
+            _expect(t, name, dt, U * p.gen_len * d, nullable=p.gen_len == 0)
 
 
 def _ws(t) -> tuple[int | None, int]:
@@ -284,7 +288,7 @@ def wf_scan_select(p, Q, K, seg_idx, tok_score, tok_idx, workspace,
 
 def wf_gather_kv(p, K, V, tok_idx, Kg, Vg, Ks, Vs, stream=None):
     U, keff = _units(p), effective_budget(p)
-    _expect_qkv(p, K=K, V=V, Kg=Kg, Vg=Vg)
+    _expect_qkv(p, K=K, V=V, Kg=Kg, Vg=Vg, tail=True)
     _expect(tok_idx, "tok_idx", torch.int32, U * keff)
     rows = keff + _remainder(p) + p.gen_len
     for name, t in (("Ks", Ks), ("Vs", Vs)):
@@ -304,7 +308,7 @@ def wf_sparse_attn(p, Q, Ks, Vs, n_kv, O, workspace, stream=None):
 
 
 def _expect_fused(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx) -> None:
-    _expect_qkv(p, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, O=O)
+    _expect_qkv(p, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, O=O, tail=True)
     _expect(tok_idx, "tok_idx", torch.int32, _units(p) * effective_budget(p),
             nullable=True)
     _expect(seg_idx, "seg_idx", torch.int32, _units(p) * p.segments,
@@ -470,7 +474,7 @@ def kept_elements(p: WfParams, proportions) -> int:
 
 def _expect_recursive(p, proportions, Q, K, V, Kg, Vg, O, tok_idx,
                       kept_idx) -> None:
-    _expect_qkv(p, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, O=O)
+    _expect_qkv(p, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, O=O, tail=True)
     counts = recursion_counts(p, proportions)
     _expect(tok_idx, "tok_idx", torch.int32, _units(p) * 2 * counts[0],
             nullable=True)

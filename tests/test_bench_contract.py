@@ -61,3 +61,25 @@ def test_cached_step_reads_the_approximation_not_the_keys():
 def test_counter_summary_is_ignored_for_another_kernel_or_workload():
     assert bench.measured_traffic("skim_tile", "headline32k") is None
     assert bench.measured_traffic("token_skim", "long16k") is None
+
+
+def test_needle_recall_counts_kept_needle_tokens():
+    """needle_recall: the share of planted needle tokens in the selection."""
+    import numpy as np
+    import torch
+    w = synth.small_variant(synth.WORKLOADS["tiny"], name="nr", needles=2,
+                            batch=2, heads=3)
+    spans = [np.concatenate([np.arange(s, s + synth.NEEDLE_LEN)
+                             for s in synth.needle_starts(w, 0, b)])
+             for b in range(w.batch)]
+    tok = torch.zeros((w.batch, w.heads, 2 * synth.NEEDLE_LEN), dtype=torch.int32)
+    for b in range(w.batch):
+        tok[b] = torch.from_numpy(np.sort(spans[b]).astype(np.int32))
+    tok[1, 2, :8] = -1                       # one unit misses 8 needle tokens
+    r = bench.needle_recall(w, tok)
+    assert r["units"] == 6 and r["min"] == 0.75
+    assert abs(r["mean"] - (5 + 0.75) / 6) < 1e-12
+
+
+def test_cpu_model_is_a_string():
+    assert isinstance(bench.cpu_model(), str)

@@ -265,12 +265,11 @@ def test_fused_edge_shapes(wf, name):
     _check_fused(wf, EDGE[name])
 
 
-@pytest.mark.parametrize("name", FULL)
-def test_fused_workloads(wf, name):
-    """Every unit of every layer of the workload."""
-    w = synth.WORKLOADS[name]
-    for layer in range(w.layers):
-        _check_fused(wf, w, layer=layer)
+@pytest.mark.parametrize("name,layer", [
+    (n, l) for n in FULL for l in range(synth.WORKLOADS[n].layers)])
+def test_fused_workloads(wf, name, layer):
+    """Every unit of the workload; the 32-layer one layer by layer."""
+    _check_fused(wf, synth.WORKLOADS[name], layer=layer)
 
 
 def test_keep_all_equals_dense_attention(wf):
