@@ -91,7 +91,9 @@ enum { WF_OP_SKIM = 0, WF_OP_SCAN = 1, WF_OP_ATTN = 2, WF_OP_FUSED = 3,
 /* Limits of this build. */
 enum {
     WF_MAX_LEVELS = 10,  /* J                                   */
-    WF_MAX_Q_LEN = 256   /* B, rows of the query block          */
+    WF_MAX_Q_LEN = 256,  /* B, rows of the query block          */
+    /* scratch bytes per device of wf_filter_attend_noalloc (32 MiB) */
+    WF_NOALLOC_SCRATCH_BYTES = 33554432
 };
 
 typedef struct wf_params {
@@ -219,6 +221,29 @@ wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
                                  int32_t* seg_idx, void* workspace,
                                  size_t workspace_bytes, void* stream,
                                  void** events, int32_t n_events);
+
+/*
+ * wf_filter_attend for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, hosts that forbid
+ * allocation.  Same arguments and results as wf_filter_attend, without the
+ * workspace: the library's own scratch array of WF_NOALLOC_SCRATCH_BYTES
+ * bytes per device (a device-side static, loaded with the library's code on
+ * each device it runs on and held until the process ends) takes its place.
+ * The call allocates and frees nothing.
+ *   Limit: parameters whose fused workspace (wf_workspace_bytes(p,
+ *   WF_OP_FUSED)) exceeds WF_NOALLOC_SCRATCH_BYTES are rejected with
+ *   WF_ERR_WORKSPACE before anything is queued.
+ *   Every call on one device shares that device's scratch, which keeps the
+ *   last call's contents (nothing in it needs to start at zero): two calls
+ *   whose kernels overlap on one device -- on different streams, or from
+ *   different host threads without ordering -- race and give undefined
+ *   results.  Calls queued on one stream are ordered and safe.
+ */
+wf_status wf_filter_attend_noalloc(const wf_params* p, const void* Q,
+                                   const void* K, const void* V,
+                                   const void* Kg, const void* Vg, void* O,
+                                   int32_t* tok_idx, int32_t* seg_idx,
+                                   void* stream);
 
 /* Kernels one wf_filter_attend call queues for these parameters, and the
  * name of the i-th one (static strings), or -1 / NULL if p is invalid. */

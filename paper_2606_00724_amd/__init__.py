@@ -22,6 +22,7 @@ EXT_SYMMETRIC, EXT_PERIODIC = 0, 1
 BF16, F32 = 0, 1
 OP_SKIM, OP_SCAN, OP_ATTN, OP_FUSED, OP_CACHED = 0, 1, 2, 3, 4
 MAX_LEVELS, MAX_Q_LEN = 10, 256
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 _STATUS = {0: "WF_OK", 1: "WF_ERR_INVALID_ARG", 2: "WF_ERR_UNSUPPORTED",
            3: "WF_ERR_WORKSPACE", 4: "WF_ERR_HIP"}
@@ -29,6 +30,7 @@ _STATUS = {0: "WF_OK", 1: "WF_ERR_INVALID_ARG", 2: "WF_ERR_UNSUPPORTED",
 EXPORTED = ("wf_workspace_bytes", "wf_effective_budget", "wf_dwt_keys",
             "wf_skim_score", "wf_scan_select", "wf_gather_kv",
             "wf_sparse_attn", "wf_filter_attend", "wf_filter_attend_timed",
+            "wf_filter_attend_noalloc",
             "wf_filter_attend_kernels", "wf_filter_attend_kernel_name",
             "wf_filter_attend_cached", "wf_filter_attend_cached_timed",
             "wf_filter_attend_cached_kernels",
@@ -79,6 +81,8 @@ def _load() -> ctypes.CDLL:
         "wf_filter_attend_timed": (ctypes.c_int,
                                    [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                     vp, ctypes.POINTER(vp), i32]),
+        "wf_filter_attend_noalloc": (ctypes.c_int,
+                                     [P, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "wf_filter_attend_kernels": (i32, [P]),
         "wf_filter_attend_kernel_name": (ctypes.c_char_p, [P, i32]),
         "wf_filter_attend_cached": (ctypes.c_int,
@@ -322,6 +326,17 @@ def wf_filter_attend(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
     _check(_lib.wf_filter_attend(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V),
                                  _ptr(Kg), _ptr(Vg), _ptr(O), _ptr(tok_idx),
                                  _ptr(seg_idx), ws, nb, _stream(stream)))
+
+
+def wf_filter_attend_noalloc(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
+                             stream=None):
+    """wf_filter_attend on the library's own per-device scratch: no
+    workspace, nothing allocated (calls that overlap on one GPU race)."""
+    _expect_fused(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx)
+    _check(_lib.wf_filter_attend_noalloc(ctypes.byref(p), _ptr(Q), _ptr(K),
+                                         _ptr(V), _ptr(Kg), _ptr(Vg), _ptr(O),
+                                         _ptr(tok_idx), _ptr(seg_idx),
+                                         _stream(stream)))
 
 
 def wf_filter_attend_timed(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,

@@ -4,6 +4,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "wf_kernels.hpp"
 #include "wf_launch.hpp"
 
@@ -288,6 +290,56 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
                           part, pstat, s)));
   WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
   return ok();
+}
+
+// ------------------------------------------------------------ no allocation
+//
+// wf_filter_attend_noalloc runs the fused sequence on a workspace that the
+// library owns: a file-scope device array, one copy per device, present from
+// the load of the code object until the process ends.  Host code never
+// passes `scratch` itself (in host code the name is a host-side stand-in, not
+// a device address); it passes the address hipGetSymbolAddress reports for
+// the current device, looked up once per device.
+constexpr size_t kScratchBytes = (size_t)WF_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+static wf_status scratch_of_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(WF_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(WF_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(WF_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return WF_OK;
+}
+
+static wf_status noalloc_impl(const wf_params* p, const void* Q, const void* K,
+                              const void* V, const void* Kg, const void* Vg, void* O,
+                              int32_t* tok_idx, int32_t* seg_idx, void* stream) {
+  WF_TRY(check_params(p));
+  const long nrows = keff_of(*p) + remainder_len(*p) + p->gen_len;
+  const size_t need = layout_for(*p, WF_OP_FUSED, nrows).total;
+  if (need > kScratchBytes)
+    return fail(WF_ERR_WORKSPACE,
+                "these parameters need %zu bytes of scratch; the allocation-free entry "
+                "point holds %zu (use wf_filter_attend with a workspace)",
+                need, kScratchBytes);
+  void* ws = nullptr;
+  WF_TRY(scratch_of_current_device(&ws));
+  return fused_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, ws, kScratchBytes, stream,
+                    nullptr, 0);
 }
 
 // ------------------------------------------------------------ cached A_J
@@ -640,6 +692,12 @@ wf_status wf_filter_attend_timed(const wf_params* p, const void* Q,
     if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
   return fused_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
                     workspace_bytes, stream, events, n_events);
+}
+
+wf_status wf_filter_attend_noalloc(const wf_params* p, const void* Q, const void* K,
+                                   const void* V, const void* Kg, const void* Vg, void* O,
+                                   int32_t* tok_idx, int32_t* seg_idx, void* stream) {
+  return noalloc_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, stream);
 }
 
 int32_t wf_filter_attend_kernels(const wf_params* p) {

@@ -288,3 +288,20 @@ def test_binding_checks_recursion_outputs(wfpkg):
     with pytest.raises(ValueError, match="tok_idx:"):
         wfpkg.wf_filter_attend_recursive(p, props, t["Q"], t["K"], t["V"],
                                          None, None, t["O"], tok[1:], None)
+
+
+def test_noalloc_rejects_oversized_parameters_on_the_host(wfpkg):
+    """The allocation-free entry point refuses parameters whose workspace is
+    larger than its scratch, before touching the device."""
+    p = _params(wfpkg, batch=4, heads=32, ctx_len=32768, head_dim=128,
+                q_len=64, levels=5, segments=128, budget=2048, dtype="bf16")
+    assert wfpkg.workspace_bytes(p, wfpkg.OP_FUSED) > wfpkg.NOALLOC_SCRATCH_BYTES
+    lib = wfpkg.library()
+    fake = ctypes.c_void_p(0x10000)
+    rc = lib.wf_filter_attend_noalloc(ctypes.byref(p), fake, fake, fake, None,
+                                      None, fake, None, None, None)
+    assert rc == 3 and b"scratch" in lib.wf_last_error()
+    bad = _params(wfpkg, head_dim=96)
+    assert lib.wf_filter_attend_noalloc(ctypes.byref(bad), fake, fake, fake,
+                                        None, None, fake, None, None,
+                                        None) == 2
