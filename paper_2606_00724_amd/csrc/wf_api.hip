@@ -147,8 +147,9 @@ static long keff_of(const wf_params& p) {
 
 // Regions of the workspace, each 256-byte aligned.  The fused entry point on
 // the token-level path keeps a log-sum-exp per (block, query) beside each
-// coarse logit instead of the scan's per-workgroup statistics, and its
-// cstats region holds the pool's final (max, sum) pair per query.
+// coarse logit instead of the scan's per-workgroup statistics (the scan
+// forms the pool normalisers from them on chip), and its attention keeps the
+// selected tokens on chip.
 static Layout layout_for(const wf_params& p, int op, long attn_rows) {
   Layout l;
   const size_t U = (size_t)p.batch * p.heads, B = p.q_len;
@@ -179,11 +180,13 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     l.seg = take(U * p.segments * sizeof(int32_t));
   }
   if (scan) {
+    // the token-level path forms the pool normalisers inside the scan
     const ScanPlan cp = plan_scan(p);
-    l.cstats = take(U * (fast ? 1 : cp.chunks) * 2 * B * sizeof(float));
+    if (!fast) l.cstats = take(U * cp.chunks * 2 * B * sizeof(float));
     l.wpool = take(U * P * sizeof(float));
   }
-  if (whole) l.tok = take(U * keff_of(p) * sizeof(int32_t));
+  // the token-level attention keeps its selected tokens on chip
+  if (whole && !fast) l.tok = take(U * keff_of(p) * sizeof(int32_t));
   if (attn) {
     const AttnPlan ap = plan_attn(p, attn_rows);
     l.part = take(U * ap.splits * B * p.head_dim * sizeof(float));
@@ -215,11 +218,10 @@ static const char* const kGeneralNames[] = {
     "skim_tile", "skim_select", "scan_stats", "scan_weights",
     "scan_select", "sparse_attn", "attn_combine"};
 static const char* const kFastNames[] = {
-    "token_skim", "skim_select", "scan_weights", "scan_select",
-    "sparse_attn", "attn_combine"};
+    "token_skim", "block_weights", "scan_weights", "sparse_attn", "attn_combine"};
 constexpr int kMaxFusedKernels = 7;
 
-static int fused_kernels(const wf_params& p) { return fast_path(p) ? 6 : 7; }
+static int fused_kernels(const wf_params& p) { return fast_path(p) ? 5 : 7; }
 static const char* const* fused_names(const wf_params& p) {
   return fast_path(p) ? kFastNames : kGeneralNames;
 }
@@ -275,19 +277,23 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
   };
   WF_HIP(mark(), "hipEventRecord");
   if (fast_path(*p)) {
+    // token logits -> block rows; W of every block; the scan takes the top-S
+    // regions and the attention the top-k tokens themselves
     WF_TRY(step(launch_token_skim(*p, Q, K, logits, sstats, s)));
-    WF_TRY(step(launch_fast_select(*p, logits, sstats, W, seg, cstats, s)));
-    WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s, 1)));
+    WF_TRY(step(launch_block_weights(*p, logits, sstats, W, s)));
+    WF_TRY(step(launch_scan_select_weights(*p, Q, K, W, logits, seg, wpool, s)));
+    WF_TRY(step(launch_attn_select(*p, Q, K, V, wpool, seg, tok_idx, Kg, Vg, nrows, part,
+                                   pstat, s)));
   } else {
     const SkimPlan sp = plan_skim(*p, true);
     WF_TRY(step(launch_skim_tiles(*p, true, Q, K, nullptr, logits, sstats, s)));
     WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
     WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
     WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s)));
+    WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
+    WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
+                            part, pstat, s)));
   }
-  WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
-  WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
-                          part, pstat, s)));
   WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
   return ok();
 }

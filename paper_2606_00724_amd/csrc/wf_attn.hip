@@ -387,7 +387,11 @@ struct RingRowPtr {
 // are split over two waves.
 constexpr int kAttnRingBlock = 512;
 
-template <int D>
+// SEL (token-level path): the workgroup first takes the unit's top-nsel
+// tokens of the scan weights itself (eq. 9 over the pool; ties to the lower
+// pool position, which is the lower token) and keeps the ascending ids of
+// its split; tok_out (nullable) receives them.
+template <int D, bool SEL = false>
 __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
   constexpr int NW = kAttnRingBlock / kWave;
   constexpr int CR = kRingRows;
@@ -406,7 +410,30 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, col = lane & 15;
 
-  if (a.tok) {
+  if constexpr (SEL) {
+    // the selection's histograms, the unit's region ids and (when they fit)
+    // its scan weights in the ring, which is free until the first chunk
+    auto& sh = *reinterpret_cast<SelectShared<kAttnRingBlock>*>(ring);
+    int32_t* segl = reinterpret_cast<int32_t*>(ring + sizeof(SelectShared<kAttnRingBlock>));
+    float* Wl = reinterpret_cast<float*>(segl + a.S);
+    const float* Wg = a.wpool + (long)u * a.P;
+    for (int i = threadIdx.x; i < a.S; i += kAttnRingBlock) segl[i] = a.seg[(long)u * a.S + i];
+    if (a.w_in_lds)
+      for (int i = threadIdx.x; i < a.P; i += kAttnRingBlock) Wl[i] = Wg[i];
+    __syncthreads();
+    const long hi = min(re0, (long)a.nsel);
+    const int J = a.J, mask = (1 << J) - 1;
+    int32_t* tout = a.tok_out ? a.tok_out + (long)u * a.nsel : nullptr;
+    block_select_topk<kAttnRingBlock>(a.w_in_lds ? Wl : Wg, a.P, a.nsel,
+                                      [&](uint32_t pos, int pp) {
+                                        if ((long)pos >= rb0 && (long)pos < hi) {
+                                          const int32_t t = (segl[pp >> J] << J) | (pp & mask);
+                                          toks[pos - rb0] = t;
+                                          if (tout) tout[pos] = t;
+                                        }
+                                      },
+                                      sh);
+  } else if (a.tok) {
     const long hi = min(re0, (long)a.nsel);
     for (long i = rb0 + threadIdx.x; i < hi; i += kAttnRingBlock)
       toks[i - rb0] = a.tok[(long)u * a.nsel + i];
@@ -418,8 +445,9 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
   vp.base = reinterpret_cast<const bf16_t*>(a.V);
   kp.tail = reinterpret_cast<const bf16_t*>(a.Kg);
   vp.tail = reinterpret_cast<const bf16_t*>(a.Vg);
-  kp.toks = vp.toks = a.tok ? toks : nullptr;
-  kp.unit_rows = vp.unit_rows = a.tok ? (long)a.L : (long)a.nrows;
+  const bool indexed = SEL || a.tok != nullptr;
+  kp.toks = vp.toks = indexed ? toks : nullptr;
+  kp.unit_rows = vp.unit_rows = indexed ? (long)a.L : (long)a.nrows;
   kp.rlast = vp.rlast = re0 - 1;
   kp.split_r0 = vp.split_r0 = rb0;
   kp.u = vp.u = u;
@@ -450,7 +478,7 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
   const int split_last = (int)(re0 - 1 - rb0);
   auto issue_kv = [&](int c, uint32_t slot) {
     const long r0 = rb0 + (long)c * CR;
-    if (a.tok && min(r0 + CR, re0) <= (long)a.nsel) {
+    if (indexed && min(r0 + CR, re0) <= (long)a.nsel) {
       constexpr int RPI = 64 / G;
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
@@ -460,12 +488,12 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
         // token ids are clamped into the unit: a bad id cannot leave K / V
         const int t = min(max(toks[min((int)(r0 - rb0) + r, split_last)], 0), a.L - 1);
         const long off = (long)t * D + 8 * k;
-        async_load16<false>(kunit + off, __builtin_amdgcn_readfirstlane(slot + 1024u * inst));
+        async_load16<true>(kunit + off, __builtin_amdgcn_readfirstlane(slot + 1024u * inst));
         async_load16<true>(vunit + off, __builtin_amdgcn_readfirstlane(slot + CHB + 1024u * inst));
       }
     } else {
       kp.r0 = vp.r0 = r0;
-      issue_chunk<CR, G, NW>(slot, kp);
+      issue_chunk<CR, G, NW, true>(slot, kp);
       issue_chunk<CR, G, NW, true>(slot + CHB, vp);
     }
   };
@@ -870,6 +898,57 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
                 : attn_launch<bf16_t, 64>(a, pl.lds_bytes, s);
   return d128 ? attn_launch<float, 128>(a, pl.lds_bytes, s)
               : attn_launch<float, 64>(a, pl.lds_bytes, s);
+}
+
+hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, const void* V,
+                              const float* wpool, const int32_t* seg, int32_t* tok_out,
+                              const void* Kg, const void* Vg, long nrows, float* part,
+                              float* pstat, hipStream_t s) {
+  if (p.dtype != WF_BF16 || p.segments > kSelectLdsSegs) return hipErrorInvalidValue;
+  const AttnPlan pl = plan_attn(p, nrows);
+  if (pl.nbuf < 2) return hipErrorInvalidValue;
+  AttnArgs a{};
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.tok = nullptr;
+  a.wpool = wpool;
+  a.seg = seg;
+  a.tok_out = tok_out;
+  a.Kg = Kg;
+  a.Vg = Vg;
+  a.part = part;
+  a.pstat = pstat;
+  a.U = p.batch * p.heads;
+  a.L = p.ctx_len;
+  a.B = p.q_len;
+  a.nsel = wf_effective_budget(&p);
+  a.P = p.segments << p.levels;
+  a.S = p.segments;
+  a.J = p.levels;
+  a.G = p.gen_len;
+  a.Lf = filtered_len(p);
+  a.R = (int)remainder_len(p);
+  a.nrows = (int)nrows;
+  a.NS = pl.splits;
+  a.rps = pl.rps;
+  a.nbuf = pl.nbuf;
+  a.scale = effective_scale(p);
+  // the unit's scan weights in the ring beside the histograms and region
+  // ids when they fit
+  const size_t ring = (size_t)pl.nbuf * 2 * kRingRows * 2 * p.head_dim;
+  const size_t fixed = sizeof(SelectShared<kAttnRingBlock>) + (size_t)a.S * sizeof(int32_t);
+  if (fixed > ring) return hipErrorInvalidValue;
+  a.w_in_lds = fixed + (size_t)a.P * sizeof(float) <= ring ? 1 : 0;
+  auto kern = p.head_dim == 128 ? attn_ring_kernel<128, true> : attn_ring_kernel<64, true>;
+  if (pl.lds_bytes > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)pl.lds_bytes);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)(a.U * a.NS)), dim3(kAttnRingBlock), pl.lds_bytes, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_attn_combine(const wf_params& p, long nrows,

@@ -570,195 +570,82 @@ __global__ __launch_bounds__(kTokBlock, 2) void token_db2_kernel(TokenSkimArgs a
   }
 }
 
-// One workgroup per unit: the coarse softmax normalisers (merged over the
-// ranges), W (eq. 8), the top-S regions (eq. 9), then the scan's pool
-// normalisers from the selected blocks' token statistics.
-constexpr int kFastSelectBlock = 1024;
+// W (eq. 8) of every coarse block from the token skim's block rows.  The
+// coarse softmax normalisers of a unit are its ranges' (max, sum of exp)
+// pairs merged; then W_j = sum_q exp(l_qj - M_q) / Z_q.  Each workgroup takes
+// one slice of one unit's blocks, so that the whole GPU reads the block rows
+// (one workgroup per unit leaves most of it idle); the top-S selection of
+// eq. 9 is taken by the workgroups of the scan that follows.
+constexpr int kWeightsBlock = 256;
 
-__global__ __launch_bounds__(kFastSelectBlock) void fast_select_kernel(FastSelectArgs a,
-                                                                       int w_in_lds,
-                                                                       int seg_in_lds) {
-  constexpr int NT = kFastSelectBlock;
+__global__ __launch_bounds__(kWeightsBlock) void block_weights_kernel(BlockWeightsArgs a) {
   __shared__ float row_c[16 * kFastMaxQBlocks];
-  __shared__ float pool_m[16 * (16 * kFastMaxQBlocks + 1)], pool_z[16 * (16 * kFastMaxQBlocks + 1)];
-  __shared__ SelectShared<NT> sh;
-  extern __shared__ float wsh[];  // W (when it fits), then the picked block ids
   // the unit on the XCD whose L2 took its block rows from the token skim
-  const int u = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / a.WPU, slice = item % a.WPU;
   const int B = a.B, nJ = a.nJ;
-  // the ranges' (max, sum of exp) pairs: thread (part, q) = (tid / B, tid % B)
-  // folds ranges part, part + parts, ..., then rows of 16 lanes per query
-  // merge the parts by rotations
-  const int parts = min(NT / B, 16);
-  {
+  if (threadIdx.x < B) {
+    // the ranges' pairs of query q, loads in flight together
+    const int q = threadIdx.x;
     const float* ws = a.wstats + (long)u * a.R * 2 * B;
-    const int q = threadIdx.x % B, part = threadIdx.x / B;
-    if (part < parts) {
-      float mx = -INFINITY, z = 0.f;
-      for (int r = part; r < a.R; r += parts)
-        stat_absorb(mx, z, ws[(long)r * 2 * B + q], ws[(long)r * 2 * B + B + q]);
-      pool_m[part * (B + 1) + q] = mx;
-      pool_z[part * (B + 1) + q] = z;
-    }
-  }
-  __syncthreads();
-  {
-    const int q = threadIdx.x >> 4, part = threadIdx.x & 15;
     float mx = -INFINITY, z = 0.f;
-    if (q < B && part < parts) {
-      mx = pool_m[part * (B + 1) + q];
-      z = pool_z[part * (B + 1) + q];
+    constexpr int SB = 8;
+    for (int r0 = 0; r0 < a.R; r0 += SB) {
+      float mr[SB], zr[SB];
+#pragma unroll
+      for (int k = 0; k < SB; ++k) {
+        const bool ok = r0 + k < a.R;
+        mr[k] = ok ? ws[(long)(r0 + k) * 2 * B + q] : -INFINITY;
+        zr[k] = ok ? ws[(long)(r0 + k) * 2 * B + B + q] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < SB; ++k) stat_absorb(mx, z, mr[k], zr[k]);
     }
-    row16_merge<8>(mx, z);
-    row16_merge<4>(mx, z);
-    row16_merge<2>(mx, z);
-    row16_merge<1>(mx, z);
     // exp(l - M_q) / Z_q = 2^(l log2(e) - c_q)
-    if (part == 0 && q < B) row_c[q] = fmaf(mx, kLog2e, __log2f(z));
+    row_c[q] = fmaf(mx, kLog2e, __log2f(z));
   }
   __syncthreads();
-  const float* lg = a.blocks + (long)u * nJ * 2 * B;  // row j: logits at 2 j B
-  float* W = a.W + (long)u * nJ;
-  if (B > 32 && (B & 3) == 0) {
-    // W_j = sum_q softmax_j(l_q.): a 16-lane row per block j, lane i holding
-    // queries 4 i .. 4 i + 3, so that a wave's loads cover whole rows; the
-    // lanes' sums meet by DPP rotations (2^-inf = 0 for queries past B)
-    const int l16 = threadIdx.x & 15, grp = threadIdx.x >> 4;
-    const bool qok = 4 * l16 < B;
-    float cq[4];
+  const int per = (nJ + a.WPU - 1) / a.WPU;
+  const int j0 = slice * per, j1 = min(nJ, j0 + per);
+  // a 16-lane row per block j, lane i holding queries 4 i .. 4 i + 3, so that
+  // a wave's loads cover whole block rows; the lanes' sums meet by DPP
+  // rotations (2^-inf = 0 for queries past B)
+  const int l16 = threadIdx.x & 15, grp = threadIdx.x >> 4;
+  constexpr int G16 = kWeightsBlock / 16;  // blocks per round
+  constexpr int RPT = 4;                   // rounds whose loads are in flight together
+  float cq[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) cq[e] = qok ? row_c[4 * l16 + e] : INFINITY;
-    constexpr int G16 = NT / 16;  // blocks per round
-    constexpr int RPT = 8;        // rounds whose loads are in flight together
-    for (int j0 = 0; j0 < nJ; j0 += RPT * G16) {
-      float4 x[RPT];
+  for (int e = 0; e < 4; ++e) cq[e] = 4 * l16 + e < B ? row_c[4 * l16 + e] : INFINITY;
+  const float* lg = a.blocks + (long)u * nJ * 2 * B;  // block row j: logits at 2 j B
+  const bool vec = (B & 3) == 0;                       // rows are 16-byte aligned
+  for (int jb = j0; jb < j1; jb += RPT * G16) {
+    float4 x[RPT];
 #pragma unroll
-      for (int r = 0; r < RPT; ++r) {
-        const int j = j0 + r * G16 + grp;
-        x[r] = qok && j < nJ ? *reinterpret_cast<const float4*>(lg + (long)j * 2 * B + 4 * l16)
-                             : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-      }
-#pragma unroll
-      for (int r = 0; r < RPT; ++r) {
-        const int j = j0 + r * G16 + grp;
-        float w = __builtin_amdgcn_exp2f(fmaf(x[r].x, kLog2e, -cq[0])) +
-                  __builtin_amdgcn_exp2f(fmaf(x[r].y, kLog2e, -cq[1])) +
-                  __builtin_amdgcn_exp2f(fmaf(x[r].z, kLog2e, -cq[2])) +
-                  __builtin_amdgcn_exp2f(fmaf(x[r].w, kLog2e, -cq[3]));
-        w = wave_sum16(w);
-        if (l16 == 0 && j < nJ) {
-          W[j] = w;
-          if (w_in_lds) wsh[j] = w;
-        }
-      }
-    }
-  } else {
-    // W_j = sum_q softmax_j(l_q.): four threads per block j, queries
-    // q0 .. q0 + 15 each; a thread's q0 is the same for all its blocks, so its
-    // normalisers stay in registers (2^-inf = 0 for queries past B)
-    const bool vec = (B & 3) == 0;
-    const int q0 = 16 * (threadIdx.x & 3);
-    const int nq = min(16, B - q0);
-    float cq[16];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) cq[k] = k < nq ? row_c[q0 + k] : INFINITY;
-    constexpr int UNR = 4;  // rows of blocks whose loads are in flight together
-    for (int base = 0; base < 4 * nJ; base += UNR * NT) {
-      float x[UNR][16];
-#pragma unroll
-      for (int r = 0; r < UNR; ++r) {
-        const int t = base + r * NT + threadIdx.x;
-        const bool ok = t < 4 * nJ && nq > 0;
-        const float* row = lg + (long)(t >> 2) * 2 * B + q0;
+    for (int r = 0; r < RPT; ++r) {
+      const int j = jb + r * G16 + grp;
+      const float* row = lg + (long)j * 2 * B + 4 * l16;
+      if (j < j1 && 4 * l16 < B) {
         if (vec) {
-#pragma unroll
-          for (int k4 = 0; k4 < 4; ++k4) {
-            const float4 f = ok && 4 * k4 < nq ? reinterpret_cast<const float4*>(row)[k4]
-                                                : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-            x[r][4 * k4] = f.x;
-            x[r][4 * k4 + 1] = f.y;
-            x[r][4 * k4 + 2] = f.z;
-            x[r][4 * k4 + 3] = f.w;
-          }
+          x[r] = *reinterpret_cast<const float4*>(row);
         } else {
-#pragma unroll
-          for (int k = 0; k < 16; ++k) x[r][k] = ok && k < nq ? row[k] : -INFINITY;
+          x[r].x = row[0];
+          x[r].y = 4 * l16 + 1 < B ? row[1] : -INFINITY;
+          x[r].z = 4 * l16 + 2 < B ? row[2] : -INFINITY;
+          x[r].w = 4 * l16 + 3 < B ? row[3] : -INFINITY;
         }
-      }
-#pragma unroll
-      for (int r = 0; r < UNR; ++r) {
-        const int t = base + r * NT + threadIdx.x;
-        float w = 0.f;
-#pragma unroll
-        for (int k = 0; k < 16; ++k) w += __builtin_amdgcn_exp2f(fmaf(x[r][k], kLog2e, -cq[k]));
-        w = add_xor2(add_xor1(w));
-        if (t < 4 * nJ && (t & 3) == 0) {
-          W[t >> 2] = w;
-          if (w_in_lds) wsh[t >> 2] = w;
-        }
+      } else {
+        x[r] = float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
       }
     }
-  }
-  __syncthreads();
-  int32_t* seg = a.seg + (long)u * a.S;
-  int32_t* seg_sh = reinterpret_cast<int32_t*>(wsh + (w_in_lds ? nJ : 0));
-  block_select_topk<NT>(w_in_lds ? wsh : W, nJ, a.S,
-                        [&](uint32_t pos, int i) {
-                          seg[pos] = i;
-                          if (seg_in_lds) seg_sh[pos] = i;
-                        },
-                        sh);
-  __syncthreads();
-  // pool normalisers from the selected blocks' log-sum-exps.  Thread
-  // (part, q) = (tid / B, tid % B) folds blocks part, part + parts, ... into
-  // a (max, sum of exp) pair (the loads of a wave cover whole rows); the
-  // pairs go through LDS to rows of 16 lanes per query, merged by rotations.
-  const int32_t* segx = seg_in_lds ? seg_sh : seg;
-  {
-    const int q = threadIdx.x % B, part = threadIdx.x / B;
-    const float* lse = a.blocks + (long)u * nJ * 2 * B + B;  // row j: log-sum-exps at (2 j + 1) B
-    float mx = -INFINITY, z = 0.f;
-    constexpr int BATCH = 8;  // loads in flight together
-    if (part < parts) {
-      for (int s0 = part; s0 < a.S; s0 += BATCH * parts) {
-        float v[BATCH];
 #pragma unroll
-        for (int k = 0; k < BATCH; ++k) {
-          const int s_ = s0 + parts * k;
-          v[k] = s_ < a.S ? lse[(long)segx[s_] * 2 * B + q] : -INFINITY;
-        }
-        float bm = v[0];
-#pragma unroll
-        for (int k = 1; k < BATCH; ++k) bm = fmaxf(bm, v[k]);
-        const float mn = fmaxf(mx, bm);
-        if (mn > -INFINITY) {
-          float zb = 0.f;
-#pragma unroll
-          for (int k = 0; k < BATCH; ++k) zb += __expf(v[k] - mn);  // e^-inf = 0
-          z = (mx > -INFINITY ? z * __expf(mx - mn) : 0.f) + zb;
-          mx = mn;
-        }
-      }
-      pool_m[part * (B + 1) + q] = mx;  // rows padded by one: no bank conflicts below
-      pool_z[part * (B + 1) + q] = z;
-    }
-  }
-  __syncthreads();
-  {
-    const int q = threadIdx.x >> 4, part = threadIdx.x & 15;
-    float mx = -INFINITY, z = 0.f;
-    if (q < B && part < parts) {
-      mx = pool_m[part * (B + 1) + q];
-      z = pool_z[part * (B + 1) + q];
-    }
-    row16_merge<8>(mx, z);
-    row16_merge<4>(mx, z);
-    row16_merge<2>(mx, z);
-    row16_merge<1>(mx, z);
-    if (part == 0 && q < B) {
-      float* ps = a.pstats + (long)u * 2 * B;
-      ps[q] = mx;
-      ps[B + q] = z;
+    for (int r = 0; r < RPT; ++r) {
+      const int j = jb + r * G16 + grp;
+      float w = __builtin_amdgcn_exp2f(fmaf(x[r].x, kLog2e, -cq[0])) +
+                __builtin_amdgcn_exp2f(fmaf(x[r].y, kLog2e, -cq[1])) +
+                __builtin_amdgcn_exp2f(fmaf(x[r].z, kLog2e, -cq[2])) +
+                __builtin_amdgcn_exp2f(fmaf(x[r].w, kLog2e, -cq[3]));
+      w = wave_sum16(w);
+      if (l16 == 0 && j < j1) a.W[(long)u * nJ + j] = w;
     }
   }
 }
@@ -772,10 +659,12 @@ bool db2_token_path(const wf_params& p) {
 
 bool fast_path(const wf_params& p) {
   // a positive scale keeps the block maximum of the raw products the maximum
-  // of the scaled logits
-  return (p.dtype == WF_BF16 && p.wavelet == WF_HAAR && p.levels >= 3 && p.levels <= 5 &&
-          p.q_len <= 16 * kFastMaxQBlocks && effective_scale(p) > 0.f) ||
-         db2_token_path(p);
+  // of the scaled logits; the scan and attention workgroups keep the unit's
+  // region ids in LDS for their selections
+  return ((p.dtype == WF_BF16 && p.wavelet == WF_HAAR && p.levels >= 3 && p.levels <= 5 &&
+           p.q_len <= 16 * kFastMaxQBlocks && effective_scale(p) > 0.f) ||
+          db2_token_path(p)) &&
+         p.segments <= kSelectLdsSegs;
 }
 
 // LDS of the db2 token skim besides its ring: the partial and statistic
@@ -962,33 +851,28 @@ hipError_t launch_rec_token_skim(const wf_params& p, int b, long n, const int32_
                            : token_skim_dispatch<64, false>(b, a, f.lds_bytes, s);
 }
 
-hipError_t launch_fast_select(const wf_params& p, const float* blocks, const float* wstats,
-                              float* W, int32_t* seg, float* pstats, hipStream_t s) {
+int weights_slices(const wf_params& p) {
+  const long U = (long)p.batch * p.heads;
+  const long nJ = (long)p.ctx_len >> p.levels;
+  // about four workgroups per CU, at least 16 blocks each
+  const long want = (4L * device_cu_count() + U - 1) / U;
+  return (int)std::max(1L, std::min(want, (nJ + 15) / 16));
+}
+
+hipError_t launch_block_weights(const wf_params& p, const float* blocks, const float* wstats,
+                                float* W, hipStream_t s) {
   if (!fast_path(p)) return hipErrorInvalidValue;
-  const FastPlan f = plan_fast(p);
-  FastSelectArgs a;
+  BlockWeightsArgs a;
   a.blocks = blocks;
   a.wstats = wstats;
   a.W = W;
-  a.seg = seg;
-  a.pstats = pstats;
   a.U = p.batch * p.heads;
   a.B = p.q_len;
   a.nJ = p.ctx_len >> p.levels;
-  a.R = f.R;
-  a.S = p.segments;
-  const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
-  const int seg_in_lds = a.S <= kSelectLdsSegs ? 1 : 0;
-  // W when it fits, then the picked block ids when they fit
-  const size_t lds =
-      ((in_lds ? (size_t)a.nJ : 0) + (seg_in_lds ? (size_t)a.S : 0)) * sizeof(float);
-  if (lds > 32768) {  // with the static arrays, past the default 64 KiB
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fast_select_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(fast_select_kernel, dim3((unsigned)a.U), dim3(kFastSelectBlock), lds, s, a,
-                     in_lds, seg_in_lds);
+  a.R = plan_fast(p).R;
+  a.WPU = weights_slices(p);
+  hipLaunchKernelGGL(block_weights_kernel, dim3((unsigned)(a.U * a.WPU)), dim3(kWeightsBlock), 0,
+                     s, a);
   return hipGetLastError();
 }
 

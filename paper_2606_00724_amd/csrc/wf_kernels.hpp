@@ -58,7 +58,16 @@ struct SkimSelectArgs {
 struct ScanArgs {
   const void* Q;        // [U][B][D]
   const void* K;        // [U][L][D]
-  const int32_t* seg;   // [U][S]
+  const int32_t* seg;   // [U][S] (the regions; unused when the scan selects them)
+  // the scan selects the regions itself (token-level path): W [U][nJ] of
+  // the block weights kernel, the token skim's block rows [U][nJ][2][B]
+  // (log-sum-exps of the selected blocks give the pool normalisers), and
+  // seg_out [U][S] for the regions, written by the unit's first workgroup
+  const float* W;
+  const float* blocks;
+  int32_t* seg_out;
+  int nJ;
+  int w_in_lds;         // W staged in LDS for the selection
   float* stats;         // [U][C][2][B]
   float* wpool;         // [U][P]  (weights mode)
   long Ls;              // rows per unit in K
@@ -94,6 +103,14 @@ struct AttnArgs {
   const void* K;        // rows: [U][L][D] indexed by tok, or [U][nrows][D]
   const void* V;
   const int32_t* tok;   // nullable: rows are contiguous when null
+  // the attention selects the tokens itself (token-level path): the top
+  // nsel of the scan weights wpool [U][P] over the pool of the regions seg
+  // [U][S] (2^J tokens each); tok_out [U][nsel] (nullable) receives them
+  const float* wpool;
+  const int32_t* seg;
+  int32_t* tok_out;
+  int P, S, J;
+  int w_in_lds;         // wpool staged in LDS for the selection
   const void* Kg;       // [U][G][D] tail (indexed mode only)
   const void* Vg;
   float* part;          // [U][NS][B][D] unnormalised partial outputs
@@ -138,13 +155,12 @@ struct Db2TokenTaps {
   float edge[6 << 6];
 };
 
-struct FastSelectArgs {
-  const float* blocks;  // [U][nJ][2][B]
+struct BlockWeightsArgs {
+  const float* blocks;  // [U][nJ][2][B] block rows of the token skim
   const float* wstats;  // [U][R][2][B]
   float* W;             // [U][nJ] out
-  int32_t* seg;         // [U][S] out
-  float* pstats;        // [U][2][B] out: pool max, pool sum of exp
-  int U, B, nJ, R, S;
+  int U, B, nJ, R;
+  int WPU;              // workgroups (block slices) per unit
 };
 
 }  // namespace wf

@@ -72,7 +72,9 @@ int device_cu_count();
 
 DwtPlan plan_dwt(const wf_params& p);
 SkimPlan plan_skim(const wf_params& p, bool fused);
-ScanPlan plan_scan(const wf_params& p);
+// select: the scan workgroups take the top-S regions themselves (all S
+// region ids in LDS)
+ScanPlan plan_scan(const wf_params& p, bool select = false);
 AttnPlan plan_attn(const wf_params& p, long nrows);
 
 // The fused path streams the keys once with token-level scores when the keys
@@ -86,9 +88,11 @@ void db2_token_taps(int J, Db2TokenTaps* out);
 FastPlan plan_fast(const wf_params& p);
 hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K,
                              float* blocks, float* wstats, hipStream_t s);
-hipError_t launch_fast_select(const wf_params& p, const float* blocks,
-                              const float* wstats, float* W, int32_t* seg,
-                              float* pstats, hipStream_t s);
+// W (eq. 8) of every coarse block from the token skim's block rows, by
+// weights_slices(p) workgroups per unit.
+int weights_slices(const wf_params& p);
+hipError_t launch_block_weights(const wf_params& p, const float* blocks,
+                                const float* wstats, float* W, hipStream_t s);
 
 hipError_t launch_dwt(const wf_params& p, const void* K, float* approx,
                       float* details, hipStream_t s);
@@ -130,6 +134,12 @@ hipError_t launch_skim_select(const wf_params& p, int ntiles,
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
                               const void* K, const int32_t* seg, float* stats,
                               float* wpool, hipStream_t s, int stat_slices = 0);
+// Token-level path: the weights pass that first takes the unit's top-S
+// regions of W itself (seg_out [U][S] receives them) and forms the pool
+// normalisers from the selected blocks' log-sum-exps (blocks [U][nJ][2][B]).
+hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const void* K,
+                                      const float* W, const float* blocks, int32_t* seg_out,
+                                      float* wpool, hipStream_t s);
 hipError_t launch_scan_select(const wf_params& p, const float* wpool,
                               const int32_t* seg, int32_t* tok,
                               hipStream_t s);
@@ -140,6 +150,13 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
                        const void* V, const int32_t* tok, int nsel,
                        const void* Kg, const void* Vg, int G, long nrows,
                        float* part, float* pstat, hipStream_t s);
+// Token-level path: the attention that first takes the unit's top-k_eff
+// tokens of the scan weights wpool [U][S 2^J] itself (the pool of the
+// regions seg [U][S]); tok_out [U][k_eff] (nullable) receives them.
+hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, const void* V,
+                              const float* wpool, const int32_t* seg, int32_t* tok_out,
+                              const void* Kg, const void* Vg, long nrows, float* part,
+                              float* pstat, hipStream_t s);
 hipError_t launch_attn_combine(const wf_params& p, long nrows,
                                const float* part, const float* pstat, void* O,
                                hipStream_t s);

@@ -230,8 +230,13 @@ __device__ __forceinline__ void stat_merge(float& m, float& z, float m2, float z
 constexpr int kPoolBlock = 512;
 constexpr int kPoolWaves = kPoolBlock / kWave;
 
-template <int WEIGHTS, int D>
+// SEL (weights pass of the token-level path, at most 64 query rows): the
+// workgroup first takes the unit's top-S regions from W (eq. 9) itself,
+// then queues its first pool chunks and, while they load, forms the pool
+// normalisers from the selected blocks' log-sum-exps.
+template <int WEIGHTS, int D, bool SEL = false>
 __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
+  static_assert(!SEL || WEIGHTS, "selection in the weights pass only");
   constexpr int NW = kPoolWaves;
   constexpr int CR = kScanChunk;
   constexpr int G = D / 8;             // 16-byte granules per row
@@ -260,12 +265,82 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, col = lane & 15;
 
-  const int s_lo = (int)(pb >> a.J);
-  const int ns = (int)((pe - 1) >> a.J) - s_lo + 1;
-  for (int i = threadIdx.x; i < ns; i += kPoolBlock) segs[i] = a.seg[(long)u * a.S + s_lo + i];
+  // region ids of this range: the span's own, or with SEL all S of the unit
+  const int s_lo = SEL ? 0 : (int)(pb >> a.J);
+  const uint32_t ring_lds = lds_offset(ring);
+  const int nbuf = a.nbuf;
+  PoolRowPtr<D> rp;
+  rp.Kunit = reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D;
+  rp.segs = segs;
+  rp.plast = pe - 1;
+  rp.last = a.Ls - 1;
+  rp.J = a.J;
+  rp.mask = (1 << a.J) - 1;
+  rp.s_lo = s_lo;
+  if constexpr (SEL) {
+    // top-S of W in the last ring slot (free until the loop queues chunk
+    // nbuf - 1): the selection's histograms, then W when it fits
+    unsigned char* spare = ring + (size_t)(nbuf - 1) * CHB;
+    auto& sh = *reinterpret_cast<SelectShared<kPoolBlock>*>(spare);
+    float* Wl = reinterpret_cast<float*>(spare + sizeof(SelectShared<kPoolBlock>));
+    const float* Wg = a.W + (long)u * a.nJ;
+    if (a.w_in_lds)
+      for (int i = threadIdx.x; i < a.nJ; i += kPoolBlock) Wl[i] = Wg[i];
+    __syncthreads();
+    int32_t* seg_out = c == 0 ? a.seg_out + (long)u * a.S : nullptr;
+    block_select_topk<kPoolBlock>(a.w_in_lds ? Wl : Wg, a.nJ, a.S,
+                                  [&](uint32_t pos, int j) {
+                                    segs[pos] = j;
+                                    if (seg_out) seg_out[pos] = j;
+                                  },
+                                  sh);
+    __syncthreads();
+    // the first chunks load while the normalisers are formed
+    for (int k = 0; k < nch && k < nbuf - 1; ++k) {
+      rp.p0 = pb + (long)k * CR;
+      issue_chunk<CR, G, NW, true>(ring_lds + (uint32_t)(k * CHB), rp);
+    }
+    // pool normalisers (M_q, Z_q) over the pool's tokens, from the selected
+    // blocks' log-sum-exps: thread (part, q) folds blocks part, part +
+    // parts, ...; the parts' pairs meet in the spare slot
+    const int B = a.B;
+    const int parts = min(kPoolBlock / B, 16);
+    float* pm = reinterpret_cast<float*>(spare);  // [parts][B + 1]
+    float* pz = pm + 16 * (B + 1);
+    {
+      const int q = threadIdx.x % B, part = threadIdx.x / B;
+      const float* lse = a.blocks + (long)u * a.nJ * 2 * B + B;  // block j: at (2 j + 1) B
+      if (part < parts) {
+        float mx = -INFINITY, z = 0.f;
+        constexpr int BATCH = 8;  // loads in flight together
+        for (int s0 = part; s0 < a.S; s0 += BATCH * parts) {
+          float v[BATCH];
+#pragma unroll
+          for (int k = 0; k < BATCH; ++k) {
+            const int s_ = s0 + parts * k;
+            v[k] = s_ < a.S ? lse[(long)segs[s_] * 2 * B + q] : -INFINITY;
+          }
+#pragma unroll
+          for (int k = 0; k < BATCH; ++k) stat_merge(mx, z, v[k], 1.f);
+        }
+        pm[part * (B + 1) + q] = mx;
+        pz[part * (B + 1) + q] = z;
+      }
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < B; q += kPoolBlock) {
+      float mx = -INFINITY, z = 0.f;
+      for (int k = 0; k < parts; ++k) stat_merge(mx, z, pm[k * (B + 1) + q], pz[k * (B + 1) + q]);
+      // exp(s - M) / Z = 2^(s log2(e) - (M log2(e) + log2(Z)))
+      lse2[q] = fmaf(mx, kLog2e, __log2f(z));
+    }
+  } else {
+    const int ns = (int)((pe - 1) >> a.J) - s_lo + 1;
+    for (int i = threadIdx.x; i < ns; i += kPoolBlock) segs[i] = a.seg[(long)u * a.S + s_lo + i];
+  }
   const bf16_t* Qunit = reinterpret_cast<const bf16_t*>(a.Q) + (long)u * a.B * D;
   stage_rows_any<bf16_t, D, kPoolBlock>(Qs, a.B, [&](int r) { return Qunit + (long)r * D; });
-  if constexpr (WEIGHTS) {
+  if constexpr (WEIGHTS && !SEL) {
     const float* stt = a.stats + (long)u * a.Cs * 2 * a.B;
     for (int q = threadIdx.x; q < a.B; q += kPoolBlock) {
       float mx = -INFINITY, z = 0.f;
@@ -286,17 +361,6 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     }
   }
   __syncthreads();  // every regular load above has been consumed
-
-  PoolRowPtr<D> rp;
-  rp.Kunit = reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D;
-  rp.segs = segs;
-  rp.plast = pe - 1;
-  rp.last = a.Ls - 1;
-  rp.J = a.J;
-  rp.mask = (1 << a.J) - 1;
-  rp.s_lo = s_lo;
-  const uint32_t ring_lds = lds_offset(ring);
-  const int nbuf = a.nbuf;
 
   const float s2 = a.scale * kLog2e;
   // LDS byte offsets of the lane's key operands: the same rows of every chunk
@@ -333,10 +397,13 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
         sm[j][i] = -INFINITY;
         sz[j][i] = 0.f;
       }
-    // ring of nbuf slots, nbuf - 1 chunks in flight ahead of the one consumed
-    for (int k = 0; k < nch && k < nbuf - 1; ++k) {
+    // ring of nbuf slots, nbuf - 1 chunks in flight ahead of the one consumed.
+    // The weights pass reads each pool row for the last time with the
+    // streaming (nt) policy: keeping the rows cached measured slower (the
+    // attention that follows loads the selected keys with nt as well).
+    for (int k = 0; k < nch && k < nbuf - 1 && !(SEL && qg == 0); ++k) {
       rp.p0 = pb + (long)k * CR;
-      issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(k * CHB), rp);
+      issue_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(k * CHB), rp);
     }
     for (int ch = 0; ch < nch; ++ch) {
       const long p0 = pb + (long)ch * CR;
@@ -345,7 +412,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
       lds_barrier();  // chunk ch visible; everyone is past chunk ch - 1
       if (ch + nbuf - 1 < nch) {
         rp.p0 = pb + (long)(ch + nbuf - 1) * CR;
-        issue_chunk<CR, G, NW>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rp);
+        issue_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rp);
       }
       const unsigned char* buf = ring + (ch % nbuf) * CHB;
 #pragma unroll
@@ -464,7 +531,7 @@ __global__ __launch_bounds__(kScanSelectBlock) void scan_select_kernel(
 // LDS a workgroup may use (gfx950: 160 KiB per CU), with a little margin.
 constexpr size_t kLdsBudget = 160 * 1024 - 1024;
 
-ScanPlan plan_scan(const wf_params& p) {
+ScanPlan plan_scan(const wf_params& p, bool select) {
   ScanPlan s{};
   const long P = (long)p.segments << p.levels;
   const long U = (long)p.batch * p.heads;
@@ -478,7 +545,8 @@ ScanPlan plan_scan(const wf_params& p) {
     cpw = std::min(cpw, 32L);  // at most 4096 positions per workgroup
     s.span = (int)(cpw * kScanChunk);
     s.chunks = (int)((P + s.span - 1) / s.span);
-    s.seg_cap = (s.span >> p.levels) + 2;
+    // region ids in LDS: the span's, or all S when the scan selects them
+    s.seg_cap = select ? p.segments : (s.span >> p.levels) + 2;
     const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
     // wave partials, the per-query normalisers, then W' of the range
     const size_t red_ring =
@@ -520,6 +588,43 @@ static hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t s) {
     return launch_with_lds(scan_ring_kernel<WEIGHTS, D>, grid, kPoolBlock, lds, s, a);
   else
     return launch_with_lds(scan_chunk_kernel<WEIGHTS, T, D>, grid, kBlock, lds, s, a);
+}
+
+hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const void* K,
+                                      const float* W, const float* blocks, int32_t* seg_out,
+                                      float* wpool, hipStream_t s) {
+  if (p.dtype != WF_BF16 || p.q_len > 64 || p.segments > kSelectLdsSegs)
+    return hipErrorInvalidValue;
+  const ScanPlan pl = plan_scan(p, true);
+  if (pl.nbuf < 2) return hipErrorInvalidValue;
+  ScanArgs a{};
+  a.Q = Q;
+  a.K = K;
+  a.W = W;
+  a.blocks = blocks;
+  a.seg_out = seg_out;
+  a.wpool = wpool;
+  a.U = p.batch * p.heads;
+  a.L = (int)filtered_len(p);
+  a.Ls = p.ctx_len;
+  a.B = p.q_len;
+  a.J = p.levels;
+  a.S = p.segments;
+  a.P = p.segments << p.levels;
+  a.nJ = p.ctx_len >> p.levels;
+  a.C = pl.chunks;
+  a.Cs = 1;
+  a.span = pl.span;
+  a.nbuf = pl.nbuf;
+  a.seg_cap = pl.seg_cap;
+  a.scale = effective_scale(p);
+  // W in the spare ring slot when it fits beside the selection's histograms
+  const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
+  a.w_in_lds = sizeof(SelectShared<kPoolBlock>) + (size_t)a.nJ * sizeof(float) <= chb ? 1 : 0;
+  const dim3 grid((unsigned)(a.U * a.C));
+  if (p.head_dim == 128)
+    return launch_with_lds(scan_ring_kernel<1, 128, true>, grid, kPoolBlock, pl.lds_bytes, s, a);
+  return launch_with_lds(scan_ring_kernel<1, 64, true>, grid, kPoolBlock, pl.lds_bytes, s, a);
 }
 
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,

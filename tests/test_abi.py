@@ -140,8 +140,8 @@ def test_fused_kernel_sequence_follows_the_path(wfpkg, change, path):
     p = _params(wfpkg, **change)
     names = wfpkg.fused_kernel_names(p)
     if path == "token":
-        assert names == ["token_skim", "skim_select", "scan_weights",
-                         "scan_select", "sparse_attn", "attn_combine"]
+        assert names == ["token_skim", "block_weights", "scan_weights",
+                         "sparse_attn", "attn_combine"]
     else:
         assert names == ["skim_tile", "skim_select", "scan_stats",
                          "scan_weights", "scan_select", "sparse_attn",
