@@ -260,7 +260,7 @@ def main() -> int:
     ap.add_argument("--layers", type=int, default=0,
                     help="layers per step, each with its own seeded inputs "
                          "(default: the workload's layer count)")
-    ap.add_argument("--touch", type=int, default=1,
+    ap.add_argument("--touch", type=int, default=4,
                     help="passes of a plain read over every device buffer "
                          "before the warmup steps (0: none)")
     ap.add_argument("--copy-calibration", action="store_true",

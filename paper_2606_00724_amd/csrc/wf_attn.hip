@@ -418,21 +418,30 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
     float* Wl = reinterpret_cast<float*>(segl + a.S);
     const float* Wg = a.wpool + (long)u * a.P;
     for (int i = threadIdx.x; i < a.S; i += kAttnRingBlock) segl[i] = a.seg[(long)u * a.S + i];
-    if (a.w_in_lds)
-      for (int i = threadIdx.x; i < a.P; i += kAttnRingBlock) Wl[i] = Wg[i];
-    __syncthreads();
     const long hi = min(re0, (long)a.nsel);
     const int J = a.J, mask = (1 << J) - 1;
     int32_t* tout = a.tok_out ? a.tok_out + (long)u * a.nsel : nullptr;
-    block_select_topk<kAttnRingBlock>(a.w_in_lds ? Wl : Wg, a.P, a.nsel,
-                                      [&](uint32_t pos, int pp) {
-                                        if ((long)pos >= rb0 && (long)pos < hi) {
-                                          const int32_t t = (segl[pp >> J] << J) | (pp & mask);
-                                          toks[pos - rb0] = t;
-                                          if (tout) tout[pos] = t;
-                                        }
-                                      },
-                                      sh);
+    auto emit = [&](uint32_t pos, int pp) {
+      if ((long)pos >= rb0 && (long)pos < hi) {
+        const int32_t t = (segl[pp >> J] << J) | (pp & mask);
+        toks[pos - rb0] = t;
+        if (tout) tout[pos] = t;
+      }
+    };
+    constexpr int EPT = 16;  // weights per thread held in registers
+    if (a.P <= EPT * kAttnRingBlock) {
+      // (the selection's first barrier publishes the region ids)
+      block_select_topk_regs<kAttnRingBlock, EPT>(Wg, a.P, a.nsel, emit, sh);
+    } else {
+      if (a.w_in_lds) {
+        for (int i = threadIdx.x; i < a.P; i += kAttnRingBlock) Wl[i] = Wg[i];
+        __syncthreads();
+        block_select_topk<kAttnRingBlock>(Wl, a.P, a.nsel, emit, sh);
+      } else {
+        __syncthreads();
+        block_select_topk<kAttnRingBlock>(Wg, a.P, a.nsel, emit, sh);
+      }
+    }
   } else if (a.tok) {
     const long hi = min(re0, (long)a.nsel);
     for (long i = rb0 + threadIdx.x; i < hi; i += kAttnRingBlock)
@@ -709,17 +718,10 @@ __device__ __forceinline__ void store8<float>(float* dst, const float* v) {
   reinterpret_cast<float4*>(dst)[1] = float4{v[4], v[5], v[6], v[7]};
 }
 
+// Output row q, channels c0 .. c0 + 7, of unit u merged from the unit's NS
+// split partials.
 template <typename T>
-__global__ __launch_bounds__(kCombineBlock) void attn_combine_kernel(AttnArgs a, int D) {
-  const int tpr = D / 8;                  // threads per row
-  const int rpb = kCombineBlock / tpr;    // rows per workgroup
-  const int nqb = (a.B + rpb - 1) / rpb;
-  // the unit on the XCD whose L2 took its partials from the attention
-  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int u = item / nqb;
-  const int q = (item % nqb) * rpb + threadIdx.x / tpr;
-  const int c0 = (threadIdx.x % tpr) * 8;
-  if (q >= a.B) return;  // no barrier follows
+__device__ __forceinline__ void merge_splits(const AttnArgs& a, int u, int q, int c0, int D) {
   const float* ps = a.pstat + (long)u * a.NS * 2 * a.B;
   // splits in groups of SB whose loads are all in flight together; each
   // group is merged into the running (max, sum, output) in one step, so up
@@ -773,6 +775,20 @@ __global__ __launch_bounds__(kCombineBlock) void attn_combine_kernel(AttnArgs a,
 #pragma unroll
   for (int i = 0; i < 8; ++i) o[i] *= inv;
   store8<T>(reinterpret_cast<T*>(a.O) + ((long)u * a.B + q) * D + c0, o);
+}
+
+template <typename T>
+__global__ __launch_bounds__(kCombineBlock) void attn_combine_kernel(AttnArgs a, int D) {
+  const int tpr = D / 8;                  // threads per row
+  const int rpb = kCombineBlock / tpr;    // rows per workgroup
+  const int nqb = (a.B + rpb - 1) / rpb;
+  // the unit on the XCD whose L2 took its partials from the attention
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / nqb;
+  const int q = (item % nqb) * rpb + threadIdx.x / tpr;
+  const int c0 = (threadIdx.x % tpr) * 8;
+  if (q >= a.B) return;  // no barrier follows
+  merge_splits<T>(a, u, q, c0, D);
 }
 
 // Sparse cache rows: [K[tok]; Kg] and [V[tok]; Vg], 16 bytes per thread.

@@ -299,9 +299,21 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
     // the histogram of the next pass was last read two passes ago
     if (pass < 3)
       for (int i = tid; i < 256; i += NT) sh.hist[(pass + 1) % 3][i] = 0;
-    for (int i = tid; i < n; i += NT) {
-      const uint32_t key = order_key(score[i]);
-      hist_add(h, (key & mask) == prefix, (key >> shift) & 255u, lane);
+    // batches of eight elements per thread whose loads are issued together
+    // (a load under a per-lane condition would be waited for at once): lanes
+    // past n load the last score and count nothing
+    for (int b0 = 0; b0 < n; b0 += 8 * NT) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (b0 + u * NT < n) v[u] = score[min(b0 + u * NT + tid, n - 1)];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (b0 + u * NT >= n) break;  // uniform
+        const uint32_t key = order_key(v[u]);
+        hist_add(h, b0 + u * NT + tid < n && (key & mask) == prefix, (key >> shift) & 255u,
+                 lane);
+      }
     }
     __syncthreads();
     // lane l looks at digits 255 - 4l - j, j < 4 (descending)
@@ -347,12 +359,16 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
   for (int base = 0; base < n; base += ROUNDS * NT, ++tile) {
     uint64_t gtm[ROUNDS], eqm[ROUNDS];
     uint32_t mine = 0;  // lane j < ROUNDS: the wave's packed counts of round j
+    float v[ROUNDS];
+#pragma unroll
+    for (int j = 0; j < ROUNDS; ++j)
+      if (base + j * NT < n) v[j] = score[min(base + j * NT + tid, n - 1)];
 #pragma unroll
     for (int j = 0; j < ROUNDS; ++j) {
       const int i = base + j * NT + tid;
       bool gt = false, eq = false;
-      if (i < n) {
-        const uint32_t key = order_key(score[i]);
+      if (base + j * NT < n && i < n) {
+        const uint32_t key = order_key(v[j]);
         gt = key > prefix;
         eq = key == prefix;
       }
@@ -398,6 +414,142 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
     gt_base += total >> 16;
     eq_base += total & 0xffffu;
   }
+}
+
+// block_select_topk for n <= EPT * NT with every key held in registers:
+// element j NT + tid is slot j of thread tid, read once (from LDS or global
+// memory), and every loop over the elements is unrolled.  Same picks, same
+// emit positions (the same radix passes and ordered compaction).
+template <int NT, int EPT, typename Emit>
+__device__ void block_select_topk_regs(const float* score, int n, int k, Emit emit,
+                                       SelectShared<NT>& sh) {
+  static_assert(NT >= 64 && NT <= 1024 && NT % 64 == 0, "block of whole waves");
+  constexpr int ROUNDS = 8;  // slots per compaction tile
+  static_assert(EPT % ROUNDS == 0 || EPT < ROUNDS, "whole tiles of slots");
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // every load of the slots in use is issued before the first is waited for
+  // (loads under a per-lane condition would each be waited for at once):
+  // lanes past n load the last score and ignore it
+  const int nslot = (n + NT - 1) / NT;  // slots in use, uniform
+  float v[EPT];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j)
+    if (j < nslot) v[j] = score[min(j * NT + tid, n - 1)];
+  uint32_t key[EPT];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) key[j] = j < nslot && j * NT + tid < n ? order_key(v[j]) : 0u;
+  for (int i = tid; i < 256; i += NT) sh.hist[0][i] = 0;
+  __syncthreads();
+  uint32_t prefix = 0, mask = 0, need = (uint32_t)k;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    uint32_t* h = sh.hist[pass % 3];
+    if (pass < 3)
+      for (int i = tid; i < 256; i += NT) sh.hist[(pass + 1) % 3][i] = 0;
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+      if (j * NT >= n) break;  // uniform
+      const bool in = j * NT + tid < n;
+      hist_add(h, in && (key[j] & mask) == prefix, (key[j] >> shift) & 255u, lane);
+    }
+    __syncthreads();
+    uint32_t c[4], sum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      c[q] = h[255 - 4 * lane - q];
+      sum += c[q];
+    }
+    uint32_t before = wave_inclusive_scan(sum) - sum;
+    int hit = 0;
+    uint32_t hit_above = 0;
+    bool found = false;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (!found && before < need && before + c[q] >= need) {
+        found = true;
+        hit = q;
+        hit_above = before;
+      }
+      before += c[q];
+    }
+    const int src = __ffsll((unsigned long long)__ballot(found)) - 1;
+    const uint32_t digit = (uint32_t)__builtin_amdgcn_readlane(255 - 4 * lane - hit, src);
+    const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)hit_above, src);
+    prefix |= digit << shift;
+    mask |= 255u << shift;
+    need -= above;
+  }
+  // ordered compaction, tiles of ROUNDS slots (as block_select_topk)
+  constexpr int NW = NT / 64;
+  constexpr int NE = ROUNDS * NW;
+  static_assert(NE <= 256, "count scan: at most four entries per lane");
+  uint32_t gt_base = 0, eq_base = 0;
+#pragma unroll
+  for (int t = 0; t < (EPT + ROUNDS - 1) / ROUNDS; ++t) {
+    const int base = t * ROUNDS * NT;
+    if (base >= n) break;  // uniform
+    uint64_t gtm[ROUNDS], eqm[ROUNDS];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int j = 0; j < ROUNDS; ++j) {
+      const int slot = t * ROUNDS + j;
+      bool gt = false, eq = false;
+      if (slot < EPT && base + j * NT + tid < n) {
+        gt = key[slot < EPT ? slot : 0] > prefix;
+        eq = key[slot < EPT ? slot : 0] == prefix;
+      }
+      gtm[j] = __ballot(gt);
+      eqm[j] = __ballot(eq);
+      if (lane == j) mine = ((uint32_t)__popcll(gtm[j]) << 16) | (uint32_t)__popcll(eqm[j]);
+    }
+    uint32_t* cnt = sh.cnt[t & 1];
+    if (lane < ROUNDS) cnt[lane * NW + wid] = mine;
+    __syncthreads();
+    uint32_t c[4], sum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * lane + q;
+      c[q] = e < NE ? cnt[e] : 0u;
+      sum += c[q];
+    }
+    const uint32_t incl = wave_inclusive_scan(sum);
+    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+    uint32_t ex[4];
+    ex[0] = incl - sum;
+#pragma unroll
+    for (int q = 1; q < 4; ++q) ex[q] = ex[q - 1] + c[q - 1];
+#pragma unroll
+    for (int j = 0; j < ROUNDS; ++j) {
+      if (base + j * NT >= n) break;  // uniform
+      const int e = j * NW + wid;
+      const int q = e & 3;
+      const uint32_t pick = q == 0 ? ex[0] : q == 1 ? ex[1] : q == 2 ? ex[2] : ex[3];
+      const uint32_t off = (uint32_t)__builtin_amdgcn_readlane((int)pick, e >> 2);
+      const uint64_t gm = gtm[j], em = eqm[j];
+      const bool gt = (gm >> lane) & 1ull, eq = (em >> lane) & 1ull;
+      const uint32_t gt_before = gt_base + (off >> 16) +
+          __builtin_amdgcn_mbcnt_hi((uint32_t)(gm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)gm, 0u));
+      const uint32_t eq_before = eq_base + (off & 0xffffu) +
+          __builtin_amdgcn_mbcnt_hi((uint32_t)(em >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)em, 0u));
+      if (gt || (eq && eq_before < need)) {
+        const uint32_t pos = gt_before + min(eq_before, need);
+        if (pos < (uint32_t)k) emit(pos, base + j * NT + tid);
+      }
+    }
+    gt_base += total >> 16;
+    eq_base += total & 0xffffu;
+  }
+}
+
+// Top-k by whichever form fits: registers for n <= EPT * NT, else the
+// general loop over `score`.
+template <int NT, int EPT, typename Emit>
+__device__ __forceinline__ void block_select_topk_any(const float* score, int n, int k, Emit emit,
+                                                      SelectShared<NT>& sh) {
+  if (n <= EPT * NT)
+    block_select_topk_regs<NT, EPT>(score, n, k, emit, sh);
+  else
+    block_select_topk<NT>(score, n, k, emit, sh);
 }
 
 // ------------------------------------------------------------ LDS staging

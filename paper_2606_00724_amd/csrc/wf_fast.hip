@@ -584,6 +584,38 @@ __global__ __launch_bounds__(kWeightsBlock) void block_weights_kernel(BlockWeigh
   const int item = xcd_swizzle(blockIdx.x, gridDim.x);
   const int u = item / a.WPU, slice = item % a.WPU;
   const int B = a.B, nJ = a.nJ;
+  const int per = (nJ + a.WPU - 1) / a.WPU;
+  const int j0 = slice * per, j1 = min(nJ, j0 + per);
+  // a 16-lane row per block j, lane i holding queries 4 i .. 4 i + 3, so that
+  // a wave's loads cover whole block rows; the lanes' sums meet by DPP
+  // rotations (2^-inf = 0 for queries past B)
+  const int l16 = threadIdx.x & 15, grp = threadIdx.x >> 4;
+  constexpr int G16 = kWeightsBlock / 16;  // blocks per round
+  constexpr int RPT = 8;                   // rounds whose loads are in flight together
+  const float* lg = a.blocks + (long)u * nJ * 2 * B;  // block row j: logits at 2 j B
+  const bool vec = (B & 3) == 0;                       // rows are 16-byte aligned
+  float4 x[RPT];
+  auto load = [&](int jb) {
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+      const int j = jb + r * G16 + grp;
+      const float* row = lg + (long)j * 2 * B + 4 * l16;
+      if (j < j1 && 4 * l16 < B) {
+        if (vec) {
+          x[r] = *reinterpret_cast<const float4*>(row);
+        } else {
+          x[r].x = row[0];
+          x[r].y = 4 * l16 + 1 < B ? row[1] : -INFINITY;
+          x[r].z = 4 * l16 + 2 < B ? row[2] : -INFINITY;
+          x[r].w = 4 * l16 + 3 < B ? row[3] : -INFINITY;
+        }
+      } else {
+        x[r] = float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      }
+    }
+  };
+  // the first rounds load while the normalisers are merged
+  load(j0);
   if (threadIdx.x < B) {
     // the ranges' pairs of query q, loads in flight together
     const int q = threadIdx.x;
@@ -605,38 +637,11 @@ __global__ __launch_bounds__(kWeightsBlock) void block_weights_kernel(BlockWeigh
     row_c[q] = fmaf(mx, kLog2e, __log2f(z));
   }
   __syncthreads();
-  const int per = (nJ + a.WPU - 1) / a.WPU;
-  const int j0 = slice * per, j1 = min(nJ, j0 + per);
-  // a 16-lane row per block j, lane i holding queries 4 i .. 4 i + 3, so that
-  // a wave's loads cover whole block rows; the lanes' sums meet by DPP
-  // rotations (2^-inf = 0 for queries past B)
-  const int l16 = threadIdx.x & 15, grp = threadIdx.x >> 4;
-  constexpr int G16 = kWeightsBlock / 16;  // blocks per round
-  constexpr int RPT = 4;                   // rounds whose loads are in flight together
   float cq[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) cq[e] = 4 * l16 + e < B ? row_c[4 * l16 + e] : INFINITY;
-  const float* lg = a.blocks + (long)u * nJ * 2 * B;  // block row j: logits at 2 j B
-  const bool vec = (B & 3) == 0;                       // rows are 16-byte aligned
   for (int jb = j0; jb < j1; jb += RPT * G16) {
-    float4 x[RPT];
-#pragma unroll
-    for (int r = 0; r < RPT; ++r) {
-      const int j = jb + r * G16 + grp;
-      const float* row = lg + (long)j * 2 * B + 4 * l16;
-      if (j < j1 && 4 * l16 < B) {
-        if (vec) {
-          x[r] = *reinterpret_cast<const float4*>(row);
-        } else {
-          x[r].x = row[0];
-          x[r].y = 4 * l16 + 1 < B ? row[1] : -INFINITY;
-          x[r].z = 4 * l16 + 2 < B ? row[2] : -INFINITY;
-          x[r].w = 4 * l16 + 3 < B ? row[3] : -INFINITY;
-        }
-      } else {
-        x[r] = float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-      }
-    }
+    if (jb != j0) load(jb);
 #pragma unroll
     for (int r = 0; r < RPT; ++r) {
       const int j = jb + r * G16 + grp;

@@ -284,16 +284,23 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     auto& sh = *reinterpret_cast<SelectShared<kPoolBlock>*>(spare);
     float* Wl = reinterpret_cast<float*>(spare + sizeof(SelectShared<kPoolBlock>));
     const float* Wg = a.W + (long)u * a.nJ;
-    if (a.w_in_lds)
-      for (int i = threadIdx.x; i < a.nJ; i += kPoolBlock) Wl[i] = Wg[i];
-    __syncthreads();
     int32_t* seg_out = c == 0 ? a.seg_out + (long)u * a.S : nullptr;
-    block_select_topk<kPoolBlock>(a.w_in_lds ? Wl : Wg, a.nJ, a.S,
-                                  [&](uint32_t pos, int j) {
-                                    segs[pos] = j;
-                                    if (seg_out) seg_out[pos] = j;
-                                  },
-                                  sh);
+    auto emit = [&](uint32_t pos, int j) {
+      segs[pos] = j;
+      if (seg_out) seg_out[pos] = j;
+    };
+    constexpr int EPT = 16;  // weights per thread held in registers
+    if (a.nJ <= EPT * kPoolBlock) {
+      block_select_topk_regs<kPoolBlock, EPT>(Wg, a.nJ, a.S, emit, sh);
+    } else {
+      if (a.w_in_lds) {
+        for (int i = threadIdx.x; i < a.nJ; i += kPoolBlock) Wl[i] = Wg[i];
+        __syncthreads();
+        block_select_topk<kPoolBlock>(Wl, a.nJ, a.S, emit, sh);
+      } else {
+        block_select_topk<kPoolBlock>(Wg, a.nJ, a.S, emit, sh);
+      }
+    }
     __syncthreads();
     // the first chunks load while the normalisers are formed
     for (int k = 0; k < nch && k < nbuf - 1; ++k) {
@@ -521,9 +528,12 @@ __global__ __launch_bounds__(kScanSelectBlock) void scan_select_kernel(
   const int J = a.J;
   const int mask = (1 << J) - 1;
   int32_t* tok = a.tok + (long)u * a.keff;
-  block_select_topk<kScanSelectBlock>(
-      w_in_lds ? wsh : W, a.P, a.keff,
-      [&](uint32_t pos, int p) { tok[pos] = (seg[p >> J] << J) | (p & mask); }, sh);
+  auto emit = [&](uint32_t pos, int p) { tok[pos] = (seg[p >> J] << J) | (p & mask); };
+  // one instance per address space of the weights
+  if (w_in_lds)
+    block_select_topk<kScanSelectBlock>(wsh, a.P, a.keff, emit, sh);
+  else
+    block_select_topk<kScanSelectBlock>(W, a.P, a.keff, emit, sh);
 }
 
 // ------------------------------------------------------------ host side

@@ -987,23 +987,25 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
     }
   }
   __syncthreads();
-  const float* src = w_in_lds ? wsh : W;
   // candidate n is block n, or on a refinement scale child n % 2 of kept
   // block parent[n / 2]; the last scale emits the two tokens of each block
   const int32_t* par = a.parent ? a.parent + (long)u * a.npar : nullptr;
   auto block_of = [&](int n) -> int32_t { return par ? 2 * par[n >> 1] + (n & 1) : n; };
-  if (a.pairs) {
-    int32_t* tok = a.seg + (long)u * 2 * a.S;
-    block_select_topk<kSelectBlock>(src, a.nJ, a.S, [&](uint32_t pos, int n) {
-      const int32_t id = block_of(n);
-      tok[2 * pos] = 2 * id;
-      tok[2 * pos + 1] = 2 * id + 1;
-    }, sh);
-  } else {
-    int32_t* seg = a.seg + (long)u * a.S;
-    block_select_topk<kSelectBlock>(src, a.nJ, a.S,
-                                    [&](uint32_t pos, int n) { seg[pos] = block_of(n); }, sh);
-  }
+  int32_t* out = a.seg + (long)u * (a.pairs ? 2 : 1) * a.S;
+  auto emit = [&](uint32_t pos, int n) {
+    const int32_t id = block_of(n);
+    if (a.pairs) {
+      out[2 * pos] = 2 * id;
+      out[2 * pos + 1] = 2 * id + 1;
+    } else {
+      out[pos] = id;
+    }
+  };
+  // one instance per address space of the weights
+  if (w_in_lds)
+    block_select_topk<kSelectBlock>(wsh, a.nJ, a.S, emit, sh);
+  else
+    block_select_topk<kSelectBlock>(W, a.nJ, a.S, emit, sh);
 }
 
 // ------------------------------------------------------------ host side
