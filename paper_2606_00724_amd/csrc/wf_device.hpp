@@ -144,6 +144,14 @@ __device__ __forceinline__ f32x4 tile_dot<float, 128>(const float* a,
 constexpr float kLog2e = 1.44269504088896341f;  // log2(e)
 constexpr float kLn2 = 0.69314718055994531f;     // ln(2)
 
+// one running (max, sum of exp) pair absorbs another
+__device__ __forceinline__ void stat_absorb(float& m, float& z, float m2, float z2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;
+  z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
+  m = mn;
+}
+
 // ------------------------------------------------------------ reductions
 
 // The value of the lane R lanes away (mod 16) in the same 16-lane row (DPP
@@ -167,6 +175,82 @@ __device__ __forceinline__ float wave_sum16(float v) {
   v += dpp_row_ror<4>(v);
   v += dpp_row_ror<2>(v);
   return v + dpp_row_ror<1>(v);
+}
+
+// W (eq. 8) of blocks j0 .. j1 - 1 of one unit from the token skim's block
+// rows lg [nJ][2][B] (coarse logits at 2 j B) and the unit's R range pairs
+// ws [R][2][B] of (max, sum of exp) of its coarse logits per query:
+// W_j = sum_q exp(l_qj - M_q) / Z_q, with (M_q, Z_q) the ranges' pairs
+// merged.  A 16-lane row per block j, lane i holding queries 4 i .. 4 i + 3,
+// so that a wave's loads cover whole block rows; the lanes' sums meet by DPP
+// rotations (2^-inf = 0 for queries past B <= 64).  row_c: B floats of LDS.
+// Every thread of the NT-thread block calls it (it has barriers); out(j, w)
+// is called by one lane per block.
+template <int NT, typename Out>
+__device__ __forceinline__ void unit_block_weights(const float* lg, const float* ws, int R, int B,
+                                                   int j0, int j1, float* row_c, Out out) {
+  const int l16 = threadIdx.x & 15, grp = threadIdx.x >> 4;
+  constexpr int G16 = NT / 16;  // blocks per round
+  constexpr int RPT = 8;        // rounds whose loads are in flight together
+  const bool vec = (B & 3) == 0;  // rows are 16-byte aligned
+  float4 x[RPT];
+  auto load = [&](int jb) {
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+      const int j = jb + r * G16 + grp;
+      const float* row = lg + (long)j * 2 * B + 4 * l16;
+      if (j < j1 && 4 * l16 < B) {
+        if (vec) {
+          x[r] = *reinterpret_cast<const float4*>(row);
+        } else {
+          x[r].x = row[0];
+          x[r].y = 4 * l16 + 1 < B ? row[1] : -INFINITY;
+          x[r].z = 4 * l16 + 2 < B ? row[2] : -INFINITY;
+          x[r].w = 4 * l16 + 3 < B ? row[3] : -INFINITY;
+        }
+      } else {
+        x[r] = float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      }
+    }
+  };
+  // the first rounds load while the normalisers are merged
+  load(j0);
+  if (threadIdx.x < B) {
+    // the ranges' pairs of query q, loads in flight together
+    const int q = threadIdx.x;
+    float mx = -INFINITY, z = 0.f;
+    constexpr int SB = 8;
+    for (int r0 = 0; r0 < R; r0 += SB) {
+      float mr[SB], zr[SB];
+#pragma unroll
+      for (int k = 0; k < SB; ++k) {
+        const bool ok = r0 + k < R;
+        mr[k] = ok ? ws[(long)(r0 + k) * 2 * B + q] : -INFINITY;
+        zr[k] = ok ? ws[(long)(r0 + k) * 2 * B + B + q] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < SB; ++k) stat_absorb(mx, z, mr[k], zr[k]);
+    }
+    // exp(l - M_q) / Z_q = 2^(l log2(e) - c_q)
+    row_c[q] = fmaf(mx, kLog2e, __log2f(z));
+  }
+  __syncthreads();
+  float cq[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) cq[e] = 4 * l16 + e < B ? row_c[4 * l16 + e] : INFINITY;
+  for (int jb = j0; jb < j1; jb += RPT * G16) {
+    if (jb != j0) load(jb);
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+      const int j = jb + r * G16 + grp;
+      float w = __builtin_amdgcn_exp2f(fmaf(x[r].x, kLog2e, -cq[0])) +
+                __builtin_amdgcn_exp2f(fmaf(x[r].y, kLog2e, -cq[1])) +
+                __builtin_amdgcn_exp2f(fmaf(x[r].z, kLog2e, -cq[2])) +
+                __builtin_amdgcn_exp2f(fmaf(x[r].w, kLog2e, -cq[3]));
+      w = wave_sum16(w);
+      if (l16 == 0 && j < j1) out(j, w);
+    }
+  }
 }
 
 // Sums of v over lane pairs (l, l ^ 1) and (l, l ^ 2), DPP quad_perm.
@@ -286,7 +370,7 @@ __device__ __forceinline__ void hist_add(uint32_t* h, bool m, uint32_t d, int la
 // counts over the positions in index order:
 //   pos = #greater before + min(#equal before, copies to take).
 template <int NT, typename Emit>
-__device__ void block_select_topk(const float* score, int n, int k, Emit emit,
+__device__ __forceinline__ void block_select_topk(const float* score, int n, int k, Emit emit,
                                   SelectShared<NT>& sh) {
   static_assert(NT >= 64 && NT <= 1024 && NT % 64 == 0, "block of whole waves");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -421,7 +505,7 @@ __device__ void block_select_topk(const float* score, int n, int k, Emit emit,
 // memory), and every loop over the elements is unrolled.  Same picks, same
 // emit positions (the same radix passes and ordered compaction).
 template <int NT, int EPT, typename Emit>
-__device__ void block_select_topk_regs(const float* score, int n, int k, Emit emit,
+__device__ __forceinline__ void block_select_topk_regs(const float* score, int n, int k, Emit emit,
                                        SelectShared<NT>& sh) {
   static_assert(NT >= 64 && NT <= 1024 && NT % 64 == 0, "block of whole waves");
   constexpr int ROUNDS = 8;  // slots per compaction tile

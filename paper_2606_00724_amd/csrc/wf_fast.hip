@@ -33,14 +33,6 @@
 
 namespace wf {
 
-// one running (max, sum of exp) pair absorbs another
-__device__ __forceinline__ void stat_absorb(float& m, float& z, float m2, float z2) {
-  const float mn = fmaxf(m, m2);
-  if (mn == -INFINITY) return;
-  z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
-  m = mn;
-}
-
 // one value joins a running (max, sum of exp) pair
 __device__ __forceinline__ void stat_add(float& m, float& z, float x) {
   if (x > m) {
@@ -586,73 +578,9 @@ __global__ __launch_bounds__(kWeightsBlock) void block_weights_kernel(BlockWeigh
   const int B = a.B, nJ = a.nJ;
   const int per = (nJ + a.WPU - 1) / a.WPU;
   const int j0 = slice * per, j1 = min(nJ, j0 + per);
-  // a 16-lane row per block j, lane i holding queries 4 i .. 4 i + 3, so that
-  // a wave's loads cover whole block rows; the lanes' sums meet by DPP
-  // rotations (2^-inf = 0 for queries past B)
-  const int l16 = threadIdx.x & 15, grp = threadIdx.x >> 4;
-  constexpr int G16 = kWeightsBlock / 16;  // blocks per round
-  constexpr int RPT = 8;                   // rounds whose loads are in flight together
-  const float* lg = a.blocks + (long)u * nJ * 2 * B;  // block row j: logits at 2 j B
-  const bool vec = (B & 3) == 0;                       // rows are 16-byte aligned
-  float4 x[RPT];
-  auto load = [&](int jb) {
-#pragma unroll
-    for (int r = 0; r < RPT; ++r) {
-      const int j = jb + r * G16 + grp;
-      const float* row = lg + (long)j * 2 * B + 4 * l16;
-      if (j < j1 && 4 * l16 < B) {
-        if (vec) {
-          x[r] = *reinterpret_cast<const float4*>(row);
-        } else {
-          x[r].x = row[0];
-          x[r].y = 4 * l16 + 1 < B ? row[1] : -INFINITY;
-          x[r].z = 4 * l16 + 2 < B ? row[2] : -INFINITY;
-          x[r].w = 4 * l16 + 3 < B ? row[3] : -INFINITY;
-        }
-      } else {
-        x[r] = float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-      }
-    }
-  };
-  // the first rounds load while the normalisers are merged
-  load(j0);
-  if (threadIdx.x < B) {
-    // the ranges' pairs of query q, loads in flight together
-    const int q = threadIdx.x;
-    const float* ws = a.wstats + (long)u * a.R * 2 * B;
-    float mx = -INFINITY, z = 0.f;
-    constexpr int SB = 8;
-    for (int r0 = 0; r0 < a.R; r0 += SB) {
-      float mr[SB], zr[SB];
-#pragma unroll
-      for (int k = 0; k < SB; ++k) {
-        const bool ok = r0 + k < a.R;
-        mr[k] = ok ? ws[(long)(r0 + k) * 2 * B + q] : -INFINITY;
-        zr[k] = ok ? ws[(long)(r0 + k) * 2 * B + B + q] : 0.f;
-      }
-#pragma unroll
-      for (int k = 0; k < SB; ++k) stat_absorb(mx, z, mr[k], zr[k]);
-    }
-    // exp(l - M_q) / Z_q = 2^(l log2(e) - c_q)
-    row_c[q] = fmaf(mx, kLog2e, __log2f(z));
-  }
-  __syncthreads();
-  float cq[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) cq[e] = 4 * l16 + e < B ? row_c[4 * l16 + e] : INFINITY;
-  for (int jb = j0; jb < j1; jb += RPT * G16) {
-    if (jb != j0) load(jb);
-#pragma unroll
-    for (int r = 0; r < RPT; ++r) {
-      const int j = jb + r * G16 + grp;
-      float w = __builtin_amdgcn_exp2f(fmaf(x[r].x, kLog2e, -cq[0])) +
-                __builtin_amdgcn_exp2f(fmaf(x[r].y, kLog2e, -cq[1])) +
-                __builtin_amdgcn_exp2f(fmaf(x[r].z, kLog2e, -cq[2])) +
-                __builtin_amdgcn_exp2f(fmaf(x[r].w, kLog2e, -cq[3]));
-      w = wave_sum16(w);
-      if (l16 == 0 && j < j1) a.W[(long)u * nJ + j] = w;
-    }
-  }
+  float* W = a.W + (long)u * nJ;
+  unit_block_weights<kWeightsBlock>(a.blocks + (long)u * nJ * 2 * B, a.wstats + (long)u * a.R * 2 * B,
+                                    a.R, B, j0, j1, row_c, [&](int j, float w) { W[j] = w; });
 }
 
 // ------------------------------------------------------------ host side

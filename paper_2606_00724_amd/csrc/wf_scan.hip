@@ -216,14 +216,6 @@ struct PoolRowPtr {
   }
 };
 
-// Online (max, sum of exp) update of a running pair with one new value set.
-__device__ __forceinline__ void stat_merge(float& m, float& z, float m2, float z2) {
-  const float mn = fmaxf(m, m2);
-  if (mn == -INFINITY) return;
-  z = (m > -INFINITY ? z * __expf(m - mn) : 0.f) + (m2 > -INFINITY ? z2 * __expf(m2 - mn) : 0.f);
-  m = mn;
-}
-
 // 8 waves: two per SIMD, so that one wave's MFMA, exp and LDS latencies
 // overlap the other's work (with one wave per SIMD the ring kernel ran at
 // well under the gather rate of its memory pattern).
@@ -278,11 +270,12 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
   rp.mask = (1 << a.J) - 1;
   rp.s_lo = s_lo;
   if constexpr (SEL) {
-    // top-S of W in the last ring slot (free until the loop queues chunk
-    // nbuf - 1): the selection's histograms, then W when it fits
+    // top-S of W: the selection's histograms in the last ring slot, and
+    // past the register select's reach W in the slots before it when it
+    // fits (the ring is free until the first chunks are queued below)
     unsigned char* spare = ring + (size_t)(nbuf - 1) * CHB;
     auto& sh = *reinterpret_cast<SelectShared<kPoolBlock>*>(spare);
-    float* Wl = reinterpret_cast<float*>(spare + sizeof(SelectShared<kPoolBlock>));
+    float* Wl = reinterpret_cast<float*>(ring);
     const float* Wg = a.W + (long)u * a.nJ;
     int32_t* seg_out = c == 0 ? a.seg_out + (long)u * a.S : nullptr;
     auto emit = [&](uint32_t pos, int j) {
@@ -328,7 +321,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
             v[k] = s_ < a.S ? lse[(long)segs[s_] * 2 * B + q] : -INFINITY;
           }
 #pragma unroll
-          for (int k = 0; k < BATCH; ++k) stat_merge(mx, z, v[k], 1.f);
+          for (int k = 0; k < BATCH; ++k) stat_absorb(mx, z, v[k], 1.f);
         }
         pm[part * (B + 1) + q] = mx;
         pz[part * (B + 1) + q] = z;
@@ -337,7 +330,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     __syncthreads();
     for (int q = threadIdx.x; q < B; q += kPoolBlock) {
       float mx = -INFINITY, z = 0.f;
-      for (int k = 0; k < parts; ++k) stat_merge(mx, z, pm[k * (B + 1) + q], pz[k * (B + 1) + q]);
+      for (int k = 0; k < parts; ++k) stat_absorb(mx, z, pm[k * (B + 1) + q], pz[k * (B + 1) + q]);
       // exp(s - M) / Z = 2^(s log2(e) - (M log2(e) + log2(Z)))
       lse2[q] = fmaf(mx, kLog2e, __log2f(z));
     }
@@ -361,7 +354,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
           zk[k] = ok ? stt[(long)(k0 + k) * 2 * a.B + a.B + q] : 0.f;
         }
 #pragma unroll
-        for (int k = 0; k < SB; ++k) stat_merge(mx, z, mk[k], zk[k]);
+        for (int k = 0; k < SB; ++k) stat_absorb(mx, z, mk[k], zk[k]);
       }
       // exp(s - M) / Z = 2^(s log2(e) - (M log2(e) + log2(Z)))
       lse2[q] = fmaf(mx, kLog2e, __log2f(z));
@@ -497,7 +490,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
       float mx = -INFINITY, z = 0.f;
 #pragma unroll
       for (int w = 0; w < NW; ++w)
-        stat_merge(mx, z, part[((qb * NW + w) * 16 + r) * 2], part[((qb * NW + w) * 16 + r) * 2 + 1]);
+        stat_absorb(mx, z, part[((qb * NW + w) * 16 + r) * 2], part[((qb * NW + w) * 16 + r) * 2 + 1]);
       stt[q] = mx;
       stt[a.B + q] = z;
     }
@@ -628,9 +621,9 @@ hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const v
   a.nbuf = pl.nbuf;
   a.seg_cap = pl.seg_cap;
   a.scale = effective_scale(p);
-  // W in the spare ring slot when it fits beside the selection's histograms
+  // W in the ring slots before the spare one when it fits there
   const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
-  a.w_in_lds = sizeof(SelectShared<kPoolBlock>) + (size_t)a.nJ * sizeof(float) <= chb ? 1 : 0;
+  a.w_in_lds = (size_t)a.nJ * sizeof(float) <= (size_t)(pl.nbuf - 1) * chb ? 1 : 0;
   const dim3 grid((unsigned)(a.U * a.C));
   if (p.head_dim == 128)
     return launch_with_lds(scan_ring_kernel<1, 128, true>, grid, kPoolBlock, pl.lds_bytes, s, a);

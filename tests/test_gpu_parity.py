@@ -123,6 +123,13 @@ EDGE = {
                     budget=1, q_len=1, **_BF),
     "db2tok_q1": V_("d2q1", ctx_len=64 * 20, head_dim=128, levels=6,
                     segments=3, budget=50, q_len=1, wavelet="db2", **_BF),
+    # the scan's selection of regions past the 8192 weights its register
+    # select holds: 12000 blocks at d = 128 (W staged in the LDS ring) and
+    # 16384 at d = 64 (W read from global memory)
+    "tok_sel_lds": V_("twl", ctx_len=8 * 12000 + 3, head_dim=128, levels=3,
+                         segments=64, budget=300, q_len=33, **_BF),
+    "tok_sel_global": V_("twk", ctx_len=8 * 16384, levels=3, segments=100,
+                       budget=400, q_len=17, **_BF),
 }
 
 FULL = ["tiny", "layer8b", "long16k", "headline32k", "stress128k", "tail32k"]
