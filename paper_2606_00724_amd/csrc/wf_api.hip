@@ -185,8 +185,9 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     if (!fast) l.cstats = take(U * cp.chunks * 2 * B * sizeof(float));
     l.wpool = take(U * P * sizeof(float));
   }
-  // the token-level attention keeps its selected tokens on chip
-  if (whole && !fast) l.tok = take(U * keff_of(p) * sizeof(int32_t));
+  // a selecting attention keeps its selected tokens on chip
+  const bool attn_selects = fast || (op == WF_OP_CACHED && attn_can_select(p, attn_rows));
+  if (whole && !attn_selects) l.tok = take(U * keff_of(p) * sizeof(int32_t));
   if (attn) {
     const AttnPlan ap = plan_attn(p, attn_rows);
     l.part = take(U * ap.splits * B * p.head_dim * sizeof(float));
@@ -354,6 +355,22 @@ static const char* const kCachedNames[] = {
     "skim_tile", "skim_select", "scan_stats", "scan_weights",
     "scan_select", "sparse_attn", "attn_combine"};
 constexpr int kCachedKernels = 7;
+// with bf16 keys the attention takes the top-k of W' itself
+static const char* const kCachedSelectNames[] = {
+    "skim_tile", "skim_select", "scan_stats", "scan_weights", "sparse_attn", "attn_combine"};
+
+static long cached_rows(const wf_params& p) {
+  return keff_of(p) + remainder_len(p) + p.gen_len;
+}
+static bool cached_attn_selects(const wf_params& p) {
+  return attn_can_select(p, cached_rows(p));
+}
+static int cached_kernels(const wf_params& p) {
+  return cached_attn_selects(p) ? kCachedKernels - 1 : kCachedKernels;
+}
+static const char* const* cached_names(const wf_params& p) {
+  return cached_attn_selects(p) ? kCachedSelectNames : kCachedNames;
+}
 
 static wf_status cached_impl(const wf_params* p, const void* Q, const float* approx,
                              const void* K, const void* V, const void* Kg, const void* Vg,
@@ -371,10 +388,12 @@ static wf_status cached_impl(const wf_params* p, const void* Q, const float* app
     WF_TRY(check_ptr(Kg, "Kg", false));
     WF_TRY(check_ptr(Vg, "Vg", false));
   }
-  if (events && n_events < kCachedKernels + 1)
-    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, kCachedKernels + 1);
+  const int nk = cached_kernels(*p);
+  const char* const* names = cached_names(*p);
+  if (events && n_events < nk + 1)
+    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, nk + 1);
   const long keff = keff_of(*p);
-  const long nrows = keff + remainder_len(*p) + p->gen_len;
+  const long nrows = cached_rows(*p);
   const Layout l = layout_for(*p, WF_OP_CACHED, nrows);
   WF_TRY(check_workspace(ws, ws_bytes, l.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -395,7 +414,7 @@ static wf_status cached_impl(const wf_params* p, const void* Q, const float* app
   };
   auto step = [&](hipError_t launched) -> wf_status {
     if (launched != hipSuccess)
-      return fail(WF_ERR_HIP, "%s: %s", kCachedNames[k], hipGetErrorString(launched));
+      return fail(WF_ERR_HIP, "%s: %s", names[k], hipGetErrorString(launched));
     ++k;
     hipError_t e = mark();
     if (e != hipSuccess) return fail(WF_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
@@ -407,9 +426,14 @@ static wf_status cached_impl(const wf_params* p, const void* Q, const float* app
   WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
   WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
   WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s)));
-  WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
-  WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows, part,
-                          pstat, s)));
+  if (cached_attn_selects(*p)) {
+    WF_TRY(step(launch_attn_select(*p, Q, K, V, wpool, seg, tok_idx, Kg, Vg, nrows, part,
+                                   pstat, s)));
+  } else {
+    WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
+    WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows, part,
+                            pstat, s)));
+  }
   WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
   return ok();
 }
@@ -732,7 +756,7 @@ wf_status wf_filter_attend_cached_timed(const wf_params* p, const void* Q,
                                         size_t workspace_bytes, void* stream, void** events,
                                         int32_t n_events) {
   if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
-  for (int i = 0; i < n_events && i <= kCachedKernels; ++i)
+  for (int i = 0; i < n_events && i <= cached_kernels(*p); ++i)
     if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
   return cached_impl(p, Q, approx, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace,
                      workspace_bytes, stream, events, n_events);
@@ -740,12 +764,12 @@ wf_status wf_filter_attend_cached_timed(const wf_params* p, const void* Q,
 
 int32_t wf_filter_attend_cached_kernels(const wf_params* p) {
   if (check_params(p) != WF_OK) return -1;
-  return kCachedKernels;
+  return cached_kernels(*p);
 }
 
 const char* wf_filter_attend_cached_kernel_name(const wf_params* p, int32_t i) {
-  if (check_params(p) != WF_OK || i < 0 || i >= kCachedKernels) return nullptr;
-  return kCachedNames[i];
+  if (check_params(p) != WF_OK || i < 0 || i >= cached_kernels(*p)) return nullptr;
+  return cached_names(*p)[i];
 }
 
 wf_status wf_recursion_counts(const wf_params* p, const float* proportions,

@@ -916,13 +916,20 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
               : attn_launch<float, 64>(a, pl.lds_bytes, s);
 }
 
+bool attn_can_select(const wf_params& p, long nrows) {
+  if (p.dtype != WF_BF16 || p.segments > kSelectLdsSegs) return false;
+  const AttnPlan pl = plan_attn(p, nrows);
+  if (pl.nbuf < 2) return false;
+  const size_t ring = (size_t)pl.nbuf * 2 * kRingRows * 2 * p.head_dim;
+  return sizeof(SelectShared<kAttnRingBlock>) + (size_t)p.segments * sizeof(int32_t) <= ring;
+}
+
 hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, const void* V,
                               const float* wpool, const int32_t* seg, int32_t* tok_out,
                               const void* Kg, const void* Vg, long nrows, float* part,
                               float* pstat, hipStream_t s) {
-  if (p.dtype != WF_BF16 || p.segments > kSelectLdsSegs) return hipErrorInvalidValue;
+  if (!attn_can_select(p, nrows)) return hipErrorInvalidValue;
   const AttnPlan pl = plan_attn(p, nrows);
-  if (pl.nbuf < 2) return hipErrorInvalidValue;
   AttnArgs a{};
   a.Q = Q;
   a.K = K;
@@ -954,7 +961,6 @@ hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, 
   // ids when they fit
   const size_t ring = (size_t)pl.nbuf * 2 * kRingRows * 2 * p.head_dim;
   const size_t fixed = sizeof(SelectShared<kAttnRingBlock>) + (size_t)a.S * sizeof(int32_t);
-  if (fixed > ring) return hipErrorInvalidValue;
   a.w_in_lds = fixed + (size_t)a.P * sizeof(float) <= ring ? 1 : 0;
   auto kern = p.head_dim == 128 ? attn_ring_kernel<128, true> : attn_ring_kernel<64, true>;
   if (pl.lds_bytes > 65536) {

@@ -153,6 +153,7 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
 // Token-level path: the attention that first takes the unit's top-k_eff
 // tokens of the scan weights wpool [U][S 2^J] itself (the pool of the
 // regions seg [U][S]); tok_out [U][k_eff] (nullable) receives them.
+bool attn_can_select(const wf_params& p, long nrows);
 hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, const void* V,
                               const float* wpool, const int32_t* seg, int32_t* tok_out,
                               const void* Kg, const void* Vg, long nrows, float* part,

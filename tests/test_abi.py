@@ -150,6 +150,20 @@ def test_fused_kernel_sequence_follows_the_path(wfpkg, change, path):
     assert wfpkg.workspace_bytes(p, wfpkg.OP_FUSED) > 0
 
 
+@pytest.mark.parametrize("change,selects", [
+    (dict(), False),                          # fp32 keys: the select kernel
+    (dict(dtype="bf16"), True),
+    (dict(dtype="bf16", q_len=256), True),
+    (dict(dtype="bf16", wavelet="db2"), True),
+])
+def test_cached_step_attention_selects_with_bf16_keys(wfpkg, change, selects):
+    p = _params(wfpkg, **change)
+    names = wfpkg.cached_kernel_names(p)
+    head = ["skim_tile", "skim_select", "scan_stats", "scan_weights"]
+    tail = ["sparse_attn", "attn_combine"]
+    assert names == head + ([] if selects else ["scan_select"]) + tail
+
+
 def test_binding_rejects_host_tensors(wfpkg):
     import torch
     p = _params(wfpkg)
