@@ -246,6 +246,36 @@ def cpu_baseline(w, Q, K, V, Kg=None, Vg=None, min_seconds: float = 10.0) -> dic
             "seconds": elapsed}
 
 
+def cpu_single_thread(name: str, min_seconds: float = 2.0) -> dict:
+    """The oracle on one thread: every unit of one layer of workload `name`
+    in calls of one unit (the oracle spreads a call's units over its
+    threads, so a one-unit call runs on one), repeated until about
+    min_seconds of oracle time have passed (at most 50 passes)."""
+    import oracle
+    import synth
+    oracle.build(force=False)
+    w = synth.WORKLOADS[name]
+    Q, K, V = synth.make_inputs(w)
+    U = w.units
+    q = Q.reshape(U, w.q_len, w.head_dim)
+    k = K.reshape(U, w.ctx_len, w.head_dim)
+    v = V.reshape(U, w.ctx_len, w.head_dim)
+    elapsed, passes = 0.0, 0
+    while passes < 50 and (passes == 0 or elapsed < min_seconds):
+        for u in range(U):
+            qa, ka, va = (oracle._f64(x[u:u + 1]) for x in (q, k, v))
+            t0 = time.perf_counter()
+            oracle.filter_attend(qa, ka, va, w.levels, w.segments, w.budget,
+                                 wavelet=w.wavelet, boundary=w.boundary)
+            elapsed += time.perf_counter() - t0
+        passes += 1
+    return {"workload": name, "value": w.batch * w.ctx_len * passes / elapsed,
+            "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"all {U} units of one {name} layer, one unit per call, "
+                      f"{passes} passes, fp64; {elapsed:.2f} s",
+            "seconds": elapsed}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -511,6 +541,9 @@ def main() -> int:
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, Q, K, V, Kg, Vg)
+        # one-thread figures on the two smallest workloads
+        result["cpu_baseline"]["single_thread"] = [
+            cpu_single_thread(n) for n in ("tiny", "layer8b")]
     print(json.dumps(result), flush=True)
     return 0
 

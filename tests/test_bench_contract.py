@@ -83,3 +83,9 @@ def test_needle_recall_counts_kept_needle_tokens():
 
 def test_cpu_model_is_a_string():
     assert isinstance(bench.cpu_model(), str)
+
+
+def test_single_thread_oracle_baseline_runs_one_unit_per_call():
+    r = bench.cpu_single_thread("tiny", min_seconds=0.0)
+    assert r["cores"] == 1 and r["workload"] == "tiny"
+    assert r["value"] > 0 and r["unit"] == "tokens/s"
