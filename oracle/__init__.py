@@ -291,5 +291,41 @@ def filter_attend_recursive(Q, K, V, levels: int, proportions,
     return O, [tok[u, :n_tok[u]].copy() for u in range(U)]
 
 
+def filter_attend_shared(Q, K, V, levels: int, segments: int, budget: int,
+                         wavelet: str = "haar", boundary: str = "symmetric",
+                         Kg=None, Vg=None, scale: float | None = None) -> dict:
+    """One selection shared by the H heads of a sequence (the layer-shared
+    variant of the per-head selection).  Q [H, B, d], K/V [H, L, d], Kg/Vg
+    [H, G, d].  eqs. 7-8 per head over its own keys, the column sums W
+    added over the heads; eq. 9 on that sum gives the regions; eq. 10 the
+    pool; the scan's W' (eqs. 7-8 over the pool, per head) added over the
+    heads; its top k_eff the tokens; then every head attends over its own
+    K/V rows at those tokens, the L mod 2^J remainder rows and its tail
+    (eq. 3 form).  Returns dict(W, seg, Wp, tok, O [H, B, d]).
+    """
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    H, B, d = Q.shape
+    L = K.shape[1]
+    Lf = (L >> levels) << levels
+    G = 0 if Kg is None else int(Kg.shape[1])
+    n = Lf >> levels
+    W = np.zeros(n)
+    for h in range(H):
+        W += skim(Q[h], dwt(K[h, :Lf], levels, wavelet, boundary), scale)
+    seg = topk(W, segments)
+    keff = min(budget, segments << levels)
+    pool = (seg[:, None] * (1 << levels) + np.arange(1 << levels)[None, :]).ravel()
+    Wp = np.zeros(pool.size)
+    for h in range(H):
+        Wp += scan(Q[h], K[h], seg, levels, budget, scale)[0]
+    tok = pool[topk(Wp, keff)]
+    keep = np.concatenate([tok, np.arange(Lf, L)])
+    O = np.empty((H, B, d))
+    for h in range(H):
+        O[h] = attend(Q[h], K[h], V[h], keep, Kg[h] if G else None,
+                      Vg[h] if G else None, scale)
+    return dict(W=W, seg=seg, Wp=Wp, tok=tok, O=O)
+
+
 def max_threads() -> int:
     return int(_load().wf_ref_max_threads())

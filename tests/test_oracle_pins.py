@@ -646,3 +646,87 @@ def test_recursion_remainder_follows_mu0(ref):
     got, _ = ref.recursive_select(Q, K, 3, [0.5, 0.5, 0.25])
     base, _ = ref.recursive_select(Q, K[:Lf], 3, [0.5, 0.5, 0.25])
     np.testing.assert_array_equal(got, np.concatenate([base, np.arange(Lf, Lf + rem)]))
+
+
+# ------------------------------------------------ layer-shared selection
+
+def _shared_case(H, L=512, d=32, B=8, seed=7):
+    rng = np.random.default_rng(seed)
+    Q = rng.standard_normal((H, B, d)) / np.sqrt(d)
+    K = rng.standard_normal((H, L, d)) * 0.3
+    V = rng.standard_normal((H, L, d))
+    return Q, K, V
+
+
+def test_shared_selection_of_one_head_is_the_per_head_selection(ref):
+    """H = 1: the shared path reduces to O1-O8 of that unit."""
+    Q, K, V = _shared_case(1)
+    sh = ref.filter_attend_shared(Q, K, V, 3, 10, 40)
+    un = ref.filter_attend_unit(Q[0], K[0], V[0], 3, 10, 40)
+    assert np.array_equal(sh["seg"], un["seg"]) and np.array_equal(sh["tok"], un["tok"])
+    assert np.allclose(sh["W"], un["W"], rtol=1e-13, atol=0)
+    assert np.allclose(sh["Wp"], un["Wp"], rtol=1e-13, atol=0)
+    assert np.allclose(sh["O"][0], un["O"], rtol=0, atol=1e-13)
+
+
+def test_shared_selection_of_identical_heads_is_each_heads_selection(ref):
+    """H copies of one unit: the summed weights are H times the unit's, so
+    the regions and tokens are the unit's and every head's output is its."""
+    Q, K, V = _shared_case(1, seed=8)
+    H = 4
+    sh = ref.filter_attend_shared(np.repeat(Q, H, 0), np.repeat(K, H, 0),
+                                     np.repeat(V, H, 0), 3, 12, 50)
+    un = ref.filter_attend_unit(Q[0], K[0], V[0], 3, 12, 50)
+    assert np.array_equal(sh["seg"], un["seg"]) and np.array_equal(sh["tok"], un["tok"])
+    assert np.allclose(sh["W"], H * un["W"], rtol=1e-12, atol=0)
+    for h in range(H):
+        assert np.allclose(sh["O"][h], un["O"], rtol=0, atol=1e-13)
+
+
+def test_shared_weights_are_the_heads_summed_softmax_column_sums(ref):
+    """Haar W recomputed from scratch: A_J as 2^(-J/2) block sums, a
+    row softmax per head, column sums added over the heads."""
+    H, J = 3, 2
+    Q, K, V = _shared_case(H, L=64, d=8, B=5, seed=9)
+    sh = ref.filter_attend_shared(Q, K, V, J, 4, 8)
+    W = np.zeros(64 >> J)
+    for h in range(H):
+        A = K[h].reshape(-1, 1 << J, 8).sum(1) * 2.0 ** (-J / 2)
+        s = Q[h] @ A.T / np.sqrt(8)
+        p = np.exp(s - s.max(1, keepdims=True))
+        W += (p / p.sum(1, keepdims=True)).sum(0)
+    assert np.allclose(sh["W"], W, rtol=1e-12, atol=0)
+    # the pool weights the same way over the shared pool, at token level
+    pool = (sh["seg"][:, None] * 4 + np.arange(4)).ravel()
+    Wp = np.zeros(pool.size)
+    for h in range(H):
+        s = Q[h] @ K[h][pool].T / np.sqrt(8)
+        p = np.exp(s - s.max(1, keepdims=True))
+        Wp += (p / p.sum(1, keepdims=True)).sum(0)
+    assert np.allclose(sh["Wp"], Wp, rtol=1e-12, atol=0)
+
+
+def test_shared_selection_keeps_each_heads_needle(ref):
+    """Head h's queries point at a needle only its own keys carry, in a
+    block of its own: with S = H every needle block is kept, although no
+    head alone scores the others' blocks."""
+    H, L, d, B, J = 3, 256, 16, 4, 3
+    rng = np.random.default_rng(11)
+    K = rng.standard_normal((H, L, d)) * 0.1
+    V = rng.standard_normal((H, L, d))
+    Q = np.zeros((H, B, d))
+    blocks = [5, 17, 26]
+    for h in range(H):
+        u = np.zeros(d)
+        u[h] = 1.0
+        K[h, blocks[h] * 8:(blocks[h] + 1) * 8] += 4 * u
+        Q[h] = 4 * u + 0.01 * rng.standard_normal((B, d))
+    sh = ref.filter_attend_shared(Q, K, V, J, H, 8 * H)
+    assert sorted(sh["seg"].tolist()) == blocks
+    assert np.array_equal(sh["tok"], np.concatenate([np.arange(b * 8, b * 8 + 8) for b in blocks]))
+    # every head attends with its own keys and values at the shared tokens
+    for h in range(H):
+        s = Q[h] @ K[h][sh["tok"]].T / np.sqrt(d)
+        p = np.exp(s - s.max(1, keepdims=True))
+        O = (p / p.sum(1, keepdims=True)) @ V[h][sh["tok"]]
+        assert np.allclose(sh["O"][h], O, rtol=0, atol=1e-12)
