@@ -30,6 +30,7 @@ import math
 import os
 import sys
 import time
+from concurrent.futures import ThreadPoolExecutor
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -188,6 +189,8 @@ def needle_recall(w, tok, layer: int = 0) -> dict:
     import numpy as np
 
     import synth
+    if tok.dim() == 2:  # one list per sequence, shared by its heads
+        tok = tok[:, None, :].expand(w.batch, w.heads, tok.shape[-1])
     t = tok.reshape(w.batch, w.heads, -1).cpu().numpy()
     rec = []
     for b in range(w.batch):
@@ -213,7 +216,10 @@ def cpu_baseline(w, Q, K, V, Kg=None, Vg=None, min_seconds: float = 10.0) -> dic
     v = V.reshape(U, w.ctx_len, w.head_dim)
     kg = Kg.reshape(U, w.gen_len, w.head_dim) if Kg is not None else None
     vg = Vg.reshape(U, w.gen_len, w.head_dim) if Vg is not None else None
-    chunk = 16
+    # whole sequences per chunk when their heads share the selection
+    shared = bool(getattr(w, "shared", False))
+    threads = min(oracle.max_threads(), w.batch) if shared else oracle.max_threads()
+    chunk = w.units if shared else 16
     elapsed = 0.0
     passes = 0
     while passes < 50 and (passes == 0 or elapsed < min_seconds):
@@ -222,7 +228,20 @@ def cpu_baseline(w, Q, K, V, Kg=None, Vg=None, min_seconds: float = 10.0) -> dic
             kga = oracle._f64(kg[u0:u0 + chunk]) if kg is not None else None
             vga = oracle._f64(vg[u0:u0 + chunk]) if vg is not None else None
             t0 = time.perf_counter()
-            if w.proportions:
+            if shared:
+                # the chunk's sequences, one per thread (the oracle's C calls
+                # release the interpreter lock): their heads share one
+                # selection
+                def seq(b0):
+                    oracle.filter_attend_shared(
+                        qa[b0:b0 + w.heads], ka[b0:b0 + w.heads],
+                        va[b0:b0 + w.heads], w.levels, w.segments, w.budget,
+                        wavelet=w.wavelet, boundary=w.boundary,
+                        Kg=None if kga is None else kga[b0:b0 + w.heads],
+                        Vg=None if vga is None else vga[b0:b0 + w.heads])
+                with ThreadPoolExecutor(max_workers=threads) as ex:
+                    list(ex.map(seq, range(0, qa.shape[0], w.heads)))
+            elif w.proportions:
                 oracle.filter_attend_recursive(
                     qa, ka, va, w.levels,
                     [float(np.float32(m)) for m in w.proportions],
@@ -238,11 +257,13 @@ def cpu_baseline(w, Q, K, V, Kg=None, Vg=None, min_seconds: float = 10.0) -> dic
     note = ("; the oracle recomputes A_J instead of reusing it"
             if getattr(w, "cached", False) else "")
     return {"value": tokens / elapsed, "unit": "tokens/s",
-            "cores": oracle.max_threads(), "cpu_model": cpu_model(),
+            "cores": threads, "cpu_model": cpu_model(),
             "kind": "oracle",
             "sample": f"all {U} (batch, head) units of one {w.name} layer, "
-                      f"{passes} passes, fp64, OpenMP over units, {chunk} "
-                      f"units per call; {elapsed:.2f} s{note}",
+                      f"{passes} passes, fp64, "
+                      + (f"one thread per sequence ({threads})"
+                         if shared else f"OpenMP over units, {chunk} units per call")
+                      + f"; {elapsed:.2f} s{note}",
             "seconds": elapsed}
 
 
@@ -322,6 +343,7 @@ def main() -> int:
     p = wf.params_for(w)
     recursive = bool(w.proportions)
     cached = bool(w.cached)
+    shared = bool(getattr(w, "shared", False))
     counts = wf.recursion_counts(p, w.proportions) if recursive else None
     keff = 2 * counts[0] if recursive else wf.effective_budget(p)
     nl = max(1, args.layers or getattr(w, "layers", 1))
@@ -351,7 +373,9 @@ def main() -> int:
                 Vg=Vg.to(dev) if Vg is not None else None))
     Qd = copies[0]["Q"]
     O = torch.empty_like(Qd)
-    tok = torch.empty((w.batch, w.heads, keff), dtype=torch.int32, device=dev)
+    # one token list per sequence when its heads share the selection
+    tok = torch.empty((w.batch, keff) if shared else (w.batch, w.heads, keff),
+                      dtype=torch.int32, device=dev)
     approx = None
     if recursive:
         ws = torch.empty(wf.recursive_workspace_bytes(p, w.proportions),
@@ -364,6 +388,9 @@ def main() -> int:
         torch.cuda.synchronize()
         ws = wf.alloc_workspace(p, wf.OP_CACHED, dev)
         names = wf.cached_kernel_names(p)
+    elif shared:
+        ws = wf.alloc_workspace(p, wf.OP_SHARED, dev)
+        names = wf.shared_kernel_names(p)
     else:
         ws = wf.alloc_workspace(p, wf.OP_FUSED, dev)
         names = wf.fused_kernel_names(p)
@@ -387,6 +414,9 @@ def main() -> int:
             wf.wf_filter_attend_cached(p, c["Q"], c["A"], c["K"], c["V"],
                                        c["Kg"], c["Vg"], O, tok, None, ws,
                                        stream)
+        elif shared:
+            wf.wf_filter_attend_shared(p, c["Q"], c["K"], c["V"], c["Kg"],
+                                       c["Vg"], O, tok, None, ws, stream)
         else:
             wf.wf_filter_attend(p, c["Q"], c["K"], c["V"], c["Kg"], c["Vg"],
                                 O, tok, None, ws, stream)
@@ -406,6 +436,10 @@ def main() -> int:
             wf.wf_filter_attend_cached_timed(p, c["Q"], c["A"], c["K"],
                                              c["V"], c["Kg"], c["Vg"], O, tok,
                                              None, ws, evs, stream)
+        elif shared:
+            wf.wf_filter_attend_shared_timed(p, c["Q"], c["K"], c["V"],
+                                             c["Kg"], c["Vg"], O, tok, None,
+                                             ws, evs, stream)
         else:
             wf.wf_filter_attend_timed(p, c["Q"], c["K"], c["V"], c["Kg"],
                                       c["Vg"], O, tok, None, ws, evs, stream)

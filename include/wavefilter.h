@@ -80,7 +80,7 @@ enum { WF_BF16 = 0, WF_F32 = 1 };
 
 /* Operations whose workspace size wf_workspace_bytes reports. */
 enum { WF_OP_SKIM = 0, WF_OP_SCAN = 1, WF_OP_ATTN = 2, WF_OP_FUSED = 3,
-       WF_OP_CACHED = 4 };
+       WF_OP_CACHED = 4, WF_OP_SHARED = 5 };
 
 /* Remainder.  When L is not a multiple of 2^J, the first
  * Lf = 2^J floor(L / 2^J) positions are filtered (transformed, scored,
@@ -284,6 +284,50 @@ wf_status wf_filter_attend_cached_timed(const wf_params* p, const void* Q,
  * NULL if p is invalid. */
 int32_t wf_filter_attend_cached_kernels(const wf_params* p);
 const char* wf_filter_attend_cached_kernel_name(const wf_params* p, int32_t i);
+
+/* ---------------------------------------------------------------------
+ * One step with one selection per sequence, shared by all its heads (the
+ * layer-shared form of the selection; the per-head form is
+ * wf_filter_attend).  Each head scores its own keys as in eqs. 7-8; the
+ * column sums W of the heads of a sequence are added before the top-S of
+ * eq. 9, which gives the sequence's regions (eq. 10: one pool for all its
+ * heads); the scan's W' of every head over that pool are added before the
+ * top-k_eff, which gives the sequence's tokens mu^0; every head then
+ * attends with its own query rows over its own K/V rows at those tokens,
+ * the L mod 2^J remainder rows and its own tail (eq. 3 form).  The sums run
+ * over the heads in order.
+ *   Q [batch][heads][B][d], K, V [batch][heads][L][d], Kg, Vg
+ *   [batch][heads][G][d] (NULL iff G == 0)      dtype
+ *   O          [batch][heads][B][d]               dtype out
+ *   tok_idx    nullable [batch][k_eff]            int32 out: mu^0, ascending
+ *   seg_idx    nullable [batch][S]                int32 out: the regions,
+ *              ascending
+ *   workspace  >= wf_workspace_bytes(p, WF_OP_SHARED)
+ * Only the token-level path is built for it: bf16 keys, Haar with 3..5
+ * levels or db2 with 6 (at least 4 coefficients), at most 64 query rows
+ * and a positive scale; other parameters return WF_ERR_UNSUPPORTED (and
+ * wf_workspace_bytes(p, WF_OP_SHARED) is 0 for them).
+ */
+wf_status wf_filter_attend_shared(const wf_params* p, const void* Q,
+                                  const void* K, const void* V, const void* Kg,
+                                  const void* Vg, void* O, int32_t* tok_idx,
+                                  int32_t* seg_idx, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* wf_filter_attend_shared with HIP events around its kernels
+ * (n = wf_filter_attend_shared_kernels(p); n_events >= n + 1). */
+wf_status wf_filter_attend_shared_timed(const wf_params* p, const void* Q,
+                                        const void* K, const void* V,
+                                        const void* Kg, const void* Vg, void* O,
+                                        int32_t* tok_idx, int32_t* seg_idx,
+                                        void* workspace,
+                                        size_t workspace_bytes, void* stream,
+                                        void** events, int32_t n_events);
+
+/* Kernels one shared call queues and the name of the i-th one, or -1 /
+ * NULL if p is invalid or outside the token-level path. */
+int32_t wf_filter_attend_shared_kernels(const wf_params* p);
+const char* wf_filter_attend_shared_kernel_name(const wf_params* p, int32_t i);
 
 /* ---------------------------------------------------------------------
  * Multi-scale recursive filtering (Section 3.2, eqs. 9-11; Algorithm 1,

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libwavefilter.so")
 HAAR, DB2 = 0, 1
 EXT_SYMMETRIC, EXT_PERIODIC = 0, 1
 BF16, F32 = 0, 1
-OP_SKIM, OP_SCAN, OP_ATTN, OP_FUSED, OP_CACHED = 0, 1, 2, 3, 4
+OP_SKIM, OP_SCAN, OP_ATTN, OP_FUSED, OP_CACHED, OP_SHARED = 0, 1, 2, 3, 4, 5
 MAX_LEVELS, MAX_Q_LEN = 10, 256
 NOALLOC_SCRATCH_BYTES = 32 << 20
 
@@ -35,6 +35,9 @@ EXPORTED = ("wf_workspace_bytes", "wf_effective_budget", "wf_dwt_keys",
             "wf_filter_attend_cached", "wf_filter_attend_cached_timed",
             "wf_filter_attend_cached_kernels",
             "wf_filter_attend_cached_kernel_name",
+            "wf_filter_attend_shared", "wf_filter_attend_shared_timed",
+            "wf_filter_attend_shared_kernels",
+            "wf_filter_attend_shared_kernel_name",
             "wf_recursion_counts", "wf_recursive_workspace_bytes",
             "wf_filter_attend_recursive", "wf_filter_attend_recursive_timed",
             "wf_filter_attend_recursive_kernels",
@@ -83,6 +86,15 @@ def _load() -> ctypes.CDLL:
                                     vp, ctypes.POINTER(vp), i32]),
         "wf_filter_attend_noalloc": (ctypes.c_int,
                                      [P, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "wf_filter_attend_shared": (ctypes.c_int,
+                                    [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                     vp]),
+        "wf_filter_attend_shared_timed": (ctypes.c_int,
+                                          [P, vp, vp, vp, vp, vp, vp, vp, vp,
+                                           vp, sz, vp, ctypes.POINTER(vp),
+                                           i32]),
+        "wf_filter_attend_shared_kernels": (i32, [P]),
+        "wf_filter_attend_shared_kernel_name": (ctypes.c_char_p, [P, i32]),
         "wf_filter_attend_kernels": (i32, [P]),
         "wf_filter_attend_kernel_name": (ctypes.c_char_p, [P, i32]),
         "wf_filter_attend_cached": (ctypes.c_int,
@@ -381,6 +393,66 @@ def filter_attend_grouped(p_kv: WfParams, group: int, Q, K, V, Kg=None,
         O, tok, seg = out
         return O.reshape(Q.shape), tok, seg
     return out.reshape(Q.shape)
+
+
+# ------------------------------------------------------------ shared selection
+# One selection per sequence, shared by its heads (W and W' summed over the
+# heads before each top-k); every head attends over the shared tokens.
+
+def shared_kernel_names(p: WfParams) -> list[str]:
+    n = _lib.wf_filter_attend_shared_kernels(ctypes.byref(p))
+    return [_lib.wf_filter_attend_shared_kernel_name(ctypes.byref(p),
+                                                     i).decode()
+            for i in range(max(n, 0))]
+
+
+def _expect_shared(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx) -> None:
+    _expect_qkv(p, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, O=O, tail=True)
+    _expect(tok_idx, "tok_idx", torch.int32, p.batch * effective_budget(p),
+            nullable=True)
+    _expect(seg_idx, "seg_idx", torch.int32, p.batch * p.segments,
+            nullable=True)
+
+
+def wf_filter_attend_shared(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
+                            workspace, stream=None):
+    _expect_shared(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx)
+    ws, nb = _ws(workspace)
+    _check(_lib.wf_filter_attend_shared(
+        ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(Kg), _ptr(Vg),
+        _ptr(O), _ptr(tok_idx), _ptr(seg_idx), ws, nb, _stream(stream)))
+
+
+def wf_filter_attend_shared_timed(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx,
+                                  workspace, events, stream=None):
+    _expect_shared(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx)
+    ws, nb = _ws(workspace)
+    arr = (ctypes.c_void_p * len(events))(*events)
+    _check(_lib.wf_filter_attend_shared_timed(
+        ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(Kg), _ptr(Vg),
+        _ptr(O), _ptr(tok_idx), _ptr(seg_idx), ws, nb, _stream(stream), arr,
+        len(events)))
+
+
+def filter_attend_shared(p: WfParams, Q, K, V, Kg=None, Vg=None,
+                         workspace=None, want_indices: bool = False,
+                         stream=None):
+    """Allocates O (and the per-sequence index outputs tok [batch, k_eff],
+    seg [batch, S]) and runs wf_filter_attend_shared.  Returns O, or (O,
+    tok, seg) when want_indices."""
+    with torch.cuda.stream(_torch_stream(stream)):
+        O = torch.empty_like(Q)
+        tok = seg = None
+        if want_indices:
+            tok = torch.empty((p.batch, effective_budget(p)),
+                              dtype=torch.int32, device=Q.device)
+            seg = torch.empty((p.batch, p.segments), dtype=torch.int32,
+                              device=Q.device)
+        if workspace is None:
+            workspace = alloc_workspace(p, OP_SHARED, Q.device)
+    wf_filter_attend_shared(p, Q, K, V, Kg, Vg, O, tok, seg, workspace,
+                            stream)
+    return (O, tok, seg) if want_indices else O
 
 
 # ------------------------------------------------------------ cached A_J

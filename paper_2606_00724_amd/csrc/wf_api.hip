@@ -137,7 +137,7 @@ static size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t logits = 0, sstats = 0, W = 0, seg = 0, cstats = 0,
-         wpool = 0, tok = 0, part = 0, pstat = 0, total = 0;
+         wpool = 0, tok = 0, part = 0, pstat = 0, wsum = 0, wpsum = 0, sseg = 0, total = 0;
 };
 
 static long keff_of(const wf_params& p) {
@@ -161,6 +161,9 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     off += up256(bytes);
     return at;
   };
+  const bool shared = op == WF_OP_SHARED;
+  if (shared && !fast_path(p)) return l;  // unsupported: total 0
+  if (shared) op = WF_OP_FUSED;           // the fused regions, then the sums
   const bool fast = op == WF_OP_FUSED && fast_path(p);
   const bool whole = op == WF_OP_FUSED || op == WF_OP_CACHED;  // a whole step
   const bool skim = op == WF_OP_SKIM || whole;
@@ -192,6 +195,13 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     const AttnPlan ap = plan_attn(p, attn_rows);
     l.part = take(U * ap.splits * B * p.head_dim * sizeof(float));
     l.pstat = take(U * ap.splits * 2 * B * sizeof(float));
+  }
+  if (shared) {
+    // W and W' of each sequence, summed over its heads; its shared regions
+    const size_t nb = (size_t)p.batch;
+    l.wsum = take(nb * nJ * sizeof(float));
+    l.wpsum = take(nb * P * sizeof(float));
+    l.sseg = take(nb * p.segments * sizeof(int32_t));
   }
   l.total = off;
   return l;
@@ -438,6 +448,78 @@ static wf_status cached_impl(const wf_params* p, const void* Q, const float* app
   return ok();
 }
 
+// ------------------------------------------------------------ shared selection
+
+// One selection per sequence, shared by its heads: the token-level sequence
+// with W and W' added over the heads before each top-k.
+static const char* const kSharedNames[] = {
+    "token_skim", "block_weights", "head_sum_w", "scan_weights",
+    "head_sum_wpool", "sparse_attn", "attn_combine"};
+constexpr int kSharedKernels = 7;
+
+static wf_status shared_impl(const wf_params* p, const void* Q, const void* K,
+                             const void* V, const void* Kg, const void* Vg, void* O,
+                             int32_t* tok_idx, int32_t* seg_idx, void* ws, size_t ws_bytes,
+                             void* stream, void** events, int n_events) {
+  WF_TRY(check_params(p));
+  if (!fast_path(*p))
+    return fail(WF_ERR_UNSUPPORTED,
+                "shared selection runs on the token-level path only (bf16 keys, Haar "
+                "with 3..5 levels or db2 with 6, at most 64 query rows)");
+  WF_TRY(check_ptr(Q, "Q", false));
+  WF_TRY(check_ptr(K, "K", false));
+  WF_TRY(check_ptr(V, "V", false));
+  WF_TRY(check_ptr(O, "O", false));
+  WF_TRY(check_ptr(tok_idx, "tok_idx", true));
+  WF_TRY(check_ptr(seg_idx, "seg_idx", true));
+  if (p->gen_len > 0) {
+    WF_TRY(check_ptr(Kg, "Kg", false));
+    WF_TRY(check_ptr(Vg, "Vg", false));
+  }
+  if (events && n_events < kSharedKernels + 1)
+    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, kSharedKernels + 1);
+  const long nrows = keff_of(*p) + remainder_len(*p) + p->gen_len;
+  const Layout l = layout_for(*p, WF_OP_SHARED, nrows);
+  WF_TRY(check_workspace(ws, ws_bytes, l.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  float* logits = reinterpret_cast<float*>(at(ws, l.logits));
+  float* sstats = reinterpret_cast<float*>(at(ws, l.sstats));
+  float* W = reinterpret_cast<float*>(at(ws, l.W));
+  float* wpool = reinterpret_cast<float*>(at(ws, l.wpool));
+  float* part = reinterpret_cast<float*>(at(ws, l.part));
+  float* pstat = reinterpret_cast<float*>(at(ws, l.pstat));
+  float* wsum = reinterpret_cast<float*>(at(ws, l.wsum));
+  float* wpsum = reinterpret_cast<float*>(at(ws, l.wpsum));
+  int32_t* seg = seg_idx ? seg_idx : reinterpret_cast<int32_t*>(at(ws, l.sseg));
+  const int H = p->heads;
+  const long nJ = (long)p->ctx_len >> p->levels;
+  const long P = (long)p->segments << p->levels;
+  int k = 0;
+  auto mark = [&]() -> hipError_t {
+    if (!events) return hipSuccess;
+    return hipEventRecord(static_cast<hipEvent_t>(events[k]), s);
+  };
+  auto step = [&](hipError_t launched) -> wf_status {
+    if (launched != hipSuccess)
+      return fail(WF_ERR_HIP, "%s: %s", kSharedNames[k], hipGetErrorString(launched));
+    ++k;
+    hipError_t e = mark();
+    if (e != hipSuccess) return fail(WF_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    return WF_OK;
+  };
+  WF_HIP(mark(), "hipEventRecord");
+  WF_TRY(step(launch_token_skim(*p, Q, K, logits, sstats, s)));
+  WF_TRY(step(launch_block_weights(*p, logits, sstats, W, s)));
+  WF_TRY(step(launch_head_sum(W, wsum, nJ, H, p->batch, s)));
+  WF_TRY(step(launch_scan_select_weights(*p, Q, K, wsum, logits, seg, wpool, s, H)));
+  WF_TRY(step(launch_head_sum(wpool, wpsum, P, H, p->batch, s)));
+  WF_TRY(step(launch_attn_select(*p, Q, K, V, wpsum, seg, tok_idx, Kg, Vg, nrows, part, pstat,
+                                 s, H)));
+  WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
+  return ok();
+}
+
 // ------------------------------------------------------------ recursion
 
 // Validates the recursion's parameters and fills counts[b - 1] = c_b.
@@ -594,7 +676,7 @@ extern "C" {
 
 size_t wf_workspace_bytes(const wf_params* p, int32_t op) {
   if (check_params(p) != WF_OK) return 0;
-  if (op < WF_OP_SKIM || op > WF_OP_CACHED) return 0;
+  if (op < WF_OP_SKIM || op > WF_OP_SHARED) return 0;
   return layout_for(*p, op, keff_of(*p) + remainder_len(*p) + p->gen_len).total;
 }
 
@@ -738,6 +820,37 @@ int32_t wf_filter_attend_kernels(const wf_params* p) {
 const char* wf_filter_attend_kernel_name(const wf_params* p, int32_t i) {
   if (check_params(p) != WF_OK || i < 0 || i >= fused_kernels(*p)) return nullptr;
   return fused_names(*p)[i];
+}
+
+wf_status wf_filter_attend_shared(const wf_params* p, const void* Q, const void* K,
+                                  const void* V, const void* Kg, const void* Vg, void* O,
+                                  int32_t* tok_idx, int32_t* seg_idx, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  return shared_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace, workspace_bytes,
+                     stream, nullptr, 0);
+}
+
+wf_status wf_filter_attend_shared_timed(const wf_params* p, const void* Q, const void* K,
+                                        const void* V, const void* Kg, const void* Vg,
+                                        void* O, int32_t* tok_idx, int32_t* seg_idx,
+                                        void* workspace, size_t workspace_bytes,
+                                        void* stream, void** events, int32_t n_events) {
+  if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
+  for (int i = 0; i < n_events && i <= kSharedKernels; ++i)
+    if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
+  return shared_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace, workspace_bytes,
+                     stream, events, n_events);
+}
+
+int32_t wf_filter_attend_shared_kernels(const wf_params* p) {
+  if (check_params(p) != WF_OK || !fast_path(*p)) return -1;
+  return kSharedKernels;
+}
+
+const char* wf_filter_attend_shared_kernel_name(const wf_params* p, int32_t i) {
+  if (check_params(p) != WF_OK || !fast_path(*p) || i < 0 || i >= kSharedKernels)
+    return nullptr;
+  return kSharedNames[i];
 }
 
 wf_status wf_filter_attend_cached(const wf_params* p, const void* Q, const float* approx,

@@ -416,11 +416,13 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
     auto& sh = *reinterpret_cast<SelectShared<kAttnRingBlock>*>(ring);
     int32_t* segl = reinterpret_cast<int32_t*>(ring + sizeof(SelectShared<kAttnRingBlock>));
     float* Wl = reinterpret_cast<float*>(segl + a.S);
-    const float* Wg = a.wpool + (long)u * a.P;
-    for (int i = threadIdx.x; i < a.S; i += kAttnRingBlock) segl[i] = a.seg[(long)u * a.S + i];
+    const int sel = u / a.share;  // the unit's selection
+    const float* Wg = a.wpool + (long)sel * a.P;
+    for (int i = threadIdx.x; i < a.S; i += kAttnRingBlock) segl[i] = a.seg[(long)sel * a.S + i];
     const long hi = min(re0, (long)a.nsel);
     const int J = a.J, mask = (1 << J) - 1;
-    int32_t* tout = a.tok_out ? a.tok_out + (long)u * a.nsel : nullptr;
+    int32_t* tout =
+        a.tok_out && u % a.share == 0 ? a.tok_out + (long)sel * a.nsel : nullptr;
     auto emit = [&](uint32_t pos, int pp) {
       if ((long)pos >= rb0 && (long)pos < hi) {
         const int32_t t = (segl[pp >> J] << J) | (pp & mask);
@@ -927,8 +929,9 @@ bool attn_can_select(const wf_params& p, long nrows) {
 hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, const void* V,
                               const float* wpool, const int32_t* seg, int32_t* tok_out,
                               const void* Kg, const void* Vg, long nrows, float* part,
-                              float* pstat, hipStream_t s) {
-  if (!attn_can_select(p, nrows)) return hipErrorInvalidValue;
+                              float* pstat, hipStream_t s, int share) {
+  if (!attn_can_select(p, nrows) || share < 1 || (p.batch * p.heads) % share != 0)
+    return hipErrorInvalidValue;
   const AttnPlan pl = plan_attn(p, nrows);
   AttnArgs a{};
   a.Q = Q;
@@ -942,6 +945,7 @@ hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, 
   a.Vg = Vg;
   a.part = part;
   a.pstat = pstat;
+  a.share = share;
   a.U = p.batch * p.heads;
   a.L = p.ctx_len;
   a.B = p.q_len;

@@ -583,6 +583,22 @@ __global__ __launch_bounds__(kWeightsBlock) void block_weights_kernel(BlockWeigh
                                     a.R, B, j0, j1, row_c, [&](int j, float w) { W[j] = w; });
 }
 
+// The selection weights of the H heads of each sequence added up, h in
+// order: one thread per output element, the H loads of a thread issued
+// together (consecutive threads read consecutive elements of every head).
+constexpr int kHeadSumBlock = 256;
+
+__global__ __launch_bounds__(kHeadSumBlock) void head_sum_kernel(HeadSumArgs a) {
+  const long i = (long)blockIdx.x * kHeadSumBlock + threadIdx.x;
+  if (i >= (long)a.groups * a.n) return;  // no barrier follows
+  const long g = i / a.n, j = i - g * a.n;
+  const float* src = a.in + g * a.H * a.n + j;
+  float s = 0.f;
+#pragma unroll 8
+  for (int h = 0; h < a.H; ++h) s += src[(long)h * a.n];
+  a.out[i] = s;
+}
+
 // ------------------------------------------------------------ host side
 
 bool db2_token_path(const wf_params& p) {
@@ -806,6 +822,16 @@ hipError_t launch_block_weights(const wf_params& p, const float* blocks, const f
   a.WPU = weights_slices(p);
   hipLaunchKernelGGL(block_weights_kernel, dim3((unsigned)(a.U * a.WPU)), dim3(kWeightsBlock), 0,
                      s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_sum(const float* in, float* out, long n, int H, int groups,
+                           hipStream_t s) {
+  if (!in || !out || n < 1 || H < 1 || groups < 1) return hipErrorInvalidValue;
+  HeadSumArgs a{in, out, n, H, groups};
+  const long total = (long)groups * n;
+  hipLaunchKernelGGL(head_sum_kernel, dim3((unsigned)((total + kHeadSumBlock - 1) / kHeadSumBlock)),
+                     dim3(kHeadSumBlock), 0, s, a);
   return hipGetLastError();
 }
 

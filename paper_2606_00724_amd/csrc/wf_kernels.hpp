@@ -77,6 +77,9 @@ struct ScanArgs {
   int nbuf;             // LDS ring depth (bf16 path)
   int seg_cap;          // region ids staged per workgroup (bf16 path)
   float scale;
+  // units per selection: the selecting scan of unit u reads W and writes
+  // seg_out of selection u / share (seg_out by the group's first unit only)
+  int share = 1;
 };
 
 struct ScanSelectArgs {
@@ -122,6 +125,9 @@ struct AttnArgs {
   int rps;              // cache rows per split (multiple of the chunk)
   int nbuf;             // LDS ring depth (bf16 path)
   float scale;
+  // units per selection: the selecting attention of unit u reads wpool and
+  // seg of selection u / share (tok_out by the group's first unit only)
+  int share = 1;
 };
 
 constexpr int kFastMaxQBlocks = 4;  // query rows <= 64 on the token-level skim
@@ -153,6 +159,14 @@ struct TokenSkimArgs {
 struct Db2TokenTaps {
   float band[3 << 6];
   float edge[6 << 6];
+};
+
+// out [groups][n] = the sum over h < H of in [groups H + h][n], h in order
+struct HeadSumArgs {
+  const float* in;
+  float* out;
+  long n;
+  int H, groups;
 };
 
 struct BlockWeightsArgs {

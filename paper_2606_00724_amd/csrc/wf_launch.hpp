@@ -137,9 +137,11 @@ hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
 // Token-level path: the weights pass that first takes the unit's top-S
 // regions of W itself (seg_out [U][S] receives them) and forms the pool
 // normalisers from the selected blocks' log-sum-exps (blocks [U][nJ][2][B]).
+// share: units per selection (W and seg_out indexed by u / share; 1 = per
+// unit).
 hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const void* K,
                                       const float* W, const float* blocks, int32_t* seg_out,
-                                      float* wpool, hipStream_t s);
+                                      float* wpool, hipStream_t s, int share = 1);
 hipError_t launch_scan_select(const wf_params& p, const float* wpool,
                               const int32_t* seg, int32_t* tok,
                               hipStream_t s);
@@ -154,10 +156,15 @@ hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
 // tokens of the scan weights wpool [U][S 2^J] itself (the pool of the
 // regions seg [U][S]); tok_out [U][k_eff] (nullable) receives them.
 bool attn_can_select(const wf_params& p, long nrows);
+// share: units per selection (wpool, seg and tok_out indexed by u / share).
 hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, const void* V,
                               const float* wpool, const int32_t* seg, int32_t* tok_out,
                               const void* Kg, const void* Vg, long nrows, float* part,
-                              float* pstat, hipStream_t s);
+                              float* pstat, hipStream_t s, int share = 1);
+// out [groups][n] = sum over h < H of in [groups H + h][n], in order of h
+// (the selection weights of a sequence's heads added up).
+hipError_t launch_head_sum(const float* in, float* out, long n, int H, int groups,
+                           hipStream_t s);
 hipError_t launch_attn_combine(const wf_params& p, long nrows,
                                const float* part, const float* pstat, void* O,
                                hipStream_t s);

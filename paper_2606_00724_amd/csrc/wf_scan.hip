@@ -276,8 +276,9 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     unsigned char* spare = ring + (size_t)(nbuf - 1) * CHB;
     auto& sh = *reinterpret_cast<SelectShared<kPoolBlock>*>(spare);
     float* Wl = reinterpret_cast<float*>(ring);
-    const float* Wg = a.W + (long)u * a.nJ;
-    int32_t* seg_out = c == 0 ? a.seg_out + (long)u * a.S : nullptr;
+    const int sel = u / a.share;  // the unit's selection
+    const float* Wg = a.W + (long)sel * a.nJ;
+    int32_t* seg_out = c == 0 && u % a.share == 0 ? a.seg_out + (long)sel * a.S : nullptr;
     auto emit = [&](uint32_t pos, int j) {
       segs[pos] = j;
       if (seg_out) seg_out[pos] = j;
@@ -595,8 +596,9 @@ static hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t s) {
 
 hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const void* K,
                                       const float* W, const float* blocks, int32_t* seg_out,
-                                      float* wpool, hipStream_t s) {
-  if (p.dtype != WF_BF16 || p.q_len > 64 || p.segments > kSelectLdsSegs)
+                                      float* wpool, hipStream_t s, int share) {
+  if (p.dtype != WF_BF16 || p.q_len > 64 || p.segments > kSelectLdsSegs || share < 1 ||
+      (p.batch * p.heads) % share != 0)
     return hipErrorInvalidValue;
   const ScanPlan pl = plan_scan(p, true);
   if (pl.nbuf < 2) return hipErrorInvalidValue;
@@ -605,6 +607,7 @@ hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const v
   a.K = K;
   a.W = W;
   a.blocks = blocks;
+  a.share = share;
   a.seg_out = seg_out;
   a.wpool = wpool;
   a.U = p.batch * p.heads;

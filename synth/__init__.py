@@ -70,6 +70,8 @@ class Workload:
     proportions: tuple = ()
     # the prompt's A_J is computed once and reused by every step
     cached: bool = False
+    # one selection per sequence, shared by its heads
+    shared: bool = False
     description: str = field(default="", compare=False)
 
     @property
@@ -157,6 +159,14 @@ _add(Workload("tail32k", batch=4, heads=32, ctx_len=32768 + 20, head_dim=128,
               description="32K context that is not a multiple of 2^J, with a "
                           "generation tail: batch 4, 32 heads, d=128, "
                           "L=32788 (20 positions always kept), G=64, B=64, "
+                          "bf16, Haar J=5, budget 2048"))
+_add(Workload("shared32k", batch=4, heads=32, ctx_len=32768, head_dim=128,
+              q_len=64, dtype="bf16", rho=0.98, needles=8, wavelet="haar",
+              boundary="symmetric", levels=5,
+              segments=_pool_segments(32768, 5, 2048), budget=2048, seed=3,
+              shared=True,
+              description="32K context with one selection per sequence shared "
+                          "by its 32 heads: batch 4, d=128, L=32768, B=64, "
                           "bf16, Haar J=5, budget 2048"))
 _add(Workload("cached32k", batch=4, heads=32, ctx_len=32768, head_dim=128,
               q_len=64, dtype="bf16", rho=0.98, needles=8, wavelet="haar",

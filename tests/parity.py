@@ -164,3 +164,35 @@ def summary(stats: list[dict]) -> str:
     return (f"{len(stats)} units, seg diffs {sum(s['seg_diff'] for s in stats)}, "
             f"tok diffs {sum(s['tok_diff'] for s in stats)}, "
             f"max O err {max(s['o_err'] for s in stats):.2e}")
+
+
+def check_shared_sequence(*, Q, K, V, levels, segments, budget, wavelet,
+                          boundary, dtype, seg_gpu, tok_gpu, O_gpu, Kg=None,
+                          Vg=None, what=""):
+    """Conditional check of one sequence's shared selection: Q/K/V [H, ...]
+    of its heads, seg_gpu [S] and tok_gpu [k_eff] shared, O_gpu [H, B, d].
+    W is the heads' eq. 8 column sums added; W' the heads' scan weights over
+    the GPU's own pool added; each head's output is checked on the GPU's own
+    tokens."""
+    H = Q.shape[0]
+    L = K.shape[1]
+    Lf = (L >> levels) << levels
+    W_ref = sum(oracle.skim(Q[h], oracle.dwt(K[h, :Lf], levels, wavelet, boundary))
+                for h in range(H))
+    n_seg_diff = check_selection(seg_gpu, W_ref, segments, f"{what} seg")
+    Wp_ref = sum(oracle.scan(Q[h], K[h], seg_gpu, levels, budget)[0] for h in range(H))
+    pool = pool_tokens(seg_gpu, levels)
+    tok = i64(tok_gpu)
+    keff = min(budget, pool.size)
+    pos = np.searchsorted(pool, tok)
+    assert np.all(pos < pool.size) and np.all(pool[np.minimum(pos, pool.size - 1)] == tok), \
+        f"{what}: tokens outside the pool of the GPU's regions"
+    n_tok_diff = check_selection(pos, Wp_ref, keff, f"{what} tok")
+    keep = np.concatenate([tok, np.arange(Lf, L)])
+    err = 0.0
+    for h in range(H):
+        O_ref = oracle.attend(Q[h], K[h], V[h], keep, None if Kg is None else Kg[h],
+                              None if Vg is None else Vg[h])
+        err = max(err, float(np.max(np.abs(f64(O_gpu[h]) - O_ref))))
+    assert err <= O_TOL[dtype], f"{what}: O max abs err {err:.3e} > {O_TOL[dtype]}"
+    return dict(seg_diff=n_seg_diff, tok_diff=n_tok_diff, o_err=err)

@@ -164,6 +164,35 @@ def test_cached_step_attention_selects_with_bf16_keys(wfpkg, change, selects):
     assert names == head + ([] if selects else ["scan_select"]) + tail
 
 
+def test_shared_selection_is_built_on_the_token_path_only(wfpkg):
+    p = _params(wfpkg, dtype="bf16", heads=4)
+    assert wfpkg.shared_kernel_names(p) == [
+        "token_skim", "block_weights", "head_sum_w", "scan_weights",
+        "head_sum_wpool", "sparse_attn", "attn_combine"]
+    # the fused regions plus the heads' sums and the shared regions
+    assert (wfpkg.workspace_bytes(p, wfpkg.OP_SHARED)
+            > wfpkg.workspace_bytes(p, wfpkg.OP_FUSED))
+    pf = _params(wfpkg, heads=4)               # fp32: the general path
+    assert wfpkg.shared_kernel_names(pf) == []
+    assert wfpkg.workspace_bytes(pf, wfpkg.OP_SHARED) == 0
+    lib = wfpkg.library()
+    good = ctypes.c_void_p(0x10000)
+    rc = lib.wf_filter_attend_shared(ctypes.byref(pf), good, good, good, None,
+                                     None, good, None, None, good, 1 << 40,
+                                     None)
+    assert rc == 2 and b"token-level" in lib.wf_last_error()
+    # the token path checks its pointers and workspace before queueing
+    rc = lib.wf_filter_attend_shared(ctypes.byref(p), good, good, good, None,
+                                     None, None, None, None, good, 1 << 40,
+                                     None)
+    assert rc == 1 and b"O" in lib.wf_last_error()
+    need = wfpkg.workspace_bytes(p, wfpkg.OP_SHARED)
+    rc = lib.wf_filter_attend_shared(ctypes.byref(p), good, good, good, None,
+                                     None, good, None, None, good, need - 1,
+                                     None)
+    assert rc == 3
+
+
 def test_binding_rejects_host_tensors(wfpkg):
     import torch
     p = _params(wfpkg)

@@ -89,3 +89,13 @@ def test_single_thread_oracle_baseline_runs_one_unit_per_call():
     r = bench.cpu_single_thread("tiny", min_seconds=0.0)
     assert r["cores"] == 1 and r["workload"] == "tiny"
     assert r["value"] > 0 and r["unit"] == "tokens/s"
+
+
+def test_shared_workload_recall_takes_one_list_per_sequence():
+    import torch
+    w = synth.small_variant(synth.WORKLOADS["tiny"], batch=2, heads=3,
+                            shared=True)
+    keff = min(w.budget, w.segments << w.levels)
+    tok = torch.arange(keff, dtype=torch.int32).repeat(w.batch, 1)
+    r = bench.needle_recall(w, tok)
+    assert r["units"] == w.batch * w.heads
