@@ -183,9 +183,10 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
   }
   const uint32_t ring_lds = lds_offset(ring);
   const int nbuf = a.nbuf;
-  // the keys stream past the caches; the gathered rows of a refinement scale
-  // are loaded normally, since the attention reads many of them again
-  auto issue_rows = [&](uint32_t slot) { issue_chunk<CR, G, NIW, !GATHER>(slot, rows); };
+  // the keys, and the gathered rows of a refinement scale, stream past the
+  // caches (for the gathered rows that measured faster than cached loads,
+  // although the attention reads many of them again)
+  auto issue_rows = [&](uint32_t slot) { issue_chunk<CR, G, NIW, true>(slot, rows); };
   if (loader) {
     for (int k = 0; k < nch && k < nbuf - 1; ++k) {
       rows.c0 = tb + (long)k * CR;
