@@ -257,6 +257,21 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, col = lane & 15;
 
+  // SEL (at most 64 query rows): the query rows are loaded into registers
+  // first and written to LDS after the selection, by when they have landed
+  const bf16_t* Qunit = reinterpret_cast<const bf16_t*>(a.Q) + (long)u * a.B * D;
+  constexpr int QVR = D / 8;                                  // 16-byte vectors per row
+  constexpr int QV = (64 * QVR + kPoolBlock - 1) / kPoolBlock;  // vectors per thread
+  const int qtotal = a.B * QVR;
+  u32x4 qpre[QV];
+  if constexpr (SEL) {
+#pragma unroll
+    for (int i = 0; i < QV; ++i) {
+      const int v = min(i * kPoolBlock + (int)threadIdx.x, qtotal - 1);
+      qpre[i] = *reinterpret_cast<const u32x4*>(Qunit + (long)(v / QVR) * D + (v % QVR) * 8);
+    }
+  }
+
   // region ids of this range: the span's own, or with SEL all S of the unit
   const int s_lo = SEL ? 0 : (int)(pb >> a.J);
   const uint32_t ring_lds = lds_offset(ring);
@@ -339,8 +354,15 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     const int ns = (int)((pe - 1) >> a.J) - s_lo + 1;
     for (int i = threadIdx.x; i < ns; i += kPoolBlock) segs[i] = a.seg[(long)u * a.S + s_lo + i];
   }
-  const bf16_t* Qunit = reinterpret_cast<const bf16_t*>(a.Q) + (long)u * a.B * D;
-  stage_rows_any<bf16_t, D, kPoolBlock>(Qs, a.B, [&](int r) { return Qunit + (long)r * D; });
+  if constexpr (SEL) {
+#pragma unroll
+    for (int i = 0; i < QV; ++i) {
+      const int v = i * kPoolBlock + (int)threadIdx.x;
+      if (v < qtotal) *reinterpret_cast<u32x4*>(Qs + (v / QVR) * QSTR + (v % QVR) * 8) = qpre[i];
+    }
+  } else {
+    stage_rows_any<bf16_t, D, kPoolBlock>(Qs, a.B, [&](int r) { return Qunit + (long)r * D; });
+  }
   if constexpr (WEIGHTS && !SEL) {
     const float* stt = a.stats + (long)u * a.Cs * 2 * a.B;
     for (int q = threadIdx.x; q < a.B; q += kPoolBlock) {
