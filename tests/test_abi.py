@@ -314,6 +314,22 @@ def test_binding_checks_the_tail_and_approximation(wfpkg):
         wfpkg.wf_dwt_keys(p, K16, A)
 
 
+def test_binding_checks_shared_outputs(wfpkg):
+    """The shared call's index outputs hold one list per sequence."""
+    import torch
+    p = _params(wfpkg, dtype="bf16", heads=4)
+    t = _fused_tensors(wfpkg, p)
+    per_unit = torch.zeros(p.batch * p.heads * wfpkg.effective_budget(p),
+                           dtype=torch.int32)
+    with pytest.raises(ValueError, match="tok_idx:"):
+        wfpkg.wf_filter_attend_shared(p, t["Q"], t["K"], t["V"], None, None,
+                                      t["O"], per_unit, None, None)
+    seg = torch.zeros(p.batch * p.segments + 1, dtype=torch.int32)
+    with pytest.raises(ValueError, match="seg_idx:"):
+        wfpkg.wf_filter_attend_shared(p, t["Q"], t["K"], t["V"], None, None,
+                                      t["O"], None, seg, None)
+
+
 def test_binding_checks_recursion_outputs(wfpkg):
     import torch
     p = _params(wfpkg, levels=3, dtype="bf16")
