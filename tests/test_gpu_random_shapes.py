@@ -1,0 +1,109 @@
+"""GPU parity on seeded random shapes: the fused, cached and (where the
+token-level path applies) shared calls against the oracle, on every unit,
+for shapes drawn across element types, head sizes, wavelets and
+extensions, 1..7 levels, lengths with and without a remainder, 1..100 query
+rows, any S and k, and generation tails.  The draw is fixed (seed 2026), so
+a failure names a reproducible case."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from parity import check_shared_sequence, check_units, f64, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def wf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2606_00724_amd as wf
+    return wf
+
+
+def _cases(n=96, seed=2026):
+    rng = np.random.default_rng(seed)
+    base = synth.WORKLOADS["tiny"]
+    out = []
+    while len(out) < n:
+        # every other case on the token-level path (bf16, Haar 3..5 levels or
+        # db2 at 6, at most 64 query rows)
+        token = len(out) % 2 == 0
+        J = int(rng.integers(3, 6)) if token else int(rng.integers(1, 8))
+        nJ = int(rng.integers(2, 160))
+        rem = int(rng.integers(1, 1 << J)) if J > 0 and rng.random() < 0.4 else 0
+        S = int(rng.integers(1, nJ + 1))
+        w = synth.small_variant(
+            base, name=f"rand{len(out)}",
+            batch=int(rng.integers(1, 3)), heads=int(rng.integers(1, 4)),
+            ctx_len=(nJ << J) + rem, head_dim=int(rng.choice([64, 128])),
+            q_len=int(rng.choice([1, 7, 16, 17, 32, 33, 48, 64] if token
+                                 else [1, 7, 16, 17, 32, 33, 48, 64, 65, 100])),
+            dtype="bf16" if token else str(rng.choice(["bf16", "bf16", "f32"])),
+            wavelet="haar" if token else str(rng.choice(["haar", "haar", "db2"])),
+            boundary=str(rng.choice(["symmetric", "periodic"])),
+            levels=J, segments=S, budget=int(rng.integers(1, (S << J) + 40)),
+            gen_len=int(rng.choice([0, 0, 8, 17])), needles=1,
+            seed=100 + len(out))
+        if w.ctx_len < synth.NEEDLE_LEN:
+            continue
+        out.append(w)
+    return out
+
+
+CASES = _cases()
+
+
+def _inputs(w):
+    Q, K, V = synth.make_inputs(w)
+    Kg = Vg = None
+    if w.gen_len:
+        Kg, Vg = synth.make_tail(w, w.gen_len)
+    return Q, K, V, Kg, Vg
+
+
+def _dev(x):
+    return None if x is None else x.cuda()
+
+
+@pytest.mark.parametrize("i", range(len(CASES)))
+def test_random_shape(wf, i):
+    w = CASES[i]
+    p = wf.params_for(w)
+    if wf.workspace_bytes(p, wf.OP_FUSED) == 0:
+        pytest.skip(f"{w} is outside the parameter limits")
+    say(f"[case] {i}: {w.batch}x{w.heads} L={w.ctx_len} d={w.head_dim} B={w.q_len} "
+        f"{w.dtype} {w.wavelet}/{w.boundary} J={w.levels} S={w.segments} "
+        f"k={w.budget} G={w.gen_len}; {wf.fused_kernel_names(p)}")
+    Q, K, V, Kg, Vg = _inputs(w)
+    O, tok, seg = wf.filter_attend(p, Q.cuda(), K.cuda(), V.cuda(), _dev(Kg),
+                                   _dev(Vg), want_indices=True)
+    torch.cuda.synchronize()
+    check_units(w, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, seg=seg.cpu(), tok=tok.cpu(),
+                O=O.cpu(), what=f"random {i} fused")
+    if i % 3 == 0:
+        Kd = K.cuda()
+        approx = wf.dwt_approx(p, Kd)
+        O, tok, seg = wf.filter_attend_cached(p, Q.cuda(), approx, Kd, V.cuda(),
+                                              _dev(Kg), _dev(Vg),
+                                              want_indices=True)
+        torch.cuda.synchronize()
+        check_units(w, Q=Q, K=K, V=V, Kg=Kg, Vg=Vg, seg=seg.cpu(),
+                    tok=tok.cpu(), O=O.cpu(), what=f"random {i} cached")
+    if wf.shared_kernel_names(p):
+        O, tok, seg = wf.filter_attend_shared(p, Q.cuda(), K.cuda(), V.cuda(),
+                                              _dev(Kg), _dev(Vg),
+                                              want_indices=True)
+        torch.cuda.synchronize()
+        O, tok, seg = O.cpu(), tok.cpu(), seg.cpu()
+        for b in range(w.batch):
+            check_shared_sequence(
+                Q=f64(Q[b]), K=f64(K[b]), V=f64(V[b]),
+                Kg=None if Kg is None else f64(Kg[b]),
+                Vg=None if Vg is None else f64(Vg[b]), levels=w.levels,
+                segments=w.segments, budget=w.budget, wavelet=w.wavelet,
+                boundary=w.boundary, dtype=w.dtype, seg_gpu=seg[b],
+                tok_gpu=tok[b], O_gpu=O[b], what=f"random {i} shared {b}")
