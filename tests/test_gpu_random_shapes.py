@@ -2,8 +2,10 @@
 token-level path applies) shared calls against the oracle, on every unit,
 for shapes drawn across element types, head sizes, wavelets and
 extensions, 1..7 levels, lengths with and without a remainder, 1..100 query
-rows, any S and k, and generation tails.  The draw is fixed (seed 2026), so
-a failure names a reproducible case."""
+rows, any S and k, and generation tails; and the multi-scale recursion
+(eqs. 9-11) with 1..6 scales and random proportions, every scale checked on
+the GPU's own kept blocks.  The draws are fixed (seeds 2026 and 2027), so a
+failure names a reproducible case."""
 from __future__ import annotations
 
 import numpy as np
@@ -107,3 +109,43 @@ def test_random_shape(wf, i):
                 segments=w.segments, budget=w.budget, wavelet=w.wavelet,
                 boundary=w.boundary, dtype=w.dtype, seg_gpu=seg[b],
                 tok_gpu=tok[b], O_gpu=O[b], what=f"random {i} shared {b}")
+
+
+def _rec_cases(n=32, seed=2027):
+    rng = np.random.default_rng(seed)
+    base = synth.WORKLOADS["tiny"]
+    out = []
+    while len(out) < n:
+        B = int(rng.integers(1, 7))
+        nB = int(rng.integers(2, 120))
+        rem = int(rng.integers(1, 1 << B)) if rng.random() < 0.4 else 0
+        w = synth.small_variant(
+            base, name=f"rrand{len(out)}",
+            batch=int(rng.integers(1, 3)), heads=int(rng.integers(1, 3)),
+            ctx_len=(nB << B) + rem, head_dim=int(rng.choice([64, 128])),
+            q_len=int(rng.choice([1, 16, 17, 32, 64, 65])),
+            dtype=str(rng.choice(["bf16", "bf16", "f32"])),
+            wavelet=str(rng.choice(["haar", "haar", "db2"])),
+            boundary=str(rng.choice(["symmetric", "periodic"])),
+            levels=B, proportions=tuple(float(x) for x in rng.uniform(0.1, 1.0, B)),
+            gen_len=int(rng.choice([0, 0, 8])), needles=1, seed=500 + len(out))
+        if w.ctx_len < synth.NEEDLE_LEN:
+            continue
+        out.append(w)
+    return out
+
+
+REC_CASES = _rec_cases()
+
+
+@pytest.mark.parametrize("i", range(len(REC_CASES)))
+def test_random_recursion(wf, i):
+    import test_gpu_recursion as rec
+    w = REC_CASES[i]
+    p = wf.params_for(w)
+    if wf.recursive_workspace_bytes(p, w.proportions) == 0:
+        pytest.skip("outside the parameter limits")
+    say(f"[case] rec {i}: {w.batch}x{w.heads} L={w.ctx_len} d={w.head_dim} "
+        f"B={w.q_len} {w.dtype} {w.wavelet}/{w.boundary} scales={w.levels} "
+        f"m={[round(m, 3) for m in w.proportions]} G={w.gen_len}")
+    rec.check(wf, w)
