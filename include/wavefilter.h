@@ -303,10 +303,12 @@ const char* wf_filter_attend_cached_kernel_name(const wf_params* p, int32_t i);
  *   seg_idx    nullable [batch][S]                int32 out: the regions,
  *              ascending
  *   workspace  >= wf_workspace_bytes(p, WF_OP_SHARED)
- * Only the token-level path is built for it: bf16 keys, Haar with 3..5
- * levels or db2 with 6 (at least 4 coefficients), at most 64 query rows
- * and a positive scale; other parameters return WF_ERR_UNSUPPORTED (and
- * wf_workspace_bytes(p, WF_OP_SHARED) is 0 for them).
+ * Every parameter set wf_filter_attend takes is supported: on its
+ * token-level path the scan and the attention take the sequence's
+ * selections themselves; otherwise the per-unit skim writes W, one select
+ * per sequence takes the regions from the heads' sum, the scan's two
+ * passes run per unit over them, and one select per sequence takes the
+ * tokens from the heads' sum of W'.
  */
 wf_status wf_filter_attend_shared(const wf_params* p, const void* Q,
                                   const void* K, const void* V, const void* Kg,

@@ -162,8 +162,7 @@ static Layout layout_for(const wf_params& p, int op, long attn_rows) {
     return at;
   };
   const bool shared = op == WF_OP_SHARED;
-  if (shared && !fast_path(p)) return l;  // unsupported: total 0
-  if (shared) op = WF_OP_FUSED;           // the fused regions, then the sums
+  if (shared) op = WF_OP_FUSED;  // the fused regions, then the sums
   const bool fast = op == WF_OP_FUSED && fast_path(p);
   const bool whole = op == WF_OP_FUSED || op == WF_OP_CACHED;  // a whole step
   const bool skim = op == WF_OP_SKIM || whole;
@@ -455,17 +454,24 @@ static wf_status cached_impl(const wf_params* p, const void* Q, const float* app
 static const char* const kSharedNames[] = {
     "token_skim", "block_weights", "head_sum_w", "scan_weights",
     "head_sum_wpool", "sparse_attn", "attn_combine"};
-constexpr int kSharedKernels = 7;
+// the general path: W per unit from the skim select (whose own regions are
+// not used), the heads' sum, one select per sequence; the scan's two passes
+// per unit over the sequence's regions, the heads' sum of W', one token
+// select per sequence; attention per unit
+static const char* const kSharedGeneralNames[] = {
+    "skim_tile", "skim_select", "head_sum_w", "select_regions", "scan_stats",
+    "scan_weights", "head_sum_wpool", "scan_select", "sparse_attn", "attn_combine"};
+constexpr int kSharedMaxKernels = 10;
+static int shared_kernels(const wf_params& p) { return fast_path(p) ? 7 : 10; }
+static const char* const* shared_names(const wf_params& p) {
+  return fast_path(p) ? kSharedNames : kSharedGeneralNames;
+}
 
 static wf_status shared_impl(const wf_params* p, const void* Q, const void* K,
                              const void* V, const void* Kg, const void* Vg, void* O,
                              int32_t* tok_idx, int32_t* seg_idx, void* ws, size_t ws_bytes,
                              void* stream, void** events, int n_events) {
   WF_TRY(check_params(p));
-  if (!fast_path(*p))
-    return fail(WF_ERR_UNSUPPORTED,
-                "shared selection runs on the token-level path only (bf16 keys, Haar "
-                "with 3..5 levels or db2 with 6, at most 64 query rows)");
   WF_TRY(check_ptr(Q, "Q", false));
   WF_TRY(check_ptr(K, "K", false));
   WF_TRY(check_ptr(V, "V", false));
@@ -476,9 +482,12 @@ static wf_status shared_impl(const wf_params* p, const void* Q, const void* K,
     WF_TRY(check_ptr(Kg, "Kg", false));
     WF_TRY(check_ptr(Vg, "Vg", false));
   }
-  if (events && n_events < kSharedKernels + 1)
-    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, kSharedKernels + 1);
-  const long nrows = keff_of(*p) + remainder_len(*p) + p->gen_len;
+  const int nk = shared_kernels(*p);
+  const char* const* names = shared_names(*p);
+  if (events && n_events < nk + 1)
+    return fail(WF_ERR_INVALID_ARG, "n_events %d < %d", n_events, nk + 1);
+  const long keff = keff_of(*p);
+  const long nrows = keff + remainder_len(*p) + p->gen_len;
   const Layout l = layout_for(*p, WF_OP_SHARED, nrows);
   WF_TRY(check_workspace(ws, ws_bytes, l.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -486,6 +495,7 @@ static wf_status shared_impl(const wf_params* p, const void* Q, const void* K,
   float* logits = reinterpret_cast<float*>(at(ws, l.logits));
   float* sstats = reinterpret_cast<float*>(at(ws, l.sstats));
   float* W = reinterpret_cast<float*>(at(ws, l.W));
+  float* cstats = reinterpret_cast<float*>(at(ws, l.cstats));
   float* wpool = reinterpret_cast<float*>(at(ws, l.wpool));
   float* part = reinterpret_cast<float*>(at(ws, l.part));
   float* pstat = reinterpret_cast<float*>(at(ws, l.pstat));
@@ -502,20 +512,39 @@ static wf_status shared_impl(const wf_params* p, const void* Q, const void* K,
   };
   auto step = [&](hipError_t launched) -> wf_status {
     if (launched != hipSuccess)
-      return fail(WF_ERR_HIP, "%s: %s", kSharedNames[k], hipGetErrorString(launched));
+      return fail(WF_ERR_HIP, "%s: %s", names[k], hipGetErrorString(launched));
     ++k;
     hipError_t e = mark();
     if (e != hipSuccess) return fail(WF_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     return WF_OK;
   };
   WF_HIP(mark(), "hipEventRecord");
-  WF_TRY(step(launch_token_skim(*p, Q, K, logits, sstats, s)));
-  WF_TRY(step(launch_block_weights(*p, logits, sstats, W, s)));
-  WF_TRY(step(launch_head_sum(W, wsum, nJ, H, p->batch, s)));
-  WF_TRY(step(launch_scan_select_weights(*p, Q, K, wsum, logits, seg, wpool, s, H)));
-  WF_TRY(step(launch_head_sum(wpool, wpsum, P, H, p->batch, s)));
-  WF_TRY(step(launch_attn_select(*p, Q, K, V, wpsum, seg, tok_idx, Kg, Vg, nrows, part, pstat,
-                                 s, H)));
+  if (fast_path(*p)) {
+    WF_TRY(step(launch_token_skim(*p, Q, K, logits, sstats, s)));
+    WF_TRY(step(launch_block_weights(*p, logits, sstats, W, s)));
+    WF_TRY(step(launch_head_sum(W, wsum, nJ, H, p->batch, s)));
+    WF_TRY(step(launch_scan_select_weights(*p, Q, K, wsum, logits, seg, wpool, s, H)));
+    WF_TRY(step(launch_head_sum(wpool, wpsum, P, H, p->batch, s)));
+    WF_TRY(step(launch_attn_select(*p, Q, K, V, wpsum, seg, tok_idx, Kg, Vg, nrows, part,
+                                   pstat, s, H)));
+  } else {
+    // one "unit" per sequence for the two selections over the heads' sums
+    wf_params pg = *p;
+    pg.heads = 1;
+    int32_t* unit_seg = reinterpret_cast<int32_t*>(at(ws, l.seg));  // not used after
+    int32_t* tok = tok_idx ? tok_idx : reinterpret_cast<int32_t*>(at(ws, l.tok));
+    const SkimPlan sp = plan_skim(*p, true);
+    WF_TRY(step(launch_skim_tiles(*p, true, Q, K, nullptr, logits, sstats, s)));
+    WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, unit_seg, s)));
+    WF_TRY(step(launch_head_sum(W, wsum, nJ, H, p->batch, s)));
+    WF_TRY(step(launch_select_w(pg, p->batch, wsum, seg, s)));
+    WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s, 0, H)));
+    WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s, 0, H)));
+    WF_TRY(step(launch_head_sum(wpool, wpsum, P, H, p->batch, s)));
+    WF_TRY(step(launch_scan_select(pg, wpsum, seg, tok, s)));
+    WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows, part,
+                            pstat, s, H)));
+  }
   WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
   return ok();
 }
@@ -836,21 +865,20 @@ wf_status wf_filter_attend_shared_timed(const wf_params* p, const void* Q, const
                                         void* workspace, size_t workspace_bytes,
                                         void* stream, void** events, int32_t n_events) {
   if (!events) return fail(WF_ERR_INVALID_ARG, "events is NULL");
-  for (int i = 0; i < n_events && i <= kSharedKernels; ++i)
+  for (int i = 0; i < n_events && i <= kSharedMaxKernels; ++i)
     if (!events[i]) return fail(WF_ERR_INVALID_ARG, "events[%d] is NULL", i);
   return shared_impl(p, Q, K, V, Kg, Vg, O, tok_idx, seg_idx, workspace, workspace_bytes,
                      stream, events, n_events);
 }
 
 int32_t wf_filter_attend_shared_kernels(const wf_params* p) {
-  if (check_params(p) != WF_OK || !fast_path(*p)) return -1;
-  return kSharedKernels;
+  if (check_params(p) != WF_OK) return -1;
+  return shared_kernels(*p);
 }
 
 const char* wf_filter_attend_shared_kernel_name(const wf_params* p, int32_t i) {
-  if (check_params(p) != WF_OK || !fast_path(*p) || i < 0 || i >= kSharedKernels)
-    return nullptr;
-  return kSharedNames[i];
+  if (check_params(p) != WF_OK || i < 0 || i >= shared_kernels(*p)) return nullptr;
+  return shared_names(*p)[i];
 }
 
 wf_status wf_filter_attend_cached(const wf_params* p, const void* Q, const float* approx,

@@ -127,7 +127,7 @@ __global__ __launch_bounds__(kBlock) void attn_kernel(AttnArgs a) {
   vsrc.base = reinterpret_cast<const T*>(a.V);
   ksrc.tail = reinterpret_cast<const T*>(a.Kg);
   vsrc.tail = reinterpret_cast<const T*>(a.Vg);
-  ksrc.tok = vsrc.tok = a.tok ? a.tok + (long)u * a.nsel : nullptr;
+  ksrc.tok = vsrc.tok = a.tok ? a.tok + (long)(u / a.share) * a.nsel : nullptr;
   ksrc.unit_rows = vsrc.unit_rows = a.tok ? (long)a.L : (long)a.nrows;
   ksrc.u = vsrc.u = u;
   ksrc.nsel = vsrc.nsel = a.nsel;
@@ -447,7 +447,7 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
   } else if (a.tok) {
     const long hi = min(re0, (long)a.nsel);
     for (long i = rb0 + threadIdx.x; i < hi; i += kAttnRingBlock)
-      toks[i - rb0] = a.tok[(long)u * a.nsel + i];
+      toks[i - rb0] = a.tok[(long)(u / a.share) * a.nsel + i];
   }
   __syncthreads();
 
@@ -885,9 +885,11 @@ static hipError_t attn_launch(const AttnArgs& a, size_t lds, hipStream_t s) {
 hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
                        const void* V, const int32_t* tok, int nsel,
                        const void* Kg, const void* Vg, int G, long nrows,
-                       float* part, float* pstat, hipStream_t s) {
+                       float* part, float* pstat, hipStream_t s, int share) {
+  if (share < 1 || (p.batch * p.heads) % share != 0) return hipErrorInvalidValue;
   const AttnPlan pl = plan_attn(p, nrows);
   AttnArgs a;
+  a.share = share;
   a.Q = Q;
   a.K = K;
   a.V = V;

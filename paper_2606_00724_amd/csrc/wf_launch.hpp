@@ -131,9 +131,11 @@ hipError_t launch_skim_select(const wf_params& p, int ntiles,
                               float* W, int32_t* seg, hipStream_t s);
 // stat_slices: 0 when `stats` holds one (max, sum) slice per scan workgroup
 // (written by the stats pass), 1 when it holds the pool's final pair.
+// share: units per selection (seg indexed by u / share).
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
                               const void* K, const int32_t* seg, float* stats,
-                              float* wpool, hipStream_t s, int stat_slices = 0);
+                              float* wpool, hipStream_t s, int stat_slices = 0,
+                              int share = 1);
 // Token-level path: the weights pass that first takes the unit's top-S
 // regions of W itself (seg_out [U][S] receives them) and forms the pool
 // normalisers from the selected blocks' log-sum-exps (blocks [U][nJ][2][B]).
@@ -148,10 +150,15 @@ hipError_t launch_scan_select(const wf_params& p, const float* wpool,
 hipError_t launch_gather(const wf_params& p, const void* K, const void* V,
                          const int32_t* tok, const void* Kg, const void* Vg,
                          void* Ks, void* Vs, hipStream_t s);
+// share: units per selection (tok indexed by u / share).
 hipError_t launch_attn(const wf_params& p, const void* Q, const void* K,
                        const void* V, const int32_t* tok, int nsel,
                        const void* Kg, const void* Vg, int G, long nrows,
-                       float* part, float* pstat, hipStream_t s);
+                       float* part, float* pstat, hipStream_t s, int share = 1);
+// The top-S regions (eq. 9) of given weights W [groups][L >> J], one
+// workgroup per group, into seg [groups][S].
+hipError_t launch_select_w(const wf_params& p, long groups, const float* W, int32_t* seg,
+                           hipStream_t s);
 // Token-level path: the attention that first takes the unit's top-k_eff
 // tokens of the scan weights wpool [U][S 2^J] itself (the pool of the
 // regions seg [U][S]); tok_out [U][k_eff] (nullable) receives them.

@@ -66,7 +66,7 @@ __global__ __launch_bounds__(kBlock) void scan_chunk_kernel(ScanArgs a) {
 
   PoolRows<T, D> src;
   src.Kunit = reinterpret_cast<const T*>(a.K) + (long)u * a.Ls * D;
-  src.seg = a.seg + (long)u * a.S;
+  src.seg = a.seg + (long)(u / a.share) * a.S;
   src.J = a.J;
   src.mask = (1 << a.J) - 1;
   src.last = a.Ls - 1;
@@ -352,7 +352,8 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     }
   } else {
     const int ns = (int)((pe - 1) >> a.J) - s_lo + 1;
-    for (int i = threadIdx.x; i < ns; i += kPoolBlock) segs[i] = a.seg[(long)u * a.S + s_lo + i];
+    const int32_t* useg = a.seg + (long)(u / a.share) * a.S;  // the unit's selection
+    for (int i = threadIdx.x; i < ns; i += kPoolBlock) segs[i] = useg[s_lo + i];
   }
   if constexpr (SEL) {
 #pragma unroll
@@ -657,9 +658,11 @@ hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const v
 
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
                               const void* K, const int32_t* seg, float* stats,
-                              float* wpool, hipStream_t s, int stat_slices) {
+                              float* wpool, hipStream_t s, int stat_slices, int share) {
+  if (share < 1 || (p.batch * p.heads) % share != 0) return hipErrorInvalidValue;
   const ScanPlan pl = plan_scan(p);
   ScanArgs a;
+  a.share = share;
   a.Q = Q;
   a.K = K;
   a.seg = seg;

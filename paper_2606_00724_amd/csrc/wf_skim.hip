@@ -1314,6 +1314,28 @@ static hipError_t skim_select_common(const wf_params& p, long nJ, int ntiles, in
   return hipGetLastError();
 }
 
+hipError_t launch_select_w(const wf_params& p, long groups, const float* W, int32_t* seg,
+                           hipStream_t s) {
+  if (groups < 1 || !W || !seg) return hipErrorInvalidValue;
+  SkimSelectArgs a{};
+  a.W = const_cast<float*>(W);
+  a.seg = seg;
+  a.U = (int)groups;
+  a.B = p.q_len;
+  a.nJ = (int)((long)p.ctx_len >> p.levels);
+  a.S = p.segments;
+  const int in_lds = a.nJ <= kSelectLdsFloats ? 1 : 0;
+  const size_t lds = in_lds ? (size_t)a.nJ * sizeof(float) : 0;
+  if (lds > 32768) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(skim_select_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kSelectBlock), lds, s, a,
+                     in_lds, 1);
+  return hipGetLastError();
+}
+
 hipError_t launch_skim_select(const wf_params& p, int ntiles,
                               const float* logits, const float* stats,
                               float* W, int32_t* seg, hipStream_t s) {

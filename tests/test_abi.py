@@ -164,7 +164,7 @@ def test_cached_step_attention_selects_with_bf16_keys(wfpkg, change, selects):
     assert names == head + ([] if selects else ["scan_select"]) + tail
 
 
-def test_shared_selection_is_built_on_the_token_path_only(wfpkg):
+def test_shared_selection_kernel_sequences(wfpkg):
     p = _params(wfpkg, dtype="bf16", heads=4)
     assert wfpkg.shared_kernel_names(p) == [
         "token_skim", "block_weights", "head_sum_w", "scan_weights",
@@ -173,15 +173,15 @@ def test_shared_selection_is_built_on_the_token_path_only(wfpkg):
     assert (wfpkg.workspace_bytes(p, wfpkg.OP_SHARED)
             > wfpkg.workspace_bytes(p, wfpkg.OP_FUSED))
     pf = _params(wfpkg, heads=4)               # fp32: the general path
-    assert wfpkg.shared_kernel_names(pf) == []
-    assert wfpkg.workspace_bytes(pf, wfpkg.OP_SHARED) == 0
+    assert wfpkg.shared_kernel_names(pf) == [
+        "skim_tile", "skim_select", "head_sum_w", "select_regions",
+        "scan_stats", "scan_weights", "head_sum_wpool", "scan_select",
+        "sparse_attn", "attn_combine"]
+    assert (wfpkg.workspace_bytes(pf, wfpkg.OP_SHARED)
+            > wfpkg.workspace_bytes(pf, wfpkg.OP_FUSED))
     lib = wfpkg.library()
     good = ctypes.c_void_p(0x10000)
-    rc = lib.wf_filter_attend_shared(ctypes.byref(pf), good, good, good, None,
-                                     None, good, None, None, good, 1 << 40,
-                                     None)
-    assert rc == 2 and b"token-level" in lib.wf_last_error()
-    # the token path checks its pointers and workspace before queueing
+    # pointers and workspace are checked before anything is queued
     rc = lib.wf_filter_attend_shared(ctypes.byref(p), good, good, good, None,
                                      None, None, None, None, good, 1 << 40,
                                      None)

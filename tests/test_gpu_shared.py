@@ -1,5 +1,6 @@
 """GPU parity of wf_filter_attend_shared (one selection per sequence,
-shared by its heads) against the oracle's filter_attend_shared: the
+shared by its heads), on the token-level and the general path, against the
+oracle's filter_attend_shared: the
 regions against the heads' summed W (tie band), the tokens conditionally on
 the GPU's regions against the heads' summed W', every head's output on the
 GPU's tokens; every sequence of every case."""
@@ -47,6 +48,19 @@ CASES = {
                       segments=64, budget=512, q_len=16, **_BF),
     "sh_one_head": V_("sh1", heads=1, ctx_len=2048, head_dim=128, levels=4,
                       segments=16, budget=100, q_len=32, **_BF),
+    # the general path: fp32 keys, J outside 3..5, more than 64 query rows,
+    # db2 on coefficient tiles, a remainder and a tail
+    "shg_f32": V_("sg1", batch=2, heads=3, ctx_len=1024, levels=3, segments=12,
+                  budget=60, q_len=17),
+    "shg_j2_b100": V_("sg2", heads=3, ctx_len=1024 + 3, head_dim=128, levels=2,
+                      segments=40, budget=90, q_len=100, gen_len=8, **_BF),
+    "shg_db2_j3": V_("sg3", heads=4, ctx_len=2048, head_dim=128, levels=3,
+                     segments=16, budget=64, wavelet="db2", **_BF),
+    "shg_j7_wide": V_("sg4", heads=2, ctx_len=128 * 40, levels=7, segments=5,
+                      budget=300, q_len=24, **_BF),
+    # 4096 coarse blocks: the per-unit W from its own wide kernel
+    "shg_f32_4096": V_("sg5", heads=2, ctx_len=8 * 4096, levels=3, segments=64,
+                       budget=300, q_len=16),
 }
 
 _cache: dict = {}
