@@ -367,6 +367,13 @@ constexpr int kCachedKernels = 7;
 // with bf16 keys the attention takes the top-k of W' itself
 static const char* const kCachedSelectNames[] = {
     "skim_tile", "skim_select", "scan_stats", "scan_weights", "sparse_attn", "attn_combine"};
+// with bf16 keys and at most 64 query rows W is formed over all CUs and the
+// statistics pass takes the top-S of W itself
+static const char* const kCachedWideNames[] = {
+    "skim_tile", "skim_weights", "scan_stats", "scan_weights",
+    "scan_select", "sparse_attn", "attn_combine"};
+static const char* const kCachedWideSelectNames[] = {
+    "skim_tile", "skim_weights", "scan_stats", "scan_weights", "sparse_attn", "attn_combine"};
 
 static long cached_rows(const wf_params& p) {
   return keff_of(p) + remainder_len(p) + p.gen_len;
@@ -374,10 +381,15 @@ static long cached_rows(const wf_params& p) {
 static bool cached_attn_selects(const wf_params& p) {
   return attn_can_select(p, cached_rows(p));
 }
+static bool cached_scan_selects(const wf_params& p) {
+  return scan_can_select(p) && ((p.ctx_len >> p.levels) & 3) == 0;
+}
 static int cached_kernels(const wf_params& p) {
   return cached_attn_selects(p) ? kCachedKernels - 1 : kCachedKernels;
 }
 static const char* const* cached_names(const wf_params& p) {
+  if (cached_scan_selects(p))
+    return cached_attn_selects(p) ? kCachedWideSelectNames : kCachedWideNames;
   return cached_attn_selects(p) ? kCachedSelectNames : kCachedNames;
 }
 
@@ -432,8 +444,13 @@ static wf_status cached_impl(const wf_params* p, const void* Q, const float* app
   WF_HIP(mark(), "hipEventRecord");
   const SkimPlan sp = plan_skim(*p, false);
   WF_TRY(step(launch_skim_tiles(*p, false, Q, nullptr, approx, logits, sstats, s)));
-  WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
-  WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
+  if (cached_scan_selects(*p)) {
+    WF_TRY(step(launch_skim_weights(*p, sp.ntiles, logits, sstats, W, s)));
+    WF_TRY(step(launch_scan_select_stats(*p, Q, K, W, seg, cstats, s)));
+  } else {
+    WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
+    WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
+  }
   WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s)));
   if (cached_attn_selects(*p)) {
     WF_TRY(step(launch_attn_select(*p, Q, K, V, wpool, seg, tok_idx, Kg, Vg, nrows, part,

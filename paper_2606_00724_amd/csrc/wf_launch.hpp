@@ -129,6 +129,11 @@ hipError_t launch_rec_select_slices(const wf_params& p, int b, long n, int keep,
 hipError_t launch_skim_select(const wf_params& p, int ntiles,
                               const float* logits, const float* stats,
                               float* W, int32_t* seg, hipStream_t s);
+// W [U][nJ] of the coarse logits [U][B][nJ] and their tiles' (max, sum)
+// pairs, spread over enough workgroups per unit to fill the chip (no
+// selection); nJ must be a multiple of 4.
+hipError_t launch_skim_weights(const wf_params& p, int ntiles, const float* logits,
+                               const float* stats, float* W, hipStream_t s);
 // stat_slices: 0 when `stats` holds one (max, sum) slice per scan workgroup
 // (written by the stats pass), 1 when it holds the pool's final pair.
 // share: units per selection (seg indexed by u / share).
@@ -144,6 +149,15 @@ hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,
 hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const void* K,
                                       const float* W, const float* blocks, int32_t* seg_out,
                                       float* wpool, hipStream_t s, int share = 1);
+// Whether the scan's workgroups can take the top-S regions themselves (bf16,
+// at most 64 query rows, the region ids and the selection fit in LDS).
+bool scan_can_select(const wf_params& p);
+// The statistics pass that first takes the unit's top-S regions of W itself
+// (seg_out [U][S] receives them, for the weights pass that follows) and
+// writes one (max, sum) slice per workgroup into stats.
+hipError_t launch_scan_select_stats(const wf_params& p, const void* Q, const void* K,
+                                    const float* W, int32_t* seg_out, float* stats,
+                                    hipStream_t s);
 hipError_t launch_scan_select(const wf_params& p, const float* wpool,
                               const int32_t* seg, int32_t* tok,
                               hipStream_t s);

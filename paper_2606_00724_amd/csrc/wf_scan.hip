@@ -222,13 +222,15 @@ struct PoolRowPtr {
 constexpr int kPoolBlock = 512;
 constexpr int kPoolWaves = kPoolBlock / kWave;
 
-// SEL (weights pass of the token-level path, at most 64 query rows): the
-// workgroup first takes the unit's top-S regions from W (eq. 9) itself,
-// then queues its first pool chunks and, while they load, forms the pool
-// normalisers from the selected blocks' log-sum-exps.
+// SEL (at most 64 query rows): the workgroup first takes the unit's top-S
+// regions from W (eq. 9) itself, then queues its first pool chunks.  In the
+// weights pass of the token-level path it forms the pool normalisers from
+// the selected blocks' log-sum-exps while they load; in the statistics pass
+// (the step from cached coefficients) the selection is all it adds, and the
+// weights pass that follows reads the region ids the unit's first range
+// wrote.
 template <int WEIGHTS, int D, bool SEL = false>
 __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
-  static_assert(!SEL || WEIGHTS, "selection in the weights pass only");
   constexpr int NW = kPoolWaves;
   constexpr int CR = kScanChunk;
   constexpr int G = D / 8;             // 16-byte granules per row
@@ -311,44 +313,47 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
       }
     }
     __syncthreads();
-    // the first chunks load while the normalisers are formed
+    // the first chunks load while the normalisers are formed (the weights
+    // pass reads the pool for the last time: streaming loads)
     for (int k = 0; k < nch && k < nbuf - 1; ++k) {
       rp.p0 = pb + (long)k * CR;
-      issue_chunk<CR, G, NW, true>(ring_lds + (uint32_t)(k * CHB), rp);
+      issue_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(k * CHB), rp);
     }
-    // pool normalisers (M_q, Z_q) over the pool's tokens, from the selected
-    // blocks' log-sum-exps: thread (part, q) folds blocks part, part +
-    // parts, ...; the parts' pairs meet in the spare slot
-    const int B = a.B;
-    const int parts = min(kPoolBlock / B, 16);
-    float* pm = reinterpret_cast<float*>(spare);  // [parts][B + 1]
-    float* pz = pm + 16 * (B + 1);
-    {
-      const int q = threadIdx.x % B, part = threadIdx.x / B;
-      const float* lse = a.blocks + (long)u * a.nJ * 2 * B + B;  // block j: at (2 j + 1) B
-      if (part < parts) {
-        float mx = -INFINITY, z = 0.f;
-        constexpr int BATCH = 8;  // loads in flight together
-        for (int s0 = part; s0 < a.S; s0 += BATCH * parts) {
-          float v[BATCH];
-#pragma unroll
-          for (int k = 0; k < BATCH; ++k) {
-            const int s_ = s0 + parts * k;
-            v[k] = s_ < a.S ? lse[(long)segs[s_] * 2 * B + q] : -INFINITY;
+    if constexpr (WEIGHTS) {
+      // pool normalisers (M_q, Z_q) over the pool's tokens, from the selected
+      // blocks' log-sum-exps: thread (part, q) folds blocks part, part +
+      // parts, ...; the parts' pairs meet in the spare slot
+      const int B = a.B;
+      const int parts = min(kPoolBlock / B, 16);
+      float* pm = reinterpret_cast<float*>(spare);  // [parts][B + 1]
+      float* pz = pm + 16 * (B + 1);
+      {
+        const int q = threadIdx.x % B, part = threadIdx.x / B;
+        const float* lse = a.blocks + (long)u * a.nJ * 2 * B + B;  // block j: at (2 j + 1) B
+        if (part < parts) {
+          float mx = -INFINITY, z = 0.f;
+          constexpr int BATCH = 8;  // loads in flight together
+          for (int s0 = part; s0 < a.S; s0 += BATCH * parts) {
+            float v[BATCH];
+  #pragma unroll
+            for (int k = 0; k < BATCH; ++k) {
+              const int s_ = s0 + parts * k;
+              v[k] = s_ < a.S ? lse[(long)segs[s_] * 2 * B + q] : -INFINITY;
+            }
+  #pragma unroll
+            for (int k = 0; k < BATCH; ++k) stat_absorb(mx, z, v[k], 1.f);
           }
-#pragma unroll
-          for (int k = 0; k < BATCH; ++k) stat_absorb(mx, z, v[k], 1.f);
+          pm[part * (B + 1) + q] = mx;
+          pz[part * (B + 1) + q] = z;
         }
-        pm[part * (B + 1) + q] = mx;
-        pz[part * (B + 1) + q] = z;
       }
-    }
-    __syncthreads();
-    for (int q = threadIdx.x; q < B; q += kPoolBlock) {
-      float mx = -INFINITY, z = 0.f;
-      for (int k = 0; k < parts; ++k) stat_absorb(mx, z, pm[k * (B + 1) + q], pz[k * (B + 1) + q]);
-      // exp(s - M) / Z = 2^(s log2(e) - (M log2(e) + log2(Z)))
-      lse2[q] = fmaf(mx, kLog2e, __log2f(z));
+      __syncthreads();
+      for (int q = threadIdx.x; q < B; q += kPoolBlock) {
+        float mx = -INFINITY, z = 0.f;
+        for (int k = 0; k < parts; ++k) stat_absorb(mx, z, pm[k * (B + 1) + q], pz[k * (B + 1) + q]);
+        // exp(s - M) / Z = 2^(s log2(e) - (M log2(e) + log2(Z)))
+        lse2[q] = fmaf(mx, kLog2e, __log2f(z));
+      }
     }
   } else {
     const int ns = (int)((pe - 1) >> a.J) - s_lo + 1;
@@ -617,22 +622,21 @@ static hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t s) {
     return launch_with_lds(scan_chunk_kernel<WEIGHTS, T, D>, grid, kBlock, lds, s, a);
 }
 
-hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const void* K,
-                                      const float* W, const float* blocks, int32_t* seg_out,
-                                      float* wpool, hipStream_t s, int share) {
+// the scan's arguments when its workgroups take the top-S regions from W
+// themselves; false when the shape does not allow it
+static bool scan_select_args(const wf_params& p, const void* Q, const void* K, const float* W,
+                             int32_t* seg_out, int share, ScanArgs& a, ScanPlan& pl) {
   if (p.dtype != WF_BF16 || p.q_len > 64 || p.segments > kSelectLdsSegs || share < 1 ||
       (p.batch * p.heads) % share != 0)
-    return hipErrorInvalidValue;
-  const ScanPlan pl = plan_scan(p, true);
-  if (pl.nbuf < 2) return hipErrorInvalidValue;
-  ScanArgs a{};
+    return false;
+  pl = plan_scan(p, true);
+  if (pl.nbuf < 2) return false;
+  a = ScanArgs{};
   a.Q = Q;
   a.K = K;
   a.W = W;
-  a.blocks = blocks;
   a.share = share;
   a.seg_out = seg_out;
-  a.wpool = wpool;
   a.U = p.batch * p.heads;
   a.L = (int)filtered_len(p);
   a.Ls = p.ctx_len;
@@ -642,7 +646,6 @@ hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const v
   a.P = p.segments << p.levels;
   a.nJ = p.ctx_len >> p.levels;
   a.C = pl.chunks;
-  a.Cs = 1;
   a.span = pl.span;
   a.nbuf = pl.nbuf;
   a.seg_cap = pl.seg_cap;
@@ -650,10 +653,42 @@ hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const v
   // W in the ring slots before the spare one when it fits there
   const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
   a.w_in_lds = (size_t)a.nJ * sizeof(float) <= (size_t)(pl.nbuf - 1) * chb ? 1 : 0;
+  return true;
+}
+
+bool scan_can_select(const wf_params& p) {
+  ScanArgs a;
+  ScanPlan pl;
+  return scan_select_args(p, nullptr, nullptr, nullptr, nullptr, 1, a, pl);
+}
+
+hipError_t launch_scan_select_weights(const wf_params& p, const void* Q, const void* K,
+                                      const float* W, const float* blocks, int32_t* seg_out,
+                                      float* wpool, hipStream_t s, int share) {
+  ScanArgs a;
+  ScanPlan pl;
+  if (!scan_select_args(p, Q, K, W, seg_out, share, a, pl)) return hipErrorInvalidValue;
+  a.blocks = blocks;
+  a.wpool = wpool;
+  a.Cs = 1;
   const dim3 grid((unsigned)(a.U * a.C));
   if (p.head_dim == 128)
     return launch_with_lds(scan_ring_kernel<1, 128, true>, grid, kPoolBlock, pl.lds_bytes, s, a);
   return launch_with_lds(scan_ring_kernel<1, 64, true>, grid, kPoolBlock, pl.lds_bytes, s, a);
+}
+
+hipError_t launch_scan_select_stats(const wf_params& p, const void* Q, const void* K,
+                                    const float* W, int32_t* seg_out, float* stats,
+                                    hipStream_t s) {
+  ScanArgs a;
+  ScanPlan pl;
+  if (!scan_select_args(p, Q, K, W, seg_out, 1, a, pl)) return hipErrorInvalidValue;
+  a.stats = stats;
+  a.Cs = pl.chunks;
+  const dim3 grid((unsigned)(a.U * a.C));
+  if (p.head_dim == 128)
+    return launch_with_lds(scan_ring_kernel<0, 128, true>, grid, kPoolBlock, pl.lds_bytes, s, a);
+  return launch_with_lds(scan_ring_kernel<0, 64, true>, grid, kPoolBlock, pl.lds_bytes, s, a);
 }
 
 hipError_t launch_scan_chunks(const wf_params& p, int weights, const void* Q,

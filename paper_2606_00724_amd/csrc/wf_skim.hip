@@ -868,16 +868,12 @@ __device__ void skim_w_columns(const SkimSelectArgs& a, int u, const float* row_
   }
 }
 
-// W of a wide candidate set spread over `parts` workgroups per unit (the
-// loads of one workgroup per unit would leave most CUs idle): every
-// workgroup merges the unit's (max, sum) slices itself, four parts of 64
-// query rows folded in sequence, then forms W for its share of the columns.
-__global__ __launch_bounds__(kBlock) void skim_weights_kernel(SkimSelectArgs a, int parts) {
-  __shared__ float row_c[WF_MAX_Q_LEN];
-  __shared__ float pm[4][64], pz[4][64];
-  // a unit's parts on the XCD of the token skim that wrote its logits
-  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int u = item / parts, part = item % parts;
+// Per query row of unit u: c_q = M_q log2(e) + log2(Z_q) of the coarse
+// logits, from the tiles' (max, sum) slices, 64 rows at a time; thread
+// (part, q) = (tid / 64, tid % 64) folds slices part, part + 4, ..., and the
+// four parts meet in pm / pz.
+__device__ void unit_row_norms(const SkimSelectArgs& a, int u, float* row_c, float (*pm)[64],
+                               float (*pz)[64]) {
   const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
   for (int qc = 0; qc < a.B; qc += 64) {
     const int q = qc + (threadIdx.x & 63), pp = threadIdx.x >> 6;
@@ -907,8 +903,87 @@ __global__ __launch_bounds__(kBlock) void skim_weights_kernel(SkimSelectArgs a, 
     }
     __syncthreads();
   }
+}
+
+// W of a wide candidate set spread over `parts` workgroups per unit (the
+// loads of one workgroup per unit would leave most CUs idle): every
+// workgroup merges the unit's (max, sum) slices itself, then forms W for its
+// share of the columns, four adjacent columns and every query row a thread.
+__global__ __launch_bounds__(kBlock) void skim_weights_kernel(SkimSelectArgs a, int parts) {
+  __shared__ float row_c[WF_MAX_Q_LEN];
+  __shared__ float pm[4][64], pz[4][64];
+  // a unit's parts on the XCD of the token skim that wrote its logits
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / parts, part = item % parts;
+  unit_row_norms(a, u, row_c, pm, pz);
   const int n4 = a.nJ / 4, per = (n4 + parts - 1) / parts;
   skim_w_columns<kBlock>(a, u, row_c, part * per, min(n4, (part + 1) * per), nullptr);
+}
+
+// The same W for a narrower candidate set (a thousand or so columns a unit),
+// where a thread per four columns leaves too few threads: thread (g, c) adds
+// the terms of query rows 16 g .. 16 g + 15 (and every 64th row after them)
+// of four adjacent columns, the four groups' partial sums meet in LDS and are
+// added in order of g.  The first batch of logits is loaded before the
+// slices are merged, so that the two loads overlap.
+__global__ __launch_bounds__(kBlock) void skim_weights_rows_kernel(SkimSelectArgs a, int parts) {
+  constexpr int QB = 16;             // query rows of one batch
+  constexpr int NQG = 4;             // query groups
+  constexpr int CPW = kBlock / NQG;  // four-column groups per step
+  __shared__ float row_c[WF_MAX_Q_LEN];
+  __shared__ float pm[4][64], pz[4][64];
+  __shared__ float4 wpart[NQG][CPW];
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / parts, part = item % parts;
+  const int n4 = a.nJ / 4, per = (n4 + parts - 1) / parts;
+  const int j4_lo = part * per, j4_hi = min(n4, j4_lo + per);
+  const int qg = threadIdx.x / CPW, cl = threadIdx.x % CPW;
+  const float* lg = a.logits + (long)u * a.B * a.nJ;
+  float4 v[QB];
+  auto load = [&](int j4, int q0) {
+#pragma unroll
+    for (int i = 0; i < QB; ++i)
+      v[i] = j4 < j4_hi && q0 + i < a.B
+                 ? *reinterpret_cast<const float4*>(lg + (long)(q0 + i) * a.nJ + 4 * j4)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  load(j4_lo + cl, QB * qg);
+  unit_row_norms(a, u, row_c, pm, pz);
+
+  float* W = a.W + (long)u * a.nJ;
+  for (int s0 = j4_lo; s0 < j4_hi; s0 += CPW) {
+    const int j4 = s0 + cl;
+    float w[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int q0 = QB * qg; q0 < a.B; q0 += QB * NQG) {
+      if (s0 != j4_lo || q0 != QB * qg) load(j4, q0);  // the first batch is in
+#pragma unroll
+      for (int i = 0; i < QB; ++i) {
+        if (q0 + i < a.B) {
+          // exp(l - M) / Z = 2^(l log2(e) - c)
+          const float c = row_c[q0 + i];
+          w[0] += __builtin_amdgcn_exp2f(fmaf(v[i].x, kLog2e, -c));
+          w[1] += __builtin_amdgcn_exp2f(fmaf(v[i].y, kLog2e, -c));
+          w[2] += __builtin_amdgcn_exp2f(fmaf(v[i].z, kLog2e, -c));
+          w[3] += __builtin_amdgcn_exp2f(fmaf(v[i].w, kLog2e, -c));
+        }
+      }
+    }
+    wpart[qg][cl] = make_float4(w[0], w[1], w[2], w[3]);
+    __syncthreads();
+    if (qg == 0 && j4 < j4_hi) {
+      float4 t = wpart[0][cl];
+#pragma unroll
+      for (int g = 1; g < NQG; ++g) {
+        const float4 o = wpart[g][cl];
+        t.x += o.x;
+        t.y += o.y;
+        t.z += o.z;
+        t.w += o.w;
+      }
+      *reinterpret_cast<float4*>(W + 4 * j4) = t;
+    }
+    __syncthreads();
+  }
 }
 
 constexpr int kSelectBlock = 1024;
@@ -1333,6 +1408,27 @@ hipError_t launch_select_w(const wf_params& p, long groups, const float* W, int3
   }
   hipLaunchKernelGGL(skim_select_kernel, dim3((unsigned)a.U), dim3(kSelectBlock), lds, s, a,
                      in_lds, 1);
+  return hipGetLastError();
+}
+
+hipError_t launch_skim_weights(const wf_params& p, int ntiles, const float* logits,
+                               const float* stats, float* W, hipStream_t s) {
+  SkimSelectArgs a{};
+  a.logits = logits;
+  a.stats = stats;
+  a.W = W;
+  a.U = p.batch * p.heads;
+  a.B = p.q_len;
+  a.nJ = (int)((long)p.ctx_len >> p.levels);
+  a.ntiles = ntiles;
+  if (!logits || !stats || !W || (a.nJ & 3) != 0 || a.nJ == 0) return hipErrorInvalidValue;
+  // at most 1024 columns a workgroup, and two workgroups per CU at least
+  const long n4 = a.nJ / 4;
+  const long want = std::max((a.nJ + 1023L) / 1024,
+                             (2L * device_cu_count() + a.U - 1) / a.U);
+  const int parts = (int)std::min(n4, want);
+  hipLaunchKernelGGL(skim_weights_rows_kernel, dim3((unsigned)(a.U * parts)), dim3(kBlock), 0,
+                     s, a, parts);
   return hipGetLastError();
 }
 

@@ -150,16 +150,22 @@ def test_fused_kernel_sequence_follows_the_path(wfpkg, change, path):
     assert wfpkg.workspace_bytes(p, wfpkg.OP_FUSED) > 0
 
 
-@pytest.mark.parametrize("change,selects", [
-    (dict(), False),                          # fp32 keys: the select kernel
-    (dict(dtype="bf16"), True),
-    (dict(dtype="bf16", q_len=256), True),
-    (dict(dtype="bf16", wavelet="db2"), True),
+@pytest.mark.parametrize("change,selects,wide", [
+    (dict(), False, False),                   # fp32 keys: the select kernels
+    (dict(dtype="bf16"), True, True),
+    (dict(dtype="bf16", q_len=256), True, False),   # past 64 query rows
+    (dict(dtype="bf16", wavelet="db2"), True, True),
+    (dict(dtype="bf16", ctx_len=1048), True, False),  # 131 coefficients
 ])
-def test_cached_step_attention_selects_with_bf16_keys(wfpkg, change, selects):
+def test_cached_step_attention_selects_with_bf16_keys(wfpkg, change, selects,
+                                                      wide):
+    """With bf16 keys the attention takes the top-k itself; with at most 64
+    query rows and a multiple of 4 coefficients W is formed over all CUs and
+    the statistics pass takes the top-S."""
     p = _params(wfpkg, **change)
     names = wfpkg.cached_kernel_names(p)
-    head = ["skim_tile", "skim_select", "scan_stats", "scan_weights"]
+    head = ["skim_tile", "skim_weights" if wide else "skim_select",
+            "scan_stats", "scan_weights"]
     tail = ["sparse_attn", "attn_combine"]
     assert names == head + ([] if selects else ["scan_select"]) + tail
 
