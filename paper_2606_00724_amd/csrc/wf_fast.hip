@@ -214,11 +214,27 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
         for (int i = t; i < nf; i += NIW * 64) dst[i] = src[i];
       }
     } else {
-      // one run of nb logits per query row ([B][nJ])
+      // one run of nb logits per query row ([B][nJ]); NBB is a power of two
+      // (no integer division in the index)
       float* dst = a.blocks + (long)u * B * a.nJ + jb0;
-      for (int i = t; i < nb * B; i += NIW * 64) {
-        const int qq = i / nb, e = i - qq * nb;
-        dst[(long)qq * a.nJ + e] = src[qq * NBB + (e ^ (qq & (NBB - 1)))];
+      constexpr int LNB = NBB == 32 ? 5 : 6;
+      static_assert((1 << LNB) == NBB, "32 or 64 blocks a batch");
+      if (J == 1 && nb == NBB && (a.nJ & 3) == 0) {
+        // a whole batch of 2-token blocks: four adjacent logits of a row per
+        // 16-byte store (jb0 is a multiple of 64)
+        constexpr int F = NBB / 4, LF = LNB - 2;
+        for (int i = t; i < F * B; i += NIW * 64) {
+          const int qq = i >> LF, e0 = 4 * (i & (F - 1)), x = qq & (NBB - 1);
+          const float* row = src + qq * NBB;
+          const float4 o = make_float4(row[e0 ^ x], row[(e0 + 1) ^ x], row[(e0 + 2) ^ x],
+                                       row[(e0 + 3) ^ x]);
+          *reinterpret_cast<float4*>(dst + (long)qq * a.nJ + e0) = o;
+        }
+      } else {
+        for (int i = t; i < NBB * B; i += NIW * 64) {
+          const int qq = i >> LNB, e = i & (NBB - 1);
+          if (e < nb) dst[(long)qq * a.nJ + e] = src[qq * NBB + (e ^ (qq & (NBB - 1)))];
+        }
       }
     }
   };
@@ -252,16 +268,42 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
     if constexpr (J <= 2) {
       // every block lies in one lane
       constexpr int VPB = 1 << J, NL = 16 / VPB;
+      if constexpr (J == 1) {
+        // eight logits a lane: their maximum first, then one rescale of the
+        // running pair and a term each (no branch per logit)
+        float lv[NL];
+        float bmx = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < NL; ++i) {
-        float s_ = 0.f;
+        for (int i = 0; i < NL; ++i) {
+          const int b = (8 * ((i * VPB) / 4) + 4 * hi + (i * VPB) % 4) >> J;
+          lv[i] = (acc[2 * i] + acc[2 * i + 1]) * cl;
+          if (q < B && (slice0 >> J) + b < jend) {
+            bmx = fmaxf(bmx, lv[i]);
+            slot[q * NBB + ((bl0 + b) ^ (q & (NBB - 1)))] = lv[i];
+          } else {
+            lv[i] = -INFINITY;
+          }
+        }
+        if (bmx > -INFINITY) {
+          const float mn = fmaxf(cm, bmx);
+          float zz = cz * __expf(cm - mn);
 #pragma unroll
-        for (int v = i * VPB; v < (i + 1) * VPB; ++v) s_ += acc[v];
-        const int b = (8 * ((i * VPB) / 4) + 4 * hi + (i * VPB) % 4) >> J;
-        const float l = s_ * cl;
-        if (q < B && (slice0 >> J) + b < jend) {
-          stat_add(cm, cz, l);
-          slot[q * NBB + ((bl0 + b) ^ (q & (NBB - 1)))] = l;
+          for (int i = 0; i < NL; ++i) zz += __expf(lv[i] - mn);
+          cm = mn;
+          cz = zz;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          float s_ = 0.f;
+#pragma unroll
+          for (int v = i * VPB; v < (i + 1) * VPB; ++v) s_ += acc[v];
+          const int b = (8 * ((i * VPB) / 4) + 4 * hi + (i * VPB) % 4) >> J;
+          const float l = s_ * cl;
+          if (q < B && (slice0 >> J) + b < jend) {
+            stat_add(cm, cz, l);
+            slot[q * NBB + ((bl0 + b) ^ (q & (NBB - 1)))] = l;
+          }
         }
       }
     } else {
