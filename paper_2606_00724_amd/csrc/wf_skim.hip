@@ -999,6 +999,30 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
   const int u = xcd_swizzle(blockIdx.x, gridDim.x);
   const float* st = a.stats + (long)u * a.ntiles * 2 * a.B;
   float* W = a.W + (long)u * a.nJ;
+  // candidate n is block n, or on a refinement scale child n % 2 of kept
+  // block parent[n / 2]; the last scale emits the two tokens of each block
+  int32_t* out = a.seg + (long)u * (a.pairs ? 2 : 1) * a.S;
+  auto put = [&](uint32_t pos, int32_t id) {
+    if (a.pairs) {
+      out[2 * pos] = 2 * id;
+      out[2 * pos + 1] = 2 * id + 1;
+    } else {
+      out[pos] = id;
+    }
+  };
+  if (w_ready && a.nJ <= 8 * NT) {
+    // W from skim_weights_kernel, eight scores a thread read once into
+    // registers; the parent ids wait in LDS (the select's first barrier
+    // orders them before any emit; n_J = 2 npar floats of LDS were sized)
+    const int32_t* pg = a.parent ? a.parent + (long)u * a.npar : nullptr;
+    int32_t* par_sh = reinterpret_cast<int32_t*>(wsh);
+    if (pg)
+      for (int i = threadIdx.x; i < a.npar; i += NT) par_sh[i] = pg[i];
+    block_select_topk_regs<NT, 8>(
+        W, a.nJ, a.S, [&](uint32_t pos, int n) { put(pos, pg ? 2 * par_sh[n >> 1] + (n & 1) : n); },
+        sh);
+    return;
+  }
   if (w_ready) {
     // W was formed by skim_weights_kernel
     if (w_in_lds)
@@ -1062,20 +1086,8 @@ __global__ __launch_bounds__(kSelectBlock) void skim_select_kernel(SkimSelectArg
     }
   }
   __syncthreads();
-  // candidate n is block n, or on a refinement scale child n % 2 of kept
-  // block parent[n / 2]; the last scale emits the two tokens of each block
   const int32_t* par = a.parent ? a.parent + (long)u * a.npar : nullptr;
-  auto block_of = [&](int n) -> int32_t { return par ? 2 * par[n >> 1] + (n & 1) : n; };
-  int32_t* out = a.seg + (long)u * (a.pairs ? 2 : 1) * a.S;
-  auto emit = [&](uint32_t pos, int n) {
-    const int32_t id = block_of(n);
-    if (a.pairs) {
-      out[2 * pos] = 2 * id;
-      out[2 * pos + 1] = 2 * id + 1;
-    } else {
-      out[pos] = id;
-    }
-  };
+  auto emit = [&](uint32_t pos, int n) { put(pos, par ? 2 * par[n >> 1] + (n & 1) : n); };
   // one instance per address space of the weights
   if (w_in_lds)
     block_select_topk<kSelectBlock>(wsh, a.nJ, a.S, emit, sh);
