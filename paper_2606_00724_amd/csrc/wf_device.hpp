@@ -333,6 +333,11 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   return x;
 }
 
+// c[j] for a lane-varying j < 4, without indexing a register array
+__device__ __forceinline__ uint32_t pick4(const uint32_t (&c)[4], int j) {
+  return j == 0 ? c[0] : j == 1 ? c[1] : j == 2 ? c[2] : c[3];
+}
+
 // One count into bin d of the LDS histogram h for every active lane with m
 // set.  When at least 8 of the wave's counting lanes share the digit of its
 // first counting lane, they add as one atomic carrying the group's size and
@@ -365,9 +370,11 @@ __device__ __forceinline__ void hist_add(uint32_t* h, bool m, uint32_t d, int la
 // wave scans the 256 bins itself to find the digit holding the need-th
 // largest candidate, so a pass costs one barrier (three histograms rotate so
 // that the next one is cleared while the current one fills).  The last pass
-// leaves the k-th largest key and the number of its copies to take.  The
-// output positions then follow from a scan of packed (greater, equal)
-// counts over the positions in index order:
+// leaves the k-th largest key and the number of its copies to take; the
+// passes stop early once the bin they narrowed to is taken whole (its keys'
+// lower digits then change nothing, and keys compare under the digits
+// resolved so far).  The output positions then follow from a scan of packed
+// (greater, equal) counts over the positions in index order:
 //   pos = #greater before + min(#equal before, copies to take).
 template <int NT, typename Emit>
 __device__ __forceinline__ void block_select_topk(const float* score, int n, int k, Emit emit,
@@ -424,11 +431,15 @@ __device__ __forceinline__ void block_select_topk(const float* score, int n, int
     // src is uniform: read the lane's values without an LDS round trip
     const uint32_t digit = (uint32_t)__builtin_amdgcn_readlane(255 - 4 * lane - hit, src);
     const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)hit_above, src);
+    const uint32_t in_bin = (uint32_t)__builtin_amdgcn_readlane((int)pick4(c, hit), src);
     prefix |= digit << shift;
     mask |= 255u << shift;
     need -= above;
+    // every key of the bin is taken: its lower digits decide nothing
+    if (need == in_bin) break;  // uniform
   }
-  // prefix is now the k-th largest key; `need` copies of it are taken.
+  // the top keys are those above prefix under mask, and `need` of those
+  // equal to it under mask (all of them when the passes stopped early).
   // Ordered compaction in tiles of ROUNDS x NT positions: position
   // base + j NT + tid is round j of the thread.  Each wave ballots its
   // (greater, equal) flags per round; one scan over the packed per-(round,
@@ -452,7 +463,7 @@ __device__ __forceinline__ void block_select_topk(const float* score, int n, int
       const int i = base + j * NT + tid;
       bool gt = false, eq = false;
       if (base + j * NT < n && i < n) {
-        const uint32_t key = order_key(v[j]);
+        const uint32_t key = order_key(v[j]) & mask;
         gt = key > prefix;
         eq = key == prefix;
       }
@@ -559,9 +570,11 @@ __device__ __forceinline__ void block_select_topk_regs(const float* score, int n
     const int src = __ffsll((unsigned long long)__ballot(found)) - 1;
     const uint32_t digit = (uint32_t)__builtin_amdgcn_readlane(255 - 4 * lane - hit, src);
     const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)hit_above, src);
+    const uint32_t in_bin = (uint32_t)__builtin_amdgcn_readlane((int)pick4(c, hit), src);
     prefix |= digit << shift;
     mask |= 255u << shift;
     need -= above;
+    if (need == in_bin) break;  // uniform: the whole bin is taken
   }
   // ordered compaction, tiles of ROUNDS slots (as block_select_topk)
   constexpr int NW = NT / 64;
@@ -579,8 +592,9 @@ __device__ __forceinline__ void block_select_topk_regs(const float* score, int n
       const int slot = t * ROUNDS + j;
       bool gt = false, eq = false;
       if (slot < EPT && base + j * NT + tid < n) {
-        gt = key[slot < EPT ? slot : 0] > prefix;
-        eq = key[slot < EPT ? slot : 0] == prefix;
+        const uint32_t km = key[slot < EPT ? slot : 0] & mask;
+        gt = km > prefix;
+        eq = km == prefix;
       }
       gtm[j] = __ballot(gt);
       eqm[j] = __ballot(eq);
