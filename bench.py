@@ -171,6 +171,35 @@ def measured_bandwidth(torch, dev, nbytes: int = 1 << 30, min_ms: float = 100.0)
     return {"copy_GBs": 2 * nbytes / (best * 1e-3) / 1e9, "copies_timed": reps}
 
 
+def measured_mfma(torch, dev, n: int = 8192, min_ms: float = 100.0) -> dict:
+    """The bf16 matrix-core rate this machine reaches with a plain library GEMM
+    (torch.matmul of two n x n bf16 matrices), the best of back-to-back timed
+    groups of four run for at least min_ms.  Run last before the warmup
+    steps, it also leaves the GPU at the clocks it keeps under a model's
+    matrix work, which in a decode step runs right before this path."""
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    c = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
+    torch.matmul(a, b, out=c)
+    torch.cuda.synchronize()
+    best, total, reps = float("inf"), 0.0, 0
+    while total < min_ms or reps < 3:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(4):
+            torch.matmul(a, b, out=c)
+        e1.record()
+        e1.synchronize()
+        t = e0.elapsed_time(e1)
+        best, total, reps = min(best, t), total + t, reps + 1
+    del a, b, c
+    return {"bf16_TFLOPs": 4 * 2 * n ** 3 / (best * 1e-3) / 1e12, "groups_timed": reps,
+            "kind": f"best of back-to-back timed groups of 4 torch.matmul of "
+                    f"{n} x {n} bf16 matrices on this GPU (dense; vendor peak "
+                    f"2.5 PFLOP/s)"}
+
+
 def touch(torch, tensors, passes: int = 1) -> None:
     """Reads every device buffer the timed steps will use (a plain sum over
     its bytes, `passes` times), so that their pages are mapped and in use on
@@ -317,6 +346,10 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before timing, run one plain 1 GiB device-to-device "
                          "copy (a known-size kernel for scaling HBM counters)")
+    ap.add_argument("--no-mfma-rate", action="store_true",
+                    help="skip the bf16 GEMM rate measured right before the "
+                         "warmup steps (the steps then start from the clocks "
+                         "the copies and buffer reads left)")
 
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -444,6 +477,8 @@ def main() -> int:
             wf.wf_filter_attend_timed(p, c["Q"], c["K"], c["V"], c["Kg"],
                                       c["Vg"], O, tok, None, ws, evs, stream)
 
+    # the library's kernels onto the GPU now, so that no step waits for them
+    wf.wf_init()
     print("[bench] measuring the copy rate", file=sys.stderr, flush=True)
     hbm = measured_bandwidth(torch, dev)
     if args.touch > 0:
@@ -456,6 +491,10 @@ def main() -> int:
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    mfma = None
+    if not args.no_mfma_rate:
+        print("[bench] measuring the bf16 GEMM rate", file=sys.stderr, flush=True)
+        mfma = measured_mfma(torch, dev)
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for i in range(args.warmup):
         step_plain(i)
@@ -564,6 +603,7 @@ def main() -> int:
             "path_frac_of_copy": alg["total"] * U * nl / (ms_step * 1e-3) / 1e9
                                  / hbm["copy_GBs"],
         },
+        "mfma_measured": mfma,
         "needle_recall": recall,
         "path_algorithmic_bytes": alg["total"] * U * nl,
         "kernel_ms": per_kernel,

@@ -413,6 +413,17 @@ const char* wf_filter_attend_recursive_kernel_name(const wf_params* p,
  * [q_len][d] is already [batch][heads_kv][g * q_len][d]: pass heads =
  * heads_kv and q_len = g * q_len (at most WF_MAX_Q_LEN). */
 
+/* Loads the library's kernels onto the current device and sets up its
+ * per-device state, so that no later call stalls for it (otherwise the
+ * first call on a device loads what it launches, a few milliseconds of host
+ * time during which the GPU waits).  Optional, for callers that want every
+ * call to cost the same (serving loops, timing harnesses); call it once per
+ * device with that device current.  Synchronous; the library allocates
+ * nothing (the HIP runtime places the code in device memory).  May be
+ * called again (it then does nothing new).  Returns WF_ERR_HIP if the HIP
+ * runtime cannot load the kernels for this device. */
+wf_status wf_init(void);
+
 /* Static description of a status code. */
 const char* wf_status_str(wf_status s);
 

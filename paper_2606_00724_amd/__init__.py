@@ -42,7 +42,7 @@ EXPORTED = ("wf_workspace_bytes", "wf_effective_budget", "wf_dwt_keys",
             "wf_filter_attend_recursive", "wf_filter_attend_recursive_timed",
             "wf_filter_attend_recursive_kernels",
             "wf_filter_attend_recursive_kernel_name",
-            "wf_status_str", "wf_last_error")
+            "wf_init", "wf_status_str", "wf_last_error")
 
 
 class WfParams(ctypes.Structure):
@@ -117,6 +117,7 @@ def _load() -> ctypes.CDLL:
                                               ctypes.POINTER(vp), i32]),
         "wf_filter_attend_recursive_kernels": (i32, [P]),
         "wf_filter_attend_recursive_kernel_name": (ctypes.c_char_p, [P, i32]),
+        "wf_init": (ctypes.c_int, []),
         "wf_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "wf_last_error": (ctypes.c_char_p, []),
     }
@@ -263,6 +264,12 @@ def _torch_stream(stream) -> torch.cuda.Stream:
 def _check(status: int) -> None:
     if status != 0:
         raise WfError(status, _lib.wf_last_error().decode())
+
+
+def wf_init():
+    """Loads the library's kernels onto the current device (optional: the
+    first call on a device otherwise does it, stalling that call)."""
+    _check(_lib.wf_init())
 
 
 def wf_dwt_keys(p, K, approx, details=None, stream=None):

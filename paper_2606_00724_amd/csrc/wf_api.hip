@@ -978,6 +978,16 @@ const char* wf_filter_attend_recursive_kernel_name(const wf_params* p, int32_t i
   return rec_kernel_name(*p, i);
 }
 
+wf_status wf_init(void) {
+  WF_HIP(load_fast_kernels(), "loading the token-skim kernels");
+  WF_HIP(load_scan_kernels(), "loading the scan kernels");
+  WF_HIP(load_attn_kernels(), "loading the attention kernels");
+  WF_HIP(load_skim_kernels(), "loading the DWT and skim kernels");
+  void* scratch_ptr = nullptr;  // this file's code object and its scratch array
+  WF_TRY(scratch_of_current_device(&scratch_ptr));
+  return ok();
+}
+
 const char* wf_status_str(wf_status s) {
   switch (s) {
     case WF_OK: return "WF_OK";

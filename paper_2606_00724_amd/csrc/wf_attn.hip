@@ -1027,4 +1027,9 @@ hipError_t launch_gather(const wf_params& p, const void* K, const void* V,
   return hipGetLastError();
 }
 
+hipError_t load_attn_kernels() {
+  hipFuncAttributes fa;
+  return hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(attn_ring_kernel<128, true>));
+}
+
 }  // namespace wf

@@ -878,4 +878,9 @@ hipError_t launch_head_sum(const float* in, float* out, long n, int H, int group
   return hipGetLastError();
 }
 
+hipError_t load_fast_kernels() {
+  hipFuncAttributes fa;
+  return hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(head_sum_kernel));
+}
+
 }  // namespace wf

@@ -186,6 +186,13 @@ hipError_t launch_attn_select(const wf_params& p, const void* Q, const void* K, 
 // (the selection weights of a sequence's heads added up).
 hipError_t launch_head_sum(const float* in, float* out, long n, int H, int groups,
                            hipStream_t s);
+// Loads the code object of one translation unit onto the current device
+// (each .hip file is its own code object; asking for a kernel's attributes
+// loads it).
+hipError_t load_fast_kernels();
+hipError_t load_scan_kernels();
+hipError_t load_attn_kernels();
+hipError_t load_skim_kernels();
 hipError_t launch_attn_combine(const wf_params& p, long nrows,
                                const float* part, const float* pstat, void* O,
                                hipStream_t s);

@@ -756,4 +756,9 @@ hipError_t launch_scan_select(const wf_params& p, const float* wpool,
   return hipGetLastError();
 }
 
+hipError_t load_scan_kernels() {
+  hipFuncAttributes fa;
+  return hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(scan_select_kernel));
+}
+
 }  // namespace wf

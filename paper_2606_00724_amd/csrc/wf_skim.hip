@@ -1492,4 +1492,9 @@ hipError_t launch_rec_select_slices(const wf_params& p, int b, long n, int keep,
                             stats, W, out, s);
 }
 
+hipError_t load_skim_kernels() {
+  hipFuncAttributes fa;
+  return hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(skim_select_kernel));
+}
+
 }  // namespace wf

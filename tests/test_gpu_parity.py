@@ -313,6 +313,20 @@ def test_constant_keys_pick_lowest_indices(wf, dtype, shape):
     assert torch.equal(out["seg"], seg) and torch.equal(out["tok"], tok)
 
 
+def test_init_is_repeatable_and_changes_no_result(wf):
+    """wf_init loads the kernels on the current device and may be called
+    again; a fused call after it gives the same bits as before it."""
+    w = synth.WORKLOADS["layer8b"]
+    Q, K, V, _, _ = inputs(w)
+    before = run_fused(wf, w, Q, K, V, None, None)
+    say("[gpu] wf_init twice")
+    wf.wf_init()
+    wf.wf_init()
+    after = run_fused(wf, w, Q, K, V, None, None)
+    for x, y in zip(before, after):
+        assert torch.equal(x, y)
+
+
 def test_fused_is_deterministic(wf):
     """Ten calls on the same inputs give bit-identical outputs and indices
     (no atomics decide an order anywhere on the path)."""
