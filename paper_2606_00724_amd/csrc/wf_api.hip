@@ -227,13 +227,35 @@ static inline char* at(void* ws, size_t off) { return static_cast<char*>(ws) + o
 static const char* const kGeneralNames[] = {
     "skim_tile", "skim_select", "scan_stats", "scan_weights",
     "scan_select", "sparse_attn", "attn_combine"};
+// with bf16 keys, at most 64 query rows and a multiple of 4 coefficients: W
+// over all CUs, the top-S in the statistics pass, and when the attention's
+// rows allow it the top-k in the attention
+static const char* const kGeneralWideNames[] = {
+    "skim_tile", "skim_weights", "scan_stats", "scan_weights",
+    "scan_select", "sparse_attn", "attn_combine"};
+static const char* const kGeneralWideSelectNames[] = {
+    "skim_tile", "skim_weights", "scan_stats", "scan_weights", "sparse_attn", "attn_combine"};
 static const char* const kFastNames[] = {
     "token_skim", "block_weights", "scan_weights", "sparse_attn", "attn_combine"};
 constexpr int kMaxFusedKernels = 7;
 
-static int fused_kernels(const wf_params& p) { return fast_path(p) ? 5 : 7; }
+static long fused_rows(const wf_params& p) {
+  return keff_of(p) + remainder_len(p) + p.gen_len;
+}
+// the general sequence with its selections in their consumers
+static bool general_wide(const wf_params& p) {
+  return !fast_path(p) && scan_can_select(p) && ((p.ctx_len >> p.levels) & 3) == 0;
+}
+static bool general_attn_selects(const wf_params& p) {
+  return general_wide(p) && attn_can_select(p, fused_rows(p));
+}
+static int fused_kernels(const wf_params& p) {
+  return fast_path(p) ? 5 : general_attn_selects(p) ? 6 : 7;
+}
 static const char* const* fused_names(const wf_params& p) {
-  return fast_path(p) ? kFastNames : kGeneralNames;
+  if (fast_path(p)) return kFastNames;
+  if (general_wide(p)) return general_attn_selects(p) ? kGeneralWideSelectNames : kGeneralWideNames;
+  return kGeneralNames;
 }
 
 static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
@@ -297,12 +319,22 @@ static wf_status fused_impl(const wf_params* p, const void* Q, const void* K,
   } else {
     const SkimPlan sp = plan_skim(*p, true);
     WF_TRY(step(launch_skim_tiles(*p, true, Q, K, nullptr, logits, sstats, s)));
-    WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
-    WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
+    if (general_wide(*p)) {
+      WF_TRY(step(launch_skim_weights(*p, sp.ntiles, logits, sstats, W, s)));
+      WF_TRY(step(launch_scan_select_stats(*p, Q, K, W, seg, cstats, s)));
+    } else {
+      WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, seg, s)));
+      WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s)));
+    }
     WF_TRY(step(launch_scan_chunks(*p, 1, Q, K, seg, cstats, wpool, s)));
-    WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
-    WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
-                            part, pstat, s)));
+    if (general_attn_selects(*p)) {
+      WF_TRY(step(launch_attn_select(*p, Q, K, V, wpool, seg, tok_idx, Kg, Vg, nrows, part,
+                                     pstat, s)));
+    } else {
+      WF_TRY(step(launch_scan_select(*p, wpool, seg, tok, s)));
+      WF_TRY(step(launch_attn(*p, Q, K, V, tok, (int)keff, Kg, Vg, p->gen_len, nrows,
+                              part, pstat, s)));
+    }
   }
   WF_TRY(step(launch_attn_combine(*p, nrows, part, pstat, O, s)));
   return ok();
@@ -478,10 +510,16 @@ static const char* const kSharedNames[] = {
 static const char* const kSharedGeneralNames[] = {
     "skim_tile", "skim_select", "head_sum_w", "select_regions", "scan_stats",
     "scan_weights", "head_sum_wpool", "scan_select", "sparse_attn", "attn_combine"};
+// with a multiple of 4 coefficients each head's W alone, over all CUs
+static const char* const kSharedGeneralWideNames[] = {
+    "skim_tile", "skim_weights", "head_sum_w", "select_regions", "scan_stats",
+    "scan_weights", "head_sum_wpool", "scan_select", "sparse_attn", "attn_combine"};
 constexpr int kSharedMaxKernels = 10;
+static bool shared_w_only(const wf_params& p) { return ((p.ctx_len >> p.levels) & 3) == 0; }
 static int shared_kernels(const wf_params& p) { return fast_path(p) ? 7 : 10; }
 static const char* const* shared_names(const wf_params& p) {
-  return fast_path(p) ? kSharedNames : kSharedGeneralNames;
+  if (fast_path(p)) return kSharedNames;
+  return shared_w_only(p) ? kSharedGeneralWideNames : kSharedGeneralNames;
 }
 
 static wf_status shared_impl(const wf_params* p, const void* Q, const void* K,
@@ -552,7 +590,10 @@ static wf_status shared_impl(const wf_params* p, const void* Q, const void* K,
     int32_t* tok = tok_idx ? tok_idx : reinterpret_cast<int32_t*>(at(ws, l.tok));
     const SkimPlan sp = plan_skim(*p, true);
     WF_TRY(step(launch_skim_tiles(*p, true, Q, K, nullptr, logits, sstats, s)));
-    WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, unit_seg, s)));
+    if (shared_w_only(*p))
+      WF_TRY(step(launch_skim_weights(*p, sp.ntiles, logits, sstats, W, s)));
+    else  // the per-unit select's regions are not used
+      WF_TRY(step(launch_skim_select(*p, sp.ntiles, logits, sstats, W, unit_seg, s)));
     WF_TRY(step(launch_head_sum(W, wsum, nJ, H, p->batch, s)));
     WF_TRY(step(launch_select_w(pg, p->batch, wsum, seg, s)));
     WF_TRY(step(launch_scan_chunks(*p, 0, Q, K, seg, cstats, wpool, s, 0, H)));

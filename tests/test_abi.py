@@ -128,20 +128,27 @@ def test_budget_and_workspace_arithmetic(wfpkg):
     (dict(), "general"),                                   # fp32 keys
     (dict(dtype="bf16"), "token"),
     (dict(dtype="bf16", levels=5), "token"),
-    (dict(dtype="bf16", levels=2), "general"),             # blocks < 8 tokens
-    (dict(dtype="bf16", levels=6), "general"),             # blocks > 32 tokens
+    (dict(dtype="bf16", levels=2), "wide"),                # blocks < 8 tokens
+    (dict(dtype="bf16", levels=6), "wide"),                # blocks > 32 tokens
     (dict(dtype="bf16", q_len=65), "general"),             # > 64 query rows
-    (dict(dtype="bf16", wavelet="db2"), "general"),
+    (dict(dtype="bf16", wavelet="db2"), "wide"),
     (dict(dtype="bf16", wavelet="db2", levels=6, segments=4), "token"),   # db2 band over token logits
     (dict(dtype="bf16", wavelet="db2", levels=6, segments=2, ctx_len=192), "general"),  # 3 coefficients
-    (dict(dtype="bf16", wavelet="db2", levels=7, segments=2), "general"),
+    (dict(dtype="bf16", wavelet="db2", levels=7, segments=2), "wide"),
 ])
 def test_fused_kernel_sequence_follows_the_path(wfpkg, change, path):
+    """Token-level path for bf16 Haar at 3..5 levels (db2 at 6); otherwise
+    coefficient tiles, and with bf16 keys, at most 64 query rows and a
+    multiple of 4 coefficients W over all CUs with the top-S in the
+    statistics pass and the top-k in the attention."""
     p = _params(wfpkg, **change)
     names = wfpkg.fused_kernel_names(p)
     if path == "token":
         assert names == ["token_skim", "block_weights", "scan_weights",
                          "sparse_attn", "attn_combine"]
+    elif path == "wide":
+        assert names == ["skim_tile", "skim_weights", "scan_stats",
+                         "scan_weights", "sparse_attn", "attn_combine"]
     else:
         assert names == ["skim_tile", "skim_select", "scan_stats",
                          "scan_weights", "scan_select", "sparse_attn",
@@ -180,9 +187,12 @@ def test_shared_selection_kernel_sequences(wfpkg):
             > wfpkg.workspace_bytes(p, wfpkg.OP_FUSED))
     pf = _params(wfpkg, heads=4)               # fp32: the general path
     assert wfpkg.shared_kernel_names(pf) == [
-        "skim_tile", "skim_select", "head_sum_w", "select_regions",
+        "skim_tile", "skim_weights", "head_sum_w", "select_regions",
         "scan_stats", "scan_weights", "head_sum_wpool", "scan_select",
         "sparse_attn", "attn_combine"]
+    # 131 coefficients: W comes from the per-unit skim select
+    po = _params(wfpkg, heads=4, ctx_len=1048)
+    assert wfpkg.shared_kernel_names(po)[1] == "skim_select"
     assert (wfpkg.workspace_bytes(pf, wfpkg.OP_SHARED)
             > wfpkg.workspace_bytes(pf, wfpkg.OP_FUSED))
     lib = wfpkg.library()
