@@ -788,15 +788,44 @@ skim_tile_kernel(SkimTileArgs a, Taps taps, EdgeTaps edge) {
       else
         transform(RowsIdentity{});
     } else {
+      // the tile of A_J rows: every load issued before the first is waited
+      // for (row indices clamped, stores guarded); with bf16 queries the
+      // rows go straight to the [hi x D][lo x D] layout of split_tile_bf16
       const float* src = a.approx + ((long)u * a.nJ + n0) * D;
-      for (int v = threadIdx.x; v < ncoef * (D / 4); v += kBlock) {
-        const int c = v / (D / 4), k = v % (D / 4);
-        *reinterpret_cast<f32x4*>(coef + c * (D + kCoefPad) + 4 * k) =
-            *reinterpret_cast<const f32x4*>(src + (long)c * D + 4 * k);
+      constexpr int GPR = D / 8;  // 8-channel groups per row
+      constexpr int MAXI = kMaxCoefTile * GPR / kBlock;
+      f32x4 v0[MAXI], v1[MAXI];
+#pragma unroll
+      for (int k = 0; k < MAXI; ++k) {
+        const int it = threadIdx.x + k * kBlock, row = min(it / GPR, ncoef - 1), grp = it % GPR;
+        v0[k] = *reinterpret_cast<const f32x4*>(src + (long)row * D + 8 * grp);
+        v1[k] = *reinterpret_cast<const f32x4*>(src + (long)row * D + 8 * grp + 4);
+      }
+#pragma unroll
+      for (int k = 0; k < MAXI; ++k) {
+        const int it = threadIdx.x + k * kBlock, row = it / GPR, grp = it % GPR;
+        if (row >= ncoef) continue;
+        if constexpr (sizeof(T) == 2) {
+          const float v[8] = {v0[k][0], v0[k][1], v0[k][2], v0[k][3],
+                              v1[k][0], v1[k][1], v1[k][2], v1[k][3]};
+          uint32_t hi[4], lo[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            hi[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+            lo[e] = pack_bf16x2(v[2 * e] - bf16_lo(hi[e]), v[2 * e + 1] - bf16_hi(hi[e]));
+          }
+          unsigned char* dst = reinterpret_cast<unsigned char*>(coef + row * (D + kCoefPad));
+          *reinterpret_cast<u32x4*>(dst + 16 * grp) = u32x4{hi[0], hi[1], hi[2], hi[3]};
+          *reinterpret_cast<u32x4*>(dst + 2 * D + 16 * grp) = u32x4{lo[0], lo[1], lo[2], lo[3]};
+        } else {
+          float* dst = coef + row * (D + kCoefPad) + 8 * grp;
+          *reinterpret_cast<f32x4*>(dst) = v0[k];
+          *reinterpret_cast<f32x4*>(dst + 4) = v1[k];
+        }
       }
     }
     __syncthreads();
-    if constexpr (sizeof(T) == 2) split_tile_bf16<D>(coef, ncoef);
+    if constexpr (sizeof(T) == 2 && SRC != kFromApprox) split_tile_bf16<D>(coef, ncoef);
     skim_epilogue<T, D>(a, u, tile, n0, ncoef, coef);
     __syncthreads();
   }
