@@ -533,13 +533,46 @@ __device__ __forceinline__ void block_select_topk_regs(const float* score, int n
   uint32_t key[EPT];
 #pragma unroll
   for (int j = 0; j < EPT; ++j) key[j] = j < nslot && j * NT + tid < n ? order_key(v[j]) : 0u;
+  // the bits every key shares need no pass: the AND and OR of the keys
+  // over the block give the highest bit in which two keys differ, and the
+  // passes start there (scores of a few octaves share their sign and high
+  // exponent bits, and their first pass would otherwise put most of its
+  // counts on a few bins)
+  constexpr int NW = NT / 64;
+  uint32_t kand = 0xffffffffu, kor = 0u;
+#pragma unroll
+  for (int j = 0; j < EPT; ++j)
+    if (j < nslot && j * NT + tid < n) {
+      kand &= key[j];
+      kor |= key[j];
+    }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    kand &= (uint32_t)__shfl_xor((int)kand, off);
+    kor |= (uint32_t)__shfl_xor((int)kor, off);
+  }
+  if (lane == 0) {  // sh.cnt is free until the compaction, after the passes' barriers
+    sh.cnt[0][wid] = kand;
+    sh.cnt[0][NW + wid] = kor;
+  }
   for (int i = tid; i < 256; i += NT) sh.hist[0][i] = 0;
   __syncthreads();
-  uint32_t prefix = 0, mask = 0, need = (uint32_t)k;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    kand &= sh.cnt[0][w];
+    kor |= sh.cnt[0][NW + w];
+  }
+  const uint32_t diff = kand ^ kor;
+  const int top = diff ? 31 - __clz((int)diff) : -1;  // highest differing bit
+  uint32_t mask = top < 0 ? 0xffffffffu : top == 31 ? 0u : ~((2u << top) - 1u);
+  uint32_t prefix = kand & mask, need = (uint32_t)k;
+  for (int pass = 0; top - 8 * pass >= 0; ++pass) {
+    // digit bits top - 8 pass .. top - 8 pass - 7; the last digit may reach
+    // below bit 0 and is then taken from bit 0 (its upper bits are resolved
+    // and equal for every candidate)
+    const int shift = max(top - 7 - 8 * pass, 0);
     uint32_t* h = sh.hist[pass % 3];
-    if (pass < 3)
+    if (top - 8 * (pass + 1) >= 0)
       for (int i = tid; i < 256; i += NT) sh.hist[(pass + 1) % 3][i] = 0;
 #pragma unroll
     for (int j = 0; j < EPT; ++j) {
@@ -577,7 +610,6 @@ __device__ __forceinline__ void block_select_topk_regs(const float* score, int n
     if (need == in_bin) break;  // uniform: the whole bin is taken
   }
   // ordered compaction, tiles of ROUNDS slots (as block_select_topk)
-  constexpr int NW = NT / 64;
   constexpr int NE = ROUNDS * NW;
   static_assert(NE <= 256, "count scan: at most four entries per lane");
   uint32_t gt_base = 0, eq_base = 0;
