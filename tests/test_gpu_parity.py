@@ -496,6 +496,34 @@ def test_cached_steps_reuse_one_approximation(wf):
         assert torch.equal(x, y)
 
 
+@pytest.mark.parametrize("name", ["j1_bf16_d64_b17", "cached"])
+def test_consumer_selections_are_deterministic(wf, name):
+    """Ten calls of the sequences whose selections run in every workgroup of
+    their consumers (the bf16 coefficient-tile path, the cached step) give
+    bit-identical outputs and indices."""
+    w = EDGE["j1_bf16_d64_b17"] if name != "cached" else synth.WORKLOADS["layer8b"]
+    Q, K, V, Kg, Vg = inputs(w)
+    p = wf.params_for(w)
+    Qd, Kd, Vd = Q.cuda(), K.cuda(), V.cuda()
+    Kgd = None if Kg is None else Kg.cuda()
+    Vgd = None if Vg is None else Vg.cuda()
+    if name == "cached":
+        approx = wf.dwt_approx(p, Kd)
+        call = lambda: wf.filter_attend_cached(p, Qd, approx, Kd, Vd, Kgd, Vgd,
+                                               want_indices=True)
+        assert wf.cached_kernel_names(p)[1] == "skim_weights"
+    else:
+        call = lambda: wf.filter_attend(p, Qd, Kd, Vd, Kgd, Vgd, want_indices=True)
+        assert wf.fused_kernel_names(p)[1] == "skim_weights"
+    say(f"[gpu] {name}: ten calls")
+    first = call()
+    for r in range(9):
+        again = call()
+        torch.cuda.synchronize()
+        for x, y in zip(first, again):
+            assert torch.equal(x, y), f"run {r + 2} differs from run 1"
+
+
 # ------------------------------------------------ grouped query heads (GQA)
 
 @pytest.mark.parametrize("group,B", [(4, 16), (2, 32), (8, 32)])
