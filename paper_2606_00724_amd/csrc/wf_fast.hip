@@ -384,6 +384,170 @@ __global__ __launch_bounds__(kTokBlock, token_skim_waves_per_simd(D, J, LSE)) vo
   }
 }
 
+// Blocks of 32 tokens with their log-sum-exps, one workgroup per CU: the
+// same products and block reductions as token_skim_kernel<D, 5, true>, but
+// every wave keeps its block results in registers and stores them only after
+// the range's last key load has landed.  Writes issued while the key stream
+// runs cost about four read-byte times per byte written (on one MI355X a
+// 1 GiB ring read at 7.25 TB/s slowed from 148 to 192 us when 64 MiB of
+// writes were spread over it, in 4 KiB or 32 KiB batches alike, and to 160 us
+// when the same writes followed it), so the results wait until the reads are
+// done.  A lane holds one value per chunk (the coarse logit of its query in
+// lanes 0..31, the block's log-sum-exp in lanes 32..63), 128 chunks in four
+// register vectors of 32, written through a wave-uniform register index;
+// that takes the register file of two waves per SIMD, hence one workgroup
+// per CU with the ring three chunks deep.
+typedef float f32x32 __attribute__((ext_vector_type(32)));
+constexpr int kHeldChunks = 128;
+
+template <int D>
+__global__ __launch_bounds__(kTokBlock, 2) void token_skim_held_kernel(TokenSkimArgs a) {
+  constexpr int NIW = kTokBlock / kWave / 2;  // loading waves
+  constexpr int CR = kScanChunk;
+  constexpr int G = D / 8;
+  constexpr int CHB = CR * 2 * D;
+  constexpr int IPW = CR * G / (64 * NIW);
+  constexpr int KS = D / 16;
+  constexpr int J = 5;
+  static_assert(CR == 32 * NIW, "four 32-token slices (one block each) per chunk");
+  const int B = a.B;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ring = smem;                   // [nbuf][CHB]
+  float* red = reinterpret_cast<float*>(smem);  // [8][32][2] once the ring is idle
+
+  const int item = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int u = item / a.R, r = item % a.R;
+  const long tb = (long)r * a.span;
+  const long te = min(tb + (long)a.span, (long)a.L);
+  const int nch = (int)((te - tb + CR - 1) / CR);  // at most kHeldChunks (host-checked)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ts = wave & 3, qt = wave >> 2;
+  const bool loader = qt == 0;
+  const int hi = lane >> 5, col = lane & 31;
+  const int q = 32 * qt + col;
+  const bool live = 32 * qt < B;  // wave-uniform: this query tile has rows
+
+  const bf16_t* qrow = reinterpret_cast<const bf16_t*>(a.Q) + ((long)u * B + min(q, B - 1)) * D;
+  u32x4 qreg[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) qreg[s] = *reinterpret_cast<const u32x4*>(qrow + 16 * s + 8 * hi);
+#pragma unroll
+  for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qreg[s]));
+
+  // row r of the chunk at c0 (rows past the range repeat its last row)
+  struct Rows {
+    const bf16_t* Kunit;
+    long c0, tlast;
+    __device__ __forceinline__ const bf16_t* operator()(int r) const {
+      return Kunit + min(c0 + r, tlast) * D;
+    }
+  } rows{reinterpret_cast<const bf16_t*>(a.K) + (long)u * a.Ls * D, tb, te - 1};
+  const uint32_t ring_lds = lds_offset(ring);
+  const int nbuf = a.nbuf;
+  if (loader) {
+    for (int k = 0; k < nch && k < nbuf - 1; ++k) {
+      rows.c0 = tb + (long)k * CR;
+      issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(k * CHB), rows);
+    }
+  }
+  const long jend = te >> J;
+  const float cl = a.scale * a.norm;
+  const float c2 = a.scale * kLog2e;
+  float cm = -INFINITY, cz = 0.f;  // running max / sum of exp of the coarse logits
+
+  // chunk ch: the lane's held value (coarse logit or block log-sum-exp)
+  auto step = [&](int ch) -> float {
+    if (loader) wait_vmcnt_chunks<IPW>(min(nch - 1 - ch, nbuf - 2));
+    lds_barrier();  // chunk ch visible; everyone is past chunk ch - 1
+    if (loader && ch + nbuf - 1 < nch) {
+      rows.c0 = tb + (long)(ch + nbuf - 1) * CR;
+      issue_chunk<CR, G, NIW, true>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rows);
+    }
+    const long slice0 = tb + (long)ch * CR + 32 * ts;
+    if (!live || slice0 >= te) return 0.f;  // uniform per wave; never stored
+    const unsigned char* buf = ring + (ch % nbuf) * CHB;
+    const int row = 32 * ts + col;
+    f32x16 acc = {};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const u32x4 ka = *reinterpret_cast<const u32x4*>(buf + granule_offset<G>(row, 2 * s + hi));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
+                                                    __builtin_bit_cast(bf16x8, qreg[s]), acc, 0, 0, 0);
+    }
+    // the lane's 16 logits and those of lane l ^ 32 are the slice's block
+    float bs = 0.f, bm = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      bs += acc[v];
+      bm = fmaxf(bm, acc[v]);
+    }
+    bs = add_xor32(bs);
+    bm = max_xor32(bm);
+    const float off = -bm * c2;
+    float be = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) be += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, off));
+    be = add_xor32(be);
+    const float l = bs * cl;
+    if (hi == 0 && q < B && (slice0 >> J) < jend) stat_add(cm, cz, l);
+    return hi ? fmaf(bm, a.scale, __logf(be)) : l;
+  };
+  f32x32 h0, h1, h2, h3;
+#define WF_HELD_GROUP(g, hv)                          \
+  for (int i = 0; i < 32; ++i) {                      \
+    const int ch = 32 * (g) + i;                      \
+    if (ch >= nch) break;                             \
+    hv[__builtin_amdgcn_readfirstlane(i)] = step(ch); \
+  }
+  WF_HELD_GROUP(0, h0)
+  WF_HELD_GROUP(1, h1)
+  WF_HELD_GROUP(2, h2)
+  WF_HELD_GROUP(3, h3)
+#undef WF_HELD_GROUP
+  __syncthreads();  // every ring read is done: its first bytes take the pairs below
+
+  // block rows [nJ][2][B]: lane l of wave (ts, qt) holds row 2 j + hi,
+  // column q, of block j = the slice's block in each chunk
+  float* out = a.blocks + (long)u * a.nJ * 2 * B;
+  auto flush = [&](const f32x32& hv, int g) {
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const int ch = 32 * g + i;
+      if (ch >= nch) break;  // uniform
+      const long slice0 = tb + (long)ch * CR + 32 * ts;
+      const long j = slice0 >> J;
+      if (live && slice0 < te && q < B && j < jend) out[(j * 2 + hi) * B + q] = hv[i];
+    }
+  };
+  flush(h0, 0);
+  flush(h1, 1);
+  flush(h2, 2);
+  flush(h3, 3);
+
+  // the range's coarse statistics, as token_skim_kernel
+  {
+    const float m2 = partner32(cm), z2 = partner32(cz);
+    stat_absorb(cm, cz, m2, z2);
+  }
+  if (hi == 0) {
+    red[(wave * 32 + col) * 2] = cm;
+    red[(wave * 32 + col) * 2 + 1] = cz;
+  }
+  __syncthreads();
+  float* ws = a.wstats + ((long)u * a.R + r) * 2 * B;
+  for (int qq = threadIdx.x; qq < B; qq += kTokBlock) {
+    const int t = qq >> 5, c = qq & 31;
+    float mx = -INFINITY, z = 0.f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int w = 4 * t + k;
+      stat_absorb(mx, z, red[(w * 32 + c) * 2], red[(w * 32 + c) * 2 + 1]);
+    }
+    ws[qq] = mx;
+    ws[B + qq] = z;
+  }
+}
+
 // Daubechies-2 at J = 6 from token logits.  The level-6 approximation is one
 // banded filter of the keys (A[n] = sum_m f[m] K[64 n + m], 190 taps), so
 // the coarse logit is the same filter over token logits:
@@ -682,6 +846,24 @@ static FastPlan plan_token(const wf_params& p, int J, long Lf, bool lse, bool ga
   const long U = (long)p.batch * p.heads;
   const long chunks = (Lf + kScanChunk - 1) / kScanChunk;
   const size_t chb = (size_t)kScanChunk * 2 * p.head_dim;
+  constexpr size_t kLdsPerCu = 160 * 1024;
+  // Blocks of 32 tokens with their log-sum-exps: one workgroup per CU that
+  // holds its results until its keys are read (token_skim_held_kernel),
+  // whenever a range of that shape has at most kHeldChunks chunks.
+  if (lse && J == 5 && !gather && !db2_token_path(p) && p.q_len <= 16 * kFastMaxQBlocks) {
+    const long R = std::min(chunks, std::max(1L, ((long)device_cu_count() + U - 1) / U));
+    const long cpr = (chunks + R - 1) / R;
+    if (cpr <= kHeldChunks) {
+      f.span = (int)(cpr * kScanChunk);
+      f.R = (int)((Lf + f.span - 1) / f.span);
+      f.par_cap = 0;
+      f.nbuf = (int)std::min<size_t>(3, kLdsPerCu / chb);
+      // (the ring also takes the end-of-range reduction pairs, 2 KiB)
+      f.lds_bytes = std::max<size_t>((size_t)f.nbuf * chb, 8 * 32 * 2 * sizeof(float));
+      f.held = true;
+      return f;
+    }
+  }
   // two batch slots of block results (the db2 skim: its partial rings); the
   // wave reduction pairs reuse the ring
   const size_t bb = db2_token_path(p) ? db2_fixed_lds(p.q_len)
@@ -690,7 +872,6 @@ static FastPlan plan_token(const wf_params& p, int J, long Lf, bool lse, bool ga
   // Two resident workgroups per CU, each two chunks deep, stream faster than
   // one three deep (the barrier of one overlaps the other's loads); that
   // shape is taken whenever two fit in the CU's LDS.
-  constexpr size_t kLdsPerCu = 160 * 1024;
   const long want0 = std::max(1L, (2L * device_cu_count() + U - 1) / U);
   const long cpr0 = (chunks + std::min(chunks, want0) - 1) / std::min(chunks, want0);
   const size_t ids = gather ? (size_t)(((cpr0 * kScanChunk) >> (J + 1)) + 2) * 4 : 0;
@@ -825,6 +1006,17 @@ hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, f
   }
   const TokenSkimArgs a = token_args(p, f, p.levels, filtered_len(p), p.ctx_len >> p.levels, Q,
                                      K, blocks, wstats);
+  if (f.held) {
+    auto kern = p.head_dim == 128 ? token_skim_held_kernel<128> : token_skim_held_kernel<64>;
+    if (f.lds_bytes > 65536) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         (int)f.lds_bytes);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)(a.U * a.R)), dim3(kTokBlock), f.lds_bytes, s, a);
+    return hipGetLastError();
+  }
   return p.head_dim == 128 ? token_skim_dispatch<128, true>(p.levels, a, f.lds_bytes, s)
                            : token_skim_dispatch<64, true>(p.levels, a, f.lds_bytes, s);
 }

@@ -51,6 +51,7 @@ struct FastPlan {
   int nbuf;          // LDS ring depth
   int par_cap;       // parent ids staged per range (gathered rows), else 0
   size_t lds_bytes;
+  bool held;         // block results kept in registers until the range's keys are read
 };
 
 // Workspace extents of the multi-scale recursion (maxima over its scales).

@@ -98,6 +98,12 @@ EDGE = {
     "tok_j5_b64_long": V_("tj5l", batch=2, heads=8, ctx_len=32 * 1001,
                           head_dim=128, levels=5, segments=64, budget=700,
                           q_len=64, **_BF),
+    # blocks of 32 tokens held in registers until a range's keys are read:
+    # 64 units, four ranges of 119 chunks (all four register groups), the
+    # last range ending one slice into its last chunk, 40 query rows (the
+    # second query tile partly live), d = 64 and a remainder
+    "held_j5_b40_d64": V_("hj5", batch=2, heads=32, ctx_len=32 * 1897 + 11,
+                          levels=5, segments=40, budget=900, q_len=40, **_BF),
     # db2 at J = 6 from token logits: ranges of one chunk (two blocks), an
     # odd coefficient count (the last range holds one block), the fewest
     # coefficients the path takes (4), both extensions, 64 query rows,
