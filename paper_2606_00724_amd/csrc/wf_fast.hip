@@ -506,23 +506,30 @@ __global__ __launch_bounds__(kTokBlock, 2) void token_skim_held_kernel(TokenSkim
 #undef WF_HELD_GROUP
   __syncthreads();  // every ring read is done: its first bytes take the pairs below
 
-  // block rows [nJ][2][B]: lane l of wave (ts, qt) holds row 2 j + hi,
-  // column q, of block j = the slice's block in each chunk
-  float* out = a.blocks + (long)u * a.nJ * 2 * B;
-  auto flush = [&](const f32x32& hv, int g) {
+  // block rows [nJ][2][B]: in chunk ch, wave (ts, qt) holds block
+  // j0 + 4 ch (j0 = tb / 32 + ts), lane l its row 2 j + hi at column q, so
+  // consecutive chunks are 8 B floats apart; the chunks whose block ends
+  // inside the range are the first nv (wave-uniform).  The addresses are one
+  // add apart: with per-store index arithmetic the dependent 64-bit products
+  // held the write phase back.
+  const long j0 = (tb >> J) + ts;
+  const int nv = __builtin_amdgcn_readfirstlane(
+      (int)max(0L, min((long)nch, (jend - j0 + 3) / 4)));
+  if (live && q < B) {
+    float* p = a.blocks + ((long)u * a.nJ + j0) * 2 * B + (long)hi * B + q;
+    const long stride = 8L * B;
+    auto flush = [&](const f32x32& hv, int g) {
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const int ch = 32 * g + i;
-      if (ch >= nch) break;  // uniform
-      const long slice0 = tb + (long)ch * CR + 32 * ts;
-      const long j = slice0 >> J;
-      if (live && slice0 < te && q < B && j < jend) out[(j * 2 + hi) * B + q] = hv[i];
-    }
-  };
-  flush(h0, 0);
-  flush(h1, 1);
-  flush(h2, 2);
-  flush(h3, 3);
+      for (int i = 0; i < 32; ++i) {
+        if (32 * g + i >= nv) break;  // uniform
+        p[(long)(32 * g + i) * stride] = hv[i];
+      }
+    };
+    flush(h0, 0);
+    flush(h1, 1);
+    flush(h2, 2);
+    flush(h3, 3);
+  }
 
   // the range's coarse statistics, as token_skim_kernel
   {
