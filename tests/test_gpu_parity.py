@@ -104,6 +104,10 @@ EDGE = {
     # second query tile partly live), d = 64 and a remainder
     "held_j5_b40_d64": V_("hj5", batch=2, heads=32, ctx_len=32 * 1897 + 11,
                           levels=5, segments=40, budget=900, q_len=40, **_BF),
+    # 256 units of 130 chunks: more than a held range takes at one workgroup
+    # per CU, so 32-token blocks go through the two-workgroup kernel
+    "tok_j5_unheld": V_("uj5", batch=8, heads=32, ctx_len=32 * 520, levels=5,
+                        segments=8, budget=64, q_len=1, **_BF),
     # db2 at J = 6 from token logits: ranges of one chunk (two blocks), an
     # odd coefficient count (the last range holds one block), the fewest
     # coefficients the path takes (4), both extensions, 64 query rows,
