@@ -570,7 +570,13 @@ __global__ __launch_bounds__(kTokBlock, 2) void token_skim_held_kernel(TokenSkim
 // last three coefficients of the unit use the end filters E_m instead, from
 // their own partials of the last three blocks, which the range owning them
 // reads (its reads stop at the unit's end).
-template <int D>
+//
+// HOLD (at most 32 query rows and 128 chunks a range): the block rows wait
+// in registers until the range's keys are read, as in token_skim_held_kernel;
+// wave 4 + c mod 4 completes the coefficients of chunk c, so that each of
+// waves 4..7 holds a coefficient pair every fourth chunk (32 slots of two
+// values a lane).
+template <int D, bool HOLD = false>
 __global__ __launch_bounds__(kTokBlock, 2) void token_db2_kernel(TokenSkimArgs a, Db2TokenTaps tp,
                                                                  int periodic) {
   constexpr int NW = kTokBlock / kWave;  // 8
@@ -645,10 +651,12 @@ __global__ __launch_bounds__(kTokBlock, 2) void token_db2_kernel(TokenSkimArgs a
   const float c2 = a.scale * kLog2e;
   float* out = a.blocks + (long)u * nJ * 2 * B;  // [nJ][2][B]
   // waves 4..7: thread (ci, cq) completes coefficient 2 c + ci of chunk c
-  const int t2 = threadIdx.x - NIW * 64;
+  // (held: lane (ci, cq) of wave 4 + c mod 4)
+  const int t2 = HOLD ? (wave >= NIW ? lane : -1) : threadIdx.x - NIW * 64;
   const int ci = t2 / B, cq = t2 - ci * B;
   const bool comb = t2 >= 0 && t2 < 2 * B;
   float cm = -INFINITY, cz = 0.f;  // running max / sum of exp of the coarse logits
+  f32x32 hl, he;                   // held coarse logits and log-sum-exps (HOLD)
   auto combine = [&](int c) {
     const long n = nb0 + 2L * c + ci;
     if (n >= jend) return;
@@ -673,9 +681,18 @@ __global__ __launch_bounds__(kTokBlock, 2) void token_db2_kernel(TokenSkimArgs a
     const float m0 = st[0], e0 = st[B], m1 = st[2 * B], e1 = st[3 * B];
     const float mx = fmaxf(m0, m1);
     const float e = e0 * __builtin_amdgcn_exp2f((m0 - mx) * c2) + e1 * __builtin_amdgcn_exp2f((m1 - mx) * c2);
-    float* o = out + n * 2 * B + cq;
-    o[0] = l;
-    o[B] = fmaf(mx, a.scale, __logf(e));
+    const float lse = fmaf(mx, a.scale, __logf(e));
+    if constexpr (HOLD) {
+      const int slot = __builtin_amdgcn_readfirstlane(c >> 2);  // c < 128 (host-checked)
+      if (slot < 32) {
+        hl[slot] = l;
+        he[slot] = lse;
+      }
+    } else {
+      float* o = out + n * 2 * B + cq;
+      o[0] = l;
+      o[B] = lse;
+    }
     stat_add(cm, cz, l);
   };
 
@@ -757,20 +774,46 @@ __global__ __launch_bounds__(kTokBlock, 2) void token_db2_kernel(TokenSkimArgs a
       }
     }
     if (ch < nch_ext && live) slice_step(ch);
-    if (comb && ch >= 2) combine(ch - 2);
+    if (comb && ch >= 2 && (!HOLD || wave == NIW + ((ch - 2) & 3))) combine(ch - 2);
+  }
+
+  if constexpr (HOLD) {
+    // slot k of wave 4 + w holds coefficient n0 + 8 k (n0 = nb0 + 2 w + ci):
+    // the rows of consecutive slots are 16 B floats apart
+    if (comb) {
+      const long n0 = nb0 + 2 * (wave - NIW) + ci;
+      const int nv = (int)max(0L, min(32L, (jend - n0 + 7) / 8));
+      float* o = out + n0 * 2 * B + cq;
+      const long stride = 16L * B;
+#pragma unroll
+      for (int k = 0; k < 32; ++k) {
+        if (k < nv) {
+          o[(long)k * stride] = hl[k];
+          o[(long)k * stride + B] = he[k];
+        }
+      }
+    }
   }
 
   // the range's (max, sum of exp) per query from the combining threads
   __syncthreads();
+  constexpr int NCW = HOLD ? 4 : 1;  // waves whose lanes hold partial pairs
   if (comb) {
-    red[2 * t2] = cm;
-    red[2 * t2 + 1] = cz;
+    const int idx = HOLD ? (wave - NIW) * 2 * B + t2 : t2;
+    red[2 * idx] = cm;
+    red[2 * idx + 1] = cz;
   }
   __syncthreads();
   float* ws = a.wstats + ((long)u * a.R + r) * 2 * B;
   for (int qq = threadIdx.x; qq < B; qq += kTokBlock) {
     float m_ = red[2 * qq], z_ = red[2 * qq + 1];
     stat_absorb(m_, z_, red[2 * (B + qq)], red[2 * (B + qq) + 1]);
+#pragma unroll
+    for (int w = 1; w < NCW; ++w) {
+      const float* rw = red + 2 * (w * 2 * B);
+      stat_absorb(m_, z_, rw[2 * qq], rw[2 * qq + 1]);
+      stat_absorb(m_, z_, rw[2 * (B + qq)], rw[2 * (B + qq) + 1]);
+    }
     ws[qq] = m_;
     ws[B + qq] = z_;
   }
@@ -980,10 +1023,10 @@ static TokenSkimArgs token_args(const wf_params& p, const FastPlan& f, int J, lo
   return a;
 }
 
-template <int D>
+template <int D, bool HOLD>
 static hipError_t token_db2_launch(const TokenSkimArgs& a, const Db2TokenTaps& t, int periodic,
                                    size_t lds, hipStream_t s) {
-  auto kern = token_db2_kernel<D>;
+  auto kern = token_db2_kernel<D, HOLD>;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1008,8 +1051,14 @@ hipError_t launch_token_skim(const wf_params& p, const void* Q, const void* K, f
     const TokenSkimArgs a = token_args(p, f, 6, filtered_len(p), p.ctx_len >> 6, Q, K, blocks,
                                        wstats);
     const int periodic = p.boundary == WF_EXT_PERIODIC ? 1 : 0;
-    return p.head_dim == 128 ? token_db2_launch<128>(a, db2_taps6(), periodic, f.lds_bytes, s)
-                             : token_db2_launch<64>(a, db2_taps6(), periodic, f.lds_bytes, s);
+    // block rows held in registers: at most 32 query rows, 128 chunks a range
+    const bool hold = p.q_len <= 32 && f.span / kScanChunk <= 128;
+    if (hold)
+      return p.head_dim == 128
+                 ? token_db2_launch<128, true>(a, db2_taps6(), periodic, f.lds_bytes, s)
+                 : token_db2_launch<64, true>(a, db2_taps6(), periodic, f.lds_bytes, s);
+    return p.head_dim == 128 ? token_db2_launch<128, false>(a, db2_taps6(), periodic, f.lds_bytes, s)
+                             : token_db2_launch<64, false>(a, db2_taps6(), periodic, f.lds_bytes, s);
   }
   const TokenSkimArgs a = token_args(p, f, p.levels, filtered_len(p), p.ctx_len >> p.levels, Q,
                                      K, blocks, wstats);
