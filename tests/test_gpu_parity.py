@@ -337,10 +337,13 @@ def test_init_is_repeatable_and_changes_no_result(wf):
         assert torch.equal(x, y)
 
 
-def test_fused_is_deterministic(wf):
+@pytest.mark.parametrize("name", ["layer8b", "held_j5_b40_d64", "db2tok_sym_odd"])
+def test_fused_is_deterministic(wf, name):
     """Ten calls on the same inputs give bit-identical outputs and indices
-    (no atomics decide an order anywhere on the path)."""
-    w = synth.WORKLOADS["layer8b"]
+    (no atomics decide an order anywhere on the path), with the block rows
+    stored as they complete (8-token blocks) or held to the end of each
+    range (32-token Haar and db2 blocks)."""
+    w = EDGE.get(name) or synth.WORKLOADS[name]
     Q, K, V, _, _ = inputs(w)
     first = run_fused(wf, w, Q, K, V, None, None)
     for r in range(9):
