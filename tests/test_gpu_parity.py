@@ -104,6 +104,15 @@ EDGE = {
     # second query tile partly live), d = 64 and a remainder
     "held_j5_b40_d64": V_("hj5", batch=2, heads=32, ctx_len=32 * 1897 + 11,
                           levels=5, segments=40, budget=900, q_len=40, **_BF),
+    # db2 block rows held until a range's keys are read: 32 units of 1020
+    # chunks (eight ranges of 128, the last of 124 with a remainder), the
+    # symmetric end filters in the last range; a periodic one with 17 query
+    # rows (the combining lanes fill part of a wave)
+    "db2tok_held_sym": V_("d2hs", heads=32, ctx_len=64 * 2040 + 5, levels=6,
+                          segments=40, budget=900, q_len=32, wavelet="db2", **_BF),
+    "db2tok_held_per_b17": V_("d2hp", heads=32, ctx_len=64 * 1024, levels=6,
+                              segments=24, budget=500, q_len=17, wavelet="db2",
+                              boundary="periodic", **_BF),
     # 256 units of 130 chunks: more than a held range takes at one workgroup
     # per CU, so 32-token blocks go through the two-workgroup kernel
     "tok_j5_unheld": V_("uj5", batch=8, heads=32, ctx_len=32 * 520, levels=5,
