@@ -491,16 +491,22 @@ __global__ __launch_bounds__(kAttnRingBlock) void attn_ring_kernel(AttnArgs a) {
     const long r0 = rb0 + (long)c * CR;
     if (indexed && min(r0 + CR, re0) <= (long)a.nsel) {
       constexpr int RPI = 64 / G;
+      // every token id is read from LDS before the first load is issued (an
+      // LDS read between two asm loads waits out its own latency each time)
+      long off[IPW];
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
-        const int inst = wave * IPW + i;
-        const int r = inst * RPI + lane / G;
+        const int r = (wave * IPW + i) * RPI + lane / G;
         const int k = (lane % G) ^ granule_swz<G>(r);
         // token ids are clamped into the unit: a bad id cannot leave K / V
         const int t = min(max(toks[min((int)(r0 - rb0) + r, split_last)], 0), a.L - 1);
-        const long off = (long)t * D + 8 * k;
-        async_load16<true>(kunit + off, __builtin_amdgcn_readfirstlane(slot + 1024u * inst));
-        async_load16<true>(vunit + off, __builtin_amdgcn_readfirstlane(slot + CHB + 1024u * inst));
+        off[i] = (long)t * D + 8 * k;
+      }
+#pragma unroll
+      for (int i = 0; i < IPW; ++i) {
+        const int inst = wave * IPW + i;
+        async_load16<true>(kunit + off[i], __builtin_amdgcn_readfirstlane(slot + 1024u * inst));
+        async_load16<true>(vunit + off[i], __builtin_amdgcn_readfirstlane(slot + CHB + 1024u * inst));
       }
     } else {
       kp.r0 = vp.r0 = r0;

@@ -216,6 +216,27 @@ struct PoolRowPtr {
   }
 };
 
+// The pool rows of one chunk into a ring slot, as issue_chunk, but every
+// row's region id is read from LDS before the first load is issued: an LDS
+// read between two of the asm loads waits out its own latency each time.
+template <int CR, int G, int NW, bool STREAM, int D>
+__device__ __forceinline__ void issue_pool_chunk(uint32_t lds_base, const PoolRowPtr<D>& rowptr) {
+  constexpr int RPI = 64 / G;
+  constexpr int IPW = CR * G / (64 * NW);
+  static_assert(IPW * 64 * NW == CR * G, "chunk must fill whole instructions");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned char* g[IPW];
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int r = (wave * IPW + i) * RPI + lane / G;
+    const int k = (lane % G) ^ granule_swz<G>(r);
+    g[i] = reinterpret_cast<const unsigned char*>(rowptr(r)) + 16 * k;
+  }
+#pragma unroll
+  for (int i = 0; i < IPW; ++i)
+    async_load16<STREAM>(g[i], __builtin_amdgcn_readfirstlane(lds_base + 1024u * (wave * IPW + i)));
+}
+
 // 8 waves: two per SIMD, so that one wave's MFMA, exp and LDS latencies
 // overlap the other's work (with one wave per SIMD the ring kernel ran at
 // well under the gather rate of its memory pattern).
@@ -317,7 +338,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     // pass reads the pool for the last time: streaming loads)
     for (int k = 0; k < nch && k < nbuf - 1; ++k) {
       rp.p0 = pb + (long)k * CR;
-      issue_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(k * CHB), rp);
+      issue_pool_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(k * CHB), rp);
     }
     if constexpr (WEIGHTS) {
       // pool normalisers (M_q, Z_q) over the pool's tokens, from the selected
@@ -432,7 +453,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
     // attention that follows loads the selected keys with nt as well).
     for (int k = 0; k < nch && k < nbuf - 1 && !(SEL && qg == 0); ++k) {
       rp.p0 = pb + (long)k * CR;
-      issue_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(k * CHB), rp);
+      issue_pool_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(k * CHB), rp);
     }
     for (int ch = 0; ch < nch; ++ch) {
       const long p0 = pb + (long)ch * CR;
@@ -441,7 +462,7 @@ __global__ __launch_bounds__(kPoolBlock) void scan_ring_kernel(ScanArgs a) {
       lds_barrier();  // chunk ch visible; everyone is past chunk ch - 1
       if (ch + nbuf - 1 < nch) {
         rp.p0 = pb + (long)(ch + nbuf - 1) * CR;
-        issue_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rp);
+        issue_pool_chunk<CR, G, NW, (bool)WEIGHTS>(ring_lds + (uint32_t)(((ch + nbuf - 1) % nbuf) * CHB), rp);
       }
       const unsigned char* buf = ring + (ch % nbuf) * CHB;
 #pragma unroll
